@@ -1,0 +1,363 @@
+"""Pins for the CPU oracle: checks against what the MicroAdam paper and plain
+mathematics fix, never against the oracle's own formulas.
+
+Each ``check_*`` function takes an ``oracle.Oracle`` and raises
+``AssertionError`` on a mismatch.  ``test_oracle_pins.py`` runs them on the
+real oracle; ``test_oracle_mutants.py`` runs them on deliberately broken
+builds of the oracle source and requires every break to be caught.
+
+What pins what:
+  - Top-K: brute-force full sort with lower-index-wins ties (Section 3.1);
+    the Top-K contraction bound of Assumption 1 per block.
+  - Q / Q^-1 (Algorithm 2): half-step error bound, min -> code 0 decoding
+    exactly, max -> code 15, all-equal bucket -> 0, half-to-even on exact
+    half steps, monotone codes.
+  - Error feedback (Algorithm 1): bucket min/max of the residual recomputed
+    by numpy; the reconstruction decode(e_{t+1}) + V ~= a_t.
+  - AdamStats: with density 1 the window moments are Adam's bias-corrected
+    EMA (t <= m, Adam recurrence) or its m-term truncation (t > m, a sliding
+    recurrence); m = 1 closed form; a spike per step pins beta^(t-s) and which
+    rows are live (Section 3, "Dynamic Statistics").
+  - Update: the t = 1 closed form theta - eta*V/(eps+|V|) on the kept
+    entries; untouched entries bit-identical for lambda = 0; decoupled decay
+    (1 - eta*lambda)*theta elsewhere (Algorithm 4).
+  - bf16 rounding: torch's CPU float32 -> bfloat16 conversion (RNE), and a
+    binary64 double-rounding case.
+"""
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+import numpy as np
+import torch
+
+BETA1, BETA2, EPS = 0.9, 0.999, 1e-8
+
+
+def _bf16(x) -> np.ndarray:
+    """float32 -> bf16 (round-half-to-even) by torch's CPU conversion."""
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).to(torch.float32).numpy()
+
+
+def _brute_topk(x: np.ndarray, k: int) -> list[int]:
+    """Positions of the k largest |x|, lower index first on ties, sorted."""
+    order = sorted(range(len(x)), key=lambda i: (-abs(float(x[i])), i))
+    return sorted(order[:k])
+
+
+def _decode(codes, lo, hi, bucket):
+    """Q^-1 per element in binary32 (x_Q * u + delta, u = (Delta-delta)/15)."""
+    b = np.arange(codes.size) // bucket
+    u = ((hi[b] - lo[b]) / np.float32(15)).astype(np.float32)
+    return (codes.astype(np.float32) * u).astype(np.float32) + lo[b]
+
+
+def _ulp(x) -> np.ndarray:
+    return np.spacing(np.abs(np.asarray(x, np.float32))).astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+def check_round_bf16(o) -> None:
+    rng = np.random.default_rng(11)
+    xs = np.concatenate([
+        rng.standard_normal(2000).astype(np.float32) * 10.0 ** rng.integers(-30, 30, 2000),
+        # exact halfway cases with even and odd kept parts
+        np.array([0x3F808000, 0x3F818000, 0xBF808000, 0x00008000, 0x00018000,
+                  0x7F7F8000, 0x7F7FFFFF, 0x00000001, 0x80000001, 0x007FFFFF],
+                 dtype=np.uint32).view(np.float32),
+    ]).astype(np.float32)
+    want = _bf16(xs)
+    got = np.array([o.round_bf16(float(x)) for x in xs], np.float32)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), "bf16 RNE"
+    # binary64 input: 1 + 2^-8 + 2^-40 lies above the bf16 midpoint 1 + 2^-8,
+    # so it rounds up; rounding through binary32 first would tie to 1.0.
+    assert o.round_bf16(1.0 + 2.0 ** -8 + 2.0 ** -40) == 1.0 + 2.0 ** -7
+    assert o.round_bf16(1.0 + 2.0 ** -8) == 1.0            # tie to even
+    assert o.round_bf16(1.0 + 3 * 2.0 ** -8) == 1.0 + 2.0 ** -6
+
+
+def check_quantizer(o) -> None:
+    # half steps round to even: lo = 0, hi = 15 gives u = 1
+    for x, want in [(0.5, 0), (1.5, 2), (2.5, 2), (3.5, 4), (14.5, 14), (0.49, 0),
+                    (0.51, 1), (15.0, 15), (0.0, 0), (7.0, 7)]:
+        assert o.quantize(x, 0.0, 15.0) == want, (x, want)
+    assert o.quantize(3.0, 3.0, 3.0) == 0 and o.dequantize(0, 3.0, 3.0) == 3.0
+    assert o.dequantize(9, -2.0, -2.0) == -2.0
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        lo, hi = np.sort(rng.standard_normal(2).astype(np.float32) * np.float32(10.0 ** rng.integers(-6, 3)))
+        lo, hi = float(lo), float(hi)
+        u = (hi - lo) / 15.0
+        assert o.quantize(lo, lo, hi) == 0 and o.dequantize(0, lo, hi) == lo
+        if hi > lo:
+            assert o.quantize(hi, lo, hi) == 15
+        xs = np.sort(rng.uniform(lo, hi, 64).astype(np.float32))
+        codes = [o.quantize(float(x), lo, hi) for x in xs]
+        assert all(0 <= c <= 15 for c in codes)
+        assert all(a <= b for a, b in zip(codes, codes[1:])), "codes not monotone"
+        slack = 4 * float(_ulp(max(abs(lo), abs(hi))))
+        for x, c in zip(xs, codes):
+            assert abs(o.dequantize(c, lo, hi) - float(x)) <= u / 2 + slack, (x, lo, hi)
+
+
+def check_topk_bruteforce(o) -> None:
+    rng = np.random.default_rng(7)
+    cases = [
+        dict(n=1000, block=128, bucket=16, density=0.05),   # k 7, tail 104 -> 6
+        dict(n=700, block=64, bucket=8, density=0.2),       # k 13, tail 60 -> 12
+        dict(n=96, block=32, bucket=32, density=0.5),       # k 16
+    ]
+    for ci, case in enumerate(cases):
+        for kind in ("normal", "ties", "zeros"):
+            n = case["n"]
+            if kind == "normal":
+                g = rng.standard_normal(n).astype(np.float32)
+            elif kind == "ties":
+                g = (rng.integers(-3, 4, n) * rng.choice([1.0, 0.5], n)).astype(np.float32)
+            else:
+                g = np.zeros(n, np.float32)
+                g[rng.integers(0, n, 5)] = -1.0
+            for value_bf16 in (False, True):
+                kw = {k: v for k, v in case.items() if k != "n"}
+                st = o.tensor(n, window=3, value_bf16=value_bf16, **kw)
+                theta = np.zeros(n, np.float32)
+                st.step(theta, g, 1, 1e-3)
+                for q in range(st.nblocks):
+                    s0 = q * case["block"]
+                    xb = g[s0:s0 + st.block_size(q)]
+                    want = _brute_topk(xb, st.block_k(q))
+                    idx, val = st.window_entries(0, q)
+                    assert list(idx) == want, (ci, kind, q)
+                    wv = xb[want]
+                    if value_bf16:
+                        wv = _bf16(wv)
+                    assert np.array_equal(val.view(np.uint32), wv.view(np.uint32)), (ci, kind, q)
+
+
+def check_k_per_block(o) -> None:
+    """k = ceil(density * s) per block (the paper sizes k as ceil(d/100) for
+    1% density), checked with exact rational arithmetic."""
+    for s, dens in [(4096, "1/100"), (768, "1/100"), (3072, "1/100"), (3584, "1/100"),
+                    (100, "1/100"), (1024, "1/100"), (65536, "1/20"), (12032, "1/20"),
+                    (60, "1/20"), (4096, "1"), (7, "1/1000"), (200, "3/100")]:
+        f = Fraction(dens)
+        want = min(s, max(1, math.ceil(f * s)))
+        assert o.block_k(s, float(f)) == want, (s, dens)
+    # and the window holds exactly that many entries per block
+    st = o.tensor(1000, block=128, bucket=16, density=0.05, window=2)
+    st.step(np.zeros(1000, np.float32), np.ones(1000, np.float32), 1, 1e-3)
+    assert st.K == 7 * 7 + math.ceil(Fraction(1, 20) * 104)
+
+
+def check_contraction(o) -> None:
+    rng = np.random.default_rng(8)
+    n, block = 5000, 500
+    g = (rng.standard_t(3, n) * 1e-2).astype(np.float32)
+    st = o.tensor(n, block=block, bucket=50, density=0.03, window=2, value_bf16=False)
+    st.step(np.zeros(n, np.float32), g, 1, 1e-3)
+    for q in range(st.nblocks):
+        a = g[q * block:(q + 1) * block].astype(np.float64)
+        idx, _ = st.window_entries(0, q)
+        r = a.copy()
+        r[idx.astype(np.int64)] = 0.0
+        k = st.block_k(q)
+        assert (r ** 2).sum() <= (1 - k / a.size) * (a ** 2).sum() * (1 + 1e-12)
+
+
+def check_ef_after_first_step(o) -> None:
+    rng = np.random.default_rng(9)
+    n, block, bucket = 1001, 128, 16          # odd n, 9-element tail bucket
+    g = rng.standard_normal(n).astype(np.float32)
+    st = o.tensor(n, block=block, bucket=bucket, density=0.05, window=4)
+    st.step(np.zeros(n, np.float32), g, 1, 1e-3)
+    r = g.copy()                               # residual a - T_k(a) at t = 1
+    for q in range(st.nblocks):
+        idx, _ = st.window_entries(0, q)
+        r[q * block + idx.astype(np.int64)] = 0.0
+    codes = st.codes()
+    assert st.ef.size == (n + 1) // 2 and (st.ef[-1] >> 4) == 0
+    for b in range(st.nbuckets):
+        x = r[b * bucket:(b + 1) * bucket]
+        lo, hi = np.float32(x.min()) + np.float32(0), np.float32(x.max()) + np.float32(0)
+        assert st.delta[b].view(np.uint32) == lo.view(np.uint32), b
+        assert st.Delta[b].view(np.uint32) == hi.view(np.uint32), b
+        c = codes[b * bucket:(b + 1) * bucket]
+        assert c[np.argmin(x)] == 0
+        if hi > lo:
+            assert c[np.argmax(x)] == 15
+
+
+def check_reconstruction(o) -> None:
+    rng = np.random.default_rng(10)
+    n, block, bucket = 3000, 256, 32
+    st = o.tensor(n, block=block, bucket=bucket, density=0.02, window=3)
+    theta = np.zeros(n, np.float32)
+    for t in range(1, 6):
+        g = rng.standard_normal(n).astype(np.float32)
+        a = (g + _decode(st.codes(), st.delta, st.Delta, bucket)).astype(np.float32)
+        st.step(theta, g, t, 1e-3)
+        rec = _decode(st.codes(), st.delta, st.Delta, bucket).astype(np.float64)
+        bound = np.zeros(n)
+        bidx = np.arange(n) // bucket
+        bound += (st.Delta[bidx].astype(np.float64) - st.delta[bidx]) / 15 / 2
+        bound += 4 * _ulp(np.maximum(np.abs(st.delta[bidx]), np.abs(st.Delta[bidx])))
+        row = st.row_of_step(t)
+        for q in range(st.nblocks):
+            idx, val = st.window_entries(row, q)
+            i = q * block + idx.astype(np.int64)
+            rec[i] += val
+            bound[i] += np.abs(val.astype(np.float64) - a[i]) + _ulp(a[i])
+        assert np.all(np.abs(rec - a) <= bound), t
+
+
+def _sliding(gs, beta, m, t):
+    """Truncated bias-corrected EMA of g_1..g_t over the last m steps, built by
+    a sliding recurrence S_t = beta*S_{t-1} + g_t - beta^m g_{t-m}."""
+    S = np.zeros_like(gs[0])
+    for s in range(1, t + 1):
+        S = beta * S + gs[s - 1]
+        if s - m >= 1:
+            S = S - beta ** m * gs[s - m - 1]
+    return (1 - beta) * S / (1 - beta ** t)
+
+
+def check_density_one_is_adam(o) -> None:
+    rng = np.random.default_rng(12)
+    n, m = 300, 4
+    st = o.tensor(n, block=64, bucket=16, density=1.0, window=m, value_bf16=False)
+    theta = np.zeros(n, np.float32)
+    gs = []
+    m1 = np.zeros(n)
+    v1 = np.zeros(n)
+    for t in range(1, 10):
+        g = rng.standard_normal(n).astype(np.float32)
+        gs.append(g.astype(np.float64))
+        st.step(theta, g, t, 1e-3)
+        assert not st.ef.any() and not st.delta.any() and not st.Delta.any()
+        mh, vh = st.moments(t)
+        if t <= m:        # plain Adam: m_t = b1 m + (1-b1) g, bias-corrected
+            m1 = BETA1 * m1 + (1 - BETA1) * gs[-1]
+            v1 = BETA2 * v1 + (1 - BETA2) * gs[-1] ** 2
+            want_m, want_v = m1 / (1 - BETA1 ** t), v1 / (1 - BETA2 ** t)
+        else:
+            want_m = _sliding(gs, BETA1, m, t)
+            want_v = _sliding([x ** 2 for x in gs], BETA2, m, t)
+        scale_m = sum(np.abs(x) for x in gs[-m:]) + 1e-30
+        assert np.all(np.abs(mh - want_m) <= 1e-10 * scale_m), t
+        assert np.allclose(vh, want_v, rtol=1e-10, atol=0), t
+
+
+def check_first_step_closed_form(o) -> None:
+    rng = np.random.default_rng(13)
+    n, lr = 2000, 1e-3
+    st = o.tensor(n, block=256, bucket=32, density=0.02, window=5)
+    theta0 = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    theta = theta0.copy()
+    st.step(theta, g, 1, lr)
+    want = theta0.copy()
+    for q in range(st.nblocks):
+        idx, val = st.window_entries(0, q)
+        i = q * 256 + idx.astype(np.int64)
+        V = val.astype(np.float64)
+        want[i] = (theta0[i].astype(np.float64) - lr * V / (EPS + np.abs(V))).astype(np.float32)
+        assert np.array_equal(val, _bf16(g[i]))
+    assert np.array_equal(theta.view(np.uint32), want.view(np.uint32))
+
+
+def check_window_one_closed_form(o) -> None:
+    rng = np.random.default_rng(14)
+    n = 1500
+    st = o.tensor(n, block=500, bucket=50, density=0.05, window=1)
+    theta = np.zeros(n, np.float32)
+    for t in range(1, 6):
+        st.step(theta, rng.standard_normal(n).astype(np.float32), t, 1e-3)
+        mh, vh = st.moments(t)
+        wm, wv = np.zeros(n), np.zeros(n)
+        for q in range(st.nblocks):
+            idx, val = st.window_entries(0, q)
+            V = val.astype(np.float64)
+            wm[q * 500 + idx.astype(np.int64)] = (1 - BETA1) / (1 - BETA1 ** t) * V
+            wv[q * 500 + idx.astype(np.int64)] = (1 - BETA2) / (1 - BETA2 ** t) * V * V
+        assert np.allclose(mh, wm, rtol=1e-12, atol=0), t
+        assert np.allclose(vh, wv, rtol=1e-12, atol=0), t
+
+
+def check_decay_exponents(o) -> None:
+    """One spike per step at a fresh position; k = 1 per block keeps exactly
+    that spike, so each live row contributes one known term beta^(t-s) V_s."""
+    n, m = 64, 3
+    pos = [5, 17, 29, 41, 53, 60, 2]
+    st = o.tensor(n, block=64, bucket=16, density=1 / 64, window=m, value_bf16=False)
+    theta = np.zeros(n, np.float32)
+    rng = np.random.default_rng(15)
+    spikes = {}
+    for t in range(1, len(pos) + 1):
+        g = (rng.standard_normal(n) * 1e-4).astype(np.float32)
+        g[pos[t - 1]] = 10.0 + t
+        st.step(theta, g, t, 1e-3)
+        idx, val = st.window_entries(st.row_of_step(t), 0)
+        assert list(idx) == [pos[t - 1]]
+        spikes[t] = float(val[0])
+        mh, vh = st.moments(t)
+        want_m, want_v = np.zeros(n), np.zeros(n)
+        for s in range(max(1, t - m + 1), t + 1):
+            want_m[pos[s - 1]] = (1 - BETA1) / (1 - BETA1 ** t) * BETA1 ** (t - s) * spikes[s]
+            want_v[pos[s - 1]] = (1 - BETA2) / (1 - BETA2 ** t) * BETA2 ** (t - s) * spikes[s] ** 2
+        assert np.allclose(mh, want_m, rtol=1e-12, atol=0), t
+        assert np.allclose(vh, want_v, rtol=1e-12, atol=0), t
+
+
+def check_untouched_and_sparsity(o) -> None:
+    rng = np.random.default_rng(16)
+    n, block, m = 4096, 512, 3
+    st = o.tensor(n, block=block, bucket=64, density=0.01, window=m)
+    theta0 = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    theta = theta0.copy()
+    for t in range(1, 7):
+        before = theta.copy()
+        st.step(theta, rng.standard_normal(n).astype(np.float32), t, 1e-3)
+        live = np.zeros(n, bool)
+        nlive = 0
+        for s in range(max(1, t - m + 1), t + 1):
+            for q in range(st.nblocks):
+                idx, _ = st.window_entries(st.row_of_step(s), q)
+                live[q * block + idx.astype(np.int64)] = True
+                nlive += idx.size
+        assert np.array_equal(theta[~live].view(np.uint32), before[~live].view(np.uint32))
+        assert np.count_nonzero(theta != before) <= nlive
+
+
+def check_weight_decay(o) -> None:
+    rng = np.random.default_rng(17)
+    n, lr, wd = 2048, 1e-2, 0.1
+    st = o.tensor(n, block=1024, bucket=64, density=0.01, window=2, weight_decay=wd)
+    theta0 = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    theta = theta0.copy()
+    st.step(theta, rng.standard_normal(n).astype(np.float32), 1, lr)
+    live = np.zeros(n, bool)
+    for q in range(st.nblocks):
+        idx, val = st.window_entries(0, q)
+        live[q * 1024 + idx.astype(np.int64)] = True
+    want = (theta0.astype(np.float64) * (1 - lr * wd)).astype(np.float32)
+    assert np.array_equal(theta[~live], want[~live])
+    assert not np.array_equal(theta[live], want[live])
+
+
+ALL_CHECKS = [
+    check_round_bf16,
+    check_quantizer,
+    check_topk_bruteforce,
+    check_k_per_block,
+    check_contraction,
+    check_ef_after_first_step,
+    check_reconstruction,
+    check_density_one_is_adam,
+    check_first_step_closed_form,
+    check_window_one_closed_form,
+    check_decay_exponents,
+    check_untouched_and_sparsity,
+    check_weight_decay,
+]

@@ -1,0 +1,60 @@
+"""Plants plausible mistakes in a copy of the oracle source (on the CPU) and
+requires the pins to catch each one.  This is how the pins are shown to be
+strong enough: a dropped term, a wrong sign, a wrong index or exponent, a
+reversed tie rule or the wrong rounding mode must all fail some pin."""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import oracle_pins
+
+# (label, text in microadam_oracle.c, replacement)
+MUTANTS = [
+    ("exponent r off by one", "pow(beta, (double)(t - s))", "pow(beta, (double)(t - s + 1))"),
+    ("bias correction dropped", "const double scale = (1.0 - beta) / (1.0 - pow(beta, (double)t));",
+     "const double scale = (1.0 - beta);"),
+    ("bias correction over the window only",
+     "const double scale = (1.0 - beta) / (1.0 - pow(beta, (double)t));",
+     "const double scale = (1.0 - beta) / (1.0 - pow(beta, (double)(t < m ? t : m)));"),
+    ("one row too many", "int64_t first = t - m + 1;", "int64_t first = t - m;"),
+    ("row pointer off by one", "const int64_t row = (t - 1) % m;", "const int64_t row = t % m;"),
+    ("higher index wins ties", "return (i < j) ? -1 : (i > j);", "return (i > j) ? -1 : (i < j);"),
+    ("signed instead of |a|", "float ai = fabsf(g_sort_vals[i]), aj = fabsf(g_sort_vals[j]);",
+     "float ai = g_sort_vals[i], aj = g_sort_vals[j];"),
+    ("kept entries not zeroed", "for (int64_t j = 0; j < k; ++j) ab[chosen[j]] = 0.0f;", ""),
+    ("round half up", "float r = nearbyintf(y);", "float r = floorf(y + 0.5f);"),
+    ("truncating quantizer", "float r = nearbyintf(y);", "float r = floorf(y);"),
+    ("decode sign", "return scaled + lo;", "return scaled - lo;"),
+    ("decode level 16", "#define EF_LEVELS 15.0f", "#define EF_LEVELS 16.0f"),
+    ("min and max swapped", "if (a[i - lo] < mn) mn = a[i - lo];", "if (a[i - lo] > mn) mn = a[i - lo];"),
+    ("update sign", "(double)theta[i] * decay - lr * upd", "(double)theta[i] * decay + lr * upd"),
+    ("eps inside sqrt", "mh[i - lo] / (c->eps + sqrt(vh[i - lo]))", "mh[i - lo] / sqrt(c->eps + vh[i - lo])"),
+    ("second moment not squared", "(squared ? v * v : v)", "(squared ? v : v)"),
+    ("decay sign", "1.0 - lr * c->weight_decay", "1.0 + lr * c->weight_decay"),
+    ("bf16 keeps 9 bits", "int q = e - 8;", "int q = e - 9;"),
+    ("accumulator ignores EF", "a[i - lo] = grad[i] + dequantize(get_code(ef, i), delta[b], Delta[b]);",
+     "a[i - lo] = grad[i];"),
+    ("nibbles swapped", "return (i & 1) ? (unsigned)(byte >> 4) : (unsigned)(byte & 0x0F);",
+     "return (i & 1) ? (unsigned)(byte & 0x0F) : (unsigned)(byte >> 4);"),
+    ("beta1 for both moments", "adam_stats(c, t, c->beta2, 1,", "adam_stats(c, t, c->beta1, 1,"),
+    ("k rounds down", "double x = ceil(density * (double)s - 1e-9);", "double x = floor(density * (double)s);"),
+]
+
+
+@pytest.mark.parametrize("label,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, label, old, new):
+    src = open(oracle.SOURCE).read()
+    assert src.count(old) == 1, f"mutation anchor not unique/present: {old!r}"
+    mutated = tmp_path / "mutant.c"
+    mutated.write_text(src.replace(old, new))
+    lib = oracle.build(str(mutated), str(tmp_path / "libmutant.so"))
+    o = oracle.Oracle(lib)
+    caught = []
+    for check in oracle_pins.ALL_CHECKS:
+        try:
+            check(o)
+        except (AssertionError, ValueError, IndexError):
+            caught.append(check.__name__)
+    assert caught, f"no pin catches mutant '{label}'"
