@@ -1,0 +1,195 @@
+/*
+ * microadam.h -- C ABI of libmicroadam.so, a MicroAdam optimizer step for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * MicroAdam ("MicroAdam: Accurate Adaptive Optimization with Low Space
+ * Overhead and Provable Convergence", Modoranu et al., 2024) keeps, per
+ * parameter tensor:
+ *   - a 4-bit error-feedback (EF) buffer e with per-bucket min/max metadata
+ *     (delta, Delta) (Algorithm 1, the quantized EF; Section 3.1,
+ *     "Quantization metadata");
+ *   - a sliding window G = (I, V) of the last m sparse gradients, m rows of
+ *     k block-relative uint16 indices and bf16 values (Section 3, notation;
+ *     Section 3.1, "Top-K"; Section 3.2 for the 4-bytes-per-entry budget).
+ * One step (Algorithm 1) decodes e and adds it to the gradient, keeps the
+ * block-wise Top-K of |a| in a new window row, re-quantizes the residual
+ * into e, rebuilds the Adam moments from the window (AdamStats, Algorithm 2)
+ * and updates the parameters, with decoupled weight decay (Algorithm 4).
+ *
+ * Conventions for every call:
+ *   - Return value: MICROADAM_OK (0) or a negative MICROADAM_ERR_* code.
+ *     Arguments are validated before any device work is queued, so a call
+ *     that fails leaves parameters and optimizer state untouched.
+ *     microadam_error_string() names a code; microadam_last_error() gives the
+ *     calling thread's most recent failure message in detail.
+ *   - Device pointers are HIP device addresses owned by the caller.  Host
+ *     pointers are plain host memory owned by the caller and only read
+ *     during the call.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Device work is queued on it and the call returns without waiting.
+ *   - A handle must be used by one host thread at a time.
+ *   - No C++ exception crosses this interface.
+ */
+#ifndef MICROADAM_H
+#define MICROADAM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  MICROADAM_OK = 0,
+  MICROADAM_ERR_INVALID_ARG = -1, /* null pointer, value out of range, misaligned buffer */
+  MICROADAM_ERR_UNSUPPORTED = -2, /* a valid but unimplemented configuration */
+  MICROADAM_ERR_SHAPE = -3,       /* tensor count or sizes differ from microadam_init */
+  MICROADAM_ERR_STATE_SIZE = -4,  /* state buffer smaller than microadam_state_bytes */
+  MICROADAM_ERR_HIP = -5,         /* a HIP runtime call failed (see microadam_last_error) */
+  MICROADAM_ERR_NO_MEMORY = -6    /* host or library-internal allocation failed */
+};
+
+/* Element types of parameters and gradients. */
+enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
+
+/*
+ * Hyper-parameters, in the paper's notation (Section 3, notation; Appendix B
+ * gives the values the paper trains with: density 0.01, m = 10, b = 4,
+ * bucket 64, beta1 0.9, beta2 0.999, eps 1e-8).
+ *
+ *   density      k/d in (0, 1].  A Top-K block of s elements keeps
+ *                k_s = min(s, max(1, ceil(density * s - 1e-9))) entries.
+ *   beta1,beta2  moment decay rates in [0, 1).
+ *   eps          added to sqrt(v-hat) in the update (Algorithm 1); >= 0.
+ *   lr           default step size eta (microadam_step may override it).
+ *   weight_decay lambda of the decoupled decay theta *= (1 - eta*lambda)
+ *                (Algorithm 4); >= 0.
+ *   window       m, rows in the sliding window, 1..64.
+ *   ef_bits      b, bits per EF code; only 4 is implemented.
+ *   ef_bucket    B_q, elements sharing one (delta, Delta) pair; a power of
+ *                two in [8, 512] dividing topk_block.
+ *   topk_block   B_d, Top-K block size; a multiple of ef_bucket, at most
+ *                65536 (block-relative indices are uint16).
+ *   window_value_dtype  MICROADAM_BF16 (the paper's choice, Section 3.2) or
+ *                MICROADAM_F32 (lossless window values, for checking the
+ *                moment rebuild).
+ */
+typedef struct microadam_config {
+  double density;
+  double beta1;
+  double beta2;
+  double eps;
+  double lr;
+  double weight_decay;
+  int32_t window;
+  int32_t ef_bits;
+  int32_t ef_bucket;
+  int32_t topk_block;
+  int32_t window_value_dtype;
+  int32_t reserved; /* must be 0 */
+} microadam_config;
+
+typedef struct microadam_handle_s* microadam_handle;
+
+/*
+ * Where one tensor's optimizer state lives inside the state buffer (byte
+ * offsets from its start; every region is 256-byte aligned).
+ *
+ *   EF codes   ef_offset, ceil(numel/2) bytes: element 2j in the low nibble
+ *              of byte j, element 2j+1 in the high nibble (an odd numel
+ *              leaves the last high nibble 0).
+ *   stats      stats_offset, num_buckets pairs of float32 (delta, Delta) =
+ *              (min, max) of the bucket's residual; bucket b covers elements
+ *              [b*B_q, min(numel, (b+1)*B_q)).
+ *   window     window_offset, block-major: block q's m rows start at
+ *              window_offset + q*m*k_full*entry_bytes; within it, row r
+ *              (the row written at step s is r = (s-1) mod m) starts at
+ *              r*k_q*entry_bytes and holds k_q entries in ascending index
+ *              order.  With bf16 values an entry is one little-endian uint32
+ *              (index | bf16_bits << 16); with float32 values it is a uint32
+ *              index followed by the float32 value.
+ */
+typedef struct microadam_layout {
+  int64_t numel;
+  int64_t num_blocks;
+  int64_t num_buckets;
+  int32_t k_full;      /* entries per row of a full block */
+  int32_t k_last;      /* entries per row of the last block */
+  int32_t entry_bytes; /* 4 (bf16 values) or 8 (float32 values) */
+  int32_t reserved;
+  uint64_t ef_offset, ef_bytes;
+  uint64_t stats_offset, stats_bytes;
+  uint64_t window_offset, window_bytes;
+} microadam_layout;
+
+/*
+ * Size in bytes of the device state buffer for tensors of the given element
+ * counts (numels[0..n_tensors), each >= 1).  Pure host computation: EF codes
+ * (ceil(n/2) B), bucket stats (8 B per bucket) and the window (m * sum of k
+ * per block entries of entry_bytes), each region 256-byte aligned.  This is
+ * the paper's 0.5d + 4mk (Section 3.2) plus the (delta, Delta) metadata of
+ * Section 3.1 and per-block rounding of k.
+ */
+int microadam_state_bytes(const microadam_config* cfg, const int64_t* numels,
+                          int32_t n_tensors, uint64_t* out_bytes);
+
+/*
+ * Creates a handle for the tensor list numels[0..n_tensors) and clears the
+ * caller-owned device buffer `state` (>= microadam_state_bytes bytes, 256-byte
+ * aligned) on `stream`: e = 0, delta = Delta = 0 as in the initialisation of
+ * Algorithm 1.  The step counter starts at 0 (the next step is t = 1).
+ * param_dtype / grad_dtype: MICROADAM_F32 or MICROADAM_BF16.
+ * The library keeps a small device table of its own (freed by destroy);
+ * `state` stays owned by the caller and must outlive the handle.
+ */
+int microadam_init(const microadam_config* cfg, const int64_t* numels,
+                   int32_t n_tensors, int32_t param_dtype, int32_t grad_dtype,
+                   void* state, uint64_t state_bytes, void* stream,
+                   microadam_handle* out);
+
+/*
+ * One MicroAdam step (Algorithm 1 with the decay of Algorithm 4) over all
+ * tensors, as one kernel launch on `stream`.  params[j] (updated in place)
+ * and grads[j] (read only) are device pointers to numels[j] contiguous
+ * elements of the init dtypes, 16-byte aligned.  lr: the step size eta for
+ * this step, or NaN to use cfg.lr.  The step counter t advances by one.
+ */
+int microadam_step(microadam_handle h, void* const* params,
+                   const void* const* grads, int32_t n_tensors, double lr,
+                   void* stream);
+
+/* Frees the handle and the library's device table (waits for nothing;
+ * the caller must not destroy a handle whose step may still be running on
+ * a stream it will not synchronize).  NULL is accepted. */
+int microadam_destroy(microadam_handle h);
+
+/* Steps taken so far (the t of the last step), or a negative error code. */
+int64_t microadam_get_step(microadam_handle h);
+
+/* Sets the step counter, e.g. after restoring a saved state buffer: the next
+ * step is t + 1.  t >= 0. */
+int microadam_set_step(microadam_handle h, int64_t t);
+
+/* Layout of tensor `tensor`'s state (see microadam_layout). */
+int microadam_tensor_layout(microadam_handle h, int32_t tensor,
+                            microadam_layout* out);
+
+/*
+ * Test support: recomputes the dense float32 m-hat and v-hat of tensor
+ * `tensor` from the window as it stands after the last step (AdamStats,
+ * Algorithm 2, at the current t >= 1), into device buffers of numel floats.
+ */
+int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat,
+                            float* vhat, void* stream);
+
+/* Static name of an error code. */
+const char* microadam_error_string(int code);
+
+/* The calling thread's most recent error message ("" if none). */
+const char* microadam_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MICROADAM_H */

@@ -1,0 +1,438 @@
+// Host side of libmicroadam: configuration checks, the state layout planner,
+// the device descriptor tables and the per-step constants.  Every entry point
+// validates its arguments before queueing device work.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "microadam.h"
+#include "microadam_device.h"
+
+using microadam::StepParams;
+using microadam::TensorDesc;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(MICROADAM_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+constexpr uint64_t kAlign = 256;
+constexpr size_t kMaxLds = 65536;        // dynamic LDS budget per workgroup
+constexpr int kMaxKernelBlock = 4096;    // largest B_d the step kernels cover
+
+uint64_t align_up(uint64_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+// k for a block of s elements: ceil(density * s), clamped to [1, s]; the
+// 1e-9 guard keeps products such as 0.01 * 100 from rounding up to 2.
+int64_t block_k(int64_t s, double density) {
+  int64_t k = (int64_t)std::ceil(density * (double)s - 1e-9);
+  if (k < 1) k = 1;
+  if (k > s) k = s;
+  return k;
+}
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int validate_config(const microadam_config* c) {
+  if (!c) return fail(MICROADAM_ERR_INVALID_ARG, "config is NULL");
+  if (!(c->density > 0.0 && c->density <= 1.0))
+    return fail(MICROADAM_ERR_INVALID_ARG, "density must be in (0, 1]");
+  if (!(c->beta1 >= 0.0 && c->beta1 < 1.0) || !(c->beta2 >= 0.0 && c->beta2 < 1.0))
+    return fail(MICROADAM_ERR_INVALID_ARG, "beta1 and beta2 must be in [0, 1)");
+  if (!(c->eps >= 0.0) || !std::isfinite(c->eps))
+    return fail(MICROADAM_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if (!std::isfinite(c->lr)) return fail(MICROADAM_ERR_INVALID_ARG, "lr must be finite");
+  if (!(c->weight_decay >= 0.0) || !std::isfinite(c->weight_decay))
+    return fail(MICROADAM_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
+  if (c->window < 1) return fail(MICROADAM_ERR_INVALID_ARG, "window must be >= 1");
+  if (c->window > microadam::kMaxWindow)
+    return fail(MICROADAM_ERR_UNSUPPORTED, "window above 64 is not supported");
+  if (c->ef_bits < 1 || c->ef_bits > 16) return fail(MICROADAM_ERR_INVALID_ARG, "ef_bits out of range");
+  if (c->ef_bits != 4) return fail(MICROADAM_ERR_UNSUPPORTED, "only ef_bits = 4 is implemented");
+  if (c->ef_bucket < 2) return fail(MICROADAM_ERR_INVALID_ARG, "ef_bucket must be >= 2");
+  if (!is_pow2(c->ef_bucket) || c->ef_bucket < 8 || c->ef_bucket > 512)
+    return fail(MICROADAM_ERR_UNSUPPORTED, "ef_bucket must be a power of two in [8, 512]");
+  if (c->topk_block < 1) return fail(MICROADAM_ERR_INVALID_ARG, "topk_block must be >= 1");
+  if (c->topk_block > microadam::kMaxBlock)
+    return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block above 65536 does not fit uint16 indices");
+  if (c->topk_block % c->ef_bucket != 0)
+    return fail(MICROADAM_ERR_INVALID_ARG, "topk_block must be a multiple of ef_bucket");
+  if (c->topk_block > kMaxKernelBlock)
+    return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block above 4096 is not implemented yet");
+  if (c->window_value_dtype != MICROADAM_BF16 && c->window_value_dtype != MICROADAM_F32)
+    return fail(MICROADAM_ERR_INVALID_ARG, "window_value_dtype must be BF16 or F32");
+  if (c->reserved != 0) return fail(MICROADAM_ERR_INVALID_ARG, "reserved must be 0");
+  return MICROADAM_OK;
+}
+
+struct TensorPlan {
+  int64_t numel, num_blocks, num_buckets, first_block;
+  int32_t k_full, k_last;
+  uint64_t ef_off, ef_bytes, stats_off, stats_bytes, win_off, win_bytes;
+};
+
+int entry_bytes(const microadam_config* c) { return c->window_value_dtype == MICROADAM_F32 ? 8 : 4; }
+
+int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
+              std::vector<TensorPlan>& out, uint64_t& total) {
+  if (n < 1) return fail(MICROADAM_ERR_INVALID_ARG, "n_tensors must be >= 1");
+  if (!numels) return fail(MICROADAM_ERR_INVALID_ARG, "numels is NULL");
+  out.clear();
+  out.reserve((size_t)n);
+  const int64_t B = c->topk_block, Bq = c->ef_bucket, m = c->window;
+  const int64_t eb = entry_bytes(c);
+  uint64_t off = 0;
+  int64_t blocks = 0;
+  for (int32_t j = 0; j < n; ++j) {
+    const int64_t d = numels[j];
+    if (d < 1) return fail(MICROADAM_ERR_INVALID_ARG, "every numel must be >= 1");
+    if (d > ((int64_t)1 << 50)) return fail(MICROADAM_ERR_INVALID_ARG, "numel too large");
+    TensorPlan p;
+    p.numel = d;
+    p.num_blocks = (d + B - 1) / B;
+    p.num_buckets = (d + Bq - 1) / Bq;
+    p.first_block = blocks;
+    p.k_full = (int32_t)block_k(B, c->density);
+    p.k_last = (int32_t)block_k(d - (p.num_blocks - 1) * B, c->density);
+    p.ef_off = off;
+    p.ef_bytes = (uint64_t)(d + 1) / 2;
+    off = align_up(off + p.ef_bytes);
+    p.stats_off = off;
+    p.stats_bytes = (uint64_t)p.num_buckets * 8;
+    off = align_up(off + p.stats_bytes);
+    p.win_off = off;
+    p.win_bytes = (uint64_t)m * eb * ((uint64_t)(p.num_blocks - 1) * p.k_full + p.k_last);
+    off = align_up(off + p.win_bytes);
+    blocks += p.num_blocks;
+    out.push_back(p);
+  }
+  total = off;
+  return MICROADAM_OK;
+}
+
+using microadam::threads_for_block;
+
+}  // namespace
+
+struct microadam_handle_s {
+  microadam_config cfg;
+  std::vector<TensorPlan> plans;
+  int32_t param_bf16 = 0, grad_bf16 = 0, value_f32 = 0;
+  int32_t bucket_log2 = 0;
+  uint8_t* state = nullptr;
+  uint64_t state_bytes = 0;
+  int64_t t = 0;
+  int64_t total_blocks = 0;
+  int device = 0;
+  TensorDesc* d_tensors = nullptr;    // device descriptor table
+  uint32_t* d_block_tensor = nullptr; // device: global block -> tensor
+  TensorDesc* h_tensors = nullptr;    // pinned host copy of the table
+  hipEvent_t upload_done = nullptr;   // last table upload finished reading h_tensors
+  hipEvent_t step_done = nullptr;     // last launch of this handle finished
+  bool uploaded = false;
+};
+
+namespace {
+
+void release(microadam_handle h) {
+  if (!h) return;
+  if (h->step_done) {
+    (void)hipEventSynchronize(h->step_done);
+    (void)hipEventDestroy(h->step_done);
+  }
+  if (h->upload_done) {
+    (void)hipEventSynchronize(h->upload_done);
+    (void)hipEventDestroy(h->upload_done);
+  }
+  if (h->d_tensors) (void)hipFree(h->d_tensors);
+  if (h->d_block_tensor) (void)hipFree(h->d_block_tensor);
+  if (h->h_tensors) (void)hipHostFree(h->h_tensors);
+  delete h;
+}
+
+// Per-step constants, derived in binary64 and rounded once to binary32:
+// beta^r for the window weights, (1 - beta)/(1 - beta^t) bias corrections
+// (AdamStats, Algorithm 2) and the decay factor 1 - eta*lambda (Algorithm 4).
+void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& p) {
+  const microadam_config& c = h->cfg;
+  const int m = c.window;
+  std::memset(&p, 0, sizeof(p));
+  p.tensors = h->d_tensors;
+  p.block_tensor = h->d_block_tensor;
+  p.state = h->state;
+  p.t = t;
+  p.block = c.topk_block;
+  p.bucket_log2 = h->bucket_log2;
+  p.window = m;
+  p.n_old = (int32_t)((t < m ? t : m) - 1);
+  p.new_slot = (int32_t)((t - 1) % m);
+  p.k_full = h->plans.empty() ? 0 : h->plans[0].k_full;
+  p.lr = (float)lr;
+  p.decay = (float)(1.0 - lr * c.weight_decay);
+  p.decay_is_one = (lr * c.weight_decay == 0.0) ? 1 : 0;
+  p.eps = (float)c.eps;
+  p.c1 = (float)((1.0 - c.beta1) / (1.0 - std::pow(c.beta1, (double)t)));
+  p.c2 = (float)((1.0 - c.beta2) / (1.0 - std::pow(c.beta2, (double)t)));
+  for (int r = 0; r < m; ++r) {
+    p.w1[r] = (float)std::pow(c.beta1, (double)r);
+    p.w2[r] = (float)std::pow(c.beta2, (double)r);
+  }
+  // Older rows are staged through LDS when they fit the per-thread budget.
+  const int64_t rows = (t > m) ? m : t - 1;
+  const int64_t words = rows * (int64_t)p.k_full * (h->value_f32 ? 2 : 1);
+  p.stage_slots = (words <= (int64_t)threads_for_block(c.topk_block) * microadam::kStageSlots)
+                      ? (int32_t)rows : 0;
+}
+
+int check_handle(microadam_handle h) {
+  if (!h) return fail(MICROADAM_ERR_INVALID_ARG, "handle is NULL");
+  return MICROADAM_OK;
+}
+
+int check_device(microadam_handle h) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != h->device)
+    return fail(MICROADAM_ERR_INVALID_ARG, "the current device differs from the one at init");
+  return MICROADAM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int microadam_state_bytes(const microadam_config* cfg, const int64_t* numels, int32_t n_tensors,
+                          uint64_t* out_bytes) {
+  if (!out_bytes) return fail(MICROADAM_ERR_INVALID_ARG, "out_bytes is NULL");
+  int rc = validate_config(cfg);
+  if (rc) return rc;
+  std::vector<TensorPlan> plans;
+  uint64_t total = 0;
+  rc = make_plan(cfg, numels, n_tensors, plans, total);
+  if (rc) return rc;
+  *out_bytes = total;
+  return MICROADAM_OK;
+}
+
+int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n_tensors,
+                   int32_t param_dtype, int32_t grad_dtype, void* state, uint64_t state_bytes,
+                   void* stream, microadam_handle* out) {
+  if (!out) return fail(MICROADAM_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  int rc = validate_config(cfg);
+  if (rc) return rc;
+  if ((param_dtype != MICROADAM_F32 && param_dtype != MICROADAM_BF16) ||
+      (grad_dtype != MICROADAM_F32 && grad_dtype != MICROADAM_BF16))
+    return fail(MICROADAM_ERR_INVALID_ARG, "param_dtype / grad_dtype must be F32 or BF16");
+  std::vector<TensorPlan> plans;
+  uint64_t total = 0;
+  rc = make_plan(cfg, numels, n_tensors, plans, total);
+  if (rc) return rc;
+  if (!state) return fail(MICROADAM_ERR_INVALID_ARG, "state is NULL");
+  if ((uintptr_t)state % kAlign) return fail(MICROADAM_ERR_INVALID_ARG, "state must be 256-byte aligned");
+  if (state_bytes < total)
+    return fail(MICROADAM_ERR_STATE_SIZE, "state buffer smaller than microadam_state_bytes");
+  const int64_t total_blocks = plans.back().first_block + plans.back().num_blocks;
+  const int nt = threads_for_block(cfg->topk_block);
+  if (total_blocks * (int64_t)nt >= ((int64_t)1 << 32) || total_blocks >= ((int64_t)1 << 31))
+    return fail(MICROADAM_ERR_UNSUPPORTED, "too many Top-K blocks for one launch");
+
+  microadam_handle h = new (std::nothrow) microadam_handle_s;
+  if (!h) return fail(MICROADAM_ERR_NO_MEMORY, "handle allocation failed");
+  h->cfg = *cfg;
+  h->plans = std::move(plans);
+  h->param_bf16 = param_dtype == MICROADAM_BF16;
+  h->grad_bf16 = grad_dtype == MICROADAM_BF16;
+  h->value_f32 = cfg->window_value_dtype == MICROADAM_F32;
+  while ((1 << h->bucket_log2) < cfg->ef_bucket) ++h->bucket_log2;
+  h->state = (uint8_t*)state;
+  h->state_bytes = state_bytes;
+  h->total_blocks = total_blocks;
+
+  {
+    StepParams probe;
+    fill_constants(h, cfg->window + 1, cfg->lr, probe);
+    probe.stage_slots = 0;
+    if (microadam::step_lds_bytes(probe, h->value_f32) > kMaxLds) {
+      release(h);
+      return fail(MICROADAM_ERR_UNSUPPORTED, "k per block too large for the LDS budget");
+    }
+  }
+
+  hipError_t e = hipGetDevice(&h->device);
+  if (e != hipSuccess) { release(h); return hip_fail(e, "hipGetDevice"); }
+  const size_t nd = h->plans.size();
+  if ((e = hipMalloc((void**)&h->d_tensors, nd * sizeof(TensorDesc))) != hipSuccess ||
+      (e = hipMalloc((void**)&h->d_block_tensor, (size_t)total_blocks * 4)) != hipSuccess ||
+      (e = hipHostMalloc((void**)&h->h_tensors, nd * sizeof(TensorDesc), hipHostMallocDefault)) != hipSuccess ||
+      (e = hipEventCreateWithFlags(&h->upload_done, hipEventDisableTiming)) != hipSuccess ||
+      (e = hipEventCreateWithFlags(&h->step_done, hipEventDisableTiming)) != hipSuccess) {
+    release(h);
+    return hip_fail(e, "allocating the descriptor tables");
+  }
+  std::vector<uint32_t> bt((size_t)total_blocks);
+  for (size_t j = 0; j < nd; ++j) {
+    const TensorPlan& p = h->plans[j];
+    for (int64_t b = 0; b < p.num_blocks; ++b) bt[(size_t)(p.first_block + b)] = (uint32_t)j;
+    TensorDesc& d = h->h_tensors[j];
+    std::memset(&d, 0, sizeof(d));
+    d.numel = p.numel;
+    d.first_block = p.first_block;
+    d.num_blocks = p.num_blocks;
+    d.ef_off = p.ef_off;
+    d.stats_off = p.stats_off;
+    d.win_off = p.win_off;
+    d.k_full = p.k_full;
+    d.k_last = p.k_last;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if ((e = hipMemcpy(h->d_block_tensor, bt.data(), bt.size() * 4, hipMemcpyHostToDevice)) != hipSuccess) {
+    release(h);
+    return hip_fail(e, "uploading the block table");
+  }
+  if ((e = hipMemsetAsync(state, 0, total, s)) != hipSuccess) {
+    release(h);
+    return hip_fail(e, "clearing the state buffer");
+  }
+  *out = h;
+  g_last_error.clear();
+  return MICROADAM_OK;
+}
+
+int microadam_step(microadam_handle h, void* const* params, const void* const* grads,
+                   int32_t n_tensors, double lr, void* stream) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (n_tensors != (int32_t)h->plans.size())
+    return fail(MICROADAM_ERR_SHAPE, "n_tensors differs from microadam_init");
+  if (!params || !grads) return fail(MICROADAM_ERR_INVALID_ARG, "params / grads is NULL");
+  for (int32_t j = 0; j < n_tensors; ++j) {
+    if (!params[j] || !grads[j]) return fail(MICROADAM_ERR_INVALID_ARG, "a param or grad pointer is NULL");
+    if ((uintptr_t)params[j] % 16 || (uintptr_t)grads[j] % 16)
+      return fail(MICROADAM_ERR_INVALID_ARG, "param and grad pointers must be 16-byte aligned");
+  }
+  if (std::isnan(lr)) lr = h->cfg.lr;
+  if (!std::isfinite(lr)) return fail(MICROADAM_ERR_INVALID_ARG, "lr must be finite");
+  rc = check_device(h);
+  if (rc) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e;
+
+  // Upload the descriptor table when the tensor addresses changed.
+  bool changed = !h->uploaded;
+  for (int32_t j = 0; j < n_tensors && !changed; ++j)
+    changed = h->h_tensors[j].param != params[j] || h->h_tensors[j].grad != grads[j];
+  if (changed) {
+    if ((e = hipEventSynchronize(h->upload_done)) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    for (int32_t j = 0; j < n_tensors; ++j) {
+      h->h_tensors[j].param = params[j];
+      h->h_tensors[j].grad = grads[j];
+    }
+    if ((e = hipMemcpyAsync(h->d_tensors, h->h_tensors, h->plans.size() * sizeof(TensorDesc),
+                            hipMemcpyHostToDevice, s)) != hipSuccess)
+      return hip_fail(e, "uploading the tensor table");
+    if ((e = hipEventRecord(h->upload_done, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    h->uploaded = true;
+  }
+
+  const int64_t t = h->t + 1;
+  StepParams p;
+  fill_constants(h, t, lr, p);
+  e = microadam::launch_step(p, h->total_blocks, h->param_bf16, h->grad_bf16, h->value_f32, s);
+  if (e != hipSuccess) return hip_fail(e, "launching the step kernel");
+  if ((e = hipEventRecord(h->step_done, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  h->t = t;
+  return MICROADAM_OK;
+}
+
+int microadam_destroy(microadam_handle h) {
+  release(h);
+  return MICROADAM_OK;
+}
+
+int64_t microadam_get_step(microadam_handle h) {
+  if (!h) return fail(MICROADAM_ERR_INVALID_ARG, "handle is NULL");
+  return h->t;
+}
+
+int microadam_set_step(microadam_handle h, int64_t t) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (t < 0) return fail(MICROADAM_ERR_INVALID_ARG, "t must be >= 0");
+  h->t = t;
+  return MICROADAM_OK;
+}
+
+int microadam_tensor_layout(microadam_handle h, int32_t tensor, microadam_layout* out) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!out) return fail(MICROADAM_ERR_INVALID_ARG, "out is NULL");
+  if (tensor < 0 || tensor >= (int32_t)h->plans.size())
+    return fail(MICROADAM_ERR_INVALID_ARG, "tensor index out of range");
+  const TensorPlan& p = h->plans[(size_t)tensor];
+  std::memset(out, 0, sizeof(*out));
+  out->numel = p.numel;
+  out->num_blocks = p.num_blocks;
+  out->num_buckets = p.num_buckets;
+  out->k_full = p.k_full;
+  out->k_last = p.k_last;
+  out->entry_bytes = entry_bytes(&h->cfg);
+  out->ef_offset = p.ef_off;
+  out->ef_bytes = p.ef_bytes;
+  out->stats_offset = p.stats_off;
+  out->stats_bytes = p.stats_bytes;
+  out->window_offset = p.win_off;
+  out->window_bytes = p.win_bytes;
+  return MICROADAM_OK;
+}
+
+int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat, float* vhat,
+                            void* stream) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (tensor < 0 || tensor >= (int32_t)h->plans.size())
+    return fail(MICROADAM_ERR_INVALID_ARG, "tensor index out of range");
+  if (!mhat || !vhat) return fail(MICROADAM_ERR_INVALID_ARG, "mhat / vhat is NULL");
+  if (h->t < 1) return fail(MICROADAM_ERR_INVALID_ARG, "no step has been taken");
+  if (!h->uploaded) return fail(MICROADAM_ERR_INVALID_ARG, "no step has been taken");
+  rc = check_device(h);
+  if (rc) return rc;
+  StepParams p;
+  fill_constants(h, h->t, h->cfg.lr, p);
+  const TensorPlan& tp = h->plans[(size_t)tensor];
+  hipError_t e = microadam::launch_moments(p, tensor, tp.first_block, tp.num_blocks, mhat, vhat,
+                                           h->value_f32, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "launching the moment kernel");
+  return MICROADAM_OK;
+}
+
+const char* microadam_error_string(int code) {
+  switch (code) {
+    case MICROADAM_OK: return "ok";
+    case MICROADAM_ERR_INVALID_ARG: return "invalid argument";
+    case MICROADAM_ERR_UNSUPPORTED: return "unsupported configuration";
+    case MICROADAM_ERR_SHAPE: return "tensor list differs from init";
+    case MICROADAM_ERR_STATE_SIZE: return "state buffer too small";
+    case MICROADAM_ERR_HIP: return "HIP runtime error";
+    case MICROADAM_ERR_NO_MEMORY: return "out of memory";
+    default: return "unknown error code";
+  }
+}
+
+const char* microadam_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,134 @@
+"""Host-side checks of libmicroadam that need no GPU: the library loads and
+exports every symbol its header declares, the state-size planner matches the
+paper's byte model, and invalid configurations are rejected before any
+device work."""
+import math
+import os
+import re
+
+import pytest
+
+import paper_2405_15593_amd as ma
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "microadam.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ma.LIBRARY):
+        from paper_2405_15593_amd import _build
+        _build.build()
+    return ma.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    decl = re.findall(r"^\S[^;(]*?\b(microadam_\w+)\s*\(", open(HEADER).read(), re.M)
+    assert set(decl) == set(ma.EXPORTS), sorted(set(decl) ^ set(ma.EXPORTS))
+    for name in decl:
+        assert hasattr(lib, name), name
+
+
+def llama7b_numels():
+    from paper_2405_15593_amd.workloads import WORKLOADS
+    return WORKLOADS["llama2_7b_bf16"].numels
+
+
+def test_state_bytes_llama2_7b(lib):
+    """0.5 B/param of EF (Section 3.2), 8 B per bucket of 64 for (delta, Delta),
+    and m rows of 41 entries per 4096-block at 4 B each; no tails here."""
+    numels = llama7b_numels()
+    d = sum(numels)
+    assert d == 6_738_415_616
+    cfg = ma.make_config()
+    got = ma.microadam_state_bytes(cfg, numels)
+    blocks = d // 4096
+    assert all(n % 4096 == 0 for n in numels)
+    want_payload = d // 2 + 8 * (d // 64) + 10 * 41 * 4 * blocks
+    # each of the 3 regions of each tensor is padded to 256 bytes
+    assert want_payload <= got <= want_payload + 3 * 256 * len(numels)
+    # the paper's 0.5d + 4mk with a global k = ceil(d/100) (Section 3.2)
+    paper = 0.5 * d + 4 * 10 * math.ceil(d / 100)
+    ours_without_stats = d // 2 + 10 * 41 * 4 * blocks
+    assert abs(ours_without_stats / paper - 1) < 2e-3   # 41/4096 vs 1/100
+    assert round(got / 2 ** 30, 3) == 6.435
+
+
+def test_state_bytes_tails_and_f32(lib):
+    cfg = ma.make_config(density=0.01, window=3, ef_bucket=16, topk_block=256,
+                         window_value_dtype=ma.MICROADAM_F32)
+    n = 1001            # 3 full blocks of 256 (k 3) and a tail of 233 (k 3)
+    got = ma.microadam_state_bytes(cfg, [n])
+    ef = 501
+    stats = 8 * 63
+    win = 3 * 8 * (3 * 3 + 3)
+    pad = lambda x: -(-x // 256) * 256
+    assert got == pad(ef) + pad(stats) + pad(win)
+
+
+BAD = [
+    (dict(density=0.0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(density=1.5), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(density=math.nan), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(beta1=1.0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(beta2=-0.1), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(eps=-1.0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(lr=math.inf), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(weight_decay=-1.0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(window=0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(window=65), ma.MICROADAM_ERR_UNSUPPORTED),
+    (dict(ef_bits=8), ma.MICROADAM_ERR_UNSUPPORTED),
+    (dict(ef_bits=0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(ef_bucket=48), ma.MICROADAM_ERR_UNSUPPORTED),
+    (dict(ef_bucket=1), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(topk_block=4000, ef_bucket=64), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(topk_block=131072), ma.MICROADAM_ERR_UNSUPPORTED),
+    (dict(topk_block=0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(window_value_dtype=7), ma.MICROADAM_ERR_INVALID_ARG),
+]
+
+
+@pytest.mark.parametrize("kw,code", BAD, ids=[str(b[0]) for b in BAD])
+def test_invalid_config_rejected(lib, kw, code):
+    cfg = ma.make_config(**kw)
+    with pytest.raises(ma.MicroAdamError) as e:
+        ma.microadam_state_bytes(cfg, [4096])
+    assert e.value.code == code
+    # init validates the same way before touching the device
+    with pytest.raises(ma.MicroAdamError) as e:
+        ma.microadam_init(cfg, [4096], ma.MICROADAM_BF16, ma.MICROADAM_BF16, 256, 1 << 20)
+    assert e.value.code == code
+
+
+def test_invalid_tensor_lists(lib):
+    cfg = ma.make_config()
+    for numels in ([], [0], [10, -3]):
+        with pytest.raises(ma.MicroAdamError) as e:
+            ma.microadam_state_bytes(cfg, numels)
+        assert e.value.code == ma.MICROADAM_ERR_INVALID_ARG
+
+
+def test_init_argument_checks_before_device_work(lib):
+    cfg = ma.make_config()
+    need = ma.microadam_state_bytes(cfg, [4096])
+    cases = [
+        ((cfg, [4096], 5, ma.MICROADAM_BF16, 256, need), ma.MICROADAM_ERR_INVALID_ARG),
+        ((cfg, [4096], ma.MICROADAM_BF16, ma.MICROADAM_BF16, 0, need), ma.MICROADAM_ERR_INVALID_ARG),
+        ((cfg, [4096], ma.MICROADAM_BF16, ma.MICROADAM_BF16, 258, need), ma.MICROADAM_ERR_INVALID_ARG),
+        ((cfg, [4096], ma.MICROADAM_BF16, ma.MICROADAM_BF16, 256, need - 1), ma.MICROADAM_ERR_STATE_SIZE),
+    ]
+    for args, code in cases:
+        with pytest.raises(ma.MicroAdamError) as e:
+            ma.microadam_init(*args)
+        assert e.value.code == code, (args, e.value)
+
+
+def test_null_handle_calls(lib):
+    for f, args in [(ma.microadam_get_step, (0,)), (ma.microadam_set_step, (0, 1)),
+                    (ma.microadam_tensor_layout, (0, 0)), (ma.microadam_debug_moments, (0, 0, 1, 1)),
+                    (ma.microadam_step, (0, [1], [1]))]:
+        with pytest.raises(ma.MicroAdamError) as e:
+            f(*args)
+        assert e.value.code == ma.MICROADAM_ERR_INVALID_ARG
+    ma.microadam_destroy(0)   # NULL is accepted
+    assert ma.microadam_error_string(ma.MICROADAM_ERR_SHAPE) == "tensor list differs from init"

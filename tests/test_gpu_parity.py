@@ -1,0 +1,83 @@
+"""GPU parity: libmicroadam (HIP, gfx950) against the CPU oracle, step by step.
+
+Every case runs several steps past the window length, so the circular window
+wraps, and mixes full Top-K blocks with ragged tail blocks, odd element
+counts and partial buckets.  State (EF codes, bucket min/max, window rows) is
+compared bit for bit, parameters and moments within tolerance (see
+gpu_harness)."""
+import pytest
+import torch
+
+from gpu_harness import GpuOracleRun
+
+pytestmark = pytest.mark.gpu
+
+bf16, f32 = torch.bfloat16, torch.float32
+
+CASES = {
+    # several full 4096-blocks, a 768-element tail, odd numel, tiny tensors
+    "bf16_tails": (dict(numels=[4096 * 3 + 768, 1001, 64, 5, 8192], param_dtype=bf16,
+                        grad_dtype=bf16, grad_scale=1e-3, density=0.01, window=4), 7),
+    "f32_student_t": (dict(numels=[20000, 333, 4096], grad_dist="student_t4", density=0.01,
+                           window=3), 6),
+    "f32_window_values": (dict(numels=[12288, 4100], value_f32=True, density=0.02, window=3), 5),
+    "block256_64threads": (dict(numels=[3000, 1024, 77], block=256, bucket=16, density=0.05,
+                                window=3), 6),
+    "block1024_bucket8": (dict(numels=[5000, 1024], block=1024, bucket=8, density=0.01,
+                               window=5), 7),
+    "bucket512": (dict(numels=[9000], block=4096, bucket=512, density=0.01, window=3,
+                       param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3), 4),
+    "bucket32": (dict(numels=[9000], block=2048, bucket=32, density=0.01, window=3), 4),
+    "density_one": (dict(numels=[500, 64, 7], block=64, bucket=8, density=1.0, window=2,
+                         value_f32=True), 4),
+    "large_k_general_path": (dict(numels=[4096 * 2 + 1000], density=0.1, window=2), 4),
+    "forced_ties": (dict(numels=[4096 * 3 + 200], grad_dist="student_t2_snapped64",
+                         grad_scale=1e-3, param_dtype=bf16, grad_dtype=bf16, density=0.05,
+                         window=3), 5),
+    "weight_decay": (dict(numels=[10000, 300], weight_decay=0.1, lr=1e-2, window=2), 4),
+    "window_one": (dict(numels=[8192, 50], window=1, param_dtype=bf16, grad_dtype=bf16,
+                        grad_scale=1e-3), 4),
+    "window_max_64": (dict(numels=[4096, 900], window=64, block=512, bucket=64, density=0.01), 66),
+    "mixed_dtypes_bf16_param_f32_grad": (dict(numels=[6000], param_dtype=bf16, grad_dtype=f32,
+                                              window=3), 4),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_parity(name):
+    kw, steps = CASES[name]
+    kw = dict(kw)
+    numels = kw.pop("numels")
+    print(f"[parity] {name} numels={numels} {kw} steps={steps}", flush=True)
+    run = GpuOracleRun(numels, **kw)
+    for _ in range(steps):
+        run.step(check_moments=run.t % 2 == 0 or steps < 8)
+    run.opt.close()
+
+
+def test_flat_1m_f32_twenty_steps():
+    """One flat tensor of 2^20 float32 elements, N(0,1) grads, block 4096,
+    k = 41, m = 10, bucket 64, lr 1e-4, 20 steps: every block checked."""
+    print("[parity] flat 1M f32, 20 steps", flush=True)
+    run = GpuOracleRun([1 << 20], lr=1e-4, density=0.01, window=10, bucket=64, block=4096)
+    for t in range(20):
+        run.step(check_moments=t in (0, 9, 19))
+    run.opt.close()
+
+
+def test_bert_base_bf16_sampled():
+    """The BERT-base parameter list (196 tensors, 108.9M bf16 parameters),
+    10 steps; the oracle checks every tensor's first and last block and every
+    97th block in between."""
+    from paper_2405_15593_amd.workloads import WORKLOADS
+    w = WORKLOADS["bert_base_bf16"]
+    print(f"[parity] bert-base sampled, {len(w.numels)} tensors", flush=True)
+
+    def sample(j, nb):
+        return sorted({0, nb - 1, *range(0, nb, 97)})
+
+    run = GpuOracleRun(w.numels, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3, lr=1e-4,
+                       density=0.01, window=10, bucket=64, block=4096, sample=sample)
+    for t in range(10):
+        run.step(check_moments=t in (0, 9))
+    run.opt.close()
