@@ -127,6 +127,18 @@ using microadam::threads_for_block;
 
 }  // namespace
 
+// A device copy of the tensor table for one set of param/grad addresses.
+// Callers that alternate between a few gradient buffers reuse their tables
+// instead of uploading one per step.
+struct TableSlot {
+  TensorDesc* d = nullptr;          // device table
+  TensorDesc* h = nullptr;          // pinned host staging of the same table
+  hipEvent_t upload_done = nullptr; // the last upload from `h` has finished
+  uint64_t last_use = 0;            // 0: never filled
+};
+
+constexpr int kTableSlots = 4;
+
 struct microadam_handle_s {
   microadam_config cfg;
   std::vector<TensorPlan> plans;
@@ -137,12 +149,11 @@ struct microadam_handle_s {
   int64_t t = 0;
   int64_t total_blocks = 0;
   int device = 0;
-  TensorDesc* d_tensors = nullptr;    // device descriptor table
   uint32_t* d_block_tensor = nullptr; // device: global block -> tensor
-  TensorDesc* h_tensors = nullptr;    // pinned host copy of the table
-  hipEvent_t upload_done = nullptr;   // last table upload finished reading h_tensors
+  TableSlot slots[kTableSlots];
+  uint64_t use_clock = 0;
+  int current = -1;                   // slot used by the last step
   hipEvent_t step_done = nullptr;     // last launch of this handle finished
-  bool uploaded = false;
 };
 
 namespace {
@@ -153,13 +164,15 @@ void release(microadam_handle h) {
     (void)hipEventSynchronize(h->step_done);
     (void)hipEventDestroy(h->step_done);
   }
-  if (h->upload_done) {
-    (void)hipEventSynchronize(h->upload_done);
-    (void)hipEventDestroy(h->upload_done);
+  for (TableSlot& t : h->slots) {
+    if (t.upload_done) {
+      (void)hipEventSynchronize(t.upload_done);
+      (void)hipEventDestroy(t.upload_done);
+    }
+    if (t.d) (void)hipFree(t.d);
+    if (t.h) (void)hipHostFree(t.h);
   }
-  if (h->d_tensors) (void)hipFree(h->d_tensors);
   if (h->d_block_tensor) (void)hipFree(h->d_block_tensor);
-  if (h->h_tensors) (void)hipHostFree(h->h_tensors);
   delete h;
 }
 
@@ -170,7 +183,7 @@ void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& 
   const microadam_config& c = h->cfg;
   const int m = c.window;
   std::memset(&p, 0, sizeof(p));
-  p.tensors = h->d_tensors;
+  p.tensors = h->current >= 0 ? h->slots[h->current].d : nullptr;
   p.block_tensor = h->d_block_tensor;
   p.state = h->state;
   p.t = t;
@@ -276,19 +289,24 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   hipError_t e = hipGetDevice(&h->device);
   if (e != hipSuccess) { release(h); return hip_fail(e, "hipGetDevice"); }
   const size_t nd = h->plans.size();
-  if ((e = hipMalloc((void**)&h->d_tensors, nd * sizeof(TensorDesc))) != hipSuccess ||
-      (e = hipMalloc((void**)&h->d_block_tensor, (size_t)total_blocks * 4)) != hipSuccess ||
-      (e = hipHostMalloc((void**)&h->h_tensors, nd * sizeof(TensorDesc), hipHostMallocDefault)) != hipSuccess ||
-      (e = hipEventCreateWithFlags(&h->upload_done, hipEventDisableTiming)) != hipSuccess ||
+  if ((e = hipMalloc((void**)&h->d_block_tensor, (size_t)total_blocks * 4)) != hipSuccess ||
       (e = hipEventCreateWithFlags(&h->step_done, hipEventDisableTiming)) != hipSuccess) {
     release(h);
-    return hip_fail(e, "allocating the descriptor tables");
+    return hip_fail(e, "allocating the block table");
+  }
+  for (TableSlot& t : h->slots) {
+    if ((e = hipMalloc((void**)&t.d, nd * sizeof(TensorDesc))) != hipSuccess ||
+        (e = hipHostMalloc((void**)&t.h, nd * sizeof(TensorDesc), hipHostMallocDefault)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&t.upload_done, hipEventDisableTiming)) != hipSuccess) {
+      release(h);
+      return hip_fail(e, "allocating the descriptor tables");
+    }
   }
   std::vector<uint32_t> bt((size_t)total_blocks);
   for (size_t j = 0; j < nd; ++j) {
     const TensorPlan& p = h->plans[j];
     for (int64_t b = 0; b < p.num_blocks; ++b) bt[(size_t)(p.first_block + b)] = (uint32_t)j;
-    TensorDesc& d = h->h_tensors[j];
+    TensorDesc d;
     std::memset(&d, 0, sizeof(d));
     d.numel = p.numel;
     d.first_block = p.first_block;
@@ -298,6 +316,7 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
     d.win_off = p.win_off;
     d.k_full = p.k_full;
     d.k_last = p.k_last;
+    for (TableSlot& t : h->slots) t.h[j] = d;
   }
   hipStream_t s = (hipStream_t)stream;
   if ((e = hipMemcpy(h->d_block_tensor, bt.data(), bt.size() * 4, hipMemcpyHostToDevice)) != hipSuccess) {
@@ -332,22 +351,36 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
   hipStream_t s = (hipStream_t)stream;
   hipError_t e;
 
-  // Upload the descriptor table when the tensor addresses changed.
-  bool changed = !h->uploaded;
-  for (int32_t j = 0; j < n_tensors && !changed; ++j)
-    changed = h->h_tensors[j].param != params[j] || h->h_tensors[j].grad != grads[j];
-  if (changed) {
-    if ((e = hipEventSynchronize(h->upload_done)) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
-    for (int32_t j = 0; j < n_tensors; ++j) {
-      h->h_tensors[j].param = params[j];
-      h->h_tensors[j].grad = grads[j];
-    }
-    if ((e = hipMemcpyAsync(h->d_tensors, h->h_tensors, h->plans.size() * sizeof(TensorDesc),
-                            hipMemcpyHostToDevice, s)) != hipSuccess)
-      return hip_fail(e, "uploading the tensor table");
-    if ((e = hipEventRecord(h->upload_done, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    h->uploaded = true;
+  // Find a device table holding exactly these addresses, else refill the
+  // least recently used one (its staging buffer is rewritten only after its
+  // previous upload has been read; the upload is ordered on `s` after every
+  // earlier launch on `s`).
+  int slot = -1;
+  for (int i = 0; i < kTableSlots && slot < 0; ++i) {
+    const TableSlot& t = h->slots[i];
+    if (!t.last_use) continue;
+    bool same = true;
+    for (int32_t j = 0; j < n_tensors && same; ++j)
+      same = t.h[j].param == params[j] && t.h[j].grad == grads[j];
+    if (same) slot = i;
   }
+  if (slot < 0) {
+    slot = 0;
+    for (int i = 1; i < kTableSlots; ++i)
+      if (h->slots[i].last_use < h->slots[slot].last_use) slot = i;
+    TableSlot& t = h->slots[slot];
+    if ((e = hipEventSynchronize(t.upload_done)) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    for (int32_t j = 0; j < n_tensors; ++j) {
+      t.h[j].param = params[j];
+      t.h[j].grad = grads[j];
+    }
+    if ((e = hipMemcpyAsync(t.d, t.h, h->plans.size() * sizeof(TensorDesc), hipMemcpyHostToDevice,
+                            s)) != hipSuccess)
+      return hip_fail(e, "uploading the tensor table");
+    if ((e = hipEventRecord(t.upload_done, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
+  h->slots[slot].last_use = ++h->use_clock;
+  h->current = slot;
 
   const int64_t t = h->t + 1;
   StepParams p;
@@ -407,8 +440,7 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat, flo
   if (tensor < 0 || tensor >= (int32_t)h->plans.size())
     return fail(MICROADAM_ERR_INVALID_ARG, "tensor index out of range");
   if (!mhat || !vhat) return fail(MICROADAM_ERR_INVALID_ARG, "mhat / vhat is NULL");
-  if (h->t < 1) return fail(MICROADAM_ERR_INVALID_ARG, "no step has been taken");
-  if (!h->uploaded) return fail(MICROADAM_ERR_INVALID_ARG, "no step has been taken");
+  if (h->t < 1 || h->current < 0) return fail(MICROADAM_ERR_INVALID_ARG, "no step has been taken");
   rc = check_device(h);
   if (rc) return rc;
   StepParams p;
