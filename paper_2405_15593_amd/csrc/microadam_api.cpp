@@ -150,6 +150,7 @@ struct microadam_handle_s {
   int64_t total_blocks = 0;
   int device = 0;
   uint32_t* d_block_tensor = nullptr; // device: global block -> tensor
+  float* d_wpow = nullptr;            // device: beta1^r, beta2^r for r < 64
   TableSlot slots[kTableSlots];
   uint64_t use_clock = 0;
   int current = -1;                   // slot used by the last step
@@ -173,20 +174,25 @@ void release(microadam_handle h) {
     if (t.h) (void)hipHostFree(t.h);
   }
   if (h->d_block_tensor) (void)hipFree(h->d_block_tensor);
+  if (h->d_wpow) (void)hipFree(h->d_wpow);
   delete h;
 }
 
-// Per-step constants, derived in binary64 and rounded once to binary32:
-// beta^r for the window weights, (1 - beta)/(1 - beta^t) bias corrections
-// (AdamStats, Algorithm 2) and the decay factor 1 - eta*lambda (Algorithm 4).
+// Per-step constants, derived in binary64 and rounded once to binary32: the
+// bias corrections (1 - beta)/(1 - beta^t) of AdamStats (Algorithm 2) and the
+// decay factor 1 - eta*lambda (Algorithm 4).  The window weights beta^r live
+// in a device table filled at init.
 void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& p) {
   const microadam_config& c = h->cfg;
   const int m = c.window;
   std::memset(&p, 0, sizeof(p));
   p.tensors = h->current >= 0 ? h->slots[h->current].d : nullptr;
   p.block_tensor = h->d_block_tensor;
+  p.wpow = h->d_wpow;
   p.state = h->state;
   p.t = t;
+  p.total_blocks = h->total_blocks;
+  p.n_tensors = (int32_t)h->plans.size();
   p.block = c.topk_block;
   p.bucket_log2 = h->bucket_log2;
   p.window = m;
@@ -199,15 +205,6 @@ void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& 
   p.eps = (float)c.eps;
   p.c1 = (float)((1.0 - c.beta1) / (1.0 - std::pow(c.beta1, (double)t)));
   p.c2 = (float)((1.0 - c.beta2) / (1.0 - std::pow(c.beta2, (double)t)));
-  for (int r = 0; r < m; ++r) {
-    p.w1[r] = (float)std::pow(c.beta1, (double)r);
-    p.w2[r] = (float)std::pow(c.beta2, (double)r);
-  }
-  // Older rows are staged through LDS when they fit the per-thread budget.
-  const int64_t rows = (t > m) ? m : t - 1;
-  const int64_t words = rows * (int64_t)p.k_full * (h->value_f32 ? 2 : 1);
-  p.stage_slots = (words <= (int64_t)threads_for_block(c.topk_block) * microadam::kStageSlots)
-                      ? (int32_t)rows : 0;
 }
 
 int check_handle(microadam_handle h) {
@@ -276,23 +273,31 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   h->state_bytes = state_bytes;
   h->total_blocks = total_blocks;
 
-  {
-    StepParams probe;
-    fill_constants(h, cfg->window + 1, cfg->lr, probe);
-    probe.stage_slots = 0;
-    if (microadam::step_lds_bytes(probe, h->value_f32) > kMaxLds) {
-      release(h);
-      return fail(MICROADAM_ERR_UNSUPPORTED, "k per block too large for the LDS budget");
-    }
+  if (microadam::step_lds_bytes(cfg->topk_block, h->plans[0].k_full, h->value_f32) > kMaxLds) {
+    release(h);
+    return fail(MICROADAM_ERR_UNSUPPORTED, "k per block too large for the LDS budget");
   }
 
   hipError_t e = hipGetDevice(&h->device);
   if (e != hipSuccess) { release(h); return hip_fail(e, "hipGetDevice"); }
   const size_t nd = h->plans.size();
   if ((e = hipMalloc((void**)&h->d_block_tensor, (size_t)total_blocks * 4)) != hipSuccess ||
+      (e = hipMalloc((void**)&h->d_wpow, 2 * microadam::kMaxWindow * sizeof(float))) != hipSuccess ||
       (e = hipEventCreateWithFlags(&h->step_done, hipEventDisableTiming)) != hipSuccess) {
     release(h);
     return hip_fail(e, "allocating the block table");
+  }
+  {
+    // beta1^r and beta2^r, r < m, from binary64 rounded once (Algorithm 2)
+    float w[2 * microadam::kMaxWindow] = {};
+    for (int r = 0; r < cfg->window; ++r) {
+      w[r] = (float)std::pow(cfg->beta1, (double)r);
+      w[microadam::kMaxWindow + r] = (float)std::pow(cfg->beta2, (double)r);
+    }
+    if ((e = hipMemcpy(h->d_wpow, w, sizeof(w), hipMemcpyHostToDevice)) != hipSuccess) {
+      release(h);
+      return hip_fail(e, "uploading the window weights");
+    }
   }
   for (TableSlot& t : h->slots) {
     if ((e = hipMalloc((void**)&t.d, nd * sizeof(TensorDesc))) != hipSuccess ||
@@ -385,7 +390,7 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
   const int64_t t = h->t + 1;
   StepParams p;
   fill_constants(h, t, lr, p);
-  e = microadam::launch_step(p, h->total_blocks, h->param_bf16, h->grad_bf16, h->value_f32, s);
+  e = microadam::launch_step(p, h->param_bf16, h->grad_bf16, h->value_f32, s);
   if (e != hipSuccess) return hip_fail(e, "launching the step kernel");
   if ((e = hipEventRecord(h->step_done, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   h->t = t;

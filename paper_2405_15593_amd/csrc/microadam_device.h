@@ -9,8 +9,6 @@ namespace microadam {
 
 constexpr int kMaxWindow = 64;       // largest supported window m
 constexpr int kMaxBlock = 65536;     // uint16 block-relative indices
-constexpr int kCandCap = 256;        // Top-K candidates resolved by one wave
-constexpr int kStageSlots = 4;       // window words staged per thread
 
 // One parameter tensor as the step kernel sees it.
 struct TensorDesc {
@@ -34,31 +32,31 @@ inline int threads_for_block(int block) { return block <= 1024 ? 64 : 256; }
 struct StepParams {
   const TensorDesc* tensors;
   const uint32_t* block_tensor;  // global block -> tensor index
+  const float* wpow;             // [2 * kMaxWindow]: beta1^r, then beta2^r
   uint8_t* state;
   int64_t t;                     // step being taken (>= 1)
+  int64_t total_blocks;
+  int32_t n_tensors;
   int32_t block;                 // B_d
   int32_t bucket_log2;           // B_q = 1 << bucket_log2
   int32_t window;                // m
   int32_t n_old;                 // live rows written before step t: min(t, m) - 1
   int32_t new_slot;              // row slot written at step t: (t - 1) mod m
-  int32_t stage_slots;           // row slots staged in LDS (0: read old rows from HBM)
   int32_t k_full;                // entries per row of a full block (all tensors)
   int32_t decay_is_one;          // weight_decay * lr == 0
   float lr, decay, eps, c1, c2;
-  float w1[kMaxWindow];          // beta1^r, r = t - s
-  float w2[kMaxWindow];          // beta2^r
 };
 
 // Launchers (defined in microadam_kernels.hip).  Return hipSuccess or the
-// launch error.  `grid` = number of Top-K blocks to process.
-hipError_t launch_step(const StepParams& p, int64_t grid, int param_bf16,
-                       int grad_bf16, int value_f32, hipStream_t stream);
+// launch error.
+hipError_t launch_step(const StepParams& p, int param_bf16, int grad_bf16, int value_f32,
+                       hipStream_t stream);
 
 hipError_t launch_moments(const StepParams& p, int32_t tensor, int64_t first_block,
                           int64_t grid, float* mhat, float* vhat, int value_f32,
                           hipStream_t stream);
 
 // Dynamic LDS bytes the step kernel needs for this configuration.
-size_t step_lds_bytes(const StepParams& p, int value_f32);
+size_t step_lds_bytes(int block, int k_full, int value_f32);
 
 }  // namespace microadam
