@@ -69,7 +69,9 @@ enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
  *   ef_bucket    B_q, elements sharing one (delta, Delta) pair; a power of
  *                two in [8, 512] dividing topk_block.
  *   topk_block   B_d, Top-K block size; a multiple of ef_bucket, at most
- *                65536 (block-relative indices are uint16).
+ *                65536 (block-relative indices are uint16).  This build
+ *                implements multiples of 16 up to 4096 and returns
+ *                MICROADAM_ERR_UNSUPPORTED for other valid sizes.
  *   window_value_dtype  MICROADAM_BF16 (the paper's choice, Section 3.2) or
  *                MICROADAM_F32 (lossless window values, for checking the
  *                moment rebuild).
@@ -93,21 +95,26 @@ typedef struct microadam_handle_s* microadam_handle;
 
 /*
  * Where one tensor's optimizer state lives inside the state buffer (byte
- * offsets from its start; every region is 256-byte aligned).
+ * offsets from its start).  The buffer holds three planes, EF codes, bucket
+ * stats and window, each starting 256-byte aligned; in each plane every
+ * Top-K block of every tensor owns a record of fixed size, in the order of
+ * the global block number (tensor 0's blocks first).  A tensor's records are
+ * therefore contiguous, and the last block's record is padded to full size.
  *
- *   EF codes   ef_offset, ceil(numel/2) bytes: element 2j in the low nibble
- *              of byte j, element 2j+1 in the high nibble (an odd numel
- *              leaves the last high nibble 0).
- *   stats      stats_offset, num_buckets pairs of float32 (delta, Delta) =
- *              (min, max) of the bucket's residual; bucket b covers elements
- *              [b*B_q, min(numel, (b+1)*B_q)).
- *   window     window_offset, block-major: block q's m rows start at
- *              window_offset + q*m*k_full*entry_bytes; within it, row r
- *              (the row written at step s is r = (s-1) mod m) starts at
- *              r*k_q*entry_bytes and holds k_q entries in ascending index
- *              order.  With bf16 values an entry is one little-endian uint32
- *              (index | bf16_bits << 16); with float32 values it is a uint32
- *              index followed by the float32 value.
+ *   EF codes   ef_offset, B_d/2 bytes per block: element 2j of the tensor in
+ *              the low nibble of byte j, element 2j+1 in the high nibble
+ *              (nibbles past numel are 0).
+ *   stats      stats_offset, B_d/B_q pairs of float32 (delta, Delta) per
+ *              block = (min, max) of the bucket's residual; bucket b covers
+ *              elements [b*B_q, min(numel, (b+1)*B_q)); pairs past
+ *              num_buckets are unused.
+ *   window     window_offset, m*k_full*entry_bytes per block: block q's rows
+ *              start at window_offset + q*m*k_full*entry_bytes; row r (the
+ *              row written at step s is r = (s-1) mod m) starts at
+ *              r*k_q*entry_bytes within it and holds the block's k_q entries
+ *              in ascending index order.  With bf16 values an entry is one
+ *              little-endian uint32 (index | bf16_bits << 16); with float32
+ *              values it is a uint32 index followed by the float32 value.
  */
 typedef struct microadam_layout {
   int64_t numel;
@@ -124,11 +131,12 @@ typedef struct microadam_layout {
 
 /*
  * Size in bytes of the device state buffer for tensors of the given element
- * counts (numels[0..n_tensors), each >= 1).  Pure host computation: EF codes
- * (ceil(n/2) B), bucket stats (8 B per bucket) and the window (m * sum of k
- * per block entries of entry_bytes), each region 256-byte aligned.  This is
- * the paper's 0.5d + 4mk (Section 3.2) plus the (delta, Delta) metadata of
- * Section 3.1 and per-block rounding of k.
+ * counts (numels[0..n_tensors), each >= 1).  Pure host computation: per
+ * Top-K block B_d/2 bytes of EF codes, 8*B_d/B_q bytes of bucket stats and
+ * m*k_full*entry_bytes of window, each plane 256-byte aligned.  This is the
+ * paper's 0.5d + 4mk (Section 3.2) plus the (delta, Delta) metadata of
+ * Section 3.1, per-block rounding of k and the padding of each tensor's last
+ * block.
  */
 int microadam_state_bytes(const microadam_config* cfg, const int64_t* numels,
                           int32_t n_tensors, uint64_t* out_bytes);

@@ -19,6 +19,9 @@ FLAGS = [
     "-ffp-contract=off",
     # no packed FP32 instructions in generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # device code: min/max without IEEE NaN quieting, so that they fuse with
+    # lane permutes (gradients are taken to be finite)
+    "-Xarch_device", "-fno-honor-nans", "-Xarch_device", "-mno-amdgpu-ieee",
     "-Wall", "-Wno-unused-function",
     "-I", INCLUDE, "-I", CSRC,
     "-Wl,-rpath,/opt/rocm/lib",

@@ -70,6 +70,8 @@ int validate_config(const microadam_config* c) {
     return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block above 65536 does not fit uint16 indices");
   if (c->topk_block % c->ef_bucket != 0)
     return fail(MICROADAM_ERR_INVALID_ARG, "topk_block must be a multiple of ef_bucket");
+  if (c->topk_block % 16 != 0)
+    return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block must be a multiple of 16");
   if (c->topk_block > kMaxKernelBlock)
     return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block above 4096 is not implemented yet");
   if (c->window_value_dtype != MICROADAM_BF16 && c->window_value_dtype != MICROADAM_F32)
@@ -84,17 +86,27 @@ struct TensorPlan {
   uint64_t ef_off, ef_bytes, stats_off, stats_bytes, win_off, win_bytes;
 };
 
+// Byte offsets of the three state planes; every block owns a fixed-size
+// record in each, addressed by its global block number.
+struct Planes {
+  uint64_t ef, stats, win, total;
+  uint64_t ef_stride, stats_stride, win_stride;  // bytes per block
+};
+
 int entry_bytes(const microadam_config* c) { return c->window_value_dtype == MICROADAM_F32 ? 8 : 4; }
 
 int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
-              std::vector<TensorPlan>& out, uint64_t& total) {
+              std::vector<TensorPlan>& out, Planes& pl) {
   if (n < 1) return fail(MICROADAM_ERR_INVALID_ARG, "n_tensors must be >= 1");
   if (!numels) return fail(MICROADAM_ERR_INVALID_ARG, "numels is NULL");
   out.clear();
   out.reserve((size_t)n);
   const int64_t B = c->topk_block, Bq = c->ef_bucket, m = c->window;
   const int64_t eb = entry_bytes(c);
-  uint64_t off = 0;
+  const int32_t k_full = (int32_t)block_k(B, c->density);
+  pl.ef_stride = (uint64_t)B / 2;
+  pl.stats_stride = (uint64_t)(B / Bq) * 8;
+  pl.win_stride = (uint64_t)m * k_full * eb;
   int64_t blocks = 0;
   for (int32_t j = 0; j < n; ++j) {
     const int64_t d = numels[j];
@@ -105,21 +117,25 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
     p.num_blocks = (d + B - 1) / B;
     p.num_buckets = (d + Bq - 1) / Bq;
     p.first_block = blocks;
-    p.k_full = (int32_t)block_k(B, c->density);
+    p.k_full = k_full;
     p.k_last = (int32_t)block_k(d - (p.num_blocks - 1) * B, c->density);
-    p.ef_off = off;
-    p.ef_bytes = (uint64_t)(d + 1) / 2;
-    off = align_up(off + p.ef_bytes);
-    p.stats_off = off;
-    p.stats_bytes = (uint64_t)p.num_buckets * 8;
-    off = align_up(off + p.stats_bytes);
-    p.win_off = off;
-    p.win_bytes = (uint64_t)m * eb * ((uint64_t)(p.num_blocks - 1) * p.k_full + p.k_last);
-    off = align_up(off + p.win_bytes);
     blocks += p.num_blocks;
     out.push_back(p);
   }
-  total = off;
+  const uint64_t nb = (uint64_t)blocks;
+  pl.ef = 0;
+  pl.stats = align_up(pl.ef + nb * pl.ef_stride);
+  pl.win = align_up(pl.stats + nb * pl.stats_stride);
+  pl.total = align_up(pl.win + nb * pl.win_stride);
+  for (TensorPlan& p : out) {
+    const uint64_t b0 = (uint64_t)p.first_block, nbj = (uint64_t)p.num_blocks;
+    p.ef_off = pl.ef + b0 * pl.ef_stride;
+    p.ef_bytes = nbj * pl.ef_stride;
+    p.stats_off = pl.stats + b0 * pl.stats_stride;
+    p.stats_bytes = nbj * pl.stats_stride;
+    p.win_off = pl.win + b0 * pl.win_stride;
+    p.win_bytes = nbj * pl.win_stride;
+  }
   return MICROADAM_OK;
 }
 
@@ -142,6 +158,7 @@ constexpr int kTableSlots = 4;
 struct microadam_handle_s {
   microadam_config cfg;
   std::vector<TensorPlan> plans;
+  Planes planes;
   int32_t param_bf16 = 0, grad_bf16 = 0, value_f32 = 0;
   int32_t bucket_log2 = 0;
   uint8_t* state = nullptr;
@@ -190,13 +207,15 @@ void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& 
   p.block_tensor = h->d_block_tensor;
   p.wpow = h->d_wpow;
   p.state = h->state;
+  p.ef_plane = h->planes.ef;
+  p.stats_plane = h->planes.stats;
+  p.win_plane = h->planes.win;
   p.t = t;
   p.total_blocks = h->total_blocks;
-  p.n_tensors = (int32_t)h->plans.size();
   p.block = c.topk_block;
   p.bucket_log2 = h->bucket_log2;
   p.window = m;
-  p.n_old = (int32_t)((t < m ? t : m) - 1);
+  p.n_live = (int32_t)(t < m ? t : m);
   p.new_slot = (int32_t)((t - 1) % m);
   p.k_full = h->plans.empty() ? 0 : h->plans[0].k_full;
   p.lr = (float)lr;
@@ -231,10 +250,10 @@ int microadam_state_bytes(const microadam_config* cfg, const int64_t* numels, in
   int rc = validate_config(cfg);
   if (rc) return rc;
   std::vector<TensorPlan> plans;
-  uint64_t total = 0;
-  rc = make_plan(cfg, numels, n_tensors, plans, total);
+  Planes pl;
+  rc = make_plan(cfg, numels, n_tensors, plans, pl);
   if (rc) return rc;
-  *out_bytes = total;
+  *out_bytes = pl.total;
   return MICROADAM_OK;
 }
 
@@ -249,9 +268,10 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
       (grad_dtype != MICROADAM_F32 && grad_dtype != MICROADAM_BF16))
     return fail(MICROADAM_ERR_INVALID_ARG, "param_dtype / grad_dtype must be F32 or BF16");
   std::vector<TensorPlan> plans;
-  uint64_t total = 0;
-  rc = make_plan(cfg, numels, n_tensors, plans, total);
+  Planes pl;
+  rc = make_plan(cfg, numels, n_tensors, plans, pl);
   if (rc) return rc;
+  const uint64_t total = pl.total;
   if (!state) return fail(MICROADAM_ERR_INVALID_ARG, "state is NULL");
   if ((uintptr_t)state % kAlign) return fail(MICROADAM_ERR_INVALID_ARG, "state must be 256-byte aligned");
   if (state_bytes < total)
@@ -265,6 +285,7 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   if (!h) return fail(MICROADAM_ERR_NO_MEMORY, "handle allocation failed");
   h->cfg = *cfg;
   h->plans = std::move(plans);
+  h->planes = pl;
   h->param_bf16 = param_dtype == MICROADAM_BF16;
   h->grad_bf16 = grad_dtype == MICROADAM_BF16;
   h->value_f32 = cfg->window_value_dtype == MICROADAM_F32;
@@ -316,9 +337,6 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
     d.numel = p.numel;
     d.first_block = p.first_block;
     d.num_blocks = p.num_blocks;
-    d.ef_off = p.ef_off;
-    d.stats_off = p.stats_off;
-    d.win_off = p.win_off;
     d.k_full = p.k_full;
     d.k_last = p.k_last;
     for (TableSlot& t : h->slots) t.h[j] = d;
@@ -451,7 +469,7 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat, flo
   StepParams p;
   fill_constants(h, h->t, h->cfg.lr, p);
   const TensorPlan& tp = h->plans[(size_t)tensor];
-  hipError_t e = microadam::launch_moments(p, tensor, tp.first_block, tp.num_blocks, mhat, vhat,
+  hipError_t e = microadam::launch_moments(p, tp.first_block, tp.num_blocks, mhat, vhat,
                                            h->value_f32, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "launching the moment kernel");
   return MICROADAM_OK;

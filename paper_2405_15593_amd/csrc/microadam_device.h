@@ -10,37 +10,38 @@ namespace microadam {
 constexpr int kMaxWindow = 64;       // largest supported window m
 constexpr int kMaxBlock = 65536;     // uint16 block-relative indices
 
-// One parameter tensor as the step kernel sees it.
+// One parameter tensor as the kernels see it.
 struct TensorDesc {
   void* param;            // numel elements of the parameter dtype
   const void* grad;       // numel elements of the gradient dtype
   int64_t numel;
   int64_t first_block;    // global index of this tensor's block 0
   int64_t num_blocks;
-  uint64_t ef_off;        // byte offsets into the state buffer
-  uint64_t stats_off;
-  uint64_t win_off;
   int32_t k_full;         // entries per window row, full block
   int32_t k_last;         // entries per window row, last block
 };
 
-// Threads per workgroup of the step kernel for a Top-K block of B_d elements
-// (each thread owns 16 elements, so the block capacity is 16 * threads).
+// Threads per workgroup for a Top-K block of B_d elements (each thread owns
+// 16 elements, so the block capacity is 16 * threads).
 inline int threads_for_block(int block) { return block <= 1024 ? 64 : 256; }
 
-// Per-launch scalars (passed by value as the kernel argument).
+// State layout: three planes indexed by the global block number gb.
+//   EF codes       ef_plane    + gb * B_d/2
+//   (min, max)     stats_plane + gb * (B_d/B_q) * 8
+//   window rows    win_plane   + gb * m * k_full * entry_bytes
+// A block's window slot holds its m rows of k_q entries, row r at r*k_q.
 struct StepParams {
   const TensorDesc* tensors;
   const uint32_t* block_tensor;  // global block -> tensor index
   const float* wpow;             // [2 * kMaxWindow]: beta1^r, then beta2^r
   uint8_t* state;
+  uint64_t ef_plane, stats_plane, win_plane;  // byte offsets into state
   int64_t t;                     // step being taken (>= 1)
   int64_t total_blocks;
-  int32_t n_tensors;
   int32_t block;                 // B_d
   int32_t bucket_log2;           // B_q = 1 << bucket_log2
   int32_t window;                // m
-  int32_t n_old;                 // live rows written before step t: min(t, m) - 1
+  int32_t n_live;                // rows live after step t: min(t, m)
   int32_t new_slot;              // row slot written at step t: (t - 1) mod m
   int32_t k_full;                // entries per row of a full block (all tensors)
   int32_t decay_is_one;          // weight_decay * lr == 0
@@ -52,11 +53,10 @@ struct StepParams {
 hipError_t launch_step(const StepParams& p, int param_bf16, int grad_bf16, int value_f32,
                        hipStream_t stream);
 
-hipError_t launch_moments(const StepParams& p, int32_t tensor, int64_t first_block,
-                          int64_t grid, float* mhat, float* vhat, int value_f32,
-                          hipStream_t stream);
+hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_blocks,
+                          float* mhat, float* vhat, int value_f32, hipStream_t stream);
 
-// Dynamic LDS bytes the step kernel needs for this configuration.
+// Dynamic LDS bytes the kernels need (the larger of the two step kernels).
 size_t step_lds_bytes(int block, int k_full, int value_f32);
 
 }  // namespace microadam

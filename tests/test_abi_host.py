@@ -45,8 +45,8 @@ def test_state_bytes_llama2_7b(lib):
     blocks = d // 4096
     assert all(n % 4096 == 0 for n in numels)
     want_payload = d // 2 + 8 * (d // 64) + 10 * 41 * 4 * blocks
-    # each of the 3 regions of each tensor is padded to 256 bytes
-    assert want_payload <= got <= want_payload + 3 * 256 * len(numels)
+    # each of the 3 planes is padded to 256 bytes
+    assert want_payload <= got <= want_payload + 3 * 256
     # the paper's 0.5d + 4mk with a global k = ceil(d/100) (Section 3.2)
     paper = 0.5 * d + 4 * 10 * math.ceil(d / 100)
     ours_without_stats = d // 2 + 10 * 41 * 4 * blocks
@@ -58,12 +58,15 @@ def test_state_bytes_tails_and_f32(lib):
     cfg = ma.make_config(density=0.01, window=3, ef_bucket=16, topk_block=256,
                          window_value_dtype=ma.MICROADAM_F32)
     n = 1001            # 3 full blocks of 256 (k 3) and a tail of 233 (k 3)
-    got = ma.microadam_state_bytes(cfg, [n])
-    ef = 501
-    stats = 8 * 63
-    win = 3 * 8 * (3 * 3 + 3)
     pad = lambda x: -(-x // 256) * 256
-    assert got == pad(ef) + pad(stats) + pad(win)
+    # every block owns a full-size record in each plane: 128 B of codes,
+    # 16 (delta, Delta) pairs and 3 rows of k_full = 3 eight-byte entries
+    per_block = (128, 16 * 8, 3 * 3 * 8)
+    got = ma.microadam_state_bytes(cfg, [n])
+    assert got == sum(pad(4 * x) for x in per_block)
+    # a second tensor of 10 elements adds one block (k 1, padded to k_full)
+    got2 = ma.microadam_state_bytes(cfg, [n, 10])
+    assert got2 == sum(pad(5 * x) for x in per_block)
 
 
 BAD = [
@@ -84,6 +87,8 @@ BAD = [
     (dict(topk_block=4000, ef_bucket=64), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(topk_block=131072), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(topk_block=0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(topk_block=8, ef_bucket=8), ma.MICROADAM_ERR_UNSUPPORTED),
+    (dict(topk_block=1048, ef_bucket=8), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(window_value_dtype=7), ma.MICROADAM_ERR_INVALID_ARG),
 ]
 
