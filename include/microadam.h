@@ -96,25 +96,28 @@ typedef struct microadam_handle_s* microadam_handle;
 /*
  * Where one tensor's optimizer state lives inside the state buffer (byte
  * offsets from its start).  The buffer holds three planes, EF codes, bucket
- * stats and window, each starting 256-byte aligned; in each plane every
- * Top-K block of every tensor owns a record of fixed size, in the order of
- * the global block number (tensor 0's blocks first).  A tensor's records are
- * therefore contiguous, and the last block's record is padded to full size.
+ * stats and window, each starting 256-byte aligned.  In each plane every
+ * Top-K block owns a record of fixed size, at plane + g * stride for its
+ * global block number g.  Full blocks (B_d elements) are numbered first,
+ * tensor by tensor, then the ragged last blocks of the tensors whose numel is
+ * not a multiple of B_d; a ragged block's record is padded to full size.
+ * Block q of a tensor has global number first_block + q, except its last
+ * block (q = num_blocks - 1), whose number is last_block.
  *
- *   EF codes   ef_offset, B_d/2 bytes per block: element 2j of the tensor in
- *              the low nibble of byte j, element 2j+1 in the high nibble
- *              (nibbles past numel are 0).
- *   stats      stats_offset, B_d/B_q pairs of float32 (delta, Delta) per
- *              block = (min, max) of the bucket's residual; bucket b covers
- *              elements [b*B_q, min(numel, (b+1)*B_q)); pairs past
- *              num_buckets are unused.
- *   window     window_offset, m*k_full*entry_bytes per block: block q's rows
- *              start at window_offset + q*m*k_full*entry_bytes; row r (the
- *              row written at step s is r = (s-1) mod m) starts at
- *              r*k_q*entry_bytes within it and holds the block's k_q entries
- *              in ascending index order.  With bf16 values an entry is one
- *              little-endian uint32 (index | bf16_bits << 16); with float32
- *              values it is a uint32 index followed by the float32 value.
+ *   EF codes   B_d/2 bytes per block: element 2j of the block in the low
+ *              nibble of byte j, element 2j+1 in the high nibble (nibbles
+ *              past the block's elements are 0).
+ *   stats      B_d/B_q pairs of float32 (delta, Delta) per block = (min,
+ *              max) of the bucket's residual; pair b covers the block's
+ *              elements [b*B_q, (b+1)*B_q); pairs past its elements are
+ *              unused.
+ *   window     m*k_full*entry_bytes per block: row r (the row written at
+ *              step s is r = (s-1) mod m) starts at r*k_q*entry_bytes within
+ *              the record and holds the block's k_q entries in ascending
+ *              index order (k_q = k_last for the last block).  With bf16
+ *              values an entry is one little-endian uint32 (index |
+ *              bf16_bits << 16); with float32 values it is a uint32 index
+ *              followed by the float32 value.
  */
 typedef struct microadam_layout {
   int64_t numel;
@@ -124,9 +127,11 @@ typedef struct microadam_layout {
   int32_t k_last;      /* entries per row of the last block */
   int32_t entry_bytes; /* 4 (bf16 values) or 8 (float32 values) */
   int32_t reserved;
-  uint64_t ef_offset, ef_bytes;
-  uint64_t stats_offset, stats_bytes;
-  uint64_t window_offset, window_bytes;
+  int64_t first_block; /* global number of block 0 */
+  int64_t last_block;  /* global number of block num_blocks - 1 */
+  uint64_t ef_plane, ef_stride;
+  uint64_t stats_plane, stats_stride;
+  uint64_t window_plane, window_stride;
 } microadam_layout;
 
 /*

@@ -56,13 +56,19 @@ class microadam_layout(ctypes.Structure):
         ("k_last", ctypes.c_int32),
         ("entry_bytes", ctypes.c_int32),
         ("reserved", ctypes.c_int32),
-        ("ef_offset", ctypes.c_uint64),
-        ("ef_bytes", ctypes.c_uint64),
-        ("stats_offset", ctypes.c_uint64),
-        ("stats_bytes", ctypes.c_uint64),
-        ("window_offset", ctypes.c_uint64),
-        ("window_bytes", ctypes.c_uint64),
+        ("first_block", ctypes.c_int64),
+        ("last_block", ctypes.c_int64),
+        ("ef_plane", ctypes.c_uint64),
+        ("ef_stride", ctypes.c_uint64),
+        ("stats_plane", ctypes.c_uint64),
+        ("stats_stride", ctypes.c_uint64),
+        ("window_plane", ctypes.c_uint64),
+        ("window_stride", ctypes.c_uint64),
     ]
+
+    def block_number(self, q: int) -> int:
+        """Global number of the tensor's block q."""
+        return self.last_block if q == self.num_blocks - 1 else self.first_block + q
 
 
 # every symbol include/microadam.h declares

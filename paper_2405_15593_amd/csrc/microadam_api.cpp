@@ -81,20 +81,22 @@ int validate_config(const microadam_config* c) {
 }
 
 struct TensorPlan {
-  int64_t numel, num_blocks, num_buckets, first_block;
-  int32_t k_full, k_last;
-  uint64_t ef_off, ef_bytes, stats_off, stats_bytes, win_off, win_bytes;
+  int64_t numel, num_blocks, num_buckets, num_full, first_block, last_block;
+  int32_t k_full, k_last, s_last;
 };
 
-// Byte offsets of the three state planes; every block owns a fixed-size
-// record in each, addressed by its global block number.
+// Byte offsets of the three state planes; every block owns a record of fixed
+// size in each, addressed by its global block number.
 struct Planes {
   uint64_t ef, stats, win, total;
   uint64_t ef_stride, stats_stride, win_stride;  // bytes per block
+  int64_t n_full, n_blocks;
 };
 
 int entry_bytes(const microadam_config* c) { return c->window_value_dtype == MICROADAM_F32 ? 8 : 4; }
 
+// Full blocks are numbered first, tensor by tensor; the ragged last blocks
+// follow, so that the kernels see one run of equal blocks.
 int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
               std::vector<TensorPlan>& out, Planes& pl) {
   if (n < 1) return fail(MICROADAM_ERR_INVALID_ARG, "n_tensors must be >= 1");
@@ -107,7 +109,7 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
   pl.ef_stride = (uint64_t)B / 2;
   pl.stats_stride = (uint64_t)(B / Bq) * 8;
   pl.win_stride = (uint64_t)m * k_full * eb;
-  int64_t blocks = 0;
+  int64_t full = 0;
   for (int32_t j = 0; j < n; ++j) {
     const int64_t d = numels[j];
     if (d < 1) return fail(MICROADAM_ERR_INVALID_ARG, "every numel must be >= 1");
@@ -116,26 +118,24 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
     p.numel = d;
     p.num_blocks = (d + B - 1) / B;
     p.num_buckets = (d + Bq - 1) / Bq;
-    p.first_block = blocks;
+    p.num_full = d / B;
+    p.first_block = full;
     p.k_full = k_full;
-    p.k_last = (int32_t)block_k(d - (p.num_blocks - 1) * B, c->density);
-    blocks += p.num_blocks;
+    p.s_last = (int32_t)(d - (p.num_blocks - 1) * B);
+    p.k_last = (int32_t)block_k(p.s_last, c->density);
+    full += p.num_full;
     out.push_back(p);
   }
-  const uint64_t nb = (uint64_t)blocks;
+  int64_t next = full;
+  for (TensorPlan& p : out)
+    p.last_block = p.num_full < p.num_blocks ? next++ : p.first_block + p.num_blocks - 1;
+  const uint64_t nb = (uint64_t)next;
+  pl.n_full = full;
+  pl.n_blocks = next;
   pl.ef = 0;
   pl.stats = align_up(pl.ef + nb * pl.ef_stride);
   pl.win = align_up(pl.stats + nb * pl.stats_stride);
   pl.total = align_up(pl.win + nb * pl.win_stride);
-  for (TensorPlan& p : out) {
-    const uint64_t b0 = (uint64_t)p.first_block, nbj = (uint64_t)p.num_blocks;
-    p.ef_off = pl.ef + b0 * pl.ef_stride;
-    p.ef_bytes = nbj * pl.ef_stride;
-    p.stats_off = pl.stats + b0 * pl.stats_stride;
-    p.stats_bytes = nbj * pl.stats_stride;
-    p.win_off = pl.win + b0 * pl.win_stride;
-    p.win_bytes = nbj * pl.win_stride;
-  }
   return MICROADAM_OK;
 }
 
@@ -212,6 +212,7 @@ void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& 
   p.win_plane = h->planes.win;
   p.t = t;
   p.total_blocks = h->total_blocks;
+  p.n_full = h->planes.n_full;
   p.block = c.topk_block;
   p.bucket_log2 = h->bucket_log2;
   p.window = m;
@@ -276,7 +277,7 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   if ((uintptr_t)state % kAlign) return fail(MICROADAM_ERR_INVALID_ARG, "state must be 256-byte aligned");
   if (state_bytes < total)
     return fail(MICROADAM_ERR_STATE_SIZE, "state buffer smaller than microadam_state_bytes");
-  const int64_t total_blocks = plans.back().first_block + plans.back().num_blocks;
+  const int64_t total_blocks = pl.n_blocks;
   const int nt = threads_for_block(cfg->topk_block);
   if (total_blocks * (int64_t)nt >= ((int64_t)1 << 32) || total_blocks >= ((int64_t)1 << 31))
     return fail(MICROADAM_ERR_UNSUPPORTED, "too many Top-K blocks for one launch");
@@ -331,14 +332,18 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   std::vector<uint32_t> bt((size_t)total_blocks);
   for (size_t j = 0; j < nd; ++j) {
     const TensorPlan& p = h->plans[j];
-    for (int64_t b = 0; b < p.num_blocks; ++b) bt[(size_t)(p.first_block + b)] = (uint32_t)j;
+    for (int64_t b = 0; b < p.num_full; ++b) bt[(size_t)(p.first_block + b)] = (uint32_t)j;
+    bt[(size_t)p.last_block] = (uint32_t)j;
     TensorDesc d;
     std::memset(&d, 0, sizeof(d));
     d.numel = p.numel;
     d.first_block = p.first_block;
     d.num_blocks = p.num_blocks;
+    d.last_block = p.last_block;
     d.k_full = p.k_full;
     d.k_last = p.k_last;
+    d.s_last = p.s_last;
+    d.num_full = (int32_t)p.num_full;
     for (TableSlot& t : h->slots) t.h[j] = d;
   }
   hipStream_t s = (hipStream_t)stream;
@@ -447,12 +452,14 @@ int microadam_tensor_layout(microadam_handle h, int32_t tensor, microadam_layout
   out->k_full = p.k_full;
   out->k_last = p.k_last;
   out->entry_bytes = entry_bytes(&h->cfg);
-  out->ef_offset = p.ef_off;
-  out->ef_bytes = p.ef_bytes;
-  out->stats_offset = p.stats_off;
-  out->stats_bytes = p.stats_bytes;
-  out->window_offset = p.win_off;
-  out->window_bytes = p.win_bytes;
+  out->first_block = p.first_block;
+  out->last_block = p.last_block;
+  out->ef_plane = h->planes.ef;
+  out->ef_stride = h->planes.ef_stride;
+  out->stats_plane = h->planes.stats;
+  out->stats_stride = h->planes.stats_stride;
+  out->window_plane = h->planes.win;
+  out->window_stride = h->planes.win_stride;
   return MICROADAM_OK;
 }
 
@@ -469,8 +476,12 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat, flo
   StepParams p;
   fill_constants(h, h->t, h->cfg.lr, p);
   const TensorPlan& tp = h->plans[(size_t)tensor];
-  hipError_t e = microadam::launch_moments(p, tp.first_block, tp.num_blocks, mhat, vhat,
-                                           h->value_f32, (hipStream_t)stream);
+  hipError_t e = hipSuccess;
+  if (tp.num_full > 0)
+    e = microadam::launch_moments(p, tp.first_block, tp.num_full, mhat, vhat, h->value_f32,
+                                  (hipStream_t)stream);
+  if (e == hipSuccess && tp.num_full < tp.num_blocks)
+    e = microadam::launch_moments(p, tp.last_block, 1, mhat, vhat, h->value_f32, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "launching the moment kernel");
   return MICROADAM_OK;
 }

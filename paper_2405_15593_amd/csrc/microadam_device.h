@@ -10,15 +10,20 @@ namespace microadam {
 constexpr int kMaxWindow = 64;       // largest supported window m
 constexpr int kMaxBlock = 65536;     // uint16 block-relative indices
 
-// One parameter tensor as the kernels see it.
+// One parameter tensor as the kernels see it.  Its full blocks are the
+// global blocks [first_block, first_block + num_full); a ragged last block
+// (numel not a multiple of B_d) is numbered after every tensor's full blocks.
 struct TensorDesc {
   void* param;            // numel elements of the parameter dtype
   const void* grad;       // numel elements of the gradient dtype
   int64_t numel;
-  int64_t first_block;    // global index of this tensor's block 0
+  int64_t first_block;    // global number of block 0
   int64_t num_blocks;
+  int64_t last_block;     // global number of block num_blocks - 1
   int32_t k_full;         // entries per window row, full block
   int32_t k_last;         // entries per window row, last block
+  int32_t s_last;         // elements in the last block
+  int32_t num_full;       // full blocks
 };
 
 // Threads per workgroup for a Top-K block of B_d elements (each thread owns
@@ -30,6 +35,8 @@ inline int threads_for_block(int block) { return block <= 1024 ? 64 : 256; }
 //   (min, max)     stats_plane + gb * (B_d/B_q) * 8
 //   window rows    win_plane   + gb * m * k_full * entry_bytes
 // A block's window slot holds its m rows of k_q entries, row r at r*k_q.
+// Global blocks [0, n_full) are full (B_d elements, k_full entries per row);
+// blocks [n_full, total_blocks) are the ragged last blocks of tensors.
 struct StepParams {
   const TensorDesc* tensors;
   const uint32_t* block_tensor;  // global block -> tensor index
@@ -38,6 +45,7 @@ struct StepParams {
   uint64_t ef_plane, stats_plane, win_plane;  // byte offsets into state
   int64_t t;                     // step being taken (>= 1)
   int64_t total_blocks;
+  int64_t n_full;                // full blocks (numbered first)
   int32_t block;                 // B_d
   int32_t bucket_log2;           // B_q = 1 << bucket_log2
   int32_t window;                // m

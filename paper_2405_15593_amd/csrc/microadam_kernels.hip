@@ -58,6 +58,13 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
 }
 __device__ __forceinline__ uint32_t popc(uint64_t m) { return (uint32_t)__popcll(m); }
 __device__ __forceinline__ uint32_t sgpr(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+// A uniform value the compiler must treat as unknown at this point, so that
+// tests on it stay where they are written instead of being computed early
+// and kept in scalar registers.
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+s"(x));
+  return x;
+}
 // Work-item and workgroup ids straight from the hardware registers (the
 // library wrappers behind threadIdx / blockIdx are not inlined into code
 // built without IEEE mode).
@@ -134,8 +141,11 @@ __device__ __forceinline__ TensorDesc load_desc(const __attribute__((address_spa
   r.numel = d->numel;
   r.first_block = d->first_block;
   r.num_blocks = d->num_blocks;
+  r.last_block = d->last_block;
   r.k_full = d->k_full;
   r.k_last = d->k_last;
+  r.s_last = d->s_last;
+  r.num_full = d->num_full;
   return r;
 }
 
@@ -257,12 +267,61 @@ __device__ __forceinline__ Block locate(const StepParams& p, int64_t gb) {
   Block b;
   const uint32_t j = constant_ptr(p.block_tensor)[gb];
   b.desc = load_desc(constant_ptr(p.tensors) + j);
-  const int64_t q = gb - b.desc.first_block;
-  b.e0 = q * p.block;
-  const int64_t rem = b.desc.numel - b.e0;
-  b.s = (int)(rem < p.block ? rem : p.block);
-  b.kq = (q == b.desc.num_blocks - 1) ? b.desc.k_last : b.desc.k_full;
+  const bool last = (int32_t)gb == (int32_t)b.desc.last_block;
+  const int32_t q = last ? (int32_t)b.desc.num_blocks - 1 : (int32_t)(gb - b.desc.first_block);
+  b.e0 = (int64_t)q * p.block;
+  b.s = last ? b.desc.s_last : p.block;
+  b.kq = last ? b.desc.k_last : b.desc.k_full;
   return b;
+}
+
+// Geometry of one block as the update kernel carries it.
+struct Span {
+  uint64_t base;          // byte address of the block's first parameter
+  int64_t e0;             // first element of the block in its tensor
+  int32_t gb;             // global block number
+  int32_t s;              // valid elements
+  int32_t kq;             // window entries per row
+};
+
+// The tensor of the full blocks a workgroup walks through in order; the
+// tables are read again only when the walk crosses into another tensor.
+// Global block numbers are below 2^31 (checked at init) and are compared as
+// 32-bit values, which keeps the comparisons scalar.
+struct Cursor {
+  uint64_t param;
+  int32_t first;          // first global block of the tensor
+  int32_t end;            // first global block past its full blocks (0: none yet)
+};
+
+// Full block gb (gb < n_full): B_d elements, k_full entries per row.
+__device__ __forceinline__ Span seek_full(const StepParams& p, Cursor& c, int32_t gb, uint32_t elem_bytes) {
+  if (gb >= c.end) {
+    const uint32_t j = constant_ptr(p.block_tensor)[gb];
+    const __attribute__((address_space(4))) TensorDesc* d = constant_ptr(p.tensors) + j;
+    c.param = (uint64_t)d->param;
+    c.first = (int32_t)d->first_block;
+    c.end = c.first + d->num_full;
+  }
+  Span u;
+  u.gb = gb;
+  u.e0 = (int64_t)(gb - c.first) * p.block;
+  u.base = c.param + (uint64_t)u.e0 * elem_bytes;
+  u.s = p.block;
+  u.kq = p.k_full;
+  return u;
+}
+
+// Any block: full, or the ragged last block of its tensor.
+__device__ __forceinline__ Span span_of(const StepParams& p, int32_t gb, uint32_t elem_bytes) {
+  const Block b = locate(p, gb);
+  Span u;
+  u.gb = gb;
+  u.e0 = b.e0;
+  u.base = (uint64_t)b.desc.param + (uint64_t)b.e0 * elem_bytes;
+  u.s = b.s;
+  u.kq = b.kq;
+  return u;
 }
 
 template <int EW>
@@ -299,7 +358,7 @@ enum { M_COUNT = 0 /* [NW] */, M_WL = 8 /* [NW] */, M_GEN = 12, M_T = 13, M_ILAS
 template <int NT>
 __device__ __forceinline__ void wg_scan(const uint32_t (&cnt)[2], uint32_t (&base)[2], uint32_t* red) {
   constexpr int NW = NT / kWave;
-  const int lane = thread_id() & (kWave - 1), wave = thread_id() / kWave;
+  const int lane = thread_id() & (kWave - 1), wave = (int)sgpr(thread_id() / kWave);
   const uint32_t c = cnt[0] + cnt[1];  // <= 16
   uint32_t pre = 0, tot = 0;
 #pragma unroll
@@ -322,7 +381,7 @@ __device__ __forceinline__ void wg_scan(const uint32_t (&cnt)[2], uint32_t (&bas
 template <int NT>
 __device__ __forceinline__ uint32_t wg_count(const uint32_t (&mask)[2], uint32_t* red) {
   constexpr int NW = NT / kWave;
-  const int lane = thread_id() & (kWave - 1), wave = thread_id() / kWave;
+  const int lane = thread_id() & (kWave - 1), wave = (int)sgpr(thread_id() / kWave);
   const uint32_t c = __popc(mask[0]) + __popc(mask[1]);  // <= 16
   uint32_t tot = 0;
 #pragma unroll
@@ -346,7 +405,7 @@ __global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
   extern __shared__ __align__(16) uint32_t smem[];
   const SelectLds<NT> l(smem);
 
-  const int tid = thread_id(), lane = tid & (kWave - 1), wave = tid / kWave;
+  const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr(tid / kWave);
   const uint32_t eb = (uint32_t)tid * kLaneElems;  // first element of this thread
   const int bl = p.bucket_log2;
   const bool pair_buckets = bl == 3;               // B_q = 8: one bucket per vector
@@ -689,15 +748,25 @@ __global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
   // ---------------------------------------------- 4. e = Q(a with a[I] = 0)
   const float Tf = __uint_as_float(T);
   float x[2][8], mn[2], mx[2];
+  // kept elements: |a| > T, and |a| == T up to index i_last; without ties
+  // at the threshold that is |a| >= T (a workgroup-uniform case)
+  if (notie) {
+#pragma unroll
+    for (int v = 0; v < 2; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[v][e] = (__builtin_fabsf(a[v][e]) >= Tf) ? 0.0f : a[v][e];
+  } else {
+#pragma unroll
+    for (int v = 0; v < 2; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float ab = __builtin_fabsf(a[v][e]);
+        const bool kept = (ab > Tf) | ((ab == Tf) & (eb + v * 8 + e <= i_last));
+        x[v][e] = kept ? 0.0f : a[v][e];
+      }
+  }
 #pragma unroll
   for (int v = 0; v < 2; ++v) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float ab = __builtin_fabsf(a[v][e]);
-      const uint32_t i = eb + v * 8 + e;
-      const bool kept = notie ? (ab >= Tf) : (ab > Tf || (ab == Tf && i <= i_last));
-      x[v][e] = kept ? 0.0f : a[v][e];
-    }
     if (full) {
       mn[v] = __builtin_fminf(__builtin_fminf(__builtin_fminf(x[v][0], x[v][1]), x[v][2]),
                               __builtin_fminf(__builtin_fminf(x[v][3], x[v][4]), x[v][5]));
@@ -751,7 +820,7 @@ __global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
     }
     uint32_t wv = d1e | (d1o << 4);
     const bool exact_u = uv >= 0x1p-125f && uv <= 0x1p+125f;
-    if (!exact_u || d1e != d2e || d1o != d2o) {
+    if (!exact_u | (d1e != d2e) | (d1o != d2o)) {
       wv = 0;
       if (uv != 0.0f) {
 #pragma unroll
@@ -787,184 +856,289 @@ __global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
 
 // ============================================================ update
 // z1 / z2 hold, per element of the block, sum beta1^r V and sum beta2^r V^2
-// (then the parameter decrement).  Element i lives at word
+// (then z1 the parameter decrement).  Element i lives at word
 // ((i >> 2) & 3) * 4*NT + (i >> 4) * 4 + (i & 3), so that the 16 elements of a
 // thread are four 16-byte words at a stride of 4*NT words and a wave's
-// 16-byte accesses fall on consecutive addresses.
+// 16-byte accesses fall on consecutive addresses.  Word CAP of each array is
+// a sink for lanes without an entry, which keeps the sparse updates free of
+// branches.
 template <int NT>
 __device__ __forceinline__ uint32_t zpos(uint32_t i) {
   return ((i >> 2) & 3u) * (4u * NT) + (i >> 4) * 4u + (i & 3u);
 }
 
+// What the update kernel holds for one block before processing it: its
+// geometry, its parameters and two entries per thread of its window record
+// (the live rows are the record's first n_live*k_q entries).
+template <bool PBF16, bool VF32>
+struct UpdateBlock {
+  Span g;
+  Raw8<PBF16> th[2];
+  typename Entry<VF32>::T w[2];
+};
+
+template <int NT, bool VF>
+constexpr size_t update_lds_bytes() {
+  return (size_t)2 * (NT * kLaneElems + 16) * 4 + (size_t)(2 * NT + 1) * (VF ? 8 : 4);
+}
+
 // One wave (rotating with the block) rebuilds the moments of the block's
-// window entries, oldest row first; then every thread updates its own
-// elements.  EXPORT = true writes dense m-hat and v-hat instead of updating
-// theta.
-template <int NT, bool PBF16, bool VF32, bool EXPORT>
-__global__ void __launch_bounds__(NT) update_kernel(StepParams p, int64_t first_block, float* mhat,
-                                                    float* vhat) {
+// window entries, oldest row first, and turns them into parameter
+// decrements; then every thread updates its own elements.  RUN = true: the
+// blocks are full and workgroups are persistent, workgroup w taking the run
+// of blocks first_block + [w*per, (w+1)*per) and loading the next block's
+// parameters and window entries before it processes the current one.
+// RUN = false: workgroup w takes block first_block + w alone.  EXPORT = true
+// writes dense m-hat and v-hat instead of updating theta.
+// LDS (about 35 KB per workgroup) allows 4 workgroups per compute unit, one
+// wave of each per SIMD; telling the compiler so lets it keep independent LDS
+// reads in flight together instead of minimising registers.
+template <int NT, bool PBF16, bool VF32, bool EXPORT, bool RUN, int KC>
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) update_kernel(StepParams p, int64_t first_block, int64_t num_blocks,
+                                                    int64_t per, float* mhat, float* vhat) {
   constexpr int NW = NT / kWave;
   constexpr int CAP = NT * kLaneElems;
-  constexpr int kChunks = VF32 ? 8 : 16;   // window entries held per lane
+  constexpr int kChunks = KC;              // 64-entry window chunks the leader holds
   using E = Entry<VF32>;
   using ET = typename E::T;
+  using UB = UpdateBlock<PBF16, VF32>;
   extern __shared__ __align__(16) uint32_t smem[];
   float* const z1 = (float*)smem;
-  float* const z2 = z1 + CAP;
+  float* const z2 = z1 + CAP + 16;
+  // [2*NT] live window entries, then one entry that is always empty
+  ET* const stage = (ET*)(z2 + CAP + 16);
 
-  const int tid = thread_id(), lane = tid & (kWave - 1), wave = tid / kWave;
+  const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr(tid / kWave);
   const uint32_t eb = (uint32_t)tid * kLaneElems;
-  const int64_t gb = first_block + block_id();
-  const int leader = (int)(gb & (NW - 1));
   const int m = p.window, n_live = p.n_live;
   // oldest live row first: the row written at step s is slot (s-1) mod m
   const int slot0 = (p.new_slot + 1 + m - n_live) % m;
+  const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
+  const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
 
-  const Block b = locate(p, gb);
-  const int s = b.s, kq = b.kq;
-  const bool full = s == CAP;
-  const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
-  const int R = (kq + kWave - 1) / kWave;   // chunks of 64 entries per row
-  const bool in_regs = n_live * R <= kChunks;
-
-  ET ent[kChunks];
-  if (wave == leader && in_regs) {
-    int row = 0, col = 0, slot = slot0;
+  if (tid == 0) stage[2 * NT] = E::none();
+  Cursor cursor = {0, 0, 0};
+  auto fetch = [&](int32_t gb, UB& u) {
+    u.g = RUN ? seek_full(p, cursor, gb, PBF16 ? 2 : 4) : span_of(p, gb, PBF16 ? 2 : 4);
+    // unconditional loads keep the count of loads in flight fixed; entries
+    // past the record read 0 and entries past the live rows are not used
+    const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, u.g.kq);
+    u.w[0] = E::load(rw, tid);
+    u.w[1] = E::load(rw, tid + NT);
+    if (!EXPORT) {
+      const Rsrc rp = make_rsrc((const void*)u.g.base, vec_bytes<PBF16>(u.g.s));
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      ent[c] = E::none();
-      if (row < n_live) {
-        const int jj = col * kWave + lane;
-        if (jj < kq) ent[c] = E::load(rw, slot * kq + jj);
+      for (int v = 0; v < 2; ++v) u.th[v] = load8<PBF16>(rp, eb + v * 8);
+    }
+  };
+
+  auto process = [&](const UB& u) {
+    const int s = u.g.s, kq = u.g.kq;
+    const int leader = u.g.gb & (NW - 1);
+    const int R = (kq + kWave - 1) / kWave;
+    const bool staged = n_live * kq <= 2 * NT && n_live * R <= kChunks;
+    {
+      const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        *(float4*)(z1 + q * 4 * NT + tid * 4) = zero;
+        *(float4*)(z2 + q * 4 * NT + tid * 4) = zero;
       }
-      if (++col == R) {
-        col = 0;
-        ++row;
-        if (++slot == m) slot = 0;
+      stage[tid] = u.w[0];
+      stage[tid + NT] = u.w[1];
+    }
+    lds_sync();
+
+    if (wave == leader) {
+      auto step_of = [&](float s1, float s2) {
+        const float mh = p.c1 * s1;
+        const float vh = p.c2 * s2;
+        const float den = p.eps + __builtin_amdgcn_sqrtf(vh);
+        return p.lr * (mh * __builtin_amdgcn_rcpf(den));
+      };
+      if (staged) {
+        // Chunk c: row c / R in age order (slot (slot0 + row) mod m), entries
+        // (c mod R)*64 + lane.  All kChunks chunks are processed without
+        // branches: chunks past the live rows read the empty entry, and
+        // lanes without an entry work on the sink word.
+        const int nch = opaque(n_live * R);
+        uint32_t zp[kChunks];
+        float val[kChunks];
+        int rr[kChunks];
+        {
+          int row = 0, col = 0, slot = slot0;
+#pragma unroll
+          for (int c = 0; c < kChunks; ++c) {
+            const int jj = col * kWave + lane;
+            const ET x = stage[(c < nch && jj < kq) ? slot * kq + jj : 2 * NT];
+            const uint32_t i = E::idx(x);
+            zp[c] = i < (uint32_t)s ? zpos<NT>(i) : (uint32_t)CAP;
+            val[c] = E::val(x);
+            rr[c] = (n_live - 1 - row) & (kMaxWindow - 1);
+            if (++col == R) {
+              col = 0;
+              ++row;
+              if (++slot == m) slot = 0;
+            }
+          }
+        }
+        // the entries of one row (or of one 64-entry part of it) have
+        // distinct indices, so each chunk reads, adds and writes back its
+        // words (the sink word's lanes race harmlessly); chunks follow each
+        // other oldest row first
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) {
+          const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), rr[c]));
+          const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), rr[c]));
+          const float v = val[c];
+          const float x1 = w1 * v;
+          const float vv = v * v;
+          const float x2 = w2 * vv;
+          const float a1 = z1[zp[c]], a2 = z2[zp[c]];
+          z1[zp[c]] = a1 + x1;
+          z2[zp[c]] = a2 + x2;
+        }
+        if (!EXPORT) {
+          // every entry's sums are read before any word is overwritten, so an
+          // index that occurs in several rows gets the same decrement from
+          // each occurrence
+          float d[kChunks];
+#pragma unroll
+          for (int c = 0; c < kChunks; ++c) d[c] = step_of(z1[zp[c]], z2[zp[c]]);
+#pragma unroll
+          for (int c = 0; c < kChunks; ++c) z1[zp[c]] = d[c];
+        }
+      } else {
+        const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, u.g.gb, kq);
+        for (int row = 0, slot = slot0; row < n_live; ++row, slot = (slot + 1 == m) ? 0 : slot + 1) {
+          const int r = n_live - 1 - row;
+          const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), r));
+          const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), r));
+          for (int jj = lane; jj < kq; jj += kWave) {
+            const ET x = E::load(rw, slot * kq + jj);
+            const uint32_t i = E::idx(x);
+            const uint32_t zp = i < (uint32_t)s ? zpos<NT>(i) : (uint32_t)CAP;
+            const float v = E::val(x);
+            const float vv = v * v;
+            const float x1 = w1 * v, x2 = w2 * vv;
+            const float a1 = z1[zp], a2 = z2[zp];
+            z1[zp] = a1 + x1;
+            z2[zp] = a2 + x2;
+          }
+        }
+        if (!EXPORT) {
+          // one 64-entry chunk at a time; z2 = -1 marks a converted word
+          for (int row = 0, slot = slot0; row < n_live; ++row, slot = (slot + 1 == m) ? 0 : slot + 1)
+            for (int jj = lane; jj < kq; jj += kWave) {
+              const uint32_t i = E::idx(E::load(rw, slot * kq + jj));
+              if (i < (uint32_t)s) {
+                const uint32_t zp = zpos<NT>(i);
+                const float s2 = z2[zp];
+                if (s2 >= 0.0f) {
+                  z1[zp] = step_of(z1[zp], s2);
+                  z2[zp] = -1.0f;
+                }
+              }
+            }
+        }
       }
     }
-  }
-  const Rsrc rp = make_rsrc((uint8_t*)b.desc.param + b.e0 * (PBF16 ? 2 : 4), vec_bytes<PBF16>(s));
-  Raw8<PBF16> th[2];
-  if (!EXPORT) {
-#pragma unroll
-    for (int v = 0; v < 2; ++v) th[v] = load8<PBF16>(rp, eb + v * 8);
-  }
+    lds_sync();
 
-  {
-    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) *(float4*)(z1 + q * 4 * NT + tid * 4) = zero;
     if (EXPORT) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) *(float4*)(z2 + q * 4 * NT + tid * 4) = zero;
-    }
-  }
-  lds_sync();
-
-  if (wave == leader) {
-    const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
-    const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
-    // the entries of one row (or of one 64-entry part of it) have distinct
-    // indices, so a chunk updates each LDS word at most once
-    auto init = [&](ET e) {
-      const uint32_t i = E::idx(e);
-      if (i < (uint32_t)s) z2[zpos<NT>(i)] = 0.0f;
-    };
-    auto accumulate = [&](ET e, int r) {
-      const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), r));
-      const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), r));
-      const uint32_t i = E::idx(e);
-      if (i < (uint32_t)s) {
-        const uint32_t zp = zpos<NT>(i);
-        const float v = E::val(e);
-        const float x1 = w1 * v;
-        const float vv = v * v;
-        const float x2 = w2 * vv;
-        z1[zp] = z1[zp] + x1;
-        z2[zp] = z2[zp] + x2;
-      }
-    };
-    // each index once: z1 <- eta * m-hat / (eps + sqrt(v-hat)), z2 <- -1
-    auto convert = [&](ET e) {
-      const uint32_t i = E::idx(e);
-      if (i < (uint32_t)s) {
-        const uint32_t zp = zpos<NT>(i);
-        const float s2 = z2[zp];
-        if (s2 >= 0.0f) {
-          const float mh = p.c1 * z1[zp];
-          const float vh = p.c2 * s2;
-          const float den = p.eps + __builtin_amdgcn_sqrtf(vh);
-          z1[zp] = p.lr * (mh * __builtin_amdgcn_rcpf(den));
-          z2[zp] = -1.0f;
+      for (int q = 0; q < 4; ++q) {
+        const float4 s1 = *(const float4*)(z1 + q * 4 * NT + tid * 4);
+        const float4 s2 = *(const float4*)(z2 + q * 4 * NT + tid * 4);
+        const float a1[4] = {s1.x, s1.y, s1.z, s1.w}, a2[4] = {s2.x, s2.y, s2.z, s2.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t i = eb + q * 4 + r;
+          if ((int)i < s) {
+            mhat[u.g.e0 + i] = p.c1 * a1[r];
+            vhat[u.g.e0 + i] = p.c2 * a2[r];
+          }
         }
       }
-    };
-    if (in_regs) {
-      if (!EXPORT) {
-#pragma unroll
-        for (int c = 0; c < kChunks; ++c) init(ent[c]);
-      }
-      int row = 0, col = 0;
-#pragma unroll
-      for (int c = 0; c < kChunks; ++c) {
-        if (row < n_live) accumulate(ent[c], n_live - 1 - row);
-        if (++col == R) { col = 0; ++row; }
-      }
-      if (!EXPORT) {
-#pragma unroll
-        for (int c = 0; c < kChunks; ++c) convert(ent[c]);
-      }
-    } else {
-      if (!EXPORT) {
-        for (int row = 0, slot = slot0; row < n_live; ++row, slot = (slot + 1 == m) ? 0 : slot + 1)
-          for (int jj = lane; jj < kq; jj += kWave) init(E::load(rw, slot * kq + jj));
-      }
-      for (int row = 0, slot = slot0; row < n_live; ++row, slot = (slot + 1 == m) ? 0 : slot + 1)
-        for (int jj = lane; jj < kq; jj += kWave) accumulate(E::load(rw, slot * kq + jj), n_live - 1 - row);
-      if (!EXPORT) {
-        for (int row = 0, slot = slot0; row < n_live; ++row, slot = (slot + 1 == m) ? 0 : slot + 1)
-          for (int jj = lane; jj < kq; jj += kWave) convert(E::load(rw, slot * kq + jj));
-      }
+      return;
     }
-  }
-  lds_sync();
 
-  if (EXPORT) {
+    // ---------------------------------------------- 6. parameter update
+    const bool full = s == NT * kLaneElems;
+    const Rsrc rp = make_rsrc((const void*)u.g.base, vec_bytes<PBF16>(s));
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float4 s1 = *(const float4*)(z1 + q * 4 * NT + tid * 4);
-      const float4 s2 = *(const float4*)(z2 + q * 4 * NT + tid * 4);
-      const float a1[4] = {s1.x, s1.y, s1.z, s1.w}, a2[4] = {s2.x, s2.y, s2.z, s2.w};
+    for (int v = 0; v < 2; ++v) {
+      const uint32_t e0 = eb + v * 8;   // vectors past s store nothing
+      const float4 u0 = *(const float4*)(z1 + (2 * v) * 4 * NT + tid * 4);
+      const float4 u1 = *(const float4*)(z1 + (2 * v + 1) * 4 * NT + tid * 4);
+      const float upd[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+      float thf[8], out[8];
+      unpack8<PBF16>(u.th[v], thf);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const uint32_t i = eb + q * 4 + r;
-        if ((int)i < s) {
-          mhat[b.e0 + i] = p.c1 * a1[r];
-          vhat[b.e0 + i] = p.c2 * a2[r];
-        }
+      for (int e = 0; e < 8; ++e) {
+        const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
+        out[e] = base - upd[e];
+      }
+      // a full block holds whole threads (B_d is a multiple of 16)
+      if (RUN) {
+        if ((int)eb < s) store8<PBF16>(rp, e0, s, true, out);
+      } else {
+        store8<PBF16>(rp, e0, s, full, out);
       }
     }
+  };
+
+  // Two register sets take turns, and the next block is always fetched (the
+  // last block of a run fetches itself again), so that the count of loads
+  // issued after any block's data is fixed and the waits for that data let
+  // the next block's loads stay in flight.
+  if (!RUN) {
+    UB A;
+    fetch((int32_t)(first_block + block_id()), A);
+    process(A);
     return;
   }
-
-  // ---------------------------------------------- 6. parameter update
-#pragma unroll
-  for (int v = 0; v < 2; ++v) {
-    const uint32_t e0 = eb + v * 8;
-    if ((int)e0 >= s) continue;
-    const float4 u0 = *(const float4*)(z1 + (2 * v) * 4 * NT + tid * 4);
-    const float4 u1 = *(const float4*)(z1 + (2 * v + 1) * 4 * NT + tid * 4);
-    const float upd[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
-    float thf[8], out[8];
-    unpack8<PBF16>(th[v], thf);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
-      out[e] = base - upd[e];
-    }
-    store8<PBF16>(rp, e0, s, full, out);
+  const int32_t nb = (int32_t)num_blocks, run = (int32_t)per;
+  const int32_t lo = (int32_t)block_id() * run;
+  if (lo >= nb) return;
+  const int32_t g0 = (int32_t)first_block;
+  const int32_t hi = g0 + (lo + run < nb ? lo + run : nb);
+  int32_t g = g0 + lo;
+  UB A, B;
+  fetch(g, A);
+  for (;;) {
+    const int32_t g1 = g + 1;
+    const bool m1 = g1 < hi;
+    fetch(m1 ? g1 : g, B);
+    process(A);
+    if (!m1) break;
+    const int32_t g2 = g1 + 1;
+    const bool m2 = g2 < hi;
+    fetch(m2 ? g2 : g1, A);
+    process(B);
+    if (!m2) break;
+    g = g2;
   }
+}
+
+
+// Resident workgroups of one update launch: enough to fill every compute
+// unit, computed once per device.
+template <int NT, bool PB, bool VF>
+int64_t update_grid(size_t lds) {
+  static int64_t cache[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
+  if (!cache[dev]) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_kernel<NT, PB, VF, false, true, 16>, NT, lds) !=
+            hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        per_cu < 1 || cus < 1)
+      return 1024;
+    cache[dev] = (int64_t)per_cu * cus;
+  }
+  return cache[dev];
 }
 
 template <int NT, bool GB, bool VF>
@@ -974,12 +1148,54 @@ hipError_t launch_select(const StepParams& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int NT, bool PB, bool VF, bool EXPORT>
-hipError_t launch_update(const StepParams& p, int64_t first_block, int64_t blocks, float* mh, float* vh,
+// Chunks of 64 window entries the update's leader wave processes per block:
+// the live rows of a full block rounded up to a multiple of 4 (at most 16).
+inline int chunk_class(const StepParams& p) {
+  const int R = (p.k_full + kWave - 1) / kWave;
+  const int nch = p.n_live * R;
+  return nch <= 4 ? 4 : nch <= 8 ? 8 : nch <= 12 ? 12 : 16;
+}
+
+template <int NT, bool PB, bool VF, int KC>
+void launch_update_run(const StepParams& p, int64_t grid, int64_t per, size_t lds, hipStream_t stream) {
+  hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, true, KC>), dim3((uint32_t)grid), dim3(NT), lds, stream, p,
+                     (int64_t)0, p.n_full, per, (float*)nullptr, (float*)nullptr);
+}
+
+// The full blocks [0, n_full) in persistent runs, then the ragged blocks one
+// workgroup each.
+template <int NT, bool PB, bool VF>
+hipError_t launch_update(const StepParams& p, hipStream_t stream) {
+  const size_t lds = update_lds_bytes<NT, VF>();
+  if (p.n_full > 0) {
+    int64_t grid = update_grid<NT, PB, VF>(lds);
+    if (grid > p.n_full) grid = p.n_full;
+    const int64_t per = (p.n_full + grid - 1) / grid;
+    grid = (p.n_full + per - 1) / per;
+    switch (chunk_class(p)) {
+      case 4: launch_update_run<NT, PB, VF, 4>(p, grid, per, lds, stream); break;
+      case 8: launch_update_run<NT, PB, VF, 8>(p, grid, per, lds, stream); break;
+      case 12: launch_update_run<NT, PB, VF, 12>(p, grid, per, lds, stream); break;
+      default: launch_update_run<NT, PB, VF, 16>(p, grid, per, lds, stream); break;
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int64_t tails = p.total_blocks - p.n_full;
+  if (tails > 0) {
+    hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, false, 16>), dim3((uint32_t)tails), dim3(NT), lds, stream,
+                       p, p.n_full, tails, (int64_t)1, (float*)nullptr, (float*)nullptr);
+    return hipGetLastError();
+  }
+  return hipSuccess;
+}
+
+template <int NT, bool VF>
+hipError_t launch_export(const StepParams& p, int64_t first_block, int64_t blocks, float* mh, float* vh,
                          hipStream_t stream) {
-  const size_t lds = (size_t)2 * NT * kLaneElems * 4;
-  hipLaunchKernelGGL((update_kernel<NT, PB, VF, EXPORT>), dim3((uint32_t)blocks), dim3(NT), lds, stream, p,
-                     first_block, mh, vh);
+  const size_t lds = update_lds_bytes<NT, VF>();
+  hipLaunchKernelGGL((update_kernel<NT, false, VF, true, false, 16>), dim3((uint32_t)blocks), dim3(NT), lds, stream,
+                     p, first_block, blocks, (int64_t)1, mh, vh);
   return hipGetLastError();
 }
 
@@ -989,10 +1205,8 @@ hipError_t launch_step_nt(const StepParams& p, int pb, int gb, int vf, hipStream
   if (gb) e = vf ? launch_select<NT, true, true>(p, stream) : launch_select<NT, true, false>(p, stream);
   else e = vf ? launch_select<NT, false, true>(p, stream) : launch_select<NT, false, false>(p, stream);
   if (e != hipSuccess) return e;
-  if (pb) return vf ? launch_update<NT, true, true, false>(p, 0, p.total_blocks, nullptr, nullptr, stream)
-                    : launch_update<NT, true, false, false>(p, 0, p.total_blocks, nullptr, nullptr, stream);
-  return vf ? launch_update<NT, false, true, false>(p, 0, p.total_blocks, nullptr, nullptr, stream)
-            : launch_update<NT, false, false, false>(p, 0, p.total_blocks, nullptr, nullptr, stream);
+  if (pb) return vf ? launch_update<NT, true, true>(p, stream) : launch_update<NT, true, false>(p, stream);
+  return vf ? launch_update<NT, false, true>(p, stream) : launch_update<NT, false, false>(p, stream);
 }
 
 }  // namespace
@@ -1002,7 +1216,7 @@ size_t step_lds_bytes(int block, int k_full, int value_f32) {
   (void)value_f32;
   const int nt = threads_for_block(block);
   const size_t sel = (nt == 64 ? SelectLds<64>::words() : SelectLds<256>::words()) * 4;
-  const size_t upd = (size_t)2 * nt * kLaneElems * 4;
+  const size_t upd = nt == 64 ? update_lds_bytes<64, true>() : update_lds_bytes<256, true>();
   return sel > upd ? sel : upd;
 }
 
@@ -1015,10 +1229,10 @@ hipError_t launch_step(const StepParams& p, int param_bf16, int grad_bf16, int v
 hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_blocks, float* mhat,
                           float* vhat, int value_f32, hipStream_t stream) {
   if (threads_for_block(p.block) == 64)
-    return value_f32 ? launch_update<64, false, true, true>(p, first_block, num_blocks, mhat, vhat, stream)
-                     : launch_update<64, false, false, true>(p, first_block, num_blocks, mhat, vhat, stream);
-  return value_f32 ? launch_update<256, false, true, true>(p, first_block, num_blocks, mhat, vhat, stream)
-                   : launch_update<256, false, false, true>(p, first_block, num_blocks, mhat, vhat, stream);
+    return value_f32 ? launch_export<64, true>(p, first_block, num_blocks, mhat, vhat, stream)
+                     : launch_export<64, false>(p, first_block, num_blocks, mhat, vhat, stream);
+  return value_f32 ? launch_export<256, true>(p, first_block, num_blocks, mhat, vhat, stream)
+                   : launch_export<256, false>(p, first_block, num_blocks, mhat, vhat, stream);
 }
 
 }  // namespace microadam

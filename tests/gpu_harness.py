@@ -103,28 +103,39 @@ class GpuOracleRun:
     def _read(self, off, nbytes) -> np.ndarray:
         return self.opt.state_view[off:off + nbytes].cpu().numpy()
 
-    def gpu_codes(self, u: Unit) -> np.ndarray:
+    def _block_elems(self, lay, q: int) -> int:
+        return min(self.block, lay.numel - q * self.block)
+
+    def gpu_codes(self, u: Unit):
+        """Codes of the unit's elements and the raw bytes of its last block."""
         lay = self.opt.layout(u.j)
-        b0 = u.e0 // 2
-        raw = self._read(lay.ef_offset + b0, (u.e1 - u.e0 + 1) // 2)
-        c = np.empty(2 * raw.size, np.uint8)
-        c[0::2] = raw & 0x0F
-        c[1::2] = raw >> 4
-        return c[: u.e1 - u.e0], raw
+        parts, raw = [], None
+        for q in range(u.q0, u.q1):
+            n = self._block_elems(lay, q)
+            raw = self._read(lay.ef_plane + lay.block_number(q) * lay.ef_stride, (n + 1) // 2)
+            c = np.empty(2 * raw.size, np.uint8)
+            c[0::2] = raw & 0x0F
+            c[1::2] = raw >> 4
+            parts.append(c[:n])
+        return np.concatenate(parts), raw
 
     def gpu_stats(self, u: Unit):
         lay = self.opt.layout(u.j)
-        nb0 = u.e0 // self.bucket
-        nb = -(-(u.e1 - u.e0) // self.bucket)
-        raw = self._read(lay.stats_offset + 8 * nb0, 8 * nb).view(np.float32).reshape(nb, 2)
-        return raw[:, 0].copy(), raw[:, 1].copy()
+        lo, hi = [], []
+        for q in range(u.q0, u.q1):
+            nb = -(-self._block_elems(lay, q) // self.bucket)
+            off = lay.stats_plane + lay.block_number(q) * lay.stats_stride
+            raw = self._read(off, 8 * nb).view(np.float32).reshape(nb, 2)
+            lo.append(raw[:, 0])
+            hi.append(raw[:, 1])
+        return np.concatenate(lo), np.concatenate(hi)
 
     def gpu_row(self, u: Unit, q: int, slot: int):
         """(indices, values) of block q (tensor-relative) in row slot `slot`."""
         lay = self.opt.layout(u.j)
         kq = lay.k_last if q == lay.num_blocks - 1 else lay.k_full
         eb = lay.entry_bytes
-        off = lay.window_offset + (q * self.window * lay.k_full + slot * kq) * eb
+        off = lay.window_plane + lay.block_number(q) * lay.window_stride + slot * kq * eb
         raw = self._read(off, kq * eb)
         if eb == 4:
             w = raw.view(np.uint32)
