@@ -5,18 +5,21 @@ Default workload: the Llama-2-7B parameter list (291 tensors, 6,738,415,616
 bf16 parameters), bf16 gradients 1e-3 * Student-t(4), Top-K block 4096 at
 density 1% (k = 41), window m = 10, 4-bit EF with bucket 64, lr 1e-4.
 
-One step = one call of microadam_step over all 291 tensors (one kernel
-launch).  The W warm-up steps fill the window (W >= m gives steady state);
-the K timed steps run back to back, bracketed by device synchronisation.
-Inputs are resident in HBM before timing starts: two gradient sets are
-generated up front and alternate between steps.
+One step = one call of microadam_step over all 291 tensors: two kernel
+launches, select (EF decode, block Top-K, new window row, EF re-quantisation)
+then update (moment rebuild from the window, parameter update).  The W
+warm-up steps fill the window (W >= m gives steady state); the K timed steps
+run back to back, bracketed by device synchronisation.  Inputs are resident
+in HBM before timing starts: two gradient sets are generated up front and
+alternate between steps.
 
-Prints one JSON line.  `roofline.achieved` is the algorithmic HBM bytes of
-one launch (see step_bytes) over the mean kernel duration, timed with HIP
-events on the launch stream.  `roofline.traffic` comes from the committed
-rocprofv3 FETCH_SIZE / WRITE_SIZE summary when it was taken on the current
-kernel source, else null.  `cpu_baseline` times the CPU oracle on a sample
-of the same workload's blocks on this host.
+Prints one JSON line.  `roofline` describes the dominant (longer) kernel:
+`achieved` is its algorithmic HBM bytes per launch (select_bytes /
+update_bytes) over its mean duration, timed with HIP events that the library
+records on the launch stream around each kernel.  `traffic` comes from the
+committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary of that kernel when it
+was taken on the current kernel source, else null.  `cpu_baseline` times the
+CPU oracle on a sample of the same workload's blocks on this host.
 """
 from __future__ import annotations
 
@@ -35,7 +38,7 @@ METRIC = "MicroAdam step params/sec + achieved HBM GB/s (% peak), Llama-2-7B sha
 HBM_PEAK_GBS = 8000.0
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2405_15593_amd", "csrc", f)
                   for f in ("microadam_kernels.hip", "microadam_device.h")]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_step_kernel_llama2_7b_bf16.txt")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_source_hash() -> str:
@@ -49,30 +52,49 @@ def block_k(s: int, density: float) -> int:
     return min(s, max(1, math.ceil(density * s - 1e-9)))
 
 
-def step_bytes(w, t: int) -> int:
-    """Algorithmic HBM bytes of step t: gradient read, parameter read and
-    write, EF codes read and write (ceil(n/2) B), bucket (delta, Delta) read and
-    write (8 B per bucket), one window row written and min(t, m) - 1 older rows
-    read (4 B per bf16 entry)."""
+def _blocks(w, n):
+    nb = -(-n // w.block)
+    k_total = (nb - 1) * block_k(w.block, w.density) + block_k(n - (nb - 1) * w.block, w.density)
+    return nb, k_total
+
+
+def select_bytes(w) -> int:
+    """Algorithmic HBM bytes of one select launch: gradient read, EF codes
+    read and written (ceil(n/2) B each way), bucket (delta, Delta) read and
+    written (8 B per bucket each way), one window row written (4 B per kept
+    bf16 entry)."""
     sg = w.grad_dtype.itemsize
-    sp = w.param_dtype.itemsize
-    rows_read = min(t, w.window) - 1
     total = 0
     for n in w.numels:
-        nb = -(-n // w.block)
-        k_total = (nb - 1) * block_k(w.block, w.density) + block_k(n - (nb - 1) * w.block, w.density)
-        total += n * sg + 2 * n * sp + 2 * ((n + 1) // 2) + 2 * 8 * (-(-n // w.bucket))
-        total += 4 * k_total * (1 + rows_read)
+        _, k_total = _blocks(w, n)
+        total += n * sg + 2 * ((n + 1) // 2) + 2 * 8 * (-(-n // w.bucket)) + 4 * k_total
     return total
 
 
-def read_traffic():
+def update_bytes(w, t: int) -> int:
+    """Algorithmic HBM bytes of one update launch at step t: parameters read
+    and written, min(t, m) window rows read (4 B per bf16 entry)."""
+    sp = w.param_dtype.itemsize
+    rows = min(t, w.window)
+    total = 0
+    for n in w.numels:
+        _, k_total = _blocks(w, n)
+        total += 2 * n * sp + 4 * k_total * rows
+    return total
+
+
+def step_bytes(w, t: int) -> int:
+    return select_bytes(w) + update_bytes(w, t)
+
+
+def read_traffic(kernel: str, workload: str):
     """(fetch+write bytes per launch, note) from the committed rocprofv3 summary
-    if it matches the current kernel source, else (None, reason)."""
-    if not os.path.exists(TRAFFIC_FILE):
-        return None, "no traffic summary"
+    of `kernel` if it matches the current kernel source, else (None, reason)."""
+    path = os.path.join(PROFILES, f"traffic_{kernel}_{workload}.txt")
+    if not os.path.exists(path):
+        return None, f"no traffic summary {os.path.basename(path)}"
     kv = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
@@ -86,9 +108,10 @@ def read_traffic():
 
 def cpu_baseline(w, blocks: int, seed: int = 0) -> dict:
     """The CPU oracle (single-threaded, as it stands) on `blocks` Top-K blocks
-    of the workload's shape, run to steady state (m + 2 steps); the last two
-    steps are timed."""
+    of the workload's shape, run for m + 2 steps; the last three steps (window
+    full) are timed."""
     import numpy as np
+    import torch
     import oracle
     o = oracle.default()
     n = blocks * w.block
@@ -96,22 +119,22 @@ def cpu_baseline(w, blocks: int, seed: int = 0) -> dict:
                   value_bf16=True, param_bf16=True)
     rng = np.random.default_rng(seed)
     theta = (rng.standard_normal(n) * w.param_std).astype(np.float32)
-    import torch
     theta = torch.from_numpy(theta).to(torch.bfloat16).float().numpy()
-    timed = 0.0
     steps = w.window + 2
+    timed_steps = 3
+    timed = 0.0
     for t in range(1, steps + 1):
         g = (rng.standard_t(4, n) * w.grad_scale).astype(np.float32)
         g = torch.from_numpy(g).to(torch.bfloat16).float().numpy()
         t0 = time.perf_counter()
         st.step(theta, g, t, w.lr)
         dt = time.perf_counter() - t0
-        if t > steps - 2:
+        if t > steps - timed_steps:
             timed += dt
-    rate = 2 * n / timed
+    rate = timed_steps * n / timed
     return {"value": rate, "unit": "params/s", "cores": 1, "kind": "oracle",
-            "sample": (f"{blocks} blocks of {w.block} ({n} params), bf16, steps {steps - 1}-{steps} "
-                       f"(window full) timed, {timed:.2f} s")}
+            "sample": (f"{blocks} blocks of {w.block} ({n} params) of the same shape, bf16, steps "
+                       f"{steps - timed_steps + 1}-{steps} (window full) timed: {timed:.2f} s")}
 
 
 def main() -> int:
@@ -120,7 +143,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama2_7b_bf16")
-    ap.add_argument("--cpu-blocks", type=int, default=4000, help="0 disables the CPU baseline")
+    ap.add_argument("--cpu-blocks", type=int, default=10000, help="0 disables the CPU baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device-to-device copy three times (the known-size "
                          "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
@@ -156,31 +179,35 @@ def main() -> int:
     cfg = ma.make_config(density=w.density, window=w.window, ef_bucket=w.bucket,
                          topk_block=w.block, lr=w.lr)
     opt = ma.MicroAdam(params, cfg)
-    stream = torch.cuda.current_stream(dev)
 
     for i in range(args.warmup):
         opt.step(grad_sets[i % 2])
     torch.cuda.synchronize()
     print(f"[bench] warm-up done (t={opt.t})", file=sys.stderr, flush=True)
 
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    opt.set_profiling(True)
     t_first = opt.t + 1
+    kernel_ms = []
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     for i in range(args.steps):
-        starts[i].record(stream)
         opt.step(grad_sets[(args.warmup + i) % 2])
-        ends[i].record(stream)
+        kernel_ms.append(opt.kernel_times())
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    kernel_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    mean_kernel_s = sum(kernel_ms) / len(kernel_ms) / 1e3
-    nbytes = [step_bytes(w, t) for t in range(t_first, t_first + args.steps)]
-    bytes_per_launch = sum(nbytes) / len(nbytes)
-    achieved = bytes_per_launch / mean_kernel_s / 1e9
-    traffic, traffic_note = read_traffic()
-    print(f"[bench] kernel ms per step: {[round(x, 3) for x in kernel_ms]}", file=sys.stderr, flush=True)
+    sel_ms = sum(k[0] for k in kernel_ms) / len(kernel_ms)
+    upd_ms = sum(k[1] for k in kernel_ms) / len(kernel_ms)
+    sel_b = select_bytes(w)
+    upd_b = sum(update_bytes(w, t) for t in range(t_first, t_first + args.steps)) / args.steps
+    kernels = {
+        "select_kernel": {"ms": sel_ms, "bytes": sel_b, "gbs": sel_b / sel_ms / 1e6},
+        "update_kernel": {"ms": upd_ms, "bytes": upd_b, "gbs": upd_b / upd_ms / 1e6},
+    }
+    dominant = max(kernels, key=lambda k: kernels[k]["ms"])
+    dk = kernels[dominant]
+    traffic, traffic_note = read_traffic(dominant, w.name)
+    print(f"[bench] kernel ms per step (select, update): "
+          f"{[(round(a, 3), round(b, 3)) for a, b in kernel_ms]}", file=sys.stderr, flush=True)
 
     cpu = None
     if args.cpu_blocks > 0:
@@ -210,16 +237,17 @@ def main() -> int:
             "ef_bits": 4, "ef_bucket": w.bucket, "steps_timed": [t_first, t_first + args.steps - 1],
             "window_full": t_first > w.window,
         },
-        "kernel_ms_mean": mean_kernel_s * 1e3,
-        "hbm_gbs": achieved,
+        "kernels": kernels,
+        "step_hbm_gbs": (sel_b + upd_b) / (sel_ms + upd_ms) / 1e6,
         "roofline": {
             "bound": "hbm",
-            "achieved": achieved,
+            "kernel": dominant,
+            "achieved": dk["gbs"],
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
+            "frac": dk["gbs"] / HBM_PEAK_GBS,
             "traffic": traffic,
-            "algorithmic_bytes_per_launch": bytes_per_launch,
+            "algorithmic_bytes_per_launch": dk["bytes"],
             "traffic_note": traffic_note,
         },
         "cpu_baseline": cpu,

@@ -196,6 +196,23 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat,
                             float* vhat, void* stream);
 
 /* Static name of an error code. */
+/*
+ * Profiling.  With profiling on (off after init), every microadam_step
+ * records HIP events on its stream around its two kernels.  Events are
+ * created on the first call that turns profiling on, with the init device
+ * current.
+ */
+int microadam_set_profiling(microadam_handle h, int32_t on);
+
+/*
+ * Durations in milliseconds of the kernels of the last step, which must have
+ * been taken with profiling on: out_ms[0] = select (EF decode, block Top-K,
+ * new window row, EF re-quantisation), out_ms[1] = update (moment rebuild
+ * from the window and parameter update).  Blocks until that step is done.
+ * out_ms: 2 host floats.
+ */
+int microadam_kernel_times(microadam_handle h, float* out_ms);
+
 const char* microadam_error_string(int code);
 
 /* The calling thread's most recent error message ("" if none). */

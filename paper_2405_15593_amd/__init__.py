@@ -75,7 +75,8 @@ class microadam_layout(ctypes.Structure):
 EXPORTS = (
     "microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
     "microadam_get_step", "microadam_set_step", "microadam_tensor_layout",
-    "microadam_debug_moments", "microadam_error_string", "microadam_last_error",
+    "microadam_debug_moments", "microadam_set_profiling", "microadam_kernel_times",
+    "microadam_error_string", "microadam_last_error",
 )
 
 
@@ -107,12 +108,15 @@ def load(path: str = LIBRARY):
     lib.microadam_set_step.argtypes = [vp, i64]
     lib.microadam_tensor_layout.argtypes = [vp, i32, P(microadam_layout)]
     lib.microadam_debug_moments.argtypes = [vp, i32, vp, vp, vp]
+    lib.microadam_set_profiling.argtypes = [vp, i32]
+    lib.microadam_kernel_times.argtypes = [vp, P(ctypes.c_float)]
     lib.microadam_error_string.argtypes = [ctypes.c_int]
     lib.microadam_error_string.restype = ctypes.c_char_p
     lib.microadam_last_error.argtypes = []
     lib.microadam_last_error.restype = ctypes.c_char_p
     for f in ("microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
-              "microadam_set_step", "microadam_tensor_layout", "microadam_debug_moments"):
+              "microadam_set_step", "microadam_tensor_layout", "microadam_debug_moments",
+              "microadam_set_profiling", "microadam_kernel_times"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -191,6 +195,17 @@ def microadam_debug_moments(h: int, tensor: int, mhat_ptr: int, vhat_ptr: int, s
            "microadam_debug_moments")
 
 
+def microadam_set_profiling(h: int, on: bool) -> None:
+    _check(load().microadam_set_profiling(ctypes.c_void_p(h), 1 if on else 0), "microadam_set_profiling")
+
+
+def microadam_kernel_times(h: int) -> tuple:
+    """(select ms, update ms) of the last profiled step."""
+    out = (ctypes.c_float * 2)()
+    _check(load().microadam_kernel_times(ctypes.c_void_p(h), out), "microadam_kernel_times")
+    return float(out[0]), float(out[1])
+
+
 def microadam_error_string(code: int) -> str:
     return load().microadam_error_string(code).decode()
 
@@ -264,6 +279,13 @@ class MicroAdam:
         v = torch.empty(n, dtype=torch.float32, device=self.device)
         microadam_debug_moments(self.handle, j, m.data_ptr(), v.data_ptr(), self._stream())
         return m, v
+
+    def set_profiling(self, on: bool = True) -> None:
+        microadam_set_profiling(self.handle, on)
+
+    def kernel_times(self) -> tuple:
+        """(select ms, update ms) of the last step taken with profiling on."""
+        return microadam_kernel_times(self.handle)
 
     def close(self) -> None:
         if self.handle is not None:

@@ -172,6 +172,9 @@ struct microadam_handle_s {
   uint64_t use_clock = 0;
   int current = -1;                   // slot used by the last step
   hipEvent_t step_done = nullptr;     // last launch of this handle finished
+  bool profiling = false;
+  bool timed = false;                 // the last step recorded kernel events
+  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};  // select start, update start, end
 };
 
 namespace {
@@ -190,6 +193,8 @@ void release(microadam_handle h) {
     if (t.d) (void)hipFree(t.d);
     if (t.h) (void)hipHostFree(t.h);
   }
+  for (hipEvent_t& e : h->ev)
+    if (e) (void)hipEventDestroy(e);
   if (h->d_block_tensor) (void)hipFree(h->d_block_tensor);
   if (h->d_wpow) (void)hipFree(h->d_wpow);
   delete h;
@@ -413,8 +418,14 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
   const int64_t t = h->t + 1;
   StepParams p;
   fill_constants(h, t, lr, p);
-  e = microadam::launch_step(p, h->param_bf16, h->grad_bf16, h->value_f32, s);
-  if (e != hipSuccess) return hip_fail(e, "launching the step kernel");
+  if (h->profiling && (e = hipEventRecord(h->ev[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  e = microadam::launch_select(p, h->grad_bf16, h->value_f32, s);
+  if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
+  if (h->profiling && (e = hipEventRecord(h->ev[1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  e = microadam::launch_update(p, h->param_bf16, h->value_f32, s);
+  if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
+  if (h->profiling && (e = hipEventRecord(h->ev[2], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  h->timed = h->profiling;
   if ((e = hipEventRecord(h->step_done, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   h->t = t;
   return MICROADAM_OK;
@@ -483,6 +494,34 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat, flo
   if (e == hipSuccess && tp.num_full < tp.num_blocks)
     e = microadam::launch_moments(p, tp.last_block, 1, mhat, vhat, h->value_f32, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "launching the moment kernel");
+  return MICROADAM_OK;
+}
+
+int microadam_set_profiling(microadam_handle h, int32_t on) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (on && !h->ev[0]) {
+    rc = check_device(h);
+    if (rc) return rc;
+    for (hipEvent_t& e : h->ev) {
+      const hipError_t err = hipEventCreate(&e);
+      if (err != hipSuccess) return hip_fail(err, "hipEventCreate");
+    }
+  }
+  h->profiling = on != 0;
+  return MICROADAM_OK;
+}
+
+int microadam_kernel_times(microadam_handle h, float* out_ms) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!out_ms) return fail(MICROADAM_ERR_INVALID_ARG, "out_ms is NULL");
+  if (!h->timed) return fail(MICROADAM_ERR_INVALID_ARG, "the last step was not profiled");
+  hipError_t e;
+  if ((e = hipEventSynchronize(h->ev[2])) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  if ((e = hipEventElapsedTime(&out_ms[0], h->ev[0], h->ev[1])) != hipSuccess ||
+      (e = hipEventElapsedTime(&out_ms[1], h->ev[1], h->ev[2])) != hipSuccess)
+    return hip_fail(e, "hipEventElapsedTime");
   return MICROADAM_OK;
 }
 

@@ -57,9 +57,9 @@ struct StepParams {
 };
 
 // Launchers (defined in microadam_kernels.hip).  Return hipSuccess or the
-// launch error.
-hipError_t launch_step(const StepParams& p, int param_bf16, int grad_bf16, int value_f32,
-                       hipStream_t stream);
+// launch error.  A step is launch_select, then launch_update, on one stream.
+hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream);
+hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, hipStream_t stream);
 
 hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_blocks,
                           float* mhat, float* vhat, int value_f32, hipStream_t stream);

@@ -1142,7 +1142,7 @@ int64_t update_grid(size_t lds) {
 }
 
 template <int NT, bool GB, bool VF>
-hipError_t launch_select(const StepParams& p, hipStream_t stream) {
+hipError_t launch_select_t(const StepParams& p, hipStream_t stream) {
   const size_t lds = SelectLds<NT>::words() * 4;
   hipLaunchKernelGGL((select_kernel<NT, GB, VF>), dim3((uint32_t)p.total_blocks), dim3(NT), lds, stream, p);
   return hipGetLastError();
@@ -1165,7 +1165,7 @@ void launch_update_run(const StepParams& p, int64_t grid, int64_t per, size_t ld
 // The full blocks [0, n_full) in persistent runs, then the ragged blocks one
 // workgroup each.
 template <int NT, bool PB, bool VF>
-hipError_t launch_update(const StepParams& p, hipStream_t stream) {
+hipError_t launch_update_t(const StepParams& p, hipStream_t stream) {
   const size_t lds = update_lds_bytes<NT, VF>();
   if (p.n_full > 0) {
     int64_t grid = update_grid<NT, PB, VF>(lds);
@@ -1199,16 +1199,6 @@ hipError_t launch_export(const StepParams& p, int64_t first_block, int64_t block
   return hipGetLastError();
 }
 
-template <int NT>
-hipError_t launch_step_nt(const StepParams& p, int pb, int gb, int vf, hipStream_t stream) {
-  hipError_t e;
-  if (gb) e = vf ? launch_select<NT, true, true>(p, stream) : launch_select<NT, true, false>(p, stream);
-  else e = vf ? launch_select<NT, false, true>(p, stream) : launch_select<NT, false, false>(p, stream);
-  if (e != hipSuccess) return e;
-  if (pb) return vf ? launch_update<NT, true, true>(p, stream) : launch_update<NT, true, false>(p, stream);
-  return vf ? launch_update<NT, false, true>(p, stream) : launch_update<NT, false, false>(p, stream);
-}
-
 }  // namespace
 
 size_t step_lds_bytes(int block, int k_full, int value_f32) {
@@ -1220,10 +1210,22 @@ size_t step_lds_bytes(int block, int k_full, int value_f32) {
   return sel > upd ? sel : upd;
 }
 
-hipError_t launch_step(const StepParams& p, int param_bf16, int grad_bf16, int value_f32,
-                       hipStream_t stream) {
-  if (threads_for_block(p.block) == 64) return launch_step_nt<64>(p, param_bf16, grad_bf16, value_f32, stream);
-  return launch_step_nt<256>(p, param_bf16, grad_bf16, value_f32, stream);
+hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream) {
+  if (threads_for_block(p.block) == 64) {
+    if (grad_bf16) return value_f32 ? launch_select_t<64, true, true>(p, stream) : launch_select_t<64, true, false>(p, stream);
+    return value_f32 ? launch_select_t<64, false, true>(p, stream) : launch_select_t<64, false, false>(p, stream);
+  }
+  if (grad_bf16) return value_f32 ? launch_select_t<256, true, true>(p, stream) : launch_select_t<256, true, false>(p, stream);
+  return value_f32 ? launch_select_t<256, false, true>(p, stream) : launch_select_t<256, false, false>(p, stream);
+}
+
+hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, hipStream_t stream) {
+  if (threads_for_block(p.block) == 64) {
+    if (param_bf16) return value_f32 ? launch_update_t<64, true, true>(p, stream) : launch_update_t<64, true, false>(p, stream);
+    return value_f32 ? launch_update_t<64, false, true>(p, stream) : launch_update_t<64, false, false>(p, stream);
+  }
+  if (param_bf16) return value_f32 ? launch_update_t<256, true, true>(p, stream) : launch_update_t<256, true, false>(p, stream);
+  return value_f32 ? launch_update_t<256, false, true>(p, stream) : launch_update_t<256, false, false>(p, stream);
 }
 
 hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_blocks, float* mhat,
