@@ -456,12 +456,14 @@ __global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
       }
     }
   }
+  // elements of this thread below the end of the block: [0, rem)
+  const int rem = s - (int)eb;
   if (!full) {  // elements past the end of the tensor are 0 and never kept
 #pragma unroll
     for (int v = 0; v < 2; ++v)
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if ((int)(eb + v * 8 + e) >= s) a[v][e] = 0.0f;
+        if (v * 8 + e >= rem) a[v][e] = 0.0f;
   }
 
   // ---------------------------------------------- 2. Top-K threshold
@@ -756,12 +758,14 @@ __global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) x[v][e] = (__builtin_fabsf(a[v][e]) >= Tf) ? 0.0f : a[v][e];
   } else {
+    // this thread's elements up to index i_last: [0, last_here]
+    const int last_here = (int)i_last - (int)eb;
 #pragma unroll
     for (int v = 0; v < 2; ++v)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float ab = __builtin_fabsf(a[v][e]);
-        const bool kept = (ab > Tf) | ((ab == Tf) & (eb + v * 8 + e <= i_last));
+        const bool kept = (ab > Tf) | ((ab == Tf) & (v * 8 + e <= last_here));
         x[v][e] = kept ? 0.0f : a[v][e];
       }
   }
@@ -779,7 +783,7 @@ __global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
       mx[v] = -__builtin_inff();
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if ((int)(eb + v * 8 + e) < s) { mn[v] = __builtin_fminf(mn[v], x[v][e]); mx[v] = __builtin_fmaxf(mx[v], x[v][e]); }
+        if (v * 8 + e < rem) { mn[v] = __builtin_fminf(mn[v], x[v][e]); mx[v] = __builtin_fmaxf(mx[v], x[v][e]); }
     }
   }
   if (!pair_buckets) {
@@ -835,7 +839,7 @@ __global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
     if (!full) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if ((int)(eb + v * 8 + e) >= s) wv &= ~(0xFu << (4 * e));
+        if (v * 8 + e >= rem) wv &= ~(0xFu << (4 * e));
     }
     w[v] = wv;
   }
@@ -916,7 +920,17 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
   const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
   const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
 
+  // this thread's 16 words of each accumulator
+  auto zero_own = [&](float* a1, float* a2) {
+    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      *(float4*)(a1 + q * 4 * NT + tid * 4) = zero;
+      *(float4*)(a2 + q * 4 * NT + tid * 4) = zero;
+    }
+  };
   if (tid == 0) stage[2 * NT] = E::none();
+  if (RUN) zero_own(z1, z2);
   Cursor cursor = {0, 0, 0};
   auto fetch = [&](int32_t gb, UB& u) {
     u.g = RUN ? seek_full(p, cursor, gb, PBF16 ? 2 : 4) : span_of(p, gb, PBF16 ? 2 : 4);
@@ -937,16 +951,12 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
     const int leader = u.g.gb & (NW - 1);
     const int R = (kq + kWave - 1) / kWave;
     const bool staged = n_live * kq <= 2 * NT && n_live * R <= kChunks;
-    {
-      const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        *(float4*)(z1 + q * 4 * NT + tid * 4) = zero;
-        *(float4*)(z2 + q * 4 * NT + tid * 4) = zero;
-      }
-      stage[tid] = u.w[0];
-      stage[tid + NT] = u.w[1];
-    }
+    // In a run the accumulators are clean when a block starts: the θ pass
+    // clears z1 behind it and the leader clears the z2 words it used.  A
+    // workgroup that takes one block starts from uninitialised LDS.
+    if (!RUN) zero_own(z1, z2);
+    stage[tid] = u.w[0];
+    stage[tid + NT] = u.w[1];
     lds_sync();
 
     if (wave == leader) {
@@ -1006,7 +1016,10 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
 #pragma unroll
           for (int c = 0; c < kChunks; ++c) d[c] = step_of(z1[zp[c]], z2[zp[c]]);
 #pragma unroll
-          for (int c = 0; c < kChunks; ++c) z1[zp[c]] = d[c];
+          for (int c = 0; c < kChunks; ++c) {
+            z1[zp[c]] = d[c];
+            z2[zp[c]] = 0.0f;
+          }
         }
       } else {
         const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, u.g.gb, kq);
@@ -1071,6 +1084,16 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
       const uint32_t e0 = eb + v * 8;   // vectors past s store nothing
       const float4 u0 = *(const float4*)(z1 + (2 * v) * 4 * NT + tid * 4);
       const float4 u1 = *(const float4*)(z1 + (2 * v + 1) * 4 * NT + tid * 4);
+      if (RUN) {
+        // clear behind the read; the unstaged path leaves marks in z2 too
+        const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+        *(float4*)(z1 + (2 * v) * 4 * NT + tid * 4) = zero;
+        *(float4*)(z1 + (2 * v + 1) * 4 * NT + tid * 4) = zero;
+        if (!staged) {
+          *(float4*)(z2 + (2 * v) * 4 * NT + tid * 4) = zero;
+          *(float4*)(z2 + (2 * v + 1) * 4 * NT + tid * 4) = zero;
+        }
+      }
       const float upd[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
       float thf[8], out[8];
       unpack8<PBF16>(u.th[v], thf);
@@ -1149,11 +1172,11 @@ hipError_t launch_select_t(const StepParams& p, hipStream_t stream) {
 }
 
 // Chunks of 64 window entries the update's leader wave processes per block:
-// the live rows of a full block rounded up to a multiple of 4 (at most 16).
+// the live rows of a full block rounded up to 4, 8, 10, 12 or 16.
 inline int chunk_class(const StepParams& p) {
   const int R = (p.k_full + kWave - 1) / kWave;
   const int nch = p.n_live * R;
-  return nch <= 4 ? 4 : nch <= 8 ? 8 : nch <= 12 ? 12 : 16;
+  return nch <= 4 ? 4 : nch <= 8 ? 8 : nch <= 10 ? 10 : nch <= 12 ? 12 : 16;
 }
 
 template <int NT, bool PB, bool VF, int KC>
@@ -1175,6 +1198,7 @@ hipError_t launch_update_t(const StepParams& p, hipStream_t stream) {
     switch (chunk_class(p)) {
       case 4: launch_update_run<NT, PB, VF, 4>(p, grid, per, lds, stream); break;
       case 8: launch_update_run<NT, PB, VF, 8>(p, grid, per, lds, stream); break;
+      case 10: launch_update_run<NT, PB, VF, 10>(p, grid, per, lds, stream); break;
       case 12: launch_update_run<NT, PB, VF, 12>(p, grid, per, lds, stream); break;
       default: launch_update_run<NT, PB, VF, 16>(p, grid, per, lds, stream); break;
     }
