@@ -144,6 +144,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama2_7b_bf16")
     ap.add_argument("--cpu-blocks", type=int, default=10000, help="0 disables the CPU baseline")
+    ap.add_argument("--ranges", type=int, default=1,
+                    help="block ranges per step (each range's update overlaps the next selects)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device-to-device copy three times (the known-size "
                          "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
@@ -179,6 +181,7 @@ def main() -> int:
     cfg = ma.make_config(density=w.density, window=w.window, ef_bucket=w.bucket,
                          topk_block=w.block, lr=w.lr)
     opt = ma.MicroAdam(params, cfg)
+    opt.set_ranges(args.ranges)
 
     for i in range(args.warmup):
         opt.step(grad_sets[i % 2])
@@ -235,7 +238,7 @@ def main() -> int:
             "grad_dist": w.grad_dist, "topk_block": w.block, "density": w.density,
             "k_per_block": block_k(w.block, w.density), "window": w.window,
             "ef_bits": 4, "ef_bucket": w.bucket, "steps_timed": [t_first, t_first + args.steps - 1],
-            "window_full": t_first > w.window,
+            "window_full": t_first > w.window, "ranges": args.ranges,
         },
         "kernels": kernels,
         "step_hbm_gbs": (sel_b + upd_b) / (sel_ms + upd_ms) / 1e6,

@@ -208,10 +208,26 @@ int microadam_set_profiling(microadam_handle h, int32_t on);
  * Durations in milliseconds of the kernels of the last step, which must have
  * been taken with profiling on: out_ms[0] = select (EF decode, block Top-K,
  * new window row, EF re-quantisation), out_ms[1] = update (moment rebuild
- * from the window and parameter update).  Blocks until that step is done.
- * out_ms: 2 host floats.
+ * from the window and parameter update).  A step split into block ranges
+ * (microadam_set_ranges) reports the sum over its ranges of each kernel's
+ * launch durations; those of the two kernels then overlap in time.  Blocks
+ * until that step is done.  out_ms: 2 host floats.
  */
 int microadam_kernel_times(microadam_handle h, float* out_ms);
+
+/*
+ * Splits every following step into `ranges` consecutive ranges of Top-K
+ * blocks, 1 <= ranges <= 32 (1 after init).  The result of a step does not
+ * depend on it: blocks share no state, and the update of a block reads only
+ * what its own select wrote (Algorithm 1 works on each block alone).  With
+ * ranges > 1 the update of range i runs on a stream the library owns
+ * (created here on the first such call, with the init device current, at
+ * default priority) while the selects of the later ranges run on the step's
+ * stream; the step's stream waits for the last update, so work queued on it
+ * afterwards sees the whole step.  Errors: MICROADAM_ERR_INVALID_ARG for
+ * ranges out of bounds.
+ */
+int microadam_set_ranges(microadam_handle h, int32_t ranges);
 
 const char* microadam_error_string(int code);
 

@@ -76,7 +76,7 @@ EXPORTS = (
     "microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
     "microadam_get_step", "microadam_set_step", "microadam_tensor_layout",
     "microadam_debug_moments", "microadam_set_profiling", "microadam_kernel_times",
-    "microadam_error_string", "microadam_last_error",
+    "microadam_set_ranges", "microadam_error_string", "microadam_last_error",
 )
 
 
@@ -110,13 +110,14 @@ def load(path: str = LIBRARY):
     lib.microadam_debug_moments.argtypes = [vp, i32, vp, vp, vp]
     lib.microadam_set_profiling.argtypes = [vp, i32]
     lib.microadam_kernel_times.argtypes = [vp, P(ctypes.c_float)]
+    lib.microadam_set_ranges.argtypes = [vp, i32]
     lib.microadam_error_string.argtypes = [ctypes.c_int]
     lib.microadam_error_string.restype = ctypes.c_char_p
     lib.microadam_last_error.argtypes = []
     lib.microadam_last_error.restype = ctypes.c_char_p
     for f in ("microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
               "microadam_set_step", "microadam_tensor_layout", "microadam_debug_moments",
-              "microadam_set_profiling", "microadam_kernel_times"):
+              "microadam_set_profiling", "microadam_kernel_times", "microadam_set_ranges"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -206,6 +207,10 @@ def microadam_kernel_times(h: int) -> tuple:
     return float(out[0]), float(out[1])
 
 
+def microadam_set_ranges(h: int, ranges: int) -> None:
+    _check(load().microadam_set_ranges(ctypes.c_void_p(h), int(ranges)), "microadam_set_ranges")
+
+
 def microadam_error_string(code: int) -> str:
     return load().microadam_error_string(code).decode()
 
@@ -240,6 +245,7 @@ class MicroAdam:
         self.state_view = self.state[off:off + nbytes]
         self.grad_dtype = None
         self.handle = None
+        self.ranges = 1
 
     def _stream(self) -> int:
         import torch
@@ -254,6 +260,8 @@ class MicroAdam:
         self.handle = microadam_init(self.cfg, self.numels, self.param_dtype, self.grad_dtype,
                                      self.state_view.data_ptr(), self.state_view.numel(),
                                      self._stream())
+        if self.ranges != 1:
+            microadam_set_ranges(self.handle, self.ranges)
 
     def step(self, grads, lr: float | None = None) -> None:
         grads = list(grads)
@@ -286,6 +294,13 @@ class MicroAdam:
     def kernel_times(self) -> tuple:
         """(select ms, update ms) of the last step taken with profiling on."""
         return microadam_kernel_times(self.handle)
+
+    def set_ranges(self, ranges: int) -> None:
+        """Split each step into block ranges whose updates overlap the next
+        ranges' selects (same results); applied from the next step on."""
+        if self.handle is not None:
+            microadam_set_ranges(self.handle, ranges)
+        self.ranges = int(ranges)
 
     def close(self) -> None:
         if self.handle is not None:

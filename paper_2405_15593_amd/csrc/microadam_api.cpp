@@ -154,6 +154,7 @@ struct TableSlot {
 };
 
 constexpr int kTableSlots = 4;
+constexpr int kMaxRanges = 32;
 
 struct microadam_handle_s {
   microadam_config cfg;
@@ -173,8 +174,13 @@ struct microadam_handle_s {
   int current = -1;                   // slot used by the last step
   hipEvent_t step_done = nullptr;     // last launch of this handle finished
   bool profiling = false;
-  bool timed = false;                 // the last step recorded kernel events
-  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};  // select start, update start, end
+  int32_t timed = 0;                  // block ranges of the last step if it recorded events
+  // per block range: select start, select end, update start, update end
+  hipEvent_t ev[4 * kMaxRanges] = {};
+  int32_t ranges = 1;                 // block ranges a step is split into
+  hipStream_t aux = nullptr;          // runs the updates of a split step
+  hipEvent_t range_done[kMaxRanges] = {};  // select of range i finished
+  hipEvent_t aux_done = nullptr;      // every update of the last split step finished
 };
 
 namespace {
@@ -193,8 +199,15 @@ void release(microadam_handle h) {
     if (t.d) (void)hipFree(t.d);
     if (t.h) (void)hipHostFree(t.h);
   }
+  if (h->aux) {
+    (void)hipStreamSynchronize(h->aux);
+    (void)hipStreamDestroy(h->aux);
+  }
   for (hipEvent_t& e : h->ev)
     if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t& e : h->range_done)
+    if (e) (void)hipEventDestroy(e);
+  if (h->aux_done) (void)hipEventDestroy(h->aux_done);
   if (h->d_block_tensor) (void)hipFree(h->d_block_tensor);
   if (h->d_wpow) (void)hipFree(h->d_wpow);
   delete h;
@@ -418,14 +431,42 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
   const int64_t t = h->t + 1;
   StepParams p;
   fill_constants(h, t, lr, p);
-  if (h->profiling && (e = hipEventRecord(h->ev[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  e = microadam::launch_select(p, h->grad_bf16, h->value_f32, s);
-  if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
-  if (h->profiling && (e = hipEventRecord(h->ev[1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  e = microadam::launch_update(p, h->param_bf16, h->value_f32, s);
-  if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
-  if (h->profiling && (e = hipEventRecord(h->ev[2], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  h->timed = h->profiling;
+  const bool prof = h->profiling;
+  const int R = h->ranges;
+  auto rec = [&](int i, hipStream_t st) { return prof ? hipEventRecord(h->ev[i], st) : hipSuccess; };
+  if (R == 1) {
+    if ((e = rec(0, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    e = microadam::launch_select(p, h->grad_bf16, h->value_f32, 0, h->total_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
+    if ((e = rec(1, s)) != hipSuccess || (e = rec(2, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    e = microadam::launch_update(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
+    if ((e = rec(3, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  } else {
+    // Range i's update runs on the auxiliary stream after range i's select,
+    // beside the selects of the ranges after it; the caller's stream waits
+    // for the last update before anything it runs next.
+    auto first_of = [&](int i) { return h->total_blocks * i / R; };
+    for (int i = 0; i < R; ++i) {
+      if ((e = rec(4 * i, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+      e = microadam::launch_select(p, h->grad_bf16, h->value_f32, first_of(i), first_of(i + 1) - first_of(i), s);
+      if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
+      if ((e = rec(4 * i + 1, s)) != hipSuccess || (e = hipEventRecord(h->range_done[i], s)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord");
+    }
+    for (int i = 0; i < R; ++i) {
+      if ((e = hipStreamWaitEvent(h->aux, h->range_done[i], 0)) != hipSuccess)
+        return hip_fail(e, "hipStreamWaitEvent");
+      if ((e = rec(4 * i + 2, h->aux)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+      e = microadam::launch_update(p, h->param_bf16, h->value_f32, first_of(i), first_of(i + 1) - first_of(i),
+                                   h->aux);
+      if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
+      if ((e = rec(4 * i + 3, h->aux)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
+    if ((e = hipEventRecord(h->aux_done, h->aux)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if ((e = hipStreamWaitEvent(s, h->aux_done, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+  }
+  h->timed = prof ? R : 0;
   if ((e = hipEventRecord(h->step_done, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   h->t = t;
   return MICROADAM_OK;
@@ -518,10 +559,38 @@ int microadam_kernel_times(microadam_handle h, float* out_ms) {
   if (!out_ms) return fail(MICROADAM_ERR_INVALID_ARG, "out_ms is NULL");
   if (!h->timed) return fail(MICROADAM_ERR_INVALID_ARG, "the last step was not profiled");
   hipError_t e;
-  if ((e = hipEventSynchronize(h->ev[2])) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
-  if ((e = hipEventElapsedTime(&out_ms[0], h->ev[0], h->ev[1])) != hipSuccess ||
-      (e = hipEventElapsedTime(&out_ms[1], h->ev[1], h->ev[2])) != hipSuccess)
-    return hip_fail(e, "hipEventElapsedTime");
+  if ((e = hipEventSynchronize(h->step_done)) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  out_ms[0] = out_ms[1] = 0.0f;
+  for (int i = 0; i < h->timed; ++i) {
+    float a = 0.0f, b = 0.0f;
+    if ((e = hipEventElapsedTime(&a, h->ev[4 * i], h->ev[4 * i + 1])) != hipSuccess ||
+        (e = hipEventElapsedTime(&b, h->ev[4 * i + 2], h->ev[4 * i + 3])) != hipSuccess)
+      return hip_fail(e, "hipEventElapsedTime");
+    out_ms[0] += a;
+    out_ms[1] += b;
+  }
+  return MICROADAM_OK;
+}
+
+int microadam_set_ranges(microadam_handle h, int32_t ranges) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (ranges < 1 || ranges > kMaxRanges) return fail(MICROADAM_ERR_INVALID_ARG, "ranges must be in [1, 32]");
+  if (ranges > 1 && !h->aux) {
+    rc = check_device(h);
+    if (rc) return rc;
+    // events first, the stream last: a handle with `aux` set has them all
+    hipError_t e;
+    if (!h->aux_done && (e = hipEventCreateWithFlags(&h->aux_done, hipEventDisableTiming)) != hipSuccess)
+      return hip_fail(e, "hipEventCreate");
+    for (hipEvent_t& ev : h->range_done)
+      if (!ev && (e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess)
+        return hip_fail(e, "hipEventCreate");
+    // default priority, like every other stream of the library
+    if ((e = hipStreamCreateWithFlags(&h->aux, hipStreamNonBlocking)) != hipSuccess)
+      return hip_fail(e, "hipStreamCreate");
+  }
+  h->ranges = ranges;
   return MICROADAM_OK;
 }
 

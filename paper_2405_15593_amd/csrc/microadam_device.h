@@ -57,9 +57,13 @@ struct StepParams {
 };
 
 // Launchers (defined in microadam_kernels.hip).  Return hipSuccess or the
-// launch error.  A step is launch_select, then launch_update, on one stream.
-hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream);
-hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, hipStream_t stream);
+// launch error.  Each takes the global blocks [first, first + count); the
+// update of a block must follow its select, and blocks share nothing, so a
+// step may run as several ranges, each range's update after its select.
+hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                         hipStream_t stream);
+hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, int64_t first, int64_t count,
+                         hipStream_t stream);
 
 hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_blocks,
                           float* mhat, float* vhat, int value_f32, hipStream_t stream);

@@ -43,8 +43,6 @@ namespace {
 
 constexpr int kWave = 64;
 constexpr int kLaneElems = 16;       // consecutive elements per thread
-constexpr int kRegion = 32;          // candidate vectors one wave can hand to the leader
-constexpr int kCand = 256;           // candidate elements the leader resolves
 constexpr uint32_t kNoEntry = 0xFFFFFFFFu;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -64,6 +62,19 @@ __device__ __forceinline__ uint32_t sgpr(uint32_t x) { return __builtin_amdgcn_r
 __device__ __forceinline__ int opaque(int x) {
   asm volatile("" : "+s"(x));
   return x;
+}
+// The same for a per-lane value: comparisons against it are made where
+// written (in the branch that needs them), not once for every branch.
+__device__ __forceinline__ int opaque_v(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+// A uniform float the compiler must treat as new: comparisons against it in
+// different loops are not merged and kept alive between them.
+__device__ __forceinline__ float opaque_f(float x) {
+  int b = __builtin_amdgcn_readfirstlane(__float_as_int(x));
+  asm volatile("" : "+s"(b));
+  return __int_as_float(b);
 }
 // Work-item and workgroup ids straight from the hardware registers (the
 // library wrappers behind threadIdx / blockIdx are not inlined into code
@@ -330,120 +341,117 @@ __device__ __forceinline__ Rsrc window_rsrc(const StepParams& p, int64_t gb, int
   return make_rsrc(p.state + p.win_plane + (uint64_t)gb * slot_bytes, (uint32_t)(p.window * kq * EW * 4));
 }
 
-// ------------------------------------------------------- select LDS
-template <int NT>
-struct SelectLds {
-  static constexpr int NW = NT / kWave;
-  float* regv;        // [NW][kRegion][8] candidate vectors per wave
-  uint32_t* regi;     // [NW][kRegion] their first element index
-  float* cval;        // candidate values (first half of regv, once read)
-  uint32_t* cidx;     // candidate indices (second half of regv, once read)
-  uint32_t* misc;     // 64 words: counts, wave bounds, broadcast, reductions
-  __device__ explicit SelectLds(uint32_t* smem) {
-    regv = (float*)smem;
-    regi = (uint32_t*)(regv + NW * kRegion * 8);
-    cval = regv;
-    cidx = (uint32_t*)(regv + NW * kRegion * 4);
-    misc = regi + NW * kRegion;
-  }
-  static constexpr size_t words() { return (size_t)NW * kRegion * 9 + 64; }
-};
-// misc word offsets
-enum { M_COUNT = 0 /* [NW] */, M_WL = 8 /* [NW] */, M_GEN = 12, M_T = 13, M_ILAST = 14,
-       M_NOTIE = 15, M_RED0 = 16, M_RED1 = 32, M_RED2 = 48 /* 16 words each */ };
+// ============================================================ select
+// One wave per block.  Lane l owns the EPL consecutive elements
+// [l*EPL, (l+1)*EPL) of the block as NV = EPL/8 vectors of 8 (EPL = 16, 32
+// or 64 for B_d up to 1024, 2048, 4096); lanes past the block hold no
+// elements.  A wave needs no barrier: its LDS traffic is ordered by
+// wave_sync alone.
+//
+// Top-K (Section 3.1) in three stages:
+//   1. a lower bound L on the k-th largest |a|: the largest 13-bit prefix
+//      value with at least k of the 128 half-lane maxima above it (each such
+//      half lane holds an element >= L, so at least k elements are >= L);
+//   2. the vectors holding some |a| >= L are gathered in LDS, and their
+//      elements >= L (the candidates, in element order) compacted;
+//   3. the k-th largest key among the candidates, bit by bit from the top.
+// Blocks where a stage overflows its LDS (or k > 128) take an exact bitwise
+// search over all elements instead.
+constexpr int kMaxCandVec = 128;   // candidate vectors gathered in LDS
+constexpr int kCandMax = 256;      // candidate elements resolved
 
-// Exclusive prefix, in element order, of per-(thread, vector) counts <= 8.
-// base[v] = counted elements before this thread's vector v.  One barrier;
-// `red` (NW words) must not be reused until a later barrier.
-template <int NT>
-__device__ __forceinline__ void wg_scan(const uint32_t (&cnt)[2], uint32_t (&base)[2], uint32_t* red) {
-  constexpr int NW = NT / kWave;
-  const int lane = thread_id() & (kWave - 1), wave = (int)sgpr(thread_id() / kWave);
-  const uint32_t c = cnt[0] + cnt[1];  // <= 16
+__host__ __device__ constexpr size_t select_lds_words() { return (size_t)kMaxCandVec * 9 + 2 * kCandMax; }
+
+// Orders the LDS accesses of one wave (each lane's writes before the other
+// lanes' later reads); LDS operations of a wave execute in order, so this
+// is only a compiler barrier and a wait for the wave's own LDS operations.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+}
+
+// Exclusive prefix over lanes (lane order) of a per-lane count below 16,
+// and the wave total.
+__device__ __forceinline__ uint32_t lane_prefix(uint32_t c, uint32_t& total) {
   uint32_t pre = 0, tot = 0;
 #pragma unroll
-  for (int b = 0; b < 5; ++b) {
+  for (int b = 0; b < 4; ++b) {
     const uint64_t m = ballot((c >> b) & 1u);
     pre += lanes_below(m) << b;
     tot += popc(m) << b;
   }
-  if (lane == 0) red[wave] = tot;
-  lds_sync();
-  uint32_t run = 0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) run += (w < wave) ? red[w] : 0u;
-  base[0] = run + pre;
-  base[1] = base[0] + cnt[0];
+  total = tot;
+  return pre;
 }
 
-// Workgroup-wide count of elements flagged in two 8-bit masks.  One barrier;
-// consecutive calls must use different `red` buffers (NW words).
-template <int NT>
-__device__ __forceinline__ uint32_t wg_count(const uint32_t (&mask)[2], uint32_t* red) {
-  constexpr int NW = NT / kWave;
-  const int lane = thread_id() & (kWave - 1), wave = (int)sgpr(thread_id() / kWave);
-  const uint32_t c = __popc(mask[0]) + __popc(mask[1]);  // <= 16
-  uint32_t tot = 0;
-#pragma unroll
-  for (int b = 0; b < 5; ++b) tot += popc(ballot((c >> b) & 1u)) << b;
-  if (lane == 0) red[wave] = tot;
-  lds_sync();
-  uint32_t s = 0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) s += red[w];
-  return s;
-}
-
-// ============================================================ select
-template <int NT, bool GBF16, bool VF32>
-__global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
-  constexpr int NW = NT / kWave;
-  constexpr int CAP = NT * kLaneElems;
-  constexpr int EW = VF32 ? 2 : 1;
-  constexpr uint32_t kCandCap = (uint32_t)(kCand < NW * kRegion * 4 ? kCand : NW * kRegion * 4);
+template <int EPL, bool LB, bool GBF16, bool VF32>
+__global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
+select_kernel(StepParams p, int64_t first) {
+  constexpr int NV = EPL / 8;
+  constexpr int CAP = kWave * EPL;
   using E = Entry<VF32>;
   extern __shared__ __align__(16) uint32_t smem[];
-  const SelectLds<NT> l(smem);
+  float* const regv = (float*)smem;                  // [kMaxCandVec][8] candidate vectors
+  uint32_t* const regi = smem + kMaxCandVec * 8;     // [kMaxCandVec] their first element
+  float* const cval = (float*)(regi + kMaxCandVec);  // [kCandMax] candidate values
+  uint32_t* const cidx = (uint32_t*)(cval + kCandMax);  // [kCandMax] candidate indices
 
-  const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr(tid / kWave);
-  const uint32_t eb = (uint32_t)tid * kLaneElems;  // first element of this thread
+  const int lane = thread_id();
+  const uint32_t eb = (uint32_t)lane * EPL;  // first element of this lane
   const int bl = p.bucket_log2;
-  const bool pair_buckets = bl == 3;               // B_q = 8: one bucket per vector
-  const int64_t gb = block_id();
+  const int64_t gb = first + block_id();
 
   // The block's EF codes and bucket pairs are addressed by gb alone, so their
   // loads go out before the tensor lookup that the gradient needs.
   const uint32_t nbk = (uint32_t)(p.block >> bl);
   const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * (p.block >> 1), (uint32_t)(p.block >> 1));
   const Rsrc rs = make_rsrc(p.state + p.stats_plane + (uint64_t)gb * nbk * 8, nbk * 8);
-  u32x4 st;
-  if (pair_buckets) {
-    st = __builtin_amdgcn_raw_buffer_load_b128(rs, eb, 0, 0);
+  constexpr int NS_ST = LB ? 1 : NV;  // bucket pairs per lane: one, or one per vector
+  u32x2 st[NS_ST];
+#pragma unroll
+  for (int v = 0; v < NS_ST; ++v) st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, 0);
+  // Codes of vector v: element e in bits [4e, 4e + 4).  16-byte accesses
+  // when the block fills every lane, else 8-byte ones (B_d is a multiple of
+  // 16, so no access then straddles the end of the block's codes).
+  const bool wide = NV > 2 && p.block == CAP;
+  uint32_t cw[NV];
+  if (wide) {
+#pragma unroll
+    for (int q = 0; q < NV / 4; ++q) {
+      const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(re, (eb >> 1) + 16 * q, 0, 0);
+#pragma unroll
+      for (int h = 0; h < 4; ++h) cw[4 * q + h] = t[h];
+    }
   } else {
-    const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(rs, (eb >> bl) * 8, 0, 0);
-    st = u32x4{t[0], t[1], 0u, 0u};
+#pragma unroll
+    for (int q = 0; q < NV / 2; ++q) {
+      const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(re, (eb >> 1) + 8 * q, 0, 0);
+      cw[2 * q] = t[0];
+      cw[2 * q + 1] = t[1];
+    }
   }
-  const u32x2 codes = __builtin_amdgcn_raw_buffer_load_b64(re, eb >> 1, 0, 0);
   const Block b = locate(p, gb);
   const int s = b.s, kq = b.kq;
   const bool full = s == CAP;
   const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + b.e0 * (GBF16 ? 2 : 4), vec_bytes<GBF16>(s));
-  Raw8<GBF16> graw[2];
+  Raw8<GBF16> graw[NV];
 #pragma unroll
-  for (int v = 0; v < 2; ++v) graw[v] = load8<GBF16>(rg, eb + v * 8);
+  for (int v = 0; v < NV; ++v) graw[v] = load8<GBF16>(rg, eb + 8 * v);
 
   // ---------------------------------------------- 1. a = g + Q^-1(e)
-  float a[2][8];
+  float a[NV][8];
   {
-    const float lo0 = __uint_as_float(st[0]), hi0 = __uint_as_float(st[1]);
-    const float u0 = div15(hi0 - lo0);
-    const float lo1 = pair_buckets ? __uint_as_float(st[2]) : lo0;
-    const float u1 = pair_buckets ? div15(__uint_as_float(st[3]) - lo1) : u0;
+    float lo0 = 0.0f, u0 = 0.0f;
+    if constexpr (LB) {
+      lo0 = __uint_as_float(st[0][0]);
+      u0 = div15(__uint_as_float(st[0][1]) - lo0);
+    }
 #pragma unroll
-    for (int v = 0; v < 2; ++v) {
-      const float lo = v ? lo1 : lo0, u = v ? u1 : u0;
-      const uint32_t w = codes[v];
-      const uint32_t ev = w & 0x0F0F0F0Fu, od = (w >> 4) & 0x0F0F0F0Fu;
+    for (int v = 0; v < NV; ++v) {
+      const float lo = LB ? lo0 : __uint_as_float(st[v][0]);
+      const float u = LB ? u0 : div15(__uint_as_float(st[v][1]) - lo);
+      const uint32_t ev = cw[v] & 0x0F0F0F0Fu, od = (cw[v] >> 4) & 0x0F0F0F0Fu;
       float g[8], c[8];
       unpack8<GBF16>(graw[v], g);
       c[0] = ubyte<0>(ev); c[2] = ubyte<1>(ev); c[4] = ubyte<2>(ev); c[6] = ubyte<3>(ev);
@@ -456,404 +464,453 @@ __global__ void __launch_bounds__(NT) select_kernel(StepParams p) {
       }
     }
   }
-  // elements of this thread below the end of the block: [0, rem)
+  // elements of this lane below the end of the block: [0, rem)
   const int rem = s - (int)eb;
   if (!full) {  // elements past the end of the tensor are 0 and never kept
+    const int r = opaque_v(rem);
 #pragma unroll
-    for (int v = 0; v < 2; ++v)
+    for (int v = 0; v < NV; ++v)
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if (v * 8 + e >= rem) a[v][e] = 0.0f;
+        if (8 * v + e >= r) a[v][e] = 0.0f;
   }
 
   // ---------------------------------------------- 2. Top-K threshold
-  // Lower bound L: per wave, the ceil(k/NW)-th largest lane maximum of |a|
-  // (resolved on its top 13 bits); at least k elements are >= the minimum
-  // over waves.
-  float vmax[2];
+  float vmax[NV];
 #pragma unroll
-  for (int v = 0; v < 2; ++v) {
+  for (int v = 0; v < NV; ++v) {
     const float m0 = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(a[v][0]), __builtin_fabsf(a[v][1])), __builtin_fabsf(a[v][2]));
-    const float m1 = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(a[v][3]), __builtin_fabsf(a[v][4])), __builtin_fabsf(a[v][5]));
-    const float m2 = __builtin_fmaxf(__builtin_fmaxf(m0, m1), __builtin_fabsf(a[v][6]));
+    const float m1 = __builtin_fmaxf(__builtin_fmaxf(m0, __builtin_fabsf(a[v][3])), __builtin_fabsf(a[v][4]));
+    const float m2 = __builtin_fmaxf(__builtin_fmaxf(m1, __builtin_fabsf(a[v][5])), __builtin_fabsf(a[v][6]));
     vmax[v] = __builtin_fmaxf(m2, __builtin_fabsf(a[v][7]));
   }
-  const bool fast_k = kq <= kWave * NW;
-  {
-    const uint32_t lmax = __float_as_uint(__builtin_fmaxf(vmax[0], vmax[1]));
-    const int kw = (kq + NW - 1) / NW;
+  const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
+  const uint32_t row0 = (uint32_t)p.new_slot * kq;
+
+  uint32_t T = 0, i_last = 0;
+  bool notie = false;
+  bool general = kq > 2 * kWave;
+  if (!general) {
+    // stage 1: L over the half-lane maxima
+    float h0 = vmax[0], h1 = vmax[NV / 2];
+#pragma unroll
+    for (int v = 1; v < NV / 2; ++v) {
+      h0 = __builtin_fmaxf(h0, vmax[v]);
+      h1 = __builtin_fmaxf(h1, vmax[NV / 2 + v]);
+    }
+    const uint32_t hb0 = __float_as_uint(h0), hb1 = __float_as_uint(h1);
     uint32_t P = 0;
 #pragma unroll
     for (int bit = 30; bit >= 18; --bit) {
       const uint32_t c = P | (1u << bit);
-      if ((int)popc(ballot(lmax >= c)) >= kw) P = c;
+      if ((int)(popc(ballot(hb0 >= c)) + popc(ballot(hb1 >= c))) >= kq) P = c;
     }
-    if (lane == 0) l.misc[M_WL + wave] = P;
-  }
-  lds_sync();  // B1 ------------------------------------------------
+    const uint32_t Lb = P;
+    const float L = __uint_as_float(Lb);
 
-  // The leader wave resolves the threshold; it rotates with the block so that
-  // the leaders of the workgroups sharing a compute unit spread over its SIMDs.
-  const int leader = (int)(gb & (NW - 1));
-  const Rsrc rw = window_rsrc<EW>(p, gb, kq);
-  float L;
-  {
-    uint32_t Lb = l.misc[M_WL];
+    // stage 2a: candidate vectors to LDS, in element order
+    bool f[NV];
+    uint32_t cnt = 0;
 #pragma unroll
-    for (int w = 1; w < NW; ++w) Lb = min(Lb, l.misc[M_WL + w]);
-    L = __uint_as_float(sgpr(Lb));
-  }
-  // candidate vectors, those holding some |a| >= L, handed to the leader in
-  // element order (wave, lane, vector)
-  {
-    const bool f0 = vmax[0] >= L, f1 = vmax[1] >= L;
-    const uint64_t m0 = ballot(f0), m1 = ballot(f1);
-    const uint32_t pos0 = lanes_below(m0) + lanes_below(m1);
-    const uint32_t pos1 = pos0 + (f0 ? 1u : 0u);
-    float* rv = l.regv + wave * kRegion * 8;
-    uint32_t* ri = l.regi + wave * kRegion;
-    if (f0 && pos0 < (uint32_t)kRegion) {
-      *(float4*)(rv + pos0 * 8) = make_float4(a[0][0], a[0][1], a[0][2], a[0][3]);
-      *(float4*)(rv + pos0 * 8 + 4) = make_float4(a[0][4], a[0][5], a[0][6], a[0][7]);
-      ri[pos0] = eb;
+    for (int v = 0; v < NV; ++v) {
+      f[v] = vmax[v] >= L;
+      cnt += f[v] ? 1u : 0u;
     }
-    if (f1 && pos1 < (uint32_t)kRegion) {
-      *(float4*)(rv + pos1 * 8) = make_float4(a[1][0], a[1][1], a[1][2], a[1][3]);
-      *(float4*)(rv + pos1 * 8 + 4) = make_float4(a[1][4], a[1][5], a[1][6], a[1][7]);
-      ri[pos1] = eb + 8;
-    }
-    if (lane == 0) l.misc[M_COUNT + wave] = popc(m0) + popc(m1);
-  }
-  lds_sync();  // B2 ------------------------------------------------
-
-  bool general;
-  {
-    uint32_t nvec = 0;
-    bool overflow = false;
+    uint32_t nvec;
+    const uint32_t pre = lane_prefix(cnt, nvec);
+    general = Lb == 0 || nvec > (uint32_t)kMaxCandVec;
+    if (!general) {
+      {
+        uint32_t pos = pre;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const uint32_t c = sgpr(l.misc[M_COUNT + w]);
-      nvec += c;
-      overflow |= c > (uint32_t)kRegion;
-    }
-    general = !fast_k || L == 0.0f || overflow || nvec > 2u * kWave;
-  }
-  if (!general && wave == leader) {
-    // this lane takes candidate vectors lane and lane + 64 (element order)
-    uint32_t src[2];
-    bool have[2];
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const uint32_t j = lane + kWave * r;
-      uint32_t off = 0, at = 0;
-      bool found = false;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        const uint32_t cw = sgpr(l.misc[M_COUNT + w]);
-        if (!found && j < off + cw) { found = true; at = w * kRegion + (j - off); }
-        off += cw;
-      }
-      have[r] = found;
-      src[r] = at;
-    }
-    // elements with |a| >= L of both vectors, in element order
-    float cv[2][8];
-    uint32_t base[2], total = 0;
-#pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const float4 x0 = *(const float4*)(l.regv + src[r] * 8);
-      const float4 x1 = *(const float4*)(l.regv + src[r] * 8 + 4);
-      cv[r][0] = x0.x; cv[r][1] = x0.y; cv[r][2] = x0.z; cv[r][3] = x0.w;
-      cv[r][4] = x1.x; cv[r][5] = x1.y; cv[r][6] = x1.z; cv[r][7] = x1.w;
-      uint32_t c = 0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) c += (have[r] && __builtin_fabsf(cv[r][e]) >= L) ? 1u : 0u;
-      const uint64_t b0 = ballot(c & 1u), b1 = ballot(c & 2u), b2 = ballot(c & 4u), b3 = ballot(c & 8u);
-      base[r] = total + lanes_below(b0) + 2u * lanes_below(b1) + 4u * lanes_below(b2) + 8u * lanes_below(b3);
-      total += popc(b0) + 2u * popc(b1) + 4u * popc(b2) + 8u * popc(b3);
-    }
-    const uint32_t cb0 = l.regi[src[0]], cb1 = l.regi[src[1]];
-    const uint32_t C = total;
-    if (C > kCandCap || C < (uint32_t)kq) {
-      if (lane == 0) l.misc[M_GEN] = 1;
-    } else {
-      // every region read above has returned before the candidate arrays,
-      // which reuse the region memory, are written
-      __builtin_amdgcn_s_waitcnt(0xC07F);
-#pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        uint32_t pos = base[r];
-        const uint32_t cb = r ? cb1 : cb0;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          if (have[r] && __builtin_fabsf(cv[r][e]) >= L) {
-            l.cval[pos] = cv[r][e];
-            l.cidx[pos] = cb + e;
+        for (int v = 0; v < NV; ++v) {
+          if (f[v]) {
+            *(float4*)(regv + pos * 8) = make_float4(a[v][0], a[v][1], a[v][2], a[v][3]);
+            *(float4*)(regv + pos * 8 + 4) = make_float4(a[v][4], a[v][5], a[v][6], a[v][7]);
+            regi[pos] = eb + 8 * v;
             ++pos;
           }
         }
       }
-      // k-th largest key among the candidates, one bit at a time from the top
-      uint32_t ck[4], ci[4];
-      float cf[4];
-      bool ok[4];
+      wave_sync();
+      // stage 2b: elements >= L of candidate vectors lane and lane + 64
+      uint32_t C = 0;
+      auto gather = [&](auto nsv_tag) {
+        constexpr int NSV = decltype(nsv_tag)::value;
+        float cv[NSV][8];
+        uint32_t cb[NSV], base[NSV], cc[NSV];
+        uint32_t total = 0;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const uint32_t j = lane + kWave * r;
-        ok[r] = j < C;
-        cf[r] = ok[r] ? l.cval[j] : 0.0f;
-        ci[r] = ok[r] ? l.cidx[j] : 0u;
-        ck[r] = ok[r] ? key_of(cf[r]) : 0u;
-      }
-      const uint32_t nslot = (C + kWave - 1) / kWave;
-      uint32_t T = 0;
-      if (nslot == 1) {
+        for (int r = 0; r < NSV; ++r) {
+          const uint32_t j = lane + kWave * r;
+          const bool have = j < nvec;
+          const uint32_t src = have ? j : 0u;
+          const float4 x0 = *(const float4*)(regv + src * 8);
+          const float4 x1 = *(const float4*)(regv + src * 8 + 4);
+          cb[r] = regi[src];
+          cv[r][0] = x0.x; cv[r][1] = x0.y; cv[r][2] = x0.z; cv[r][3] = x0.w;
+          cv[r][4] = x1.x; cv[r][5] = x1.y; cv[r][6] = x1.z; cv[r][7] = x1.w;
+          uint32_t c = 0;
 #pragma unroll
-        for (int bit = 30; bit >= 0; --bit) {
-          const uint32_t c = T | (1u << bit);
-          if (popc(ballot(ck[0] >= c)) >= (uint32_t)kq) T = c;
+          for (int e = 0; e < 8; ++e) {
+            if (!have) cv[r][e] = 0.0f;  // key 0 < L: never a candidate
+            c += __builtin_fabsf(cv[r][e]) >= L ? 1u : 0u;
+          }
+          cc[r] = c;
         }
-      } else if (nslot == 2) {
 #pragma unroll
-        for (int bit = 30; bit >= 0; --bit) {
-          const uint32_t c = T | (1u << bit);
-          if (popc(ballot(ck[0] >= c)) + popc(ballot(ck[1] >= c)) >= (uint32_t)kq) T = c;
+        for (int r = 0; r < NSV; ++r) {
+          uint32_t t;
+          base[r] = total + lane_prefix(cc[r], t);
+          total += t;
         }
-      } else {
-        for (int bit = 30; bit >= 0; --bit) {
-          const uint32_t c = T | (1u << bit);
-          uint32_t n = popc(ballot(ck[0] >= c)) + popc(ballot(ck[1] >= c)) + popc(ballot(ck[2] >= c));
-          if (nslot > 3) n += popc(ballot(ck[3] >= c));
-          if (n >= (uint32_t)kq) T = c;
+        C = total;
+        if (C <= (uint32_t)kCandMax) {
+#pragma unroll
+          for (int r = 0; r < NSV; ++r) {
+            uint32_t pos = base[r];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              if (__builtin_fabsf(cv[r][e]) >= L) {
+                cval[pos] = cv[r][e];
+                cidx[pos] = cb[r] + e;
+                ++pos;
+              }
+            }
+          }
         }
-      }
-      uint32_t ngt = 0, neq = 0;
+      };
+      if (nvec <= (uint32_t)kWave) gather(std::integral_constant<int, 1>{});
+      else gather(std::integral_constant<int, 2>{});
+      general = C > (uint32_t)kCandMax || C < (uint32_t)kq;
+      if (!general) {
+        wave_sync();
+        // stage 3: the k-th largest key among the C candidates (NS slots of 64)
+        auto resolve = [&](auto ns_tag) {
+          constexpr int NS = decltype(ns_tag)::value;
+          uint32_t ck[NS], ci[NS];
+          float cf[NS];
+          bool ok[NS];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        ngt += popc(ballot(ok[r] && ck[r] > T));
-        neq += popc(ballot(ok[r] && ck[r] == T));
-      }
-      const uint32_t need = (uint32_t)kq - ngt;  // >= 1 of the keys equal to T are kept
-      uint32_t eq_before = 0, sel_before = 0;
-      const uint32_t row0 = (uint32_t)p.new_slot * kq;
+          for (int r = 0; r < NS; ++r) {
+            const uint32_t j = lane + kWave * r;
+            ok[r] = j < C;
+            cf[r] = ok[r] ? cval[j] : 0.0f;
+            ci[r] = ok[r] ? cidx[j] : 0u;
+            ck[r] = ok[r] ? key_of(cf[r]) : 0u;
+          }
+          // The search stops early once exactly k candidates are >= the
+          // threshold so far: those are then the k largest.  Below L the
+          // candidate count is not the block's, hence c >= L.  (The
+          // remaining steps are skipped by a uniform test rather than left
+          // by a loop exit, which keeps the control flow simple.)
+          uint32_t t = 0;
+          bool exact = false;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool gt = ok[r] && ck[r] > T;
-        const bool eq = ok[r] && ck[r] == T;
-        const uint64_t em = ballot(eq);
-        const uint32_t rank = eq_before + lanes_below(em);
-        eq_before += popc(em);
-        if (eq && rank == need - 1) l.misc[M_ILAST] = ci[r];
-        const bool sel = gt || (eq && rank < need);
-        const uint64_t sm = ballot(sel);
-        const uint32_t pos = sel_before + lanes_below(sm);
-        sel_before += popc(sm);
-        if (sel) E::store(rw, row0 + pos, E::make(ci[r], cf[r]));
-      }
-      if (lane == 0) {
-        l.misc[M_T] = T;
-        l.misc[M_NOTIE] = (neq == need) ? 1u : 0u;
-        l.misc[M_GEN] = 0;
+          for (int bit = 30; bit >= 0; --bit) {
+            if (!exact) {
+              const uint32_t c = t | (1u << bit);
+              uint32_t n = 0;
+#pragma unroll
+              for (int r = 0; r < NS; ++r) n += popc(ballot(ck[r] >= c));
+              if (n >= (uint32_t)kq) {
+                t = c;
+                exact = n == (uint32_t)kq && c >= Lb;
+              }
+            }
+          }
+          T = t;
+          uint32_t ngt = 0, neq = 0;
+          if (!exact) {
+#pragma unroll
+            for (int r = 0; r < NS; ++r) {
+              ngt += popc(ballot(ok[r] && ck[r] > t));
+              neq += popc(ballot(ok[r] && ck[r] == t));
+            }
+          }
+          // exact: every key >= t is kept; else the keys above t and the
+          // first `need` keys equal to t in element order
+          const uint32_t need = exact ? 0u : (uint32_t)kq - ngt;
+          notie = exact || neq == need;
+          uint32_t eq_before = 0, sel_before = 0;
+#pragma unroll
+          for (int r = 0; r < NS; ++r) {
+            const bool gt = ok[r] && (exact ? ck[r] >= t : ck[r] > t);
+            const bool eq = !exact && ok[r] && ck[r] == t;
+            const uint64_t em = ballot(eq);
+            const uint32_t rank = eq_before + lanes_below(em);
+            eq_before += popc(em);
+            const uint64_t lm = ballot(eq && rank == need - 1);
+            if (lm) i_last = __builtin_amdgcn_readlane(ci[r], (int)__builtin_ctzll(lm));
+            const bool sel = gt || (eq && rank < need);
+            const uint64_t sm = ballot(sel);
+            if (sel) E::store(rw, row0 + sel_before + lanes_below(sm), E::make(ci[r], cf[r]));
+            sel_before += popc(sm);
+          }
+        };
+        const uint32_t nslot = (C + kWave - 1) / kWave;
+        if (nslot == 1) resolve(std::integral_constant<int, 1>{});
+        else if (nslot == 2) resolve(std::integral_constant<int, 2>{});
+        else resolve(std::integral_constant<int, 4>{});
       }
     }
   }
-  if (!general) {
-    lds_sync();  // B3 ----------------------------------------------
-    general = sgpr(l.misc[M_GEN]) != 0;
-  }
-
-  uint32_t T, i_last;
-  bool notie;
-  if (!general) {
-    T = sgpr(l.misc[M_T]);
-    i_last = sgpr(l.misc[M_ILAST]);
-    notie = sgpr(l.misc[M_NOTIE]) != 0;
-  } else {
-    // Exact bitwise search over the whole block (ties, large k or many
-    // candidates): the largest T with #{key >= T} >= k.
-    int buf = 0;
-    uint32_t P = 0;
-    for (int bit = 30; bit >= 0; --bit) {
-      const uint32_t c = P | (1u << bit);
-      uint32_t mk[2];
+  if (general) {
+    // Exact bitwise search over every element (ties, large k, many
+    // candidates): the largest T with #{key >= T} >= k.  Keys are compared
+    // as |a| against the float with the same bits (the same order for
+    // finite values; the thresholds tried never exceed +inf's bits).
+    uint32_t t = 0;
+    bool exact = false;
+    for (int bit = 30; bit >= 0 && !exact; --bit) {
+      const uint32_t c = t | (1u << bit);
+      const float cf = __uint_as_float(c);
+      uint32_t n = 0;
 #pragma unroll
-      for (int v = 0; v < 2; ++v) {
-        uint32_t x = 0;
+      for (int v = 0; v < NV; ++v) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x |= (uint32_t)(key_of(a[v][e]) >= c) << e;
-        mk[v] = x;
+        for (int e = 0; e < 8; ++e) n += popc(ballot(__builtin_fabsf(a[v][e]) >= cf));
+        __builtin_amdgcn_sched_barrier(0);  // bounds the masks in flight
       }
-      const uint32_t n = wg_count<NT>(mk, l.misc + (buf ? M_RED1 : M_RED0));
-      buf ^= 1;
-      if ((int)n >= kq) P = c;
-    }
-    T = P;
-    uint32_t gtm[2], eqm[2];
-#pragma unroll
-    for (int v = 0; v < 2; ++v) {
-      uint32_t g = 0, e2 = 0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        g |= (uint32_t)(key_of(a[v][e]) > T) << e;
-        e2 |= (uint32_t)(key_of(a[v][e]) == T) << e;
+      if (n >= (uint32_t)kq) {
+        t = c;
+        exact = n == (uint32_t)kq;
       }
-      gtm[v] = g;
-      eqm[v] = e2;
     }
-    const uint32_t ngt = wg_count<NT>(gtm, l.misc + (buf ? M_RED1 : M_RED0));
-    buf ^= 1;
-    const uint32_t need = (uint32_t)kq - ngt;
-    uint32_t ecnt[2], ebase[2];
+    T = t;
+    // kept: with an exact count |a| >= t; else |a| > t, and |a| == t for the
+    // first `need` such elements in element order
+    uint32_t sel_l = 0;
+    if (exact) {
+      notie = true;
+      const float tf = opaque_f(__uint_as_float(t));
 #pragma unroll
-    for (int v = 0; v < 2; ++v) ecnt[v] = __popc(eqm[v]);
-    wg_scan<NT>(ecnt, ebase, l.misc + (buf ? M_RED1 : M_RED0));
+      for (int v = 0; v < NV; ++v)
 #pragma unroll
-    for (int v = 0; v < 2; ++v) {
-      uint32_t r = ebase[v];
+        for (int e = 0; e < 8; ++e) sel_l += __builtin_fabsf(a[v][e]) >= tf ? 1u : 0u;
+    } else {
+      const float tf = opaque_f(__uint_as_float(t));
+      uint32_t ngt_l = 0, neq_l = 0;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        if ((eqm[v] >> e) & 1u) {
-          if (r == need - 1) l.misc[M_ILAST] = eb + v * 8 + e;
-          ++r;
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          ngt_l += __builtin_fabsf(a[v][e]) > tf ? 1u : 0u;
+          neq_l += __builtin_fabsf(a[v][e]) == tf ? 1u : 0u;
         }
+      uint32_t ngt = 0;
+#pragma unroll
+      for (int b2 = 0; b2 < 7; ++b2) ngt += popc(ballot((ngt_l >> b2) & 1u)) << b2;
+      const uint32_t need = (uint32_t)kq - ngt;  // >= 1
+      // keys equal to t in the lanes before this one
+      uint32_t eq_pre = 0;
+#pragma unroll
+      for (int b2 = 0; b2 < 7; ++b2) eq_pre += lanes_below(ballot((neq_l >> b2) & 1u)) << b2;
+      // the lane holding the need-th key equal to t finds its index
+      const bool mine = eq_pre < need && eq_pre + neq_l >= need;
+      uint32_t my_last = 0;
+      if (mine) {
+        const float tf2 = opaque_f(tf);
+        uint32_t r = eq_pre;
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (__builtin_fabsf(a[v][e]) == tf2) {
+              if (r == need - 1) my_last = eb + 8 * v + e;
+              ++r;
+            }
       }
-    }
-    lds_sync();
-    i_last = sgpr(l.misc[M_ILAST]);
-    notie = false;
-    uint32_t scnt[2], sbase[2];
+      const uint64_t mm = ballot(mine);
+      i_last = __builtin_amdgcn_readlane(my_last, (int)__builtin_ctzll(mm));
+      const int last_here = (int)i_last - (int)eb;
+      const float tf3 = opaque_f(tf);
 #pragma unroll
-    for (int v = 0; v < 2; ++v) {
-      uint32_t c = 0;
+      for (int v = 0; v < NV; ++v)
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        c += ((gtm[v] >> e) & 1u) || (((eqm[v] >> e) & 1u) && eb + v * 8 + e <= i_last);
-      scnt[v] = c;
-    }
-    wg_scan<NT>(scnt, sbase, l.misc + M_RED2);
-    const uint32_t row0 = (uint32_t)p.new_slot * kq;
-#pragma unroll
-    for (int v = 0; v < 2; ++v) {
-      uint32_t pos = sbase[v];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t i = eb + v * 8 + e;
-        const bool sel = ((gtm[v] >> e) & 1u) || (((eqm[v] >> e) & 1u) && i <= i_last);
-        if (sel) {
-          E::store(rw, row0 + pos, E::make(i, a[v][e]));
-          ++pos;
+        for (int e = 0; e < 8; ++e) {
+          const float ab = __builtin_fabsf(a[v][e]);
+          sel_l += ((ab > tf3) | ((ab == tf3) & (8 * v + e <= last_here))) ? 1u : 0u;
         }
-      }
+    }
+    // the kept elements of this lane, stored in element order
+    uint32_t pos = 0;
+#pragma unroll
+    for (int b2 = 0; b2 < 7; ++b2) pos += lanes_below(ballot((sel_l >> b2) & 1u)) << b2;
+    if (sel_l) {
+      const float tf = opaque_f(__uint_as_float(t));
+      const int last_here = notie ? (int)kWave * EPL : (int)i_last - (int)eb;
+#pragma unroll
+      for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float ab = __builtin_fabsf(a[v][e]);
+          if ((ab > tf) | ((ab == tf) & (8 * v + e <= last_here))) {
+            E::store(rw, row0 + pos, E::make(eb + 8 * v + e, a[v][e]));
+            ++pos;
+          }
+        }
     }
   }
 
   // ---------------------------------------------- 4. e = Q(a with a[I] = 0)
-  const float Tf = __uint_as_float(T);
-  float x[2][8], mn[2], mx[2];
   // kept elements: |a| > T, and |a| == T up to index i_last; without ties
-  // at the threshold that is |a| >= T (a workgroup-uniform case)
-  if (notie) {
+  // at the threshold that is |a| >= T (a wave-uniform case).  With ties the
+  // kept elements equal to T are zeroed first, and the rest are those
+  // with |a| >= the next float above T.
+  uint32_t Tk = T;
+  if (!notie) {
+    const float tf = opaque_f(__uint_as_float(T));
+    const int last_here = (int)i_last - (int)eb;  // this lane's elements up to i_last: [0, last_here]
 #pragma unroll
-    for (int v = 0; v < 2; ++v)
+    for (int v = 0; v < NV; ++v)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[v][e] = (__builtin_fabsf(a[v][e]) >= Tf) ? 0.0f : a[v][e];
-  } else {
-    // this thread's elements up to index i_last: [0, last_here]
-    const int last_here = (int)i_last - (int)eb;
-#pragma unroll
-    for (int v = 0; v < 2; ++v)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float ab = __builtin_fabsf(a[v][e]);
-        const bool kept = (ab > Tf) | ((ab == Tf) & (v * 8 + e <= last_here));
-        x[v][e] = kept ? 0.0f : a[v][e];
-      }
+      for (int e = 0; e < 8; ++e)
+        if ((__builtin_fabsf(a[v][e]) == tf) & (8 * v + e <= last_here)) a[v][e] = 0.0f;
+    Tk = T + 1u;
   }
+  // (the values pass through an empty asm so that the compiler does not
+  // carry |a| of the tie pass into the test below in extra registers)
 #pragma unroll
-  for (int v = 0; v < 2; ++v) {
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) asm volatile("" : "+v"(a[v][e]));
+  {
+    const float tk = __uint_as_float(Tk);
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a[v][e] = (__builtin_fabsf(a[v][e]) >= tk) ? 0.0f : a[v][e];
+  }
+  // bucket min / max: per vector, then over the vectors of a bucket inside
+  // the lane, then over the lanes of a bucket
+  float mn[NV], mx[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
     if (full) {
-      mn[v] = __builtin_fminf(__builtin_fminf(__builtin_fminf(x[v][0], x[v][1]), x[v][2]),
-                              __builtin_fminf(__builtin_fminf(x[v][3], x[v][4]), x[v][5]));
-      mn[v] = __builtin_fminf(mn[v], __builtin_fminf(x[v][6], x[v][7]));
-      mx[v] = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(x[v][0], x[v][1]), x[v][2]),
-                              __builtin_fmaxf(__builtin_fmaxf(x[v][3], x[v][4]), x[v][5]));
-      mx[v] = __builtin_fmaxf(mx[v], __builtin_fmaxf(x[v][6], x[v][7]));
+      mn[v] = __builtin_fminf(__builtin_fminf(__builtin_fminf(a[v][0], a[v][1]), a[v][2]),
+                              __builtin_fminf(__builtin_fminf(a[v][3], a[v][4]), a[v][5]));
+      mn[v] = __builtin_fminf(mn[v], __builtin_fminf(a[v][6], a[v][7]));
+      mx[v] = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(a[v][0], a[v][1]), a[v][2]),
+                              __builtin_fmaxf(__builtin_fmaxf(a[v][3], a[v][4]), a[v][5]));
+      mx[v] = __builtin_fmaxf(mx[v], __builtin_fmaxf(a[v][6], a[v][7]));
     } else {
       mn[v] = __builtin_inff();
       mx[v] = -__builtin_inff();
+      const int r = opaque_v(rem);
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if (v * 8 + e < rem) { mn[v] = __builtin_fminf(mn[v], x[v][e]); mx[v] = __builtin_fmaxf(mx[v], x[v][e]); }
+        if (8 * v + e < r) { mn[v] = __builtin_fminf(mn[v], a[v][e]); mx[v] = __builtin_fmaxf(mx[v], a[v][e]); }
     }
   }
-  if (!pair_buckets) {
-    float lo = __builtin_fminf(mn[0], mn[1]), hi = __builtin_fmaxf(mx[0], mx[1]);
-    group_minmax(lo, hi, bl - 4);
-    mn[0] = mn[1] = lo;
-    mx[0] = mx[1] = hi;
-  }
-  uint32_t w[2];
-  float u[2];
+  if constexpr (LB) {
+    float lo = mn[0], hi = mx[0];
 #pragma unroll
-  for (int v = 0; v < 2; ++v) {
-    mn[v] = mn[v] + 0.0f;  // a bucket bound of -0 is stored as +0
-    mx[v] = mx[v] + 0.0f;
-    u[v] = div15(mx[v] - mn[v]);
-  }
-#pragma unroll
-  for (int v = 0; v < 2; ++v) {
-    // Codes from two products that bracket the quotient: v_rcp is within
-    // 1 ulp for these u, so r_lo < 1/u < r_hi and
-    // rint((x-min)*r_lo) <= rint((x-min)/u) <= rint((x-min)*r_hi).  Where
-    // the two agree (all but a few elements in a million) the code is
-    // exact; elsewhere it is recomputed with an IEEE division.
-    const float uv = u[v], mnv = mn[v];
-    const float rcp = __builtin_amdgcn_rcpf(uv);
-    const float r_lo = __uint_as_float(__float_as_uint(rcp) - 2u);
-    const float r_hi = __uint_as_float(__float_as_uint(rcp) + 2u);
-    uint32_t d1e = 0, d1o = 0, d2e = 0, d2o = 0;
-#pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      const float ye = x[v][2 * h] - mnv, yo = x[v][2 * h + 1] - mnv;
-      const float p1e = ye * r_lo, p1o = yo * r_lo;
-      const float p2e = ye * r_hi, p2o = yo * r_hi;
-      d1e = __builtin_amdgcn_cvt_pk_u8_f32(p1e, h, d1e);  // round half to even, clamp to [0, 255]
-      d1o = __builtin_amdgcn_cvt_pk_u8_f32(p1o, h, d1o);
-      d2e = __builtin_amdgcn_cvt_pk_u8_f32(p2e, h, d2e);
-      d2o = __builtin_amdgcn_cvt_pk_u8_f32(p2o, h, d2o);
+    for (int v = 1; v < NV; ++v) {
+      lo = __builtin_fminf(lo, mn[v]);
+      hi = __builtin_fmaxf(hi, mx[v]);
     }
-    uint32_t wv = d1e | (d1o << 4);
-    const bool exact_u = uv >= 0x1p-125f && uv <= 0x1p+125f;
-    if (!exact_u | (d1e != d2e) | (d1o != d2o)) {
-      wv = 0;
-      if (uv != 0.0f) {
+    constexpr int lg = EPL == 16 ? 4 : EPL == 32 ? 5 : 6;
+    group_minmax(lo, hi, bl - lg);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float y = x[v][e] - mnv;
-          float rr = __builtin_rintf(y / uv);
-          rr = __builtin_fminf(__builtin_fmaxf(rr, 0.0f), 15.0f);
-          wv |= (uint32_t)rr << (4 * e);
+    for (int v = 0; v < NV; ++v) {
+      mn[v] = lo;
+      mx[v] = hi;
+    }
+  } else {
+    // B_q = 8 << j vectors... combine the 2^j vectors of each bucket
+#pragma unroll
+    for (int j = 0; (1 << j) < NV; ++j) {
+      if (bl - 3 > j) {
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          const int w = v ^ (1 << j);
+          if (w > v) {
+            const float l2 = __builtin_fminf(mn[v], mn[w]), h2 = __builtin_fmaxf(mx[v], mx[w]);
+            mn[v] = mn[w] = l2;
+            mx[v] = mx[w] = h2;
+          }
         }
       }
     }
-    if (!full) {
+  }
+  uint32_t wv[NV];
+  {
+    float uq = 0.0f, mnq = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (v * 8 + e >= rem) wv &= ~(0xFu << (4 * e));
+    for (int v = 0; v < NV; ++v) {
+      if (!LB || v == 0) {
+        mn[v] = mn[v] + 0.0f;  // a bucket bound of -0 is stored as +0
+        mx[v] = mx[v] + 0.0f;
+        mnq = mn[v];
+        uq = div15(mx[v] - mn[v]);
+      }
+      // Codes from two products that bracket the quotient: v_rcp is within
+      // 1 ulp for these u, so r_lo < 1/u < r_hi and
+      // rint((x-min)*r_lo) <= rint((x-min)/u) <= rint((x-min)*r_hi).  Where
+      // the two agree (all but a few elements in a million) the code is
+      // exact; elsewhere it is recomputed with an IEEE division.
+      const float uv = uq, mnv = mnq;
+      const float rcp = __builtin_amdgcn_rcpf(uv);
+      const float r_lo = __uint_as_float(__float_as_uint(rcp) - 2u);
+      const float r_hi = __uint_as_float(__float_as_uint(rcp) + 2u);
+      uint32_t d1e = 0, d1o = 0, d2e = 0, d2o = 0;
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const float ye = a[v][2 * h] - mnv, yo = a[v][2 * h + 1] - mnv;
+        const float p1e = ye * r_lo, p1o = yo * r_lo;
+        const float p2e = ye * r_hi, p2o = yo * r_hi;
+        d1e = __builtin_amdgcn_cvt_pk_u8_f32(p1e, h, d1e);  // round half to even, clamp to [0, 255]
+        d1o = __builtin_amdgcn_cvt_pk_u8_f32(p1o, h, d1o);
+        d2e = __builtin_amdgcn_cvt_pk_u8_f32(p2e, h, d2e);
+        d2o = __builtin_amdgcn_cvt_pk_u8_f32(p2o, h, d2o);
+      }
+      uint32_t w = d1e | (d1o << 4);
+      const bool exact_u = uv >= 0x1p-125f && uv <= 0x1p+125f;
+      if (!exact_u | (d1e != d2e) | (d1o != d2o)) {
+        w = 0;
+        if (uv != 0.0f) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float y = a[v][e] - mnv;
+            float rr = __builtin_rintf(y / uv);
+            rr = __builtin_fminf(__builtin_fmaxf(rr, 0.0f), 15.0f);
+            w |= (uint32_t)rr << (4 * e);
+          }
+        }
+      }
+      if (!full) {
+        const int r = opaque_v(rem);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (8 * v + e >= r) w &= ~(0xFu << (4 * e));
+      }
+      wv[v] = w;
     }
-    w[v] = wv;
   }
   if ((int)eb < s) {
-    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w[0], w[1]}, re, eb >> 1, 0, 0);
-    if (pair_buckets) {
-      __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[0]), __float_as_uint(mx[0])}, rs,
-                                            eb, 0, 0);
-      if ((int)eb + 8 < s)
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[1]), __float_as_uint(mx[1])}, rs,
-                                              eb + 8, 0, 0);
-    } else if ((eb & ((1u << bl) - 1)) == 0) {
-      __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[0]), __float_as_uint(mx[0])}, rs,
-                                            (eb >> bl) * 8, 0, 0);
+    if (wide) {
+#pragma unroll
+      for (int q = 0; q < NV / 4; ++q)
+        __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]}, re,
+                                               (eb >> 1) + 16 * q, 0, 0);
+    } else {
+#pragma unroll
+      for (int q = 0; q < NV / 2; ++q)
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{wv[2 * q], wv[2 * q + 1]}, re, (eb >> 1) + 8 * q, 0, 0);
+    }
+    if constexpr (LB) {
+      if ((eb & ((1u << bl) - 1)) == 0)
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[0]), __float_as_uint(mx[0])}, rs,
+                                              (eb >> bl) * 8, 0, 0);
+    } else {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const uint32_t e0 = eb + 8 * v;
+        if ((e0 & ((1u << bl) - 1)) == 0 && (int)e0 < s)
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[v]), __float_as_uint(mx[v])}, rs,
+                                                (e0 >> bl) * 8, 0, 0);
+      }
     }
   }
 }
@@ -1164,11 +1221,31 @@ int64_t update_grid(size_t lds) {
   return cache[dev];
 }
 
-template <int NT, bool GB, bool VF>
-hipError_t launch_select_t(const StepParams& p, hipStream_t stream) {
-  const size_t lds = SelectLds<NT>::words() * 4;
-  hipLaunchKernelGGL((select_kernel<NT, GB, VF>), dim3((uint32_t)p.total_blocks), dim3(NT), lds, stream, p);
+template <int EPL, bool LB, bool GB, bool VF>
+hipError_t launch_select_t(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  const size_t lds = select_lds_words() * 4;
+  hipLaunchKernelGGL((select_kernel<EPL, LB, GB, VF>), dim3((uint32_t)count), dim3(kWave), lds, stream, p, first);
   return hipGetLastError();
+}
+
+// Elements per lane of the select kernel: 16, 32 or 64.
+inline int select_epl(int block) { return block <= 1024 ? 16 : block <= 2048 ? 32 : 64; }
+
+template <int EPL, bool GB, bool VF>
+hipError_t launch_select_e(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  // whole buckets per lane (B_q >= EPL) or buckets of whole vectors
+  if ((1 << p.bucket_log2) >= EPL) return launch_select_t<EPL, true, GB, VF>(p, first, count, stream);
+  return launch_select_t<EPL, false, GB, VF>(p, first, count, stream);
+}
+
+template <bool GB, bool VF>
+hipError_t launch_select_d(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  switch (select_epl(p.block)) {
+    case 16: return launch_select_e<16, GB, VF>(p, first, count, stream);
+    case 32: return launch_select_e<32, GB, VF>(p, first, count, stream);
+    default: return launch_select_e<64, GB, VF>(p, first, count, stream);
+  }
 }
 
 // Chunks of 64 window entries the update's leader wave processes per block:
@@ -1180,35 +1257,40 @@ inline int chunk_class(const StepParams& p) {
 }
 
 template <int NT, bool PB, bool VF, int KC>
-void launch_update_run(const StepParams& p, int64_t grid, int64_t per, size_t lds, hipStream_t stream) {
+void launch_update_run(const StepParams& p, int64_t first, int64_t count, int64_t grid, int64_t per, size_t lds,
+                       hipStream_t stream) {
   hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, true, KC>), dim3((uint32_t)grid), dim3(NT), lds, stream, p,
-                     (int64_t)0, p.n_full, per, (float*)nullptr, (float*)nullptr);
+                     first, count, per, (float*)nullptr, (float*)nullptr);
 }
 
-// The full blocks [0, n_full) in persistent runs, then the ragged blocks one
-// workgroup each.
+// The full blocks of [first, first + count) in persistent runs, then its
+// ragged blocks one workgroup each.
 template <int NT, bool PB, bool VF>
-hipError_t launch_update_t(const StepParams& p, hipStream_t stream) {
+hipError_t launch_update_t(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
   const size_t lds = update_lds_bytes<NT, VF>();
-  if (p.n_full > 0) {
+  const int64_t end = first + count;
+  const int64_t full_end = end < p.n_full ? end : p.n_full;
+  const int64_t n_run = full_end - first;
+  if (n_run > 0) {
     int64_t grid = update_grid<NT, PB, VF>(lds);
-    if (grid > p.n_full) grid = p.n_full;
-    const int64_t per = (p.n_full + grid - 1) / grid;
-    grid = (p.n_full + per - 1) / per;
+    if (grid > n_run) grid = n_run;
+    const int64_t per = (n_run + grid - 1) / grid;
+    grid = (n_run + per - 1) / per;
     switch (chunk_class(p)) {
-      case 4: launch_update_run<NT, PB, VF, 4>(p, grid, per, lds, stream); break;
-      case 8: launch_update_run<NT, PB, VF, 8>(p, grid, per, lds, stream); break;
-      case 10: launch_update_run<NT, PB, VF, 10>(p, grid, per, lds, stream); break;
-      case 12: launch_update_run<NT, PB, VF, 12>(p, grid, per, lds, stream); break;
-      default: launch_update_run<NT, PB, VF, 16>(p, grid, per, lds, stream); break;
+      case 4: launch_update_run<NT, PB, VF, 4>(p, first, n_run, grid, per, lds, stream); break;
+      case 8: launch_update_run<NT, PB, VF, 8>(p, first, n_run, grid, per, lds, stream); break;
+      case 10: launch_update_run<NT, PB, VF, 10>(p, first, n_run, grid, per, lds, stream); break;
+      case 12: launch_update_run<NT, PB, VF, 12>(p, first, n_run, grid, per, lds, stream); break;
+      default: launch_update_run<NT, PB, VF, 16>(p, first, n_run, grid, per, lds, stream); break;
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const int64_t tails = p.total_blocks - p.n_full;
+  const int64_t t0 = first > p.n_full ? first : p.n_full;
+  const int64_t tails = end - t0;
   if (tails > 0) {
     hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, false, 16>), dim3((uint32_t)tails), dim3(NT), lds, stream,
-                       p, p.n_full, tails, (int64_t)1, (float*)nullptr, (float*)nullptr);
+                       p, t0, tails, (int64_t)1, (float*)nullptr, (float*)nullptr);
     return hipGetLastError();
   }
   return hipSuccess;
@@ -1229,27 +1311,34 @@ size_t step_lds_bytes(int block, int k_full, int value_f32) {
   (void)k_full;
   (void)value_f32;
   const int nt = threads_for_block(block);
-  const size_t sel = (nt == 64 ? SelectLds<64>::words() : SelectLds<256>::words()) * 4;
+  const size_t sel = select_lds_words() * 4;
   const size_t upd = nt == 64 ? update_lds_bytes<64, true>() : update_lds_bytes<256, true>();
   return sel > upd ? sel : upd;
 }
 
-hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream) {
-  if (threads_for_block(p.block) == 64) {
-    if (grad_bf16) return value_f32 ? launch_select_t<64, true, true>(p, stream) : launch_select_t<64, true, false>(p, stream);
-    return value_f32 ? launch_select_t<64, false, true>(p, stream) : launch_select_t<64, false, false>(p, stream);
-  }
-  if (grad_bf16) return value_f32 ? launch_select_t<256, true, true>(p, stream) : launch_select_t<256, true, false>(p, stream);
-  return value_f32 ? launch_select_t<256, false, true>(p, stream) : launch_select_t<256, false, false>(p, stream);
+hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                         hipStream_t stream) {
+  if (grad_bf16)
+    return value_f32 ? launch_select_d<true, true>(p, first, count, stream)
+                     : launch_select_d<true, false>(p, first, count, stream);
+  return value_f32 ? launch_select_d<false, true>(p, first, count, stream)
+                   : launch_select_d<false, false>(p, first, count, stream);
 }
 
-hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, hipStream_t stream) {
+hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, int64_t first, int64_t count,
+                         hipStream_t stream) {
   if (threads_for_block(p.block) == 64) {
-    if (param_bf16) return value_f32 ? launch_update_t<64, true, true>(p, stream) : launch_update_t<64, true, false>(p, stream);
-    return value_f32 ? launch_update_t<64, false, true>(p, stream) : launch_update_t<64, false, false>(p, stream);
+    if (param_bf16)
+      return value_f32 ? launch_update_t<64, true, true>(p, first, count, stream)
+                       : launch_update_t<64, true, false>(p, first, count, stream);
+    return value_f32 ? launch_update_t<64, false, true>(p, first, count, stream)
+                     : launch_update_t<64, false, false>(p, first, count, stream);
   }
-  if (param_bf16) return value_f32 ? launch_update_t<256, true, true>(p, stream) : launch_update_t<256, true, false>(p, stream);
-  return value_f32 ? launch_update_t<256, false, true>(p, stream) : launch_update_t<256, false, false>(p, stream);
+  if (param_bf16)
+    return value_f32 ? launch_update_t<256, true, true>(p, first, count, stream)
+                     : launch_update_t<256, true, false>(p, first, count, stream);
+  return value_f32 ? launch_update_t<256, false, true>(p, first, count, stream)
+                   : launch_update_t<256, false, false>(p, first, count, stream);
 }
 
 hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_blocks, float* mhat,

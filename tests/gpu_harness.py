@@ -45,7 +45,7 @@ class GpuOracleRun:
     def __init__(self, numels, *, param_dtype=torch.float32, grad_dtype=torch.float32,
                  grad_dist="normal", grad_scale=1.0, lr=1e-3, seed=0, sample=None,
                  density=0.01, window=10, bucket=64, block=4096, value_f32=False,
-                 beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, device="cuda"):
+                 beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, ranges=1, device="cuda"):
         self.numels = list(numels)
         self.lr = lr
         self.device = torch.device(device)
@@ -59,6 +59,8 @@ class GpuOracleRun:
         self.params = [wl.draw(n, "normal", 0.02, seed + 7919 * (j + 1), self.device, param_dtype)
                        for j, n in enumerate(self.numels)]
         self.opt = ma.MicroAdam(self.params, self.cfg)
+        if ranges != 1:
+            self.opt.set_ranges(ranges)
         self.o = oracle.default()
         okw = dict(bucket=bucket, window=window, density=density, value_bf16=not value_f32,
                    param_bf16=param_dtype == torch.bfloat16, beta1=beta1, beta2=beta2, eps=eps,

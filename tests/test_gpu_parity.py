@@ -40,6 +40,12 @@ CASES = {
     "window_max_64": (dict(numels=[4096, 900], window=64, block=512, bucket=64, density=0.01), 66),
     "mixed_dtypes_bf16_param_f32_grad": (dict(numels=[6000], param_dtype=bf16, grad_dtype=f32,
                                               window=3), 4),
+    # steps split into block ranges (updates on the library's own stream):
+    # 7 blocks (5 full, 2 ragged) in 3 ranges, the last holding both kinds,
+    # and in 9 ranges, two of them empty
+    "ranges_3": (dict(numels=[4096 * 4 + 100, 70, 4096], param_dtype=bf16, grad_dtype=bf16,
+                      grad_scale=1e-3, window=3, ranges=3), 5),
+    "ranges_9": (dict(numels=[4096 * 4 + 100, 70, 4096], window=2, ranges=9), 4),
 }
 
 
