@@ -1168,36 +1168,43 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
     }
   };
 
-  // Two register sets take turns, and the next block is always fetched (the
-  // last block of a run fetches itself again), so that the count of loads
-  // issued after any block's data is fixed and the waits for that data let
-  // the next block's loads stay in flight.
+  // Workgroup w takes the blocks first_block + w + i*G (G workgroups), so
+  // that the blocks in work at any time are neighbours in memory.  Three
+  // register sets take turns, and the block two ahead is always fetched
+  // (past the last one the last block is fetched again), so that the count
+  // of loads issued after any block's data is fixed and the waits for that
+  // data let the next two blocks' loads stay in flight.
   if (!RUN) {
     UB A;
     fetch((int32_t)(first_block + block_id()), A);
     process(A);
     return;
   }
-  const int32_t nb = (int32_t)num_blocks, run = (int32_t)per;
-  const int32_t lo = (int32_t)block_id() * run;
-  if (lo >= nb) return;
-  const int32_t g0 = (int32_t)first_block;
-  const int32_t hi = g0 + (lo + run < nb ? lo + run : nb);
-  int32_t g = g0 + lo;
-  UB A, B;
+  (void)per;
+  const int32_t G = (int32_t)__builtin_amdgcn_grid_size_x() / NT;
+  const int32_t end = (int32_t)(first_block + num_blocks);
+  int32_t g = (int32_t)first_block + (int32_t)block_id();
+  if (g >= end) return;
+  auto nxt = [&](int32_t x) { return x + G < end ? x + G : x; };
+  UB A, B, C;
   fetch(g, A);
+  int32_t g1 = nxt(g);
+  fetch(g1, B);
   for (;;) {
-    const int32_t g1 = g + 1;
-    const bool m1 = g1 < hi;
-    fetch(m1 ? g1 : g, B);
+    const int32_t g2 = nxt(g1);
+    fetch(g2, C);
     process(A);
-    if (!m1) break;
-    const int32_t g2 = g1 + 1;
-    const bool m2 = g2 < hi;
-    fetch(m2 ? g2 : g1, A);
+    if (g1 == g) break;
+    const int32_t g3 = nxt(g2);
+    fetch(g3, A);
     process(B);
-    if (!m2) break;
-    g = g2;
+    if (g2 == g1) break;
+    const int32_t g4 = nxt(g3);
+    fetch(g4, B);
+    process(C);
+    if (g3 == g2) break;
+    g = g3;
+    g1 = g4;
   }
 }
 
