@@ -111,7 +111,8 @@ typedef struct microadam_handle_s* microadam_handle;
  *              max) of the bucket's residual; pair b covers the block's
  *              elements [b*B_q, (b+1)*B_q); pairs past its elements are
  *              unused.
- *   window     m*k_full*entry_bytes per block: row r (the row written at
+ *   window     m*k_full*entry_bytes per block, rounded up to a multiple
+ *              of 128 bytes (the stride): row r (the row written at
  *              step s is r = (s-1) mod m) starts at r*k_q*entry_bytes within
  *              the record and holds the block's k_q entries in ascending
  *              index order (k_q = k_last for the last block).  With bf16
@@ -138,7 +139,8 @@ typedef struct microadam_layout {
  * Size in bytes of the device state buffer for tensors of the given element
  * counts (numels[0..n_tensors), each >= 1).  Pure host computation: per
  * Top-K block B_d/2 bytes of EF codes, 8*B_d/B_q bytes of bucket stats and
- * m*k_full*entry_bytes of window, each plane 256-byte aligned.  This is the
+ * m*k_full*entry_bytes of window rounded up to 128 bytes, each plane
+ * 256-byte aligned.  This is the
  * paper's 0.5d + 4mk (Section 3.2) plus the (delta, Delta) metadata of
  * Section 3.1, per-block rounding of k and the padding of each tensor's last
  * block.

@@ -108,7 +108,9 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
   const int32_t k_full = (int32_t)block_k(B, c->density);
   pl.ef_stride = (uint64_t)B / 2;
   pl.stats_stride = (uint64_t)(B / Bq) * 8;
-  pl.win_stride = (uint64_t)m * k_full * eb;
+  // whole 128-byte lines per record, so that a row can be written as whole
+  // lines without touching another block's record
+  pl.win_stride = ((uint64_t)m * k_full * eb + 127) & ~(uint64_t)127;
   int64_t full = 0;
   for (int32_t j = 0; j < n; ++j) {
     const int64_t d = numels[j];
@@ -228,6 +230,7 @@ void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& 
   p.ef_plane = h->planes.ef;
   p.stats_plane = h->planes.stats;
   p.win_plane = h->planes.win;
+  p.win_stride = h->planes.win_stride;
   p.t = t;
   p.total_blocks = h->total_blocks;
   p.n_full = h->planes.n_full;

@@ -33,7 +33,8 @@ inline int threads_for_block(int block) { return block <= 1024 ? 64 : 256; }
 // State layout: three planes indexed by the global block number gb.
 //   EF codes       ef_plane    + gb * B_d/2
 //   (min, max)     stats_plane + gb * (B_d/B_q) * 8
-//   window rows    win_plane   + gb * m * k_full * entry_bytes
+//   window rows    win_plane   + gb * win_stride (m * k_full * entry_bytes
+//                  rounded up to whole 128-byte lines)
 // A block's window slot holds its m rows of k_q entries, row r at r*k_q.
 // Global blocks [0, n_full) are full (B_d elements, k_full entries per row);
 // blocks [n_full, total_blocks) are the ragged last blocks of tensors.
@@ -43,6 +44,7 @@ struct StepParams {
   const float* wpow;             // [2 * kMaxWindow]: beta1^r, then beta2^r
   uint8_t* state;
   uint64_t ef_plane, stats_plane, win_plane;  // byte offsets into state
+  uint64_t win_stride;           // bytes per block in the window plane (a multiple of 128)
   int64_t t;                     // step being taken (>= 1)
   int64_t total_blocks;
   int64_t n_full;                // full blocks (numbered first)

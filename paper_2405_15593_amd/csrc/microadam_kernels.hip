@@ -337,8 +337,7 @@ __device__ __forceinline__ Span span_of(const StepParams& p, int32_t gb, uint32_
 
 template <int EW>
 __device__ __forceinline__ Rsrc window_rsrc(const StepParams& p, int64_t gb, int kq) {
-  const uint64_t slot_bytes = (uint64_t)p.window * p.k_full * EW * 4;
-  return make_rsrc(p.state + p.win_plane + (uint64_t)gb * slot_bytes, (uint32_t)(p.window * kq * EW * 4));
+  return make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)(p.window * kq * EW * 4));
 }
 
 // ============================================================ select
@@ -360,7 +359,11 @@ __device__ __forceinline__ Rsrc window_rsrc(const StepParams& p, int64_t gb, int
 constexpr int kMaxCandVec = 128;   // candidate vectors gathered in LDS
 constexpr int kCandMax = 256;      // candidate elements resolved
 
-__host__ __device__ constexpr size_t select_lds_words() { return (size_t)kMaxCandVec * 9 + 2 * kCandMax; }
+constexpr int kRowBufWords = 320;  // the new row's 128-byte lines: k <= 128 entries of <= 8 bytes, + 2 lines
+
+__host__ __device__ constexpr size_t select_lds_words() {
+  return (size_t)kMaxCandVec * 9 + 2 * kCandMax + kRowBufWords;
+}
 
 // Orders the LDS accesses of one wave (each lane's writes before the other
 // lanes' later reads); LDS operations of a wave execute in order, so this
@@ -396,6 +399,7 @@ select_kernel(StepParams p, int64_t first) {
   uint32_t* const regi = smem + kMaxCandVec * 8;     // [kMaxCandVec] their first element
   float* const cval = (float*)(regi + kMaxCandVec);  // [kCandMax] candidate values
   uint32_t* const cidx = (uint32_t*)(cval + kCandMax);  // [kCandMax] candidate indices
+  uint32_t* const rowbuf = cidx + kCandMax;          // [kRowBufWords] the new row's lines
 
   const int lane = thread_id();
   const uint32_t eb = (uint32_t)lane * EPL;  // first element of this lane
@@ -438,6 +442,18 @@ select_kernel(StepParams p, int64_t first) {
   Raw8<GBF16> graw[NV];
 #pragma unroll
   for (int v = 0; v < NV; ++v) graw[v] = load8<GBF16>(rg, eb + 8 * v);
+  // The new row, bytes [row_lo, row_hi) of the block's window record, is
+  // written as the whole 128-byte lines [span_lo, span_hi) that cover it
+  // (records are whole lines): partial-line writes cost the memory system
+  // far more than their bytes.  The words of the first and last line that
+  // lie outside the row are read here and written back unchanged.
+  constexpr uint32_t EB = VF32 ? 8u : 4u;
+  const uint32_t row_lo = (uint32_t)p.new_slot * (uint32_t)kq * EB;
+  const uint32_t row_hi = row_lo + (uint32_t)kq * EB;
+  const uint32_t span_lo = row_lo & ~127u, span_hi = (row_hi + 127u) & ~127u;
+  const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
+  const uint32_t edge_off = lane < 32 ? span_lo + 4 * lane : span_hi - 128 + 4 * (lane - 32);
+  const uint32_t edge_old = __builtin_amdgcn_raw_buffer_load_b32(rrec, edge_off, 0, 0);
 
   // ---------------------------------------------- 1. a = g + Q^-1(e)
   float a[NV][8];
@@ -644,7 +660,12 @@ select_kernel(StepParams p, int64_t first) {
             if (lm) i_last = __builtin_amdgcn_readlane(ci[r], (int)__builtin_ctzll(lm));
             const bool sel = gt || (eq && rank < need);
             const uint64_t sm = ballot(sel);
-            if (sel) E::store(rw, row0 + sel_before + lanes_below(sm), E::make(ci[r], cf[r]));
+            if (sel) {
+              const uint32_t w = ((row_lo - span_lo) >> 2) + (sel_before + lanes_below(sm)) * (EB / 4);
+              const typename E::T x = E::make(ci[r], cf[r]);
+              if constexpr (VF32) *(u32x2*)(rowbuf + w) = x;
+              else rowbuf[w] = x;
+            }
             sel_before += popc(sm);
           }
         };
@@ -652,6 +673,13 @@ select_kernel(StepParams p, int64_t first) {
         if (nslot == 1) resolve(std::integral_constant<int, 1>{});
         else if (nslot == 2) resolve(std::integral_constant<int, 2>{});
         else resolve(std::integral_constant<int, 4>{});
+        // the lines of the new row: the row from the resolve, the rest of
+        // the first and last line as read
+        if (edge_off < row_lo || edge_off >= row_hi) rowbuf[(edge_off - span_lo) >> 2] = edge_old;
+        wave_sync();
+        const uint32_t nvec4 = (span_hi - span_lo) >> 4;
+        for (uint32_t q = (uint32_t)lane; q < nvec4; q += kWave)
+          __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)(rowbuf + 4 * q), rrec, span_lo + 16 * q, 0, 0);
       }
     }
   }
