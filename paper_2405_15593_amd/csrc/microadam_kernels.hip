@@ -3,14 +3,16 @@
 // One optimizer step is two launches over all Top-K blocks (B_d elements of
 // one tensor each; blocks share nothing):
 //
-//   select_kernel   one workgroup per block:
+//   select_kernel   one wave per block (lane l: elements [l*EPL, (l+1)*EPL)):
 //     1. a = g + Q^-1(e)                          (Algorithm 1; Algorithm 2, Q^-1)
 //     2. block Top-K of |a|, lower index wins ties (Section 3.1, "Top-K")
 //     3. the new window row (I, bf16(V)) is stored (Section 3.2)
-//     4. a[I] = 0; bucket (delta, Delta) = (min, max) by lane shuffles;
-//        e = Q(a, delta, Delta), two 4-bit codes per byte (Algorithm 1; Section 3.1)
+//     4. a[I] = 0; bucket (delta, Delta) = (min, max) in the lane or by lane
+//        shuffles; e = Q(a, delta, Delta), two 4-bit codes per byte
+//        (Algorithm 1; Section 3.1)
 //
-//   update_kernel   one workgroup per block:
+//   update_kernel   persistent workgroups of 256 threads (thread tid: the 16
+//   consecutive elements tid*16 + [0, 16) of each block it takes):
 //     5. one wave rebuilds m-hat, v-hat of the block's window entries in LDS
 //        from the m rows with weights beta^(t-s) (Algorithm 2, AdamStats)
 //     6. every wave applies theta <- (1 - eta*lambda) theta
@@ -18,11 +20,6 @@
 //
 // Splitting the step costs one extra read of the new window row (4 bytes per
 // kept entry) and lets each kernel keep a small register and LDS footprint.
-//
-// Element layout inside a block: thread `tid` owns the 16 consecutive
-// elements tid*16 + [0, 16), handled as two vectors of 8.  An EF bucket of
-// B_q >= 16 elements is held by B_q/16 neighbouring lanes; with B_q = 8 each
-// vector is one bucket.
 //
 // Arithmetic that decides an integer (EF decode, accumulator, Top-K order,
 // bucket min/max, codes) is binary32 with one rounding per written operation
