@@ -31,7 +31,6 @@ int hip_fail(hipError_t e, const char* what) {
 
 constexpr uint64_t kAlign = 256;
 constexpr size_t kMaxLds = 65536;        // dynamic LDS budget per workgroup
-constexpr int kMaxKernelBlock = 4096;    // largest B_d the step kernels cover
 
 uint64_t align_up(uint64_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 
@@ -72,8 +71,6 @@ int validate_config(const microadam_config* c) {
     return fail(MICROADAM_ERR_INVALID_ARG, "topk_block must be a multiple of ef_bucket");
   if (c->topk_block % 16 != 0)
     return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block must be a multiple of 16");
-  if (c->topk_block > kMaxKernelBlock)
-    return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block above 4096 is not implemented yet");
   if (c->window_value_dtype != MICROADAM_BF16 && c->window_value_dtype != MICROADAM_F32)
     return fail(MICROADAM_ERR_INVALID_ARG, "window_value_dtype must be BF16 or F32");
   if (c->reserved != 0) return fail(MICROADAM_ERR_INVALID_ARG, "reserved must be 0");
@@ -109,8 +106,10 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
   pl.ef_stride = (uint64_t)B / 2;
   pl.stats_stride = (uint64_t)(B / Bq) * 8;
   // whole 128-byte lines per record, so that a row can be written as whole
-  // lines without touching another block's record
-  pl.win_stride = ((uint64_t)m * k_full * eb + 127) & ~(uint64_t)127;
+  // lines without touching another block's record; blocks above 4096 add a
+  // table of m * ceil(B_d/4096) uint32 segment starts behind the rows
+  const uint64_t table = B > 4096 ? (uint64_t)m * ((B + 4095) / 4096) * 4 : 0;
+  pl.win_stride = ((uint64_t)m * k_full * eb + table + 127) & ~(uint64_t)127;
   int64_t full = 0;
   for (int32_t j = 0; j < n; ++j) {
     const int64_t d = numels[j];

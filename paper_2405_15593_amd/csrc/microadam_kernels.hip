@@ -385,6 +385,272 @@ __device__ __forceinline__ uint32_t lane_prefix(uint32_t c, uint32_t& total) {
   return pre;
 }
 
+// ------------------------------------------------ select: one lane's part
+// A lane (thread) of a select kernel owns the EPL consecutive elements
+// [eb, eb + EPL) of its block as NV = EPL/8 vectors of 8.  LB: its buckets
+// are the lane or groups of lanes (B_q >= EPL); else buckets of whole
+// vectors inside the lane.
+template <int EPL, bool LB, bool GBF16>
+struct LaneIn {
+  static constexpr int NV = EPL / 8;
+  u32x2 st[LB ? 1 : NV];  // bucket (min, max) pairs: one, or one per vector
+  uint32_t cw[NV];        // codes of vector v: element e in bits [4e, 4e + 4)
+  Raw8<GBF16> graw[NV];   // gradient
+};
+
+// Bucket pairs and codes of the lane.  `wide`: 16-byte code accesses (the
+// block fills every lane of the kernel), else 8-byte ones (B_d is a multiple
+// of 16, so no access then straddles the end of the block's codes).
+template <int EPL, bool LB, bool GBF16>
+__device__ __forceinline__ void lane_load_state(LaneIn<EPL, LB, GBF16>& in, Rsrc re, Rsrc rs, uint32_t eb, int bl,
+                                                bool wide) {
+  constexpr int NV = EPL / 8;
+#pragma unroll
+  for (int v = 0; v < (LB ? 1 : NV); ++v)
+    in.st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, 0);
+  if (NV > 2 && wide) {
+#pragma unroll
+    for (int q = 0; q < NV / 4; ++q) {
+      const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(re, (eb >> 1) + 16 * q, 0, 0);
+#pragma unroll
+      for (int h = 0; h < 4; ++h) in.cw[4 * q + h] = t[h];
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < NV / 2; ++q) {
+      const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(re, (eb >> 1) + 8 * q, 0, 0);
+      in.cw[2 * q] = t[0];
+      in.cw[2 * q + 1] = t[1];
+    }
+  }
+}
+
+template <int EPL, bool LB, bool GBF16>
+__device__ __forceinline__ void lane_load_grad(LaneIn<EPL, LB, GBF16>& in, Rsrc rg, uint32_t eb) {
+#pragma unroll
+  for (int v = 0; v < EPL / 8; ++v) in.graw[v] = load8<GBF16>(rg, eb + 8 * v);
+}
+
+// a = g + Q^-1(e) (Algorithm 1; Algorithm 2, Q^-1).  rem: the lane's
+// elements below the end of the block, [0, rem); the others are 0.
+template <int EPL, bool LB, bool GBF16>
+__device__ __forceinline__ void lane_decode(const LaneIn<EPL, LB, GBF16>& in, float (&a)[EPL / 8][8], int rem,
+                                            bool full) {
+  constexpr int NV = EPL / 8;
+  {
+    float lo0 = 0.0f, u0 = 0.0f;
+    if constexpr (LB) {
+      lo0 = __uint_as_float(in.st[0][0]);
+      u0 = div15(__uint_as_float(in.st[0][1]) - lo0);
+    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const float lo = LB ? lo0 : __uint_as_float(in.st[v][0]);
+      const float u = LB ? u0 : div15(__uint_as_float(in.st[v][1]) - lo);
+      const uint32_t ev = in.cw[v] & 0x0F0F0F0Fu, od = (in.cw[v] >> 4) & 0x0F0F0F0Fu;
+      float g[8], c[8];
+      unpack8<GBF16>(in.graw[v], g);
+      c[0] = ubyte<0>(ev); c[2] = ubyte<1>(ev); c[4] = ubyte<2>(ev); c[6] = ubyte<3>(ev);
+      c[1] = ubyte<0>(od); c[3] = ubyte<1>(od); c[5] = ubyte<2>(od); c[7] = ubyte<3>(od);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float sc = c[e] * u;
+        const float d = sc + lo;
+        a[v][e] = g[e] + d;
+      }
+    }
+  }
+  if (!full) {  // elements past the end of the tensor are 0 and never kept
+    const int r = opaque_v(rem);
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (8 * v + e >= r) a[v][e] = 0.0f;
+  }
+}
+
+template <int EPL>
+__device__ __forceinline__ void lane_vmax(const float (&a)[EPL / 8][8], float (&vmax)[EPL / 8]) {
+#pragma unroll
+  for (int v = 0; v < EPL / 8; ++v) {
+    const float m0 = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(a[v][0]), __builtin_fabsf(a[v][1])), __builtin_fabsf(a[v][2]));
+    const float m1 = __builtin_fmaxf(__builtin_fmaxf(m0, __builtin_fabsf(a[v][3])), __builtin_fabsf(a[v][4]));
+    const float m2 = __builtin_fmaxf(__builtin_fmaxf(m1, __builtin_fabsf(a[v][5])), __builtin_fabsf(a[v][6]));
+    vmax[v] = __builtin_fmaxf(m2, __builtin_fabsf(a[v][7]));
+  }
+}
+
+// e = Q(a with a[I] = 0) (Algorithm 1; Algorithm 2, Q; Section 3.1): zeroes
+// the kept elements (|a| > T, and |a| == T up to index i_last; every
+// |a| >= T when notie), computes the bucket (min, max) pairs and the codes,
+// and stores both.
+template <int EPL, bool LB>
+__device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint32_t T, bool notie,
+                                                    uint32_t i_last, uint32_t eb, int s, int rem, bool full, int bl,
+                                                    bool wide, Rsrc re, Rsrc rs) {
+  constexpr int NV = EPL / 8;
+  constexpr int lg = EPL == 16 ? 4 : EPL == 32 ? 5 : 6;
+  // kept elements: |a| > T, and |a| == T up to index i_last; without ties
+  // at the threshold that is |a| >= T (a wave-uniform case).  With ties the
+  // kept elements equal to T are zeroed first, and the rest are those
+  // with |a| >= the next float above T.
+  uint32_t Tk = T;
+  if (!notie) {
+    const float tf = opaque_f(__uint_as_float(T));
+    const int last_here = (int)i_last - (int)eb;  // this lane's elements up to i_last: [0, last_here]
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if ((__builtin_fabsf(a[v][e]) == tf) & (8 * v + e <= last_here)) a[v][e] = 0.0f;
+    Tk = T + 1u;
+  }
+  // (the values pass through an empty asm so that the compiler does not
+  // carry |a| of the tie pass into the test below in extra registers)
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) asm volatile("" : "+v"(a[v][e]));
+  {
+    const float tk = __uint_as_float(Tk);
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a[v][e] = (__builtin_fabsf(a[v][e]) >= tk) ? 0.0f : a[v][e];
+  }
+  // bucket min / max: per vector, then over the vectors of a bucket inside
+  // the lane, then over the lanes of a bucket
+  float mn[NV], mx[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    if (full) {
+      mn[v] = __builtin_fminf(__builtin_fminf(__builtin_fminf(a[v][0], a[v][1]), a[v][2]),
+                              __builtin_fminf(__builtin_fminf(a[v][3], a[v][4]), a[v][5]));
+      mn[v] = __builtin_fminf(mn[v], __builtin_fminf(a[v][6], a[v][7]));
+      mx[v] = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(a[v][0], a[v][1]), a[v][2]),
+                              __builtin_fmaxf(__builtin_fmaxf(a[v][3], a[v][4]), a[v][5]));
+      mx[v] = __builtin_fmaxf(mx[v], __builtin_fmaxf(a[v][6], a[v][7]));
+    } else {
+      mn[v] = __builtin_inff();
+      mx[v] = -__builtin_inff();
+      const int r = opaque_v(rem);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (8 * v + e < r) { mn[v] = __builtin_fminf(mn[v], a[v][e]); mx[v] = __builtin_fmaxf(mx[v], a[v][e]); }
+    }
+  }
+  if constexpr (LB) {
+    float lo = mn[0], hi = mx[0];
+#pragma unroll
+    for (int v = 1; v < NV; ++v) {
+      lo = __builtin_fminf(lo, mn[v]);
+      hi = __builtin_fmaxf(hi, mx[v]);
+    }
+    group_minmax(lo, hi, bl - lg);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      mn[v] = lo;
+      mx[v] = hi;
+    }
+  } else {
+    // B_q = 8 << j vectors... combine the 2^j vectors of each bucket
+#pragma unroll
+    for (int j = 0; (1 << j) < NV; ++j) {
+      if (bl - 3 > j) {
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          const int w = v ^ (1 << j);
+          if (w > v) {
+            const float l2 = __builtin_fminf(mn[v], mn[w]), h2 = __builtin_fmaxf(mx[v], mx[w]);
+            mn[v] = mn[w] = l2;
+            mx[v] = mx[w] = h2;
+          }
+        }
+      }
+    }
+  }
+  uint32_t wv[NV];
+  {
+    float uq = 0.0f, mnq = 0.0f;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      if (!LB || v == 0) {
+        mn[v] = mn[v] + 0.0f;  // a bucket bound of -0 is stored as +0
+        mx[v] = mx[v] + 0.0f;
+        mnq = mn[v];
+        uq = div15(mx[v] - mn[v]);
+      }
+      // Codes from two products that bracket the quotient: v_rcp is within
+      // 1 ulp for these u, so r_lo < 1/u < r_hi and
+      // rint((x-min)*r_lo) <= rint((x-min)/u) <= rint((x-min)*r_hi).  Where
+      // the two agree (all but a few elements in a million) the code is
+      // exact; elsewhere it is recomputed with an IEEE division.
+      const float uv = uq, mnv = mnq;
+      const float rcp = __builtin_amdgcn_rcpf(uv);
+      const float r_lo = __uint_as_float(__float_as_uint(rcp) - 2u);
+      const float r_hi = __uint_as_float(__float_as_uint(rcp) + 2u);
+      uint32_t d1e = 0, d1o = 0, d2e = 0, d2o = 0;
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const float ye = a[v][2 * h] - mnv, yo = a[v][2 * h + 1] - mnv;
+        const float p1e = ye * r_lo, p1o = yo * r_lo;
+        const float p2e = ye * r_hi, p2o = yo * r_hi;
+        d1e = __builtin_amdgcn_cvt_pk_u8_f32(p1e, h, d1e);  // round half to even, clamp to [0, 255]
+        d1o = __builtin_amdgcn_cvt_pk_u8_f32(p1o, h, d1o);
+        d2e = __builtin_amdgcn_cvt_pk_u8_f32(p2e, h, d2e);
+        d2o = __builtin_amdgcn_cvt_pk_u8_f32(p2o, h, d2o);
+      }
+      uint32_t w = d1e | (d1o << 4);
+      const bool exact_u = uv >= 0x1p-125f && uv <= 0x1p+125f;
+      if (!exact_u | (d1e != d2e) | (d1o != d2o)) {
+        w = 0;
+        if (uv != 0.0f) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float y = a[v][e] - mnv;
+            float rr = __builtin_rintf(y / uv);
+            rr = __builtin_fminf(__builtin_fmaxf(rr, 0.0f), 15.0f);
+            w |= (uint32_t)rr << (4 * e);
+          }
+        }
+      }
+      if (!full) {
+        const int r = opaque_v(rem);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (8 * v + e >= r) w &= ~(0xFu << (4 * e));
+      }
+      wv[v] = w;
+    }
+  }
+  if ((int)eb < s) {
+    if (NV > 2 && wide) {
+#pragma unroll
+      for (int q = 0; q < NV / 4; ++q)
+        __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]}, re,
+                                               (eb >> 1) + 16 * q, 0, 0);
+    } else {
+#pragma unroll
+      for (int q = 0; q < NV / 2; ++q)
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{wv[2 * q], wv[2 * q + 1]}, re, (eb >> 1) + 8 * q, 0, 0);
+    }
+    if constexpr (LB) {
+      if ((eb & ((1u << bl) - 1)) == 0)
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[0]), __float_as_uint(mx[0])}, rs,
+                                              (eb >> bl) * 8, 0, 0);
+    } else {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const uint32_t e0 = eb + 8 * v;
+        if ((e0 & ((1u << bl) - 1)) == 0 && (int)e0 < s)
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[v]), __float_as_uint(mx[v])}, rs,
+                                                (e0 >> bl) * 8, 0, 0);
+      }
+    }
+  }
+}
+
 template <int EPL, bool LB, bool GBF16, bool VF32>
 __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
 select_kernel(StepParams p, int64_t first) {
@@ -408,37 +674,14 @@ select_kernel(StepParams p, int64_t first) {
   const uint32_t nbk = (uint32_t)(p.block >> bl);
   const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * (p.block >> 1), (uint32_t)(p.block >> 1));
   const Rsrc rs = make_rsrc(p.state + p.stats_plane + (uint64_t)gb * nbk * 8, nbk * 8);
-  constexpr int NS_ST = LB ? 1 : NV;  // bucket pairs per lane: one, or one per vector
-  u32x2 st[NS_ST];
-#pragma unroll
-  for (int v = 0; v < NS_ST; ++v) st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, 0);
-  // Codes of vector v: element e in bits [4e, 4e + 4).  16-byte accesses
-  // when the block fills every lane, else 8-byte ones (B_d is a multiple of
-  // 16, so no access then straddles the end of the block's codes).
-  const bool wide = NV > 2 && p.block == CAP;
-  uint32_t cw[NV];
-  if (wide) {
-#pragma unroll
-    for (int q = 0; q < NV / 4; ++q) {
-      const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(re, (eb >> 1) + 16 * q, 0, 0);
-#pragma unroll
-      for (int h = 0; h < 4; ++h) cw[4 * q + h] = t[h];
-    }
-  } else {
-#pragma unroll
-    for (int q = 0; q < NV / 2; ++q) {
-      const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(re, (eb >> 1) + 8 * q, 0, 0);
-      cw[2 * q] = t[0];
-      cw[2 * q + 1] = t[1];
-    }
-  }
+  const bool wide = p.block == CAP;
+  LaneIn<EPL, LB, GBF16> in;
+  lane_load_state(in, re, rs, eb, bl, wide);
   const Block b = locate(p, gb);
   const int s = b.s, kq = b.kq;
   const bool full = s == CAP;
   const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + b.e0 * (GBF16 ? 2 : 4), vec_bytes<GBF16>(s));
-  Raw8<GBF16> graw[NV];
-#pragma unroll
-  for (int v = 0; v < NV; ++v) graw[v] = load8<GBF16>(rg, eb + 8 * v);
+  lane_load_grad(in, rg, eb);
   // The new row, bytes [row_lo, row_hi) of the block's window record, is
   // written as the whole 128-byte lines [span_lo, span_hi) that cover it
   // (records are whole lines): partial-line writes cost the memory system
@@ -454,49 +697,12 @@ select_kernel(StepParams p, int64_t first) {
 
   // ---------------------------------------------- 1. a = g + Q^-1(e)
   float a[NV][8];
-  {
-    float lo0 = 0.0f, u0 = 0.0f;
-    if constexpr (LB) {
-      lo0 = __uint_as_float(st[0][0]);
-      u0 = div15(__uint_as_float(st[0][1]) - lo0);
-    }
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      const float lo = LB ? lo0 : __uint_as_float(st[v][0]);
-      const float u = LB ? u0 : div15(__uint_as_float(st[v][1]) - lo);
-      const uint32_t ev = cw[v] & 0x0F0F0F0Fu, od = (cw[v] >> 4) & 0x0F0F0F0Fu;
-      float g[8], c[8];
-      unpack8<GBF16>(graw[v], g);
-      c[0] = ubyte<0>(ev); c[2] = ubyte<1>(ev); c[4] = ubyte<2>(ev); c[6] = ubyte<3>(ev);
-      c[1] = ubyte<0>(od); c[3] = ubyte<1>(od); c[5] = ubyte<2>(od); c[7] = ubyte<3>(od);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float sc = c[e] * u;
-        const float d = sc + lo;
-        a[v][e] = g[e] + d;
-      }
-    }
-  }
-  // elements of this lane below the end of the block: [0, rem)
-  const int rem = s - (int)eb;
-  if (!full) {  // elements past the end of the tensor are 0 and never kept
-    const int r = opaque_v(rem);
-#pragma unroll
-    for (int v = 0; v < NV; ++v)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (8 * v + e >= r) a[v][e] = 0.0f;
-  }
+  const int rem = s - (int)eb;  // this lane's elements below the end of the block: [0, rem)
+  lane_decode(in, a, rem, full);
 
   // ---------------------------------------------- 2. Top-K threshold
   float vmax[NV];
-#pragma unroll
-  for (int v = 0; v < NV; ++v) {
-    const float m0 = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(a[v][0]), __builtin_fabsf(a[v][1])), __builtin_fabsf(a[v][2]));
-    const float m1 = __builtin_fmaxf(__builtin_fmaxf(m0, __builtin_fabsf(a[v][3])), __builtin_fabsf(a[v][4]));
-    const float m2 = __builtin_fmaxf(__builtin_fmaxf(m1, __builtin_fabsf(a[v][5])), __builtin_fabsf(a[v][6]));
-    vmax[v] = __builtin_fmaxf(m2, __builtin_fabsf(a[v][7]));
-  }
+  lane_vmax<EPL>(a, vmax);
   const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
   const uint32_t row0 = (uint32_t)p.new_slot * kq;
 
@@ -779,164 +985,351 @@ select_kernel(StepParams p, int64_t first) {
   }
 
   // ---------------------------------------------- 4. e = Q(a with a[I] = 0)
-  // kept elements: |a| > T, and |a| == T up to index i_last; without ties
-  // at the threshold that is |a| >= T (a wave-uniform case).  With ties the
-  // kept elements equal to T are zeroed first, and the rest are those
-  // with |a| >= the next float above T.
-  uint32_t Tk = T;
-  if (!notie) {
-    const float tf = opaque_f(__uint_as_float(T));
-    const int last_here = (int)i_last - (int)eb;  // this lane's elements up to i_last: [0, last_here]
+  lane_quantize_store<EPL, LB>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs);
+}
+
+// ================================================ select, blocks above 4096
+// NW waves per block (B_d <= NW*4096); thread t owns the 64 consecutive
+// elements [64t, 64t + 64), so wave w holds the block's 4096-element
+// sub-block w.  The k-th largest |a| comes from an exact bitwise search over
+// every element with workgroup-wide counts (one barrier per bit).  The new
+// row is written in element order, and for each sub-block the position in
+// the row of its first entry goes to the record's segment table, behind the
+// m rows, where the update finds the entries of one sub-block.
+constexpr int kSubBlock = 4096;
+
+template <int NW>
+struct LargeLds {
+  static constexpr size_t words() { return (size_t)2 * NW + 2 * NW + 4; }
+};
+
+template <int NW, bool LB, bool GBF16, bool VF32>
+__global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, int64_t first) {
+  constexpr int EPL = 64, NV = 8, NT = NW * kWave, CAP = NT * EPL;
+  using E = Entry<VF32>;
+  extern __shared__ __align__(16) uint32_t smem[];
+  uint32_t* const cnt = smem;           // [2][NW] per-wave counts, alternating between searches
+  uint32_t* const pre = cnt + 2 * NW;   // [2][NW] per-wave totals of the two element-order scans
+  uint32_t* const misc = pre + 2 * NW;  // [4]
+
+  const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
+  const uint32_t eb = (uint32_t)tid * EPL;
+  const int bl = p.bucket_log2;
+  const int64_t gb = first + block_id();
+
+  const uint32_t nbk = (uint32_t)(p.block >> bl);
+  const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * (p.block >> 1), (uint32_t)(p.block >> 1));
+  const Rsrc rs = make_rsrc(p.state + p.stats_plane + (uint64_t)gb * nbk * 8, nbk * 8);
+  const bool wide = p.block == CAP;
+  LaneIn<EPL, LB, GBF16> in;
+  lane_load_state(in, re, rs, eb, bl, wide);
+  const Block b = locate(p, gb);
+  const int s = b.s, kq = b.kq;
+  const bool full = s == CAP;
+  const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + b.e0 * (GBF16 ? 2 : 4), vec_bytes<GBF16>(s));
+  lane_load_grad(in, rg, eb);
+
+  // ---------------------------------------------- 1. a = g + Q^-1(e)
+  float a[NV][8];
+  const int rem = s - (int)eb;
+  lane_decode(in, a, rem, full);
+
+  // workgroup sum of one value per wave; `buf` alternates between calls
+  auto wg_sum = [&](uint32_t wave_value, int buf) {
+    if (lane == 0) cnt[buf * NW + wave] = wave_value;
+    lds_sync();
+    uint32_t t = 0;
 #pragma unroll
-    for (int v = 0; v < NV; ++v)
+    for (int w = 0; w < NW; ++w) t += cnt[buf * NW + w];
+    return sgpr(t);
+  };
+  // exclusive prefix in element order of a per-thread count below 128, and
+  // the workgroup total; `slot` selects one of the two scan buffers
+  auto wg_scan = [&](uint32_t c, int slot, uint32_t& total) {
+    uint32_t in_wave = 0, wave_total = 0;
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if ((__builtin_fabsf(a[v][e]) == tf) & (8 * v + e <= last_here)) a[v][e] = 0.0f;
-    Tk = T + 1u;
-  }
-  // (the values pass through an empty asm so that the compiler does not
-  // carry |a| of the tie pass into the test below in extra registers)
-#pragma unroll
-  for (int v = 0; v < NV; ++v)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) asm volatile("" : "+v"(a[v][e]));
-  {
-    const float tk = __uint_as_float(Tk);
-#pragma unroll
-    for (int v = 0; v < NV; ++v)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) a[v][e] = (__builtin_fabsf(a[v][e]) >= tk) ? 0.0f : a[v][e];
-  }
-  // bucket min / max: per vector, then over the vectors of a bucket inside
-  // the lane, then over the lanes of a bucket
-  float mn[NV], mx[NV];
-#pragma unroll
-  for (int v = 0; v < NV; ++v) {
-    if (full) {
-      mn[v] = __builtin_fminf(__builtin_fminf(__builtin_fminf(a[v][0], a[v][1]), a[v][2]),
-                              __builtin_fminf(__builtin_fminf(a[v][3], a[v][4]), a[v][5]));
-      mn[v] = __builtin_fminf(mn[v], __builtin_fminf(a[v][6], a[v][7]));
-      mx[v] = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(a[v][0], a[v][1]), a[v][2]),
-                              __builtin_fmaxf(__builtin_fmaxf(a[v][3], a[v][4]), a[v][5]));
-      mx[v] = __builtin_fmaxf(mx[v], __builtin_fmaxf(a[v][6], a[v][7]));
-    } else {
-      mn[v] = __builtin_inff();
-      mx[v] = -__builtin_inff();
-      const int r = opaque_v(rem);
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (8 * v + e < r) { mn[v] = __builtin_fminf(mn[v], a[v][e]); mx[v] = __builtin_fmaxf(mx[v], a[v][e]); }
+    for (int b2 = 0; b2 < 7; ++b2) {
+      const uint64_t m = ballot((c >> b2) & 1u);
+      in_wave += lanes_below(m) << b2;
+      wave_total += popc(m) << b2;
     }
-  }
-  if constexpr (LB) {
-    float lo = mn[0], hi = mx[0];
+    if (lane == 0) pre[slot * NW + wave] = wave_total;
+    lds_sync();
+    uint32_t before = 0, all = 0;
 #pragma unroll
-    for (int v = 1; v < NV; ++v) {
-      lo = __builtin_fminf(lo, mn[v]);
-      hi = __builtin_fmaxf(hi, mx[v]);
+    for (int w = 0; w < NW; ++w) {
+      const uint32_t x = pre[slot * NW + w];
+      all += x;
+      before += w < wave ? x : 0u;
     }
-    constexpr int lg = EPL == 16 ? 4 : EPL == 32 ? 5 : 6;
-    group_minmax(lo, hi, bl - lg);
+    total = sgpr(all);
+    return sgpr(before) + in_wave;
+  };
+
+  // ---------------------------------------------- 2. Top-K (exact search)
+  uint32_t t = 0;
+  bool exact = false;
+  int buf = 0;
+  for (int bit = 30; bit >= 0 && !exact; --bit) {
+    const uint32_t c = t | (1u << bit);
+    const float cf = __uint_as_float(c);
+    uint32_t n = 0;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
-      mn[v] = lo;
-      mx[v] = hi;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) n += popc(ballot(__builtin_fabsf(a[v][e]) >= cf));
+      __builtin_amdgcn_sched_barrier(0);  // bounds the masks in flight
     }
+    n = wg_sum(n, buf);
+    buf ^= 1;
+    if (n >= (uint32_t)kq) {
+      t = c;
+      exact = n == (uint32_t)kq;
+    }
+  }
+  const uint32_t T = t;
+  uint32_t i_last = 0;
+  bool notie = exact;
+  uint32_t sel_l = 0;
+  if (exact) {
+    const float tf = opaque_f(__uint_as_float(t));
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sel_l += __builtin_fabsf(a[v][e]) >= tf ? 1u : 0u;
   } else {
-    // B_q = 8 << j vectors... combine the 2^j vectors of each bucket
+    // the keys above t are kept, then the first `need` keys equal to t in
+    // element order
+    const float tf = opaque_f(__uint_as_float(t));
+    uint32_t ngt_l = 0, neq_l = 0;
 #pragma unroll
-    for (int j = 0; (1 << j) < NV; ++j) {
-      if (bl - 3 > j) {
+    for (int v = 0; v < NV; ++v)
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          const int w = v ^ (1 << j);
-          if (w > v) {
-            const float l2 = __builtin_fminf(mn[v], mn[w]), h2 = __builtin_fmaxf(mx[v], mx[w]);
-            mn[v] = mn[w] = l2;
-            mx[v] = mx[w] = h2;
-          }
-        }
+      for (int e = 0; e < 8; ++e) {
+        ngt_l += __builtin_fabsf(a[v][e]) > tf ? 1u : 0u;
+        neq_l += __builtin_fabsf(a[v][e]) == tf ? 1u : 0u;
       }
-    }
-  }
-  uint32_t wv[NV];
-  {
-    float uq = 0.0f, mnq = 0.0f;
+    uint32_t ngt_w = 0;
 #pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      if (!LB || v == 0) {
-        mn[v] = mn[v] + 0.0f;  // a bucket bound of -0 is stored as +0
-        mx[v] = mx[v] + 0.0f;
-        mnq = mn[v];
-        uq = div15(mx[v] - mn[v]);
-      }
-      // Codes from two products that bracket the quotient: v_rcp is within
-      // 1 ulp for these u, so r_lo < 1/u < r_hi and
-      // rint((x-min)*r_lo) <= rint((x-min)/u) <= rint((x-min)*r_hi).  Where
-      // the two agree (all but a few elements in a million) the code is
-      // exact; elsewhere it is recomputed with an IEEE division.
-      const float uv = uq, mnv = mnq;
-      const float rcp = __builtin_amdgcn_rcpf(uv);
-      const float r_lo = __uint_as_float(__float_as_uint(rcp) - 2u);
-      const float r_hi = __uint_as_float(__float_as_uint(rcp) + 2u);
-      uint32_t d1e = 0, d1o = 0, d2e = 0, d2o = 0;
+    for (int b2 = 0; b2 < 7; ++b2) ngt_w += popc(ballot((ngt_l >> b2) & 1u)) << b2;
+    const uint32_t need = (uint32_t)kq - wg_sum(ngt_w, buf);  // >= 1
+    uint32_t neq_all;
+    const uint32_t eq_pre = wg_scan(neq_l, 0, neq_all);
+    if (eq_pre < need && eq_pre + neq_l >= need) {  // the thread holding the need-th equal key
+      const float tf2 = opaque_f(tf);
+      uint32_t r = eq_pre, my_last = 0;
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        const float ye = a[v][2 * h] - mnv, yo = a[v][2 * h + 1] - mnv;
-        const float p1e = ye * r_lo, p1o = yo * r_lo;
-        const float p2e = ye * r_hi, p2o = yo * r_hi;
-        d1e = __builtin_amdgcn_cvt_pk_u8_f32(p1e, h, d1e);  // round half to even, clamp to [0, 255]
-        d1o = __builtin_amdgcn_cvt_pk_u8_f32(p1o, h, d1o);
-        d2e = __builtin_amdgcn_cvt_pk_u8_f32(p2e, h, d2e);
-        d2o = __builtin_amdgcn_cvt_pk_u8_f32(p2o, h, d2o);
-      }
-      uint32_t w = d1e | (d1o << 4);
-      const bool exact_u = uv >= 0x1p-125f && uv <= 0x1p+125f;
-      if (!exact_u | (d1e != d2e) | (d1o != d2o)) {
-        w = 0;
-        if (uv != 0.0f) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float y = a[v][e] - mnv;
-            float rr = __builtin_rintf(y / uv);
-            rr = __builtin_fminf(__builtin_fmaxf(rr, 0.0f), 15.0f);
-            w |= (uint32_t)rr << (4 * e);
-          }
-        }
-      }
-      if (!full) {
-        const int r = opaque_v(rem);
+      for (int v = 0; v < NV; ++v)
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          if (8 * v + e >= r) w &= ~(0xFu << (4 * e));
+          if (__builtin_fabsf(a[v][e]) == tf2) {
+            if (r == need - 1) my_last = eb + 8 * v + e;
+            ++r;
+          }
+      misc[0] = my_last;
+    }
+    lds_sync();
+    i_last = sgpr(misc[0]);
+    notie = neq_all == need;
+    const int last_here = (int)i_last - (int)eb;
+    const float tf3 = opaque_f(tf);
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float ab = __builtin_fabsf(a[v][e]);
+        sel_l += ((ab > tf3) | ((ab == tf3) & (8 * v + e <= last_here))) ? 1u : 0u;
       }
-      wv[v] = w;
-    }
   }
-  if ((int)eb < s) {
-    if (wide) {
-#pragma unroll
-      for (int q = 0; q < NV / 4; ++q)
-        __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]}, re,
-                                               (eb >> 1) + 16 * q, 0, 0);
-    } else {
-#pragma unroll
-      for (int q = 0; q < NV / 2; ++q)
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{wv[2 * q], wv[2 * q + 1]}, re, (eb >> 1) + 8 * q, 0, 0);
-    }
-    if constexpr (LB) {
-      if ((eb & ((1u << bl) - 1)) == 0)
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[0]), __float_as_uint(mx[0])}, rs,
-                                              (eb >> bl) * 8, 0, 0);
-    } else {
+  {
+    // the new row in element order, and the segment table entry of this
+    // wave's sub-block: the row position of its first entry
+    uint32_t kept_all;
+    uint32_t pos = wg_scan(sel_l, 1, kept_all);
+    constexpr uint32_t EB = VF32 ? 8u : 4u;
+    const int nsub = (p.block + kSubBlock - 1) / kSubBlock;
+    const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
+    if (lane == 0 && wave < nsub)
+      __builtin_amdgcn_raw_buffer_store_b32(pos, rrec,
+                                            (uint32_t)p.window * p.k_full * EB + ((uint32_t)p.new_slot * nsub + wave) * 4,
+                                            0, 0);
+    if (sel_l) {
+      const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
+      const uint32_t row0 = (uint32_t)p.new_slot * kq;
+      const float tf = opaque_f(__uint_as_float(T));
+      const int last_here = notie ? CAP : (int)i_last - (int)eb;
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
-        const uint32_t e0 = eb + 8 * v;
-        if ((e0 & ((1u << bl) - 1)) == 0 && (int)e0 < s)
-          __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[v]), __float_as_uint(mx[v])}, rs,
-                                                (e0 >> bl) * 8, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float ab = __builtin_fabsf(a[v][e]);
+          if ((ab > tf) | ((ab == tf) & (8 * v + e <= last_here))) {
+            E::store(rw, row0 + pos, E::make(eb + 8 * v + e, a[v][e]));
+            ++pos;
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);  // one vector's stores at a time
       }
     }
+  }
+
+  // ---------------------------------------------- 4. e = Q(a with a[I] = 0)
+  lane_quantize_store<EPL, LB>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs);
+}
+
+// ================================================ update, blocks above 4096
+// One workgroup of 256 threads per 4096-element sub-block j of a block
+// (thread tid: the sub-block's elements 16*tid + [0, 16)).  The live rows'
+// entries of sub-block j are the segments the select kernel recorded; they are
+// staged in LDS in batches of kStageLarge, oldest row first, and one wave
+// rebuilds z1 = sum beta1^r V and z2 = sum beta2^r V^2 from them in that
+// order (Algorithm 2, AdamStats).  Every thread then turns its own 16
+// elements' sums into the update (an element without entries has sums 0 and
+// a decrement of 0) and applies it (Algorithm 1; Algorithm 4).
+constexpr int kStageLarge = 2048;
+
+template <bool VF>
+constexpr size_t update_large_lds_bytes() {
+  return (size_t)2 * (kSubBlock + kWave) * 4 + (size_t)3 * kWave * 4 + (size_t)kStageLarge * (VF ? 8 : 4);
+}
+
+template <bool PBF16, bool VF32, bool EXPORT>
+__global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t first_block, int32_t nsub,
+                                                           float* mhat, float* vhat) {
+  constexpr int NT = 256;
+  using E = Entry<VF32>;
+  using ET = typename E::T;
+  extern __shared__ __align__(16) uint32_t smem[];
+  float* const z1 = (float*)smem;                // [kSubBlock] + sink words
+  float* const z2 = z1 + kSubBlock + kWave;
+  uint32_t* const seg_lo = (uint32_t*)(z2 + kSubBlock + kWave);  // [kWave] by row age
+  uint32_t* const seg_n = seg_lo + kWave;
+  uint32_t* const seg_at = seg_n + kWave;       // position of the row's first entry in the staged order
+  ET* const stage = (ET*)(seg_at + kWave);       // [kStageLarge]
+
+  const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
+  const int64_t wg = block_id();
+  const int32_t gb = (int32_t)(first_block + wg / nsub);
+  const int j = (int)(wg % nsub);
+  const Span g = span_of(p, gb, PBF16 ? 2 : 4);
+  const int lo = j * kSubBlock;
+  if (lo >= g.s) return;  // a sub-block past the end of a ragged block
+  const int s = g.s - lo < kSubBlock ? g.s - lo : kSubBlock;
+  const int kq = g.kq, m = p.window, n_live = p.n_live;
+  const int slot0 = (p.new_slot + 1 + m - n_live) % m;  // oldest live row first
+  const int nsub_blk = (p.block + kSubBlock - 1) / kSubBlock;  // table entries per row
+
+  // the live rows' segments of sub-block j (row age r = 0 is the oldest)
+  constexpr uint32_t EB = VF32 ? 8u : 4u;
+  const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
+  const uint32_t table = (uint32_t)m * p.k_full * EB;
+  if (tid < n_live) {
+    const int slot = (slot0 + tid) % m;
+    const uint32_t a0 = __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)slot * nsub_blk + j) * 4, 0, 0);
+    const uint32_t a1 = j + 1 < nsub_blk
+                            ? __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)slot * nsub_blk + j + 1) * 4, 0, 0)
+                            : (uint32_t)kq;
+    seg_lo[tid] = (uint32_t)slot * kq + a0;  // entry number in the record
+    seg_n[tid] = a1 - a0;
+  }
+  {
+    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      *(float4*)(z1 + tid * 16 + 4 * q) = zero;
+      *(float4*)(z2 + tid * 16 + 4 * q) = zero;
+    }
+  }
+  lds_sync();
+  uint32_t total = 0;
+  for (int r = 0; r < n_live; ++r) total += seg_n[r];
+  if (tid == 0) {
+    uint32_t at = 0;
+    for (int r = 0; r < n_live; ++r) {
+      seg_at[r] = at;
+      at += seg_n[r];
+    }
+  }
+  lds_sync();
+
+  const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
+  const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
+  const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
+  for (uint32_t b0 = 0; b0 < total; b0 += kStageLarge) {
+    const uint32_t b1 = total - b0 < (uint32_t)kStageLarge ? total : b0 + kStageLarge;
+    // stage the entries [b0, b1) of the concatenated segments
+    for (int r = 0; r < n_live; ++r) {
+      const uint32_t at = seg_at[r], n = seg_n[r];
+      const uint32_t x0 = at > b0 ? at : b0, x1 = at + n < b1 ? at + n : b1;
+      for (uint32_t x = x0 + tid; x < x1; x += NT) stage[x - b0] = E::load(rw, seg_lo[r] + (x - at));
+    }
+    lds_sync();
+    if (wave == 0) {
+      // row by row, oldest first, 64 entries at a time: the entries of one
+      // row have distinct indices, so each chunk reads, adds and writes its
+      // words (lanes without an entry work on the sink words)
+      for (int r = 0; r < n_live; ++r) {
+        const uint32_t at = seg_at[r], n = seg_n[r];
+        const uint32_t x0 = at > b0 ? at : b0, x1 = at + n < b1 ? at + n : b1;
+        const int age = n_live - 1 - r;
+        const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), age));
+        const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), age));
+        for (uint32_t x = x0; x < x1; x += kWave) {
+          const bool have = x + lane < x1;
+          const ET e = stage[have ? x + lane - b0 : 0];
+          const uint32_t i = E::idx(e) - (uint32_t)lo;
+          const uint32_t zp = have && i < (uint32_t)s ? i : (uint32_t)(kSubBlock + lane);
+          const float v = E::val(e);
+          const float x1v = w1 * v, x2v = w2 * (v * v);
+          const float a1 = z1[zp], a2 = z2[zp];
+          z1[zp] = a1 + x1v;
+          z2[zp] = a2 + x2v;
+        }
+      }
+    }
+    lds_sync();
+  }
+
+  // every thread: its 16 elements
+  const uint32_t eb = (uint32_t)tid * 16;
+  if ((int)eb >= s) return;
+  float s1[16], s2[16];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 u1 = *(const float4*)(z1 + eb + 4 * q);
+    const float4 u2 = *(const float4*)(z2 + eb + 4 * q);
+    s1[4 * q] = u1.x; s1[4 * q + 1] = u1.y; s1[4 * q + 2] = u1.z; s1[4 * q + 3] = u1.w;
+    s2[4 * q] = u2.x; s2[4 * q + 1] = u2.y; s2[4 * q + 2] = u2.z; s2[4 * q + 3] = u2.w;
+  }
+  if (EXPORT) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if ((int)eb + e < s) {
+        mhat[g.e0 + lo + eb + e] = p.c1 * s1[e];
+        vhat[g.e0 + lo + eb + e] = p.c2 * s2[e];
+      }
+    return;
+  }
+  const int es = PBF16 ? 2 : 4;
+  const Rsrc rp = make_rsrc((const void*)(g.base + (uint64_t)lo * es), vec_bytes<PBF16>(s));
+  const bool full = s == kSubBlock;
+#pragma unroll
+  for (int v = 0; v < 2; ++v) {
+    const Raw8<PBF16> th = load8<PBF16>(rp, eb + 8 * v);
+    float thf[8], out[8];
+    unpack8<PBF16>(th, thf);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float mh = p.c1 * s1[8 * v + e];
+      const float vh = p.c2 * s2[8 * v + e];
+      const float den = p.eps + __builtin_amdgcn_sqrtf(vh);
+      // an element without entries is left to the decay alone
+      const bool none = (s1[8 * v + e] == 0.0f) & (s2[8 * v + e] == 0.0f);
+      const float d = none ? 0.0f : p.lr * (mh * __builtin_amdgcn_rcpf(den));
+      const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
+      out[e] = base - d;
+    }
+    store8<PBF16>(rp, eb + 8 * v, s, full, out);
   }
 }
 
@@ -1264,6 +1657,46 @@ hipError_t launch_select_t(const StepParams& p, int64_t first, int64_t count, hi
 // Elements per lane of the select kernel: 16, 32 or 64.
 inline int select_epl(int block) { return block <= 1024 ? 16 : block <= 2048 ? 32 : 64; }
 
+// Waves of the large-block select kernel: 4096 elements each, 2 to 16.
+inline int large_waves(int block) {
+  const int w = (block + kSubBlock - 1) / kSubBlock;
+  return w <= 2 ? 2 : w <= 4 ? 4 : w <= 8 ? 8 : 16;
+}
+
+template <int NW, bool GB, bool VF>
+hipError_t launch_select_large_t(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  const size_t lds = LargeLds<NW>::words() * 4;
+  if ((1 << p.bucket_log2) >= 64)
+    hipLaunchKernelGGL((select_large_kernel<NW, true, GB, VF>), dim3((uint32_t)count), dim3(NW * kWave), lds, stream,
+                       p, first);
+  else
+    hipLaunchKernelGGL((select_large_kernel<NW, false, GB, VF>), dim3((uint32_t)count), dim3(NW * kWave), lds,
+                       stream, p, first);
+  return hipGetLastError();
+}
+
+template <bool GB, bool VF>
+hipError_t launch_select_large(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  switch (large_waves(p.block)) {
+    case 2: return launch_select_large_t<2, GB, VF>(p, first, count, stream);
+    case 4: return launch_select_large_t<4, GB, VF>(p, first, count, stream);
+    case 8: return launch_select_large_t<8, GB, VF>(p, first, count, stream);
+    default: return launch_select_large_t<16, GB, VF>(p, first, count, stream);
+  }
+}
+
+// One workgroup per 4096-element sub-block of each block of [first, first + count).
+template <bool PB, bool VF, bool EXPORT>
+hipError_t launch_update_large(const StepParams& p, int64_t first, int64_t count, float* mh, float* vh,
+                               hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  const int32_t nsub = (p.block + kSubBlock - 1) / kSubBlock;
+  hipLaunchKernelGGL((update_large_kernel<PB, VF, EXPORT>), dim3((uint32_t)(count * nsub)), dim3(256),
+                     update_large_lds_bytes<VF>(), stream, p, first, nsub, mh, vh);
+  return hipGetLastError();
+}
+
 template <int EPL, bool GB, bool VF>
 hipError_t launch_select_e(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
   // whole buckets per lane (B_q >= EPL) or buckets of whole vectors
@@ -1273,6 +1706,7 @@ hipError_t launch_select_e(const StepParams& p, int64_t first, int64_t count, hi
 
 template <bool GB, bool VF>
 hipError_t launch_select_d(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  if (p.block > kSubBlock) return launch_select_large<GB, VF>(p, first, count, stream);
   switch (select_epl(p.block)) {
     case 16: return launch_select_e<16, GB, VF>(p, first, count, stream);
     case 32: return launch_select_e<32, GB, VF>(p, first, count, stream);
@@ -1343,6 +1777,7 @@ size_t step_lds_bytes(int block, int k_full, int value_f32) {
   (void)k_full;
   (void)value_f32;
   const int nt = threads_for_block(block);
+  if (block > kSubBlock) return update_large_lds_bytes<true>();
   const size_t sel = select_lds_words() * 4;
   const size_t upd = nt == 64 ? update_lds_bytes<64, true>() : update_lds_bytes<256, true>();
   return sel > upd ? sel : upd;
@@ -1359,6 +1794,13 @@ hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, int6
 
 hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, int64_t first, int64_t count,
                          hipStream_t stream) {
+  if (p.block > kSubBlock) {
+    if (param_bf16)
+      return value_f32 ? launch_update_large<true, true, false>(p, first, count, nullptr, nullptr, stream)
+                       : launch_update_large<true, false, false>(p, first, count, nullptr, nullptr, stream);
+    return value_f32 ? launch_update_large<false, true, false>(p, first, count, nullptr, nullptr, stream)
+                     : launch_update_large<false, false, false>(p, first, count, nullptr, nullptr, stream);
+  }
   if (threads_for_block(p.block) == 64) {
     if (param_bf16)
       return value_f32 ? launch_update_t<64, true, true>(p, first, count, stream)
@@ -1375,6 +1817,9 @@ hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, int
 
 hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_blocks, float* mhat,
                           float* vhat, int value_f32, hipStream_t stream) {
+  if (p.block > kSubBlock)
+    return value_f32 ? launch_update_large<false, true, true>(p, first_block, num_blocks, mhat, vhat, stream)
+                     : launch_update_large<false, false, true>(p, first_block, num_blocks, mhat, vhat, stream);
   if (threads_for_block(p.block) == 64)
     return value_f32 ? launch_export<64, true>(p, first_block, num_blocks, mhat, vhat, stream)
                      : launch_export<64, false>(p, first_block, num_blocks, mhat, vhat, stream);

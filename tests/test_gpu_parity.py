@@ -46,6 +46,14 @@ CASES = {
     "ranges_3": (dict(numels=[4096 * 4 + 100, 70, 4096], param_dtype=bf16, grad_dtype=bf16,
                       grad_scale=1e-3, window=3, ranges=3), 5),
     "ranges_9": (dict(numels=[4096 * 4 + 100, 70, 4096], window=2, ranges=9), 4),
+    # blocks above 4096 (several waves per block in the select, sub-blocks of
+    # 4096 in the update): B_d = 8192 with binary32 window values, and a
+    # B_d = 20000 block (not a multiple of 4096) with buckets of 16
+    "block8192_f32_window": (dict(numels=[8192 * 3 + 100], block=8192, bucket=64, density=0.01,
+                                  value_f32=True, window=3), 5),
+    "block20000_bucket16": (dict(numels=[20000 * 2 + 777, 5000], block=20000, bucket=16,
+                                 density=0.02, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
+                                 window=4), 6),
 }
 
 
@@ -102,4 +110,18 @@ def test_persistent_unstaged_sampled():
                        lr=1e-4, density=0.05, window=3, bucket=64, block=4096, sample=sample)
     for t in range(5):
         run.step(check_moments=t in (0, 4))
+    run.opt.close()
+
+
+def test_c5_shape_block65536_forced_ties():
+    """The flat workload's settings at two and a half blocks: B_d = 65536,
+    k = 3277 (density 5%), m = 20, B_q = 128, bf16, Student-t(2) gradients
+    snapped to 64 magnitudes (large tie groups at the threshold), and a tail
+    of 12032 elements (k 602); 22 steps, so the window wraps."""
+    print("[parity] C5 shape, 2 blocks of 65536 + tail", flush=True)
+    run = GpuOracleRun([65536 * 2 + 12032], block=65536, bucket=128, density=0.05, window=20,
+                       param_dtype=bf16, grad_dtype=bf16, grad_dist="student_t2_snapped64",
+                       grad_scale=1e-3, lr=1e-4)
+    for t in range(22):
+        run.step(check_moments=t in (0, 9, 19, 21))
     run.opt.close()
