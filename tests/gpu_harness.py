@@ -191,12 +191,20 @@ class GpuOracleRun:
     def check_moments(self, t):
         b1, b2 = self.betas
         c1 = (1 - b1) / (1 - b1 ** t)
-        cache = {}
+        # dense moments of one tensor at a time, on the device; only the
+        # units' slices come to the host
+        by_tensor = {}
         for u in self.units:
-            if u.j not in cache:
-                cache[u.j] = tuple(_f32(x) for x in self.opt.debug_moments(u.j))
-            gm, gv = cache[u.j]
-            gm, gv = gm[u.e0:u.e1].astype(np.float64), gv[u.e0:u.e1].astype(np.float64)
+            by_tensor.setdefault(u.j, []).append(u)
+        slices = {}
+        for j, units in by_tensor.items():
+            dm, dv = self.opt.debug_moments(j)
+            for u in units:
+                slices[id(u)] = (_f32(dm[u.e0:u.e1]), _f32(dv[u.e0:u.e1]))
+            del dm, dv
+        for u in self.units:
+            gm, gv = slices[id(u)]
+            gm, gv = gm.astype(np.float64), gv.astype(np.float64)
             rm, rv = u.state.moments(t)
             scale = np.zeros_like(rm)
             for s in range(max(1, t - self.window + 1), t + 1):

@@ -125,3 +125,41 @@ def test_c5_shape_block65536_forced_ties():
     for t in range(22):
         run.step(check_moments=t in (0, 9, 19, 21))
     run.opt.close()
+
+
+def _workload_sampled(name, steps, every, check_at, lr=1e-4):
+    """A parameter list of the benchmark workloads at full size, in the
+    launch configuration bench.py times; the oracle checks every tensor's
+    first and last block and every `every`-th block in between."""
+    from paper_2405_15593_amd.workloads import WORKLOADS
+    w = WORKLOADS[name]
+    print(f"[parity] {name} sampled, {len(w.numels)} tensors, d={w.d}, {steps} steps", flush=True)
+
+    def sample(j, nb):
+        return sorted({0, nb - 1, *range(0, nb, every)})
+
+    run = GpuOracleRun(w.numels, param_dtype=w.param_dtype, grad_dtype=w.grad_dtype,
+                       grad_dist=w.grad_dist, grad_scale=w.grad_scale, lr=lr, density=w.density,
+                       window=w.window, bucket=w.bucket, block=w.block, sample=sample)
+    for t in range(steps):
+        run.step(check_moments=t in check_at)
+        print(f"[parity] {name} step {t + 1} checked", flush=True)
+    run.opt.close()
+
+
+def test_llama2_7b_bf16_sampled_window_full():
+    """The benchmark step itself: the Llama-2-7B list (291 tensors, 6.74e9
+    bf16 parameters, Student-t(4) gradients), 12 steps so that the window of
+    10 is full and wraps, as in the timed steps."""
+    _workload_sampled("llama2_7b_bf16", 12, 499, (0, 11))
+
+
+def test_llama2_13b_bf16_sampled():
+    """The Llama-2-13B list (363 tensors, 1.30e10 bf16 parameters), 3 steps."""
+    _workload_sampled("llama2_13b_bf16", 3, 997, (2,))
+
+
+def test_flat_1p5e9_ties_sampled():
+    """One 1.5e9-element bf16 tensor, B_d = 65536, k = 3277, m = 20,
+    B_q = 128, Student-t(2) gradients snapped to 64 magnitudes; 5 steps."""
+    _workload_sampled("flat1p5b_ties_bf16", 5, 4999, (4,))
