@@ -70,7 +70,7 @@ enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
  *                two in [8, 512] dividing topk_block.
  *   topk_block   B_d, Top-K block size; a multiple of ef_bucket, at most
  *                65536 (block-relative indices are uint16).  This build
- *                implements multiples of 16 up to 4096 and returns
+ *                implements multiples of 16 and returns
  *                MICROADAM_ERR_UNSUPPORTED for other valid sizes.
  *   window_value_dtype  MICROADAM_BF16 (the paper's choice, Section 3.2) or
  *                MICROADAM_F32 (lossless window values, for checking the
@@ -118,7 +118,13 @@ typedef struct microadam_handle_s* microadam_handle;
  *              index order (k_q = k_last for the last block).  With bf16
  *              values an entry is one little-endian uint32 (index |
  *              bf16_bits << 16); with float32 values it is a uint32 index
- *              followed by the float32 value.
+ *              followed by the float32 value.  For B_d > 4096 the record
+ *              continues, after the m rows (at byte m*k_full*entry_bytes),
+ *              with a table of m*ceil(B_d/4096) uint32: entry (r, j) is the
+ *              position in row r of the first entry whose index is at least
+ *              4096*j (the entries of the block's 4096-element sub-block j
+ *              are the positions [entry (r, j), entry (r, j+1)), the last
+ *              ending at k_q).
  */
 typedef struct microadam_layout {
   int64_t numel;
