@@ -263,6 +263,16 @@ class MicroAdam:
         if self.ranges != 1:
             microadam_set_ranges(self.handle, self.ranges)
 
+    def restore(self, state, t: int, grads) -> None:
+        """Creates the handle for gradients like `grads`, then loads a saved
+        state buffer (from ``state_view``) and step counter."""
+        import torch
+        self._ensure(list(grads))
+        if state.numel() != self.state_view.numel():
+            raise ValueError("saved state has another size")
+        self.state_view.copy_(state.to(self.device, torch.uint8))
+        microadam_set_step(self.handle, int(t))
+
     def step(self, grads, lr: float | None = None) -> None:
         grads = list(grads)
         assert len(grads) == len(self.params)
