@@ -252,6 +252,15 @@ template <bool VF32> struct Entry {
     if constexpr (VF32) return __uint_as_float(e[1]);
     else return __uint_as_float(e & 0xFFFF0000u);
   }
+  // the entry with its index replaced by w (an accumulator word, < 2^16)
+  __device__ static T with_word(T e, uint32_t w) {
+    if constexpr (VF32) return u32x2{w, e[1]};
+    else return (e & 0xFFFF0000u) | w;
+  }
+  __device__ static uint32_t word(T e) {
+    if constexpr (VF32) return e[0];
+    else return e & 0xFFFFu;
+  }
   __device__ static T load(Rsrc r, uint32_t entry) {
     if constexpr (VF32) return __builtin_amdgcn_raw_buffer_load_b64(r, entry * 8, 0, 0);
     else return __builtin_amdgcn_raw_buffer_load_b32(r, entry * 4, 0, 0);
@@ -1349,16 +1358,18 @@ __device__ __forceinline__ uint32_t zpos(uint32_t i) {
 // What the update kernel holds for one block before processing it: its
 // geometry, its parameters and two entries per thread of its window record
 // (the live rows are the record's first n_live*k_q entries).
-template <bool PBF16, bool VF32>
+template <bool PBF16, bool VF32, int NP>
 struct UpdateBlock {
   Span g;
   Raw8<PBF16> th[2];
-  typename Entry<VF32>::T w[2];
+  typename Entry<VF32>::T w[NP];
 };
 
-template <int NT, bool VF>
+// LDS: the two accumulators, then the staged window entries in chunk order
+// (KC chunks of 64).
+template <int NT, bool VF, int KC>
 constexpr size_t update_lds_bytes() {
-  return (size_t)2 * (NT * kLaneElems + 16) * 4 + (size_t)(2 * NT + 1) * (VF ? 8 : 4);
+  return (size_t)2 * (NT * kLaneElems + 16) * 4 + (size_t)KC * kWave * (VF ? 8 : 4);
 }
 
 // One wave (rotating with the block) rebuilds the moments of the block's
@@ -1378,14 +1389,20 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
   constexpr int NW = NT / kWave;
   constexpr int CAP = NT * kLaneElems;
   constexpr int kChunks = KC;              // 64-entry window chunks the leader holds
+  // Window entries are staged in the order the leader wave reads them:
+  // position q = 64*c + lane of chunk c, where chunk c is part c mod R of the
+  // live row c / R (oldest first, R = ceil(k_q/64) parts of 64 entries).
+  // Each thread loads the positions tid + NT*i of the block two ahead, and
+  // stages them with the entry's index replaced by its accumulator word (the
+  // sink word CAP for positions without an entry).
+  constexpr int NP = (KC * kWave + NT - 1) / NT;  // staged positions per thread
   using E = Entry<VF32>;
   using ET = typename E::T;
-  using UB = UpdateBlock<PBF16, VF32>;
+  using UB = UpdateBlock<PBF16, VF32, NP>;
   extern __shared__ __align__(16) uint32_t smem[];
   float* const z1 = (float*)smem;
   float* const z2 = z1 + CAP + 16;
-  // [2*NT] live window entries, then one entry that is always empty
-  ET* const stage = (ET*)(z2 + CAP + 16);
+  ET* const stage = (ET*)(z2 + CAP + 16);  // [KC * 64]
 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr(tid / kWave);
   const uint32_t eb = (uint32_t)tid * kLaneElems;
@@ -1404,16 +1421,33 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
       *(float4*)(a2 + q * 4 * NT + tid * 4) = zero;
     }
   };
-  if (tid == 0) stage[2 * NT] = E::none();
   if (RUN) zero_own(z1, z2);
+  // chunk c -> (live row, part): the row and the entry of staged position
+  // q, and whether it holds an entry (uniform per block: kq, R, n_live)
+  auto position = [&](int q, int kq, int R, float rcp_r, uint32_t& entry) {
+    const int c = q >> 6;
+    const int row = (int)(((float)c + 0.5f) * rcp_r);  // c / R for c < 2^10
+    const int jj = (c - row * R) * kWave + (q & (kWave - 1));
+    int slot = slot0 + row;
+    if (slot >= m) slot -= m;
+    const bool valid = row < n_live && jj < kq;
+    entry = valid ? (uint32_t)(slot * kq + jj) : 0u;
+    return valid;
+  };
   Cursor cursor = {0, 0, 0};
   auto fetch = [&](int32_t gb, UB& u) {
     u.g = RUN ? seek_full(p, cursor, gb, PBF16 ? 2 : 4) : span_of(p, gb, PBF16 ? 2 : 4);
-    // unconditional loads keep the count of loads in flight fixed; entries
-    // past the record read 0 and entries past the live rows are not used
+    // unconditional loads keep the count of loads in flight fixed; positions
+    // without an entry read entry 0 and are not used
     const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, u.g.kq);
-    u.w[0] = E::load(rw, tid);
-    u.w[1] = E::load(rw, tid + NT);
+    const int R = (u.g.kq + kWave - 1) / kWave;
+    const float rcp_r = 1.0f / (float)R;
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      uint32_t entry;
+      position(tid + NT * i, u.g.kq, R, rcp_r, entry);
+      u.w[i] = E::load(rw, entry);
+    }
     if (!EXPORT) {
       const Rsrc rp = make_rsrc((const void*)u.g.base, vec_bytes<PBF16>(u.g.s));
 #pragma unroll
@@ -1425,13 +1459,25 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
     const int s = u.g.s, kq = u.g.kq;
     const int leader = u.g.gb & (NW - 1);
     const int R = (kq + kWave - 1) / kWave;
-    const bool staged = n_live * kq <= 2 * NT && n_live * R <= kChunks;
+    const bool staged = n_live * R <= kChunks;
     // In a run the accumulators are clean when a block starts: the θ pass
     // clears z1 behind it and the leader clears the z2 words it used.  A
     // workgroup that takes one block starts from uninitialised LDS.
     if (!RUN) zero_own(z1, z2);
-    stage[tid] = u.w[0];
-    stage[tid + NT] = u.w[1];
+    {
+      const float rcp_r = 1.0f / (float)R;
+#pragma unroll
+      for (int i = 0; i < NP; ++i) {
+        const int q = tid + NT * i;
+        if (NP * NT == KC * kWave || q < KC * kWave) {
+          uint32_t entry;
+          const bool valid = position(q, kq, R, rcp_r, entry);
+          const uint32_t idx = E::idx(u.w[i]);
+          const uint32_t w = valid && idx < (uint32_t)s ? zpos<NT>(idx) : (uint32_t)CAP;
+          stage[q] = E::with_word(u.w[i], w);
+        }
+      }
+    }
     lds_sync();
 
     if (wave == leader) {
@@ -1442,28 +1488,22 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
         return p.lr * (mh * __builtin_amdgcn_rcpf(den));
       };
       if (staged) {
-        // Chunk c: row c / R in age order (slot (slot0 + row) mod m), entries
-        // (c mod R)*64 + lane.  All kChunks chunks are processed without
-        // branches: chunks past the live rows read the empty entry, and
-        // lanes without an entry work on the sink word.
-        const int nch = opaque(n_live * R);
+        // Chunk c: staged positions 64*c + lane, part c mod R of the live row
+        // c / R (age order); chunks past the live rows hold only sink words.
         uint32_t zp[kChunks];
         float val[kChunks];
         int rr[kChunks];
         {
-          int row = 0, col = 0, slot = slot0;
+          int row = 0, col = 0;
 #pragma unroll
           for (int c = 0; c < kChunks; ++c) {
-            const int jj = col * kWave + lane;
-            const ET x = stage[(c < nch && jj < kq) ? slot * kq + jj : 2 * NT];
-            const uint32_t i = E::idx(x);
-            zp[c] = i < (uint32_t)s ? zpos<NT>(i) : (uint32_t)CAP;
+            const ET x = stage[c * kWave + lane];
+            zp[c] = E::word(x);
             val[c] = E::val(x);
             rr[c] = (n_live - 1 - row) & (kMaxWindow - 1);
             if (++col == R) {
               col = 0;
               ++row;
-              if (++slot == m) slot = 0;
             }
           }
         }
@@ -1629,15 +1669,15 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
 
 // Resident workgroups of one update launch: enough to fill every compute
 // unit, computed once per device.
-template <int NT, bool PB, bool VF>
-int64_t update_grid(size_t lds) {
+template <int NT, bool PB, bool VF, int KC>
+int64_t update_grid() {
   static int64_t cache[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
   if (!cache[dev]) {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_kernel<NT, PB, VF, false, true, 16>, NT, lds) !=
-            hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_kernel<NT, PB, VF, false, true, KC>, NT,
+                                                     update_lds_bytes<NT, VF, KC>()) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         per_cu < 1 || cus < 1)
       return 1024;
@@ -1723,8 +1763,12 @@ inline int chunk_class(const StepParams& p) {
 }
 
 template <int NT, bool PB, bool VF, int KC>
-void launch_update_run(const StepParams& p, int64_t first, int64_t count, int64_t grid, int64_t per, size_t lds,
-                       hipStream_t stream) {
+void launch_update_run(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  int64_t grid = update_grid<NT, PB, VF, KC>();
+  if (grid > count) grid = count;
+  const int64_t per = (count + grid - 1) / grid;
+  grid = (count + per - 1) / per;
+  const size_t lds = update_lds_bytes<NT, VF, KC>();
   hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, true, KC>), dim3((uint32_t)grid), dim3(NT), lds, stream, p,
                      first, count, per, (float*)nullptr, (float*)nullptr);
 }
@@ -1733,21 +1777,16 @@ void launch_update_run(const StepParams& p, int64_t first, int64_t count, int64_
 // ragged blocks one workgroup each.
 template <int NT, bool PB, bool VF>
 hipError_t launch_update_t(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
-  const size_t lds = update_lds_bytes<NT, VF>();
   const int64_t end = first + count;
   const int64_t full_end = end < p.n_full ? end : p.n_full;
   const int64_t n_run = full_end - first;
   if (n_run > 0) {
-    int64_t grid = update_grid<NT, PB, VF>(lds);
-    if (grid > n_run) grid = n_run;
-    const int64_t per = (n_run + grid - 1) / grid;
-    grid = (n_run + per - 1) / per;
     switch (chunk_class(p)) {
-      case 4: launch_update_run<NT, PB, VF, 4>(p, first, n_run, grid, per, lds, stream); break;
-      case 8: launch_update_run<NT, PB, VF, 8>(p, first, n_run, grid, per, lds, stream); break;
-      case 10: launch_update_run<NT, PB, VF, 10>(p, first, n_run, grid, per, lds, stream); break;
-      case 12: launch_update_run<NT, PB, VF, 12>(p, first, n_run, grid, per, lds, stream); break;
-      default: launch_update_run<NT, PB, VF, 16>(p, first, n_run, grid, per, lds, stream); break;
+      case 4: launch_update_run<NT, PB, VF, 4>(p, first, n_run, stream); break;
+      case 8: launch_update_run<NT, PB, VF, 8>(p, first, n_run, stream); break;
+      case 10: launch_update_run<NT, PB, VF, 10>(p, first, n_run, stream); break;
+      case 12: launch_update_run<NT, PB, VF, 12>(p, first, n_run, stream); break;
+      default: launch_update_run<NT, PB, VF, 16>(p, first, n_run, stream); break;
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -1755,6 +1794,7 @@ hipError_t launch_update_t(const StepParams& p, int64_t first, int64_t count, hi
   const int64_t t0 = first > p.n_full ? first : p.n_full;
   const int64_t tails = end - t0;
   if (tails > 0) {
+    const size_t lds = update_lds_bytes<NT, VF, 16>();
     hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, false, 16>), dim3((uint32_t)tails), dim3(NT), lds, stream,
                        p, t0, tails, (int64_t)1, (float*)nullptr, (float*)nullptr);
     return hipGetLastError();
@@ -1765,7 +1805,7 @@ hipError_t launch_update_t(const StepParams& p, int64_t first, int64_t count, hi
 template <int NT, bool VF>
 hipError_t launch_export(const StepParams& p, int64_t first_block, int64_t blocks, float* mh, float* vh,
                          hipStream_t stream) {
-  const size_t lds = update_lds_bytes<NT, VF>();
+  const size_t lds = update_lds_bytes<NT, VF, 16>();
   hipLaunchKernelGGL((update_kernel<NT, false, VF, true, false, 16>), dim3((uint32_t)blocks), dim3(NT), lds, stream,
                      p, first_block, blocks, (int64_t)1, mh, vh);
   return hipGetLastError();
@@ -1779,7 +1819,7 @@ size_t step_lds_bytes(int block, int k_full, int value_f32) {
   const int nt = threads_for_block(block);
   if (block > kSubBlock) return update_large_lds_bytes<true>();
   const size_t sel = select_lds_words() * 4;
-  const size_t upd = nt == 64 ? update_lds_bytes<64, true>() : update_lds_bytes<256, true>();
+  const size_t upd = nt == 64 ? update_lds_bytes<64, true, 16>() : update_lds_bytes<256, true, 16>();
   return sel > upd ? sel : upd;
 }
 
