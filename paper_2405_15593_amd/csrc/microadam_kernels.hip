@@ -301,34 +301,6 @@ struct Span {
   int32_t kq;             // window entries per row
 };
 
-// The tensor of the full blocks a workgroup walks through in order; the
-// tables are read again only when the walk crosses into another tensor.
-// Global block numbers are below 2^31 (checked at init) and are compared as
-// 32-bit values, which keeps the comparisons scalar.
-struct Cursor {
-  uint64_t param;
-  int32_t first;          // first global block of the tensor
-  int32_t end;            // first global block past its full blocks (0: none yet)
-};
-
-// Full block gb (gb < n_full): B_d elements, k_full entries per row.
-__device__ __forceinline__ Span seek_full(const StepParams& p, Cursor& c, int32_t gb, uint32_t elem_bytes) {
-  if (gb >= c.end) {
-    const uint32_t j = constant_ptr(p.block_tensor)[gb];
-    const __attribute__((address_space(4))) TensorDesc* d = constant_ptr(p.tensors) + j;
-    c.param = (uint64_t)d->param;
-    c.first = (int32_t)d->first_block;
-    c.end = c.first + d->num_full;
-  }
-  Span u;
-  u.gb = gb;
-  u.e0 = (int64_t)(gb - c.first) * p.block;
-  u.base = c.param + (uint64_t)u.e0 * elem_bytes;
-  u.s = p.block;
-  u.kq = p.k_full;
-  return u;
-}
-
 // Any block: full, or the ragged last block of its tensor.
 __device__ __forceinline__ Span span_of(const StepParams& p, int32_t gb, uint32_t elem_bytes) {
   const Block b = locate(p, gb);
@@ -1355,76 +1327,77 @@ __device__ __forceinline__ uint32_t zpos(uint32_t i) {
   return ((i >> 2) & 3u) * (4u * NT) + (i >> 4) * 4u + (i & 3u);
 }
 
-// What the update kernel holds for one block before processing it: its
-// geometry, its parameters and two entries per thread of its window record
-// (the live rows are the record's first n_live*k_q entries).
-template <bool PBF16, bool VF32, int NP>
-struct UpdateBlock {
-  Span g;
-  Raw8<PBF16> th[2];
-  typename Entry<VF32>::T w[NP];
-};
+// Staged window positions of the update kernel: KC chunks of 64, rounded up
+// to whole multiples of the workgroup so that every thread stages the same
+// count.
+template <int NT, int KC>
+constexpr int update_stage_entries() { return (KC * kWave + NT - 1) / NT * NT; }
 
-// LDS: the two accumulators, then the staged window entries in chunk order
-// (KC chunks of 64).
-template <int NT, bool VF, int KC>
+// LDS: the accumulators (two, or one with ONE), then the staged window
+// entries in chunk order.
+template <int NT, bool VF, int KC, bool ONE>
 constexpr size_t update_lds_bytes() {
-  return (size_t)2 * (NT * kLaneElems + 16) * 4 + (size_t)KC * kWave * (VF ? 8 : 4);
+  return (size_t)(ONE ? 1 : 2) * (NT * kLaneElems + 16) * 4 + (size_t)update_stage_entries<NT, KC>() * (VF ? 8 : 4);
 }
 
-// One wave (rotating with the block) rebuilds the moments of the block's
-// window entries, oldest row first, and turns them into parameter
-// decrements; then every thread updates its own elements.  RUN = true: the
-// blocks are full and workgroups are persistent, workgroup w taking the run
-// of blocks first_block + [w*per, (w+1)*per) and loading the next block's
-// parameters and window entries before it processes the current one.
-// RUN = false: workgroup w takes block first_block + w alone.  EXPORT = true
-// writes dense m-hat and v-hat instead of updating theta.
-// LDS (about 35 KB per workgroup) allows 4 workgroups per compute unit, one
-// wave of each per SIMD; telling the compiler so lets it keep independent LDS
-// reads in flight together instead of minimising registers.
-template <int NT, bool PBF16, bool VF32, bool EXPORT, bool RUN, int KC>
-__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) update_kernel(StepParams p, int64_t first_block, int64_t num_blocks,
-                                                    int64_t per, float* mhat, float* vhat) {
+// One workgroup per block.  One wave (rotating with the block) rebuilds the
+// moments of the block's window entries, oldest row first, and turns them
+// into parameter decrements; then every thread updates its own elements.
+//
+// Window entries are staged in LDS in the order the leader wave reads them:
+// position q = 64*c + lane of chunk c, where chunk c is part c mod R of the
+// live row c / R (oldest row first, R = ceil(k_q/64) parts of 64 entries),
+// each with its index replaced by its accumulator word (the sink word CAP for
+// positions without an entry).  A block whose live rows need more than KC
+// chunks is read by the leader straight from the window record.
+//
+// ONE = true: one accumulator; the leader makes two passes over the staged
+// entries (first moments, read back and cleared, then second moments), which
+// halves the LDS of a workgroup so that eight fit on a compute unit.  The
+// host launches it only where every block's live rows fit in KC chunks.
+// ONE = false: two accumulators, any block.  EXPORT = true writes dense m-hat
+// and v-hat instead of updating theta.
+// Waves per SIMD that the LDS of an update workgroup allows (160 KB per
+// compute unit, four SIMDs); telling the compiler lets it spend registers
+// up to that occupancy on keeping LDS reads in flight.
+template <int NT, bool VF, int KC, bool ONE>
+constexpr int update_waves_per_eu() {
+  const int per_cu = (int)(163840 / update_lds_bytes<NT, VF, KC, ONE>());
+  const int w = per_cu * (NT / kWave) / 4;
+  return w < 1 ? 1 : w > 8 ? 8 : w;
+}
+
+template <int NT, bool PBF16, bool VF32, bool EXPORT, int KC, bool ONE>
+__global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(update_waves_per_eu<NT, VF32, KC, ONE>())))
+update_kernel(StepParams p, int64_t first_block, float* mhat, float* vhat) {
+  static_assert(!ONE || !EXPORT, "one accumulator: parameter update only");
   constexpr int NW = NT / kWave;
   constexpr int CAP = NT * kLaneElems;
-  constexpr int kChunks = KC;              // 64-entry window chunks the leader holds
-  // Window entries are staged in the order the leader wave reads them:
-  // position q = 64*c + lane of chunk c, where chunk c is part c mod R of the
-  // live row c / R (oldest first, R = ceil(k_q/64) parts of 64 entries).
-  // Each thread loads the positions tid + NT*i of the block two ahead, and
-  // stages them with the entry's index replaced by its accumulator word (the
-  // sink word CAP for positions without an entry).
-  constexpr int NP = (KC * kWave + NT - 1) / NT;  // staged positions per thread
+  constexpr int kChunks = KC;                             // 64-entry chunks the leader holds
+  constexpr int NP = update_stage_entries<NT, KC>() / NT;  // staged positions per thread
   using E = Entry<VF32>;
   using ET = typename E::T;
-  using UB = UpdateBlock<PBF16, VF32, NP>;
   extern __shared__ __align__(16) uint32_t smem[];
   float* const z1 = (float*)smem;
-  float* const z2 = z1 + CAP + 16;
-  ET* const stage = (ET*)(z2 + CAP + 16);  // [KC * 64]
+  float* const z2 = z1 + CAP + 16;                        // not allocated with ONE
+  ET* const stage = (ET*)(ONE ? z2 : z2 + CAP + 16);      // [NP * NT]; chunks past KC are not read
 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr(tid / kWave);
   const uint32_t eb = (uint32_t)tid * kLaneElems;
   const int m = p.window, n_live = p.n_live;
   // oldest live row first: the row written at step s is slot (s-1) mod m
   const int slot0 = (p.new_slot + 1 + m - n_live) % m;
-  const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
-  const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
 
-  // this thread's 16 words of each accumulator
-  auto zero_own = [&](float* a1, float* a2) {
-    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      *(float4*)(a1 + q * 4 * NT + tid * 4) = zero;
-      *(float4*)(a2 + q * 4 * NT + tid * 4) = zero;
-    }
-  };
-  if (RUN) zero_own(z1, z2);
-  // chunk c -> (live row, part): the row and the entry of staged position
-  // q, and whether it holds an entry (uniform per block: kq, R, n_live)
-  auto position = [&](int q, int kq, int R, float rcp_r, uint32_t& entry) {
+  const Span u = span_of(p, (int32_t)(first_block + block_id()), PBF16 ? 2 : 4);
+  const int s = u.s, kq = u.kq;
+  const int leader = u.gb & (NW - 1);
+  const int R = (kq + kWave - 1) / kWave;
+  const float rcp_r = 1.0f / (float)R;
+  const bool staged = n_live * R <= kChunks;
+
+  // chunk c -> (live row, part): the entry of staged position q, and whether
+  // it holds one (uniform per block: kq, R, n_live)
+  auto position = [&](int q, uint32_t& entry) {
     const int c = q >> 6;
     const int row = (int)(((float)c + 0.5f) * rcp_r);  // c / R for c < 2^10
     const int jj = (c - row * R) * kWave + (q & (kWave - 1));
@@ -1434,83 +1407,102 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
     entry = valid ? (uint32_t)(slot * kq + jj) : 0u;
     return valid;
   };
-  Cursor cursor = {0, 0, 0};
-  auto fetch = [&](int32_t gb, UB& u) {
-    u.g = RUN ? seek_full(p, cursor, gb, PBF16 ? 2 : 4) : span_of(p, gb, PBF16 ? 2 : 4);
-    // unconditional loads keep the count of loads in flight fixed; positions
-    // without an entry read entry 0 and are not used
-    const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, u.g.kq);
-    const int R = (u.g.kq + kWave - 1) / kWave;
-    const float rcp_r = 1.0f / (float)R;
-#pragma unroll
-    for (int i = 0; i < NP; ++i) {
-      uint32_t entry;
-      position(tid + NT * i, u.g.kq, R, rcp_r, entry);
-      u.w[i] = E::load(rw, entry);
-    }
-    if (!EXPORT) {
-      const Rsrc rp = make_rsrc((const void*)u.g.base, vec_bytes<PBF16>(u.g.s));
-#pragma unroll
-      for (int v = 0; v < 2; ++v) u.th[v] = load8<PBF16>(rp, eb + v * 8);
-    }
-  };
 
-  auto process = [&](const UB& u) {
-    const int s = u.g.s, kq = u.g.kq;
-    const int leader = u.g.gb & (NW - 1);
-    const int R = (kq + kWave - 1) / kWave;
-    const bool staged = n_live * R <= kChunks;
-    // In a run the accumulators are clean when a block starts: the θ pass
-    // clears z1 behind it and the leader clears the z2 words it used.  A
-    // workgroup that takes one block starts from uninitialised LDS.
-    if (!RUN) zero_own(z1, z2);
-    {
-      const float rcp_r = 1.0f / (float)R;
+  // loads: window positions (unconditional; positions without an entry read
+  // entry 0 and are not used), then the parameters
+  const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, u.gb, kq);
+  ET w[NP];
 #pragma unroll
-      for (int i = 0; i < NP; ++i) {
-        const int q = tid + NT * i;
-        if (NP * NT == KC * kWave || q < KC * kWave) {
-          uint32_t entry;
-          const bool valid = position(q, kq, R, rcp_r, entry);
-          const uint32_t idx = E::idx(u.w[i]);
-          const uint32_t w = valid && idx < (uint32_t)s ? zpos<NT>(idx) : (uint32_t)CAP;
-          stage[q] = E::with_word(u.w[i], w);
-        }
-      }
-    }
-    lds_sync();
+  for (int i = 0; i < NP; ++i) {
+    uint32_t entry;
+    position(tid + NT * i, entry);
+    w[i] = E::load(rw, entry);
+  }
+  const Rsrc rp = make_rsrc((const void*)u.base, vec_bytes<PBF16>(s));
+  Raw8<PBF16> th[2];
+  if (!EXPORT) {
+#pragma unroll
+    for (int v = 0; v < 2; ++v) th[v] = load8<PBF16>(rp, eb + v * 8);
+  }
+  const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
+  const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
 
-    if (wave == leader) {
-      auto step_of = [&](float s1, float s2) {
-        const float mh = p.c1 * s1;
-        const float vh = p.c2 * s2;
-        const float den = p.eps + __builtin_amdgcn_sqrtf(vh);
-        return p.lr * (mh * __builtin_amdgcn_rcpf(den));
-      };
-      if (staged) {
-        // Chunk c: staged positions 64*c + lane, part c mod R of the live row
-        // c / R (age order); chunks past the live rows hold only sink words.
-        uint32_t zp[kChunks];
-        float val[kChunks];
-        int rr[kChunks];
-        {
-          int row = 0, col = 0;
+  {
+    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-          for (int c = 0; c < kChunks; ++c) {
-            const ET x = stage[c * kWave + lane];
-            zp[c] = E::word(x);
-            val[c] = E::val(x);
-            rr[c] = (n_live - 1 - row) & (kMaxWindow - 1);
-            if (++col == R) {
-              col = 0;
-              ++row;
-            }
+    for (int q = 0; q < 4; ++q) {
+      *(float4*)(z1 + q * 4 * NT + tid * 4) = zero;
+      if (!ONE) *(float4*)(z2 + q * 4 * NT + tid * 4) = zero;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NP; ++i) {
+    const int q = tid + NT * i;
+    uint32_t entry;
+    const bool valid = position(q, entry);
+    const uint32_t idx = E::idx(w[i]);
+    const uint32_t zw = valid && idx < (uint32_t)s ? zpos<NT>(idx) : (uint32_t)CAP;
+    stage[q] = E::with_word(w[i], zw);
+  }
+  lds_sync();
+
+  if (wave == leader) {
+    auto step_of = [&](float s1, float s2) {
+      const float mh = p.c1 * s1;
+      const float vh = p.c2 * s2;
+      const float den = p.eps + __builtin_amdgcn_sqrtf(vh);
+      return p.lr * (mh * __builtin_amdgcn_rcpf(den));
+    };
+    if (staged) {
+      // chunks past the live rows hold only sink words
+      uint32_t zp[kChunks];
+      float val[kChunks];
+      int rr[kChunks];
+      {
+        int row = 0, col = 0;
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) {
+          const ET x = stage[c * kWave + lane];
+          zp[c] = E::word(x);
+          val[c] = E::val(x);
+          rr[c] = (n_live - 1 - row) & (kMaxWindow - 1);
+          if (++col == R) {
+            col = 0;
+            ++row;
           }
         }
-        // the entries of one row (or of one 64-entry part of it) have
-        // distinct indices, so each chunk reads, adds and writes back its
-        // words (the sink word's lanes race harmlessly); chunks follow each
-        // other oldest row first
+      }
+      // The entries of one row (or of one 64-entry part of it) have distinct
+      // indices, so each chunk reads, adds and writes back its words (the
+      // sink word's lanes race harmlessly); chunks follow each other oldest
+      // row first.  Every entry's sums are read before any word is
+      // overwritten, so an index that occurs in several rows gets the same
+      // decrement from each occurrence.
+      if constexpr (ONE) {
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) {
+          const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), rr[c]));
+          const float a1 = z1[zp[c]];
+          z1[zp[c]] = a1 + w1 * val[c];
+        }
+        float s1[kChunks];
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) s1[c] = z1[zp[c]];
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) z1[zp[c]] = 0.0f;
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) {
+          const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), rr[c]));
+          const float vv = val[c] * val[c];
+          const float a2 = z1[zp[c]];
+          z1[zp[c]] = a2 + w2 * vv;
+        }
+        float d[kChunks];
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) d[c] = step_of(s1[c], z1[zp[c]]);
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c) z1[zp[c]] = d[c];
+      } else {
 #pragma unroll
         for (int c = 0; c < kChunks; ++c) {
           const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), rr[c]));
@@ -1524,166 +1516,84 @@ __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) up
           z2[zp[c]] = a2 + x2;
         }
         if (!EXPORT) {
-          // every entry's sums are read before any word is overwritten, so an
-          // index that occurs in several rows gets the same decrement from
-          // each occurrence
           float d[kChunks];
 #pragma unroll
           for (int c = 0; c < kChunks; ++c) d[c] = step_of(z1[zp[c]], z2[zp[c]]);
 #pragma unroll
-          for (int c = 0; c < kChunks; ++c) {
-            z1[zp[c]] = d[c];
-            z2[zp[c]] = 0.0f;
-          }
+          for (int c = 0; c < kChunks; ++c) z1[zp[c]] = d[c];
         }
-      } else {
-        const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, u.g.gb, kq);
-        for (int row = 0, slot = slot0; row < n_live; ++row, slot = (slot + 1 == m) ? 0 : slot + 1) {
-          const int r = n_live - 1 - row;
-          const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), r));
-          const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), r));
+      }
+    } else if constexpr (!ONE) {
+      for (int row = 0, slot = slot0; row < n_live; ++row, slot = (slot + 1 == m) ? 0 : slot + 1) {
+        const int r = n_live - 1 - row;
+        const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), r));
+        const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), r));
+        for (int jj = lane; jj < kq; jj += kWave) {
+          const ET x = E::load(rw, slot * kq + jj);
+          const uint32_t i = E::idx(x);
+          const uint32_t zp = i < (uint32_t)s ? zpos<NT>(i) : (uint32_t)CAP;
+          const float v = E::val(x);
+          const float vv = v * v;
+          const float x1 = w1 * v, x2 = w2 * vv;
+          const float a1 = z1[zp], a2 = z2[zp];
+          z1[zp] = a1 + x1;
+          z2[zp] = a2 + x2;
+        }
+      }
+      if (!EXPORT) {
+        // one 64-entry chunk at a time; z2 = -1 marks a converted word
+        for (int row = 0, slot = slot0; row < n_live; ++row, slot = (slot + 1 == m) ? 0 : slot + 1)
           for (int jj = lane; jj < kq; jj += kWave) {
-            const ET x = E::load(rw, slot * kq + jj);
-            const uint32_t i = E::idx(x);
-            const uint32_t zp = i < (uint32_t)s ? zpos<NT>(i) : (uint32_t)CAP;
-            const float v = E::val(x);
-            const float vv = v * v;
-            const float x1 = w1 * v, x2 = w2 * vv;
-            const float a1 = z1[zp], a2 = z2[zp];
-            z1[zp] = a1 + x1;
-            z2[zp] = a2 + x2;
-          }
-        }
-        if (!EXPORT) {
-          // one 64-entry chunk at a time; z2 = -1 marks a converted word
-          for (int row = 0, slot = slot0; row < n_live; ++row, slot = (slot + 1 == m) ? 0 : slot + 1)
-            for (int jj = lane; jj < kq; jj += kWave) {
-              const uint32_t i = E::idx(E::load(rw, slot * kq + jj));
-              if (i < (uint32_t)s) {
-                const uint32_t zp = zpos<NT>(i);
-                const float s2 = z2[zp];
-                if (s2 >= 0.0f) {
-                  z1[zp] = step_of(z1[zp], s2);
-                  z2[zp] = -1.0f;
-                }
+            const uint32_t i = E::idx(E::load(rw, slot * kq + jj));
+            if (i < (uint32_t)s) {
+              const uint32_t zp = zpos<NT>(i);
+              const float s2 = z2[zp];
+              if (s2 >= 0.0f) {
+                z1[zp] = step_of(z1[zp], s2);
+                z2[zp] = -1.0f;
               }
             }
-        }
-      }
-    }
-    lds_sync();
-
-    if (EXPORT) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 s1 = *(const float4*)(z1 + q * 4 * NT + tid * 4);
-        const float4 s2 = *(const float4*)(z2 + q * 4 * NT + tid * 4);
-        const float a1[4] = {s1.x, s1.y, s1.z, s1.w}, a2[4] = {s2.x, s2.y, s2.z, s2.w};
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const uint32_t i = eb + q * 4 + r;
-          if ((int)i < s) {
-            mhat[u.g.e0 + i] = p.c1 * a1[r];
-            vhat[u.g.e0 + i] = p.c2 * a2[r];
           }
-        }
-      }
-      return;
-    }
-
-    // ---------------------------------------------- 6. parameter update
-    const bool full = s == NT * kLaneElems;
-    const Rsrc rp = make_rsrc((const void*)u.g.base, vec_bytes<PBF16>(s));
-#pragma unroll
-    for (int v = 0; v < 2; ++v) {
-      const uint32_t e0 = eb + v * 8;   // vectors past s store nothing
-      const float4 u0 = *(const float4*)(z1 + (2 * v) * 4 * NT + tid * 4);
-      const float4 u1 = *(const float4*)(z1 + (2 * v + 1) * 4 * NT + tid * 4);
-      if (RUN) {
-        // clear behind the read; the unstaged path leaves marks in z2 too
-        const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-        *(float4*)(z1 + (2 * v) * 4 * NT + tid * 4) = zero;
-        *(float4*)(z1 + (2 * v + 1) * 4 * NT + tid * 4) = zero;
-        if (!staged) {
-          *(float4*)(z2 + (2 * v) * 4 * NT + tid * 4) = zero;
-          *(float4*)(z2 + (2 * v + 1) * 4 * NT + tid * 4) = zero;
-        }
-      }
-      const float upd[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
-      float thf[8], out[8];
-      unpack8<PBF16>(u.th[v], thf);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
-        out[e] = base - upd[e];
-      }
-      // a full block holds whole threads (B_d is a multiple of 16)
-      if (RUN) {
-        if ((int)eb < s) store8<PBF16>(rp, e0, s, true, out);
-      } else {
-        store8<PBF16>(rp, e0, s, full, out);
       }
     }
-  };
+  }
+  lds_sync();
 
-  // Workgroup w takes the blocks first_block + w + i*G (G workgroups), so
-  // that the blocks in work at any time are neighbours in memory.  Three
-  // register sets take turns, and the block two ahead is always fetched
-  // (past the last one the last block is fetched again), so that the count
-  // of loads issued after any block's data is fixed and the waits for that
-  // data let the next two blocks' loads stay in flight.
-  if (!RUN) {
-    UB A;
-    fetch((int32_t)(first_block + block_id()), A);
-    process(A);
+  if (EXPORT) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 s1 = *(const float4*)(z1 + q * 4 * NT + tid * 4);
+      const float4 s2 = *(const float4*)(z2 + q * 4 * NT + tid * 4);
+      const float a1[4] = {s1.x, s1.y, s1.z, s1.w}, a2[4] = {s2.x, s2.y, s2.z, s2.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t i = eb + q * 4 + r;
+        if ((int)i < s) {
+          mhat[u.e0 + i] = p.c1 * a1[r];
+          vhat[u.e0 + i] = p.c2 * a2[r];
+        }
+      }
+    }
     return;
   }
-  (void)per;
-  const int32_t G = (int32_t)__builtin_amdgcn_grid_size_x() / NT;
-  const int32_t end = (int32_t)(first_block + num_blocks);
-  int32_t g = (int32_t)first_block + (int32_t)block_id();
-  if (g >= end) return;
-  auto nxt = [&](int32_t x) { return x + G < end ? x + G : x; };
-  UB A, B, C;
-  fetch(g, A);
-  int32_t g1 = nxt(g);
-  fetch(g1, B);
-  for (;;) {
-    const int32_t g2 = nxt(g1);
-    fetch(g2, C);
-    process(A);
-    if (g1 == g) break;
-    const int32_t g3 = nxt(g2);
-    fetch(g3, A);
-    process(B);
-    if (g2 == g1) break;
-    const int32_t g4 = nxt(g3);
-    fetch(g4, B);
-    process(C);
-    if (g3 == g2) break;
-    g = g3;
-    g1 = g4;
-  }
-}
 
-
-// Resident workgroups of one update launch: enough to fill every compute
-// unit, computed once per device.
-template <int NT, bool PB, bool VF, int KC>
-int64_t update_grid() {
-  static int64_t cache[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
-  if (!cache[dev]) {
-    int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_kernel<NT, PB, VF, false, true, KC>, NT,
-                                                     update_lds_bytes<NT, VF, KC>()) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        per_cu < 1 || cus < 1)
-      return 1024;
-    cache[dev] = (int64_t)per_cu * cus;
+  // ------------------------------------------------ 6. parameter update
+  const bool full = s == NT * kLaneElems;
+#pragma unroll
+  for (int v = 0; v < 2; ++v) {
+    const uint32_t e0 = eb + v * 8;   // vectors past s store nothing
+    const float4 u0 = *(const float4*)(z1 + (2 * v) * 4 * NT + tid * 4);
+    const float4 u1 = *(const float4*)(z1 + (2 * v + 1) * 4 * NT + tid * 4);
+    const float upd[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+    float thf[8], out[8];
+    unpack8<PBF16>(th[v], thf);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
+      out[e] = base - upd[e];
+    }
+    store8<PBF16>(rp, e0, s, full, out);
   }
-  return cache[dev];
 }
 
 template <int EPL, bool LB, bool GB, bool VF>
@@ -1762,52 +1672,38 @@ inline int chunk_class(const StepParams& p) {
   return nch <= 4 ? 4 : nch <= 8 ? 8 : nch <= 10 ? 10 : nch <= 12 ? 12 : 16;
 }
 
-template <int NT, bool PB, bool VF, int KC>
-void launch_update_run(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
-  int64_t grid = update_grid<NT, PB, VF, KC>();
-  if (grid > count) grid = count;
-  const int64_t per = (count + grid - 1) / grid;
-  grid = (count + per - 1) / per;
-  const size_t lds = update_lds_bytes<NT, VF, KC>();
-  hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, true, KC>), dim3((uint32_t)grid), dim3(NT), lds, stream, p,
-                     first, count, per, (float*)nullptr, (float*)nullptr);
+template <int NT, bool PB, bool VF, int KC, bool ONE>
+hipError_t launch_update_k(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  const size_t lds = update_lds_bytes<NT, VF, KC, ONE>();
+  hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, KC, ONE>), dim3((uint32_t)count), dim3(NT), lds, stream, p,
+                     first, (float*)nullptr, (float*)nullptr);
+  return hipGetLastError();
 }
 
-// The full blocks of [first, first + count) in persistent runs, then its
-// ragged blocks one workgroup each.
+// Blocks [first, first + count), one workgroup each: with one accumulator
+// where the live rows of a full block, and so of every block, fit in 16
+// chunks; else with two.
 template <int NT, bool PB, bool VF>
 hipError_t launch_update_t(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
-  const int64_t end = first + count;
-  const int64_t full_end = end < p.n_full ? end : p.n_full;
-  const int64_t n_run = full_end - first;
-  if (n_run > 0) {
-    switch (chunk_class(p)) {
-      case 4: launch_update_run<NT, PB, VF, 4>(p, first, n_run, stream); break;
-      case 8: launch_update_run<NT, PB, VF, 8>(p, first, n_run, stream); break;
-      case 10: launch_update_run<NT, PB, VF, 10>(p, first, n_run, stream); break;
-      case 12: launch_update_run<NT, PB, VF, 12>(p, first, n_run, stream); break;
-      default: launch_update_run<NT, PB, VF, 16>(p, first, n_run, stream); break;
-    }
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+  const int R = (p.k_full + kWave - 1) / kWave;
+  if (p.n_live * R > 16) return launch_update_k<NT, PB, VF, 16, false>(p, first, count, stream);
+  switch (chunk_class(p)) {
+    case 4: return launch_update_k<NT, PB, VF, 4, true>(p, first, count, stream);
+    case 8: return launch_update_k<NT, PB, VF, 8, true>(p, first, count, stream);
+    case 10: return launch_update_k<NT, PB, VF, 10, true>(p, first, count, stream);
+    case 12: return launch_update_k<NT, PB, VF, 12, true>(p, first, count, stream);
+    default: return launch_update_k<NT, PB, VF, 16, true>(p, first, count, stream);
   }
-  const int64_t t0 = first > p.n_full ? first : p.n_full;
-  const int64_t tails = end - t0;
-  if (tails > 0) {
-    const size_t lds = update_lds_bytes<NT, VF, 16>();
-    hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, false, 16>), dim3((uint32_t)tails), dim3(NT), lds, stream,
-                       p, t0, tails, (int64_t)1, (float*)nullptr, (float*)nullptr);
-    return hipGetLastError();
-  }
-  return hipSuccess;
 }
 
 template <int NT, bool VF>
 hipError_t launch_export(const StepParams& p, int64_t first_block, int64_t blocks, float* mh, float* vh,
                          hipStream_t stream) {
-  const size_t lds = update_lds_bytes<NT, VF, 16>();
-  hipLaunchKernelGGL((update_kernel<NT, false, VF, true, false, 16>), dim3((uint32_t)blocks), dim3(NT), lds, stream,
-                     p, first_block, blocks, (int64_t)1, mh, vh);
+  if (blocks <= 0) return hipSuccess;
+  const size_t lds = update_lds_bytes<NT, VF, 16, false>();
+  hipLaunchKernelGGL((update_kernel<NT, false, VF, true, 16, false>), dim3((uint32_t)blocks), dim3(NT), lds, stream,
+                     p, first_block, mh, vh);
   return hipGetLastError();
 }
 
@@ -1819,7 +1715,7 @@ size_t step_lds_bytes(int block, int k_full, int value_f32) {
   const int nt = threads_for_block(block);
   if (block > kSubBlock) return update_large_lds_bytes<true>();
   const size_t sel = select_lds_words() * 4;
-  const size_t upd = nt == 64 ? update_lds_bytes<64, true, 16>() : update_lds_bytes<256, true, 16>();
+  const size_t upd = nt == 64 ? update_lds_bytes<64, true, 16, false>() : update_lds_bytes<256, true, 16, false>();
   return sel > upd ? sel : upd;
 }
 
