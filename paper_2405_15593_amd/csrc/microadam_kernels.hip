@@ -11,8 +11,8 @@
 //        shuffles; e = Q(a, delta, Delta), two 4-bit codes per byte
 //        (Algorithm 1; Section 3.1)
 //
-//   update_kernel   persistent workgroups of 256 threads (thread tid: the 16
-//   consecutive elements tid*16 + [0, 16) of each block it takes):
+//   update_kernel   one workgroup of 256 threads per block (thread tid: the
+//   16 consecutive elements tid*16 + [0, 16) of the block):
 //     5. one wave rebuilds m-hat, v-hat of the block's window entries in LDS
 //        from the m rows with weights beta^(t-s) (Algorithm 2, AdamStats)
 //     6. every wave applies theta <- (1 - eta*lambda) theta
@@ -1315,8 +1315,9 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
 }
 
 // ============================================================ update
-// z1 / z2 hold, per element of the block, sum beta1^r V and sum beta2^r V^2
-// (then z1 the parameter decrement).  Element i lives at word
+// The accumulators hold, per element of the block, sum beta1^r V and sum
+// beta2^r V^2 (z1 and z2; or z1 alone, one after the other), then z1 the
+// parameter decrement.  Element i lives at word
 // ((i >> 2) & 3) * 4*NT + (i >> 4) * 4 + (i & 3), so that the 16 elements of a
 // thread are four 16-byte words at a stride of 4*NT words and a wave's
 // 16-byte accesses fall on consecutive addresses.  Word CAP of each array is

@@ -97,19 +97,20 @@ def test_bert_base_bf16_sampled():
     run.opt.close()
 
 
-def test_persistent_unstaged_sampled():
-    """3000 full 4096-blocks plus a tail, k = 205, m = 3: the window entries of
-    a block exceed what the update stages in LDS, and each persistent
-    workgroup runs several such blocks back to back.  Sampled blocks."""
-    print("[parity] persistent unstaged, 3000 blocks, k=205", flush=True)
+def test_unstaged_two_accumulators_sampled():
+    """3000 full 4096-blocks plus a tail, k = 205, m = 5: the live rows of a
+    block need 20 chunks of 64 entries, more than the update stages in LDS, so
+    the update takes its two-accumulator form and reads the window record
+    directly.  Sampled blocks."""
+    print("[parity] unstaged update, 3000 blocks, k=205, m=5", flush=True)
 
     def sample(j, nb):
         return sorted({0, 1, 2, nb - 2, nb - 1, *range(0, nb, 61)})
 
     run = GpuOracleRun([4096 * 3000 + 123], grad_dtype=bf16, param_dtype=bf16, grad_scale=1e-3,
-                       lr=1e-4, density=0.05, window=3, bucket=64, block=4096, sample=sample)
-    for t in range(5):
-        run.step(check_moments=t in (0, 4))
+                       lr=1e-4, density=0.05, window=5, bucket=64, block=4096, sample=sample)
+    for t in range(7):
+        run.step(check_moments=t in (0, 6))
     run.opt.close()
 
 
