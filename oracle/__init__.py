@@ -1,13 +1,15 @@
 """MicroAdam CPU oracle -- TEST INFRASTRUCTURE ONLY.
 
 A ctypes front end over ``microadam_oracle.c``: a plain, slow, single-threaded
-CPU statement of one MicroAdam step (Algorithms 1, 2 and 4 and Section 3.1 of
-the MicroAdam paper).  Only ``tests/``, ``__graft_entry__.smoke()`` and the
-CPU-baseline leg of ``bench.py`` may import this package.  It shares no code
+CPU statement of one MicroAdam step (Algorithms 1, 2 and 4, Section 3.1 and,
+as an option, the randomized quantizer of Lemma 1, of the MicroAdam paper).
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It shares no code
 with the HIP path and must never be used to produce a product result.
 
 State is held in the oracle's own layout (see the C file's header):
     ef       uint8[(n+1)//2]  4-bit codes, element 2j in the low nibble
+             uint8[n]         (ef_bits = 8) one code per byte
     delta    float32[nb]      bucket minimum   (nb = ceil(n / bucket))
     Delta    float32[nb]      bucket maximum
     win_idx  uint16[m, K]     window rows of block-relative indices
@@ -45,12 +47,15 @@ class _Cfg(ctypes.Structure):
         ("window", ctypes.c_int32),
         ("value_bf16", ctypes.c_int32),
         ("param_bf16", ctypes.c_int32),
-        ("pad_", ctypes.c_int32),
+        ("ef_bits", ctypes.c_int32),
         ("density", ctypes.c_double),
         ("beta1", ctypes.c_double),
         ("beta2", ctypes.c_double),
         ("eps", ctypes.c_double),
         ("weight_decay", ctypes.c_double),
+        ("rounding", ctypes.c_int32),
+        ("tensor", ctypes.c_int32),
+        ("seed", ctypes.c_uint64),
     ]
 
 
@@ -87,10 +92,18 @@ class Oracle:
         lib.oracle_moments.restype = None
         lib.oracle_round_bf16.argtypes = [ctypes.c_double]
         lib.oracle_round_bf16.restype = ctypes.c_float
-        lib.oracle_dequantize.argtypes = [ctypes.c_uint, ctypes.c_float, ctypes.c_float]
+        lib.oracle_dequantize.argtypes = [ctypes.c_uint, ctypes.c_float, ctypes.c_float, ctypes.c_int]
         lib.oracle_dequantize.restype = ctypes.c_float
-        lib.oracle_quantize.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float]
+        lib.oracle_quantize.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_int]
         lib.oracle_quantize.restype = ctypes.c_uint
+        lib.oracle_quantize_randomized.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                                   ctypes.c_int, ctypes.c_float]
+        lib.oracle_quantize_randomized.restype = ctypes.c_uint
+        lib.oracle_philox4x32_10.argtypes = [P(ctypes.c_uint32), ctypes.c_uint32, ctypes.c_uint32,
+                                             P(ctypes.c_uint32)]
+        lib.oracle_philox4x32_10.restype = None
+        lib.oracle_uniform_xi.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64]
+        lib.oracle_uniform_xi.restype = ctypes.c_float
         self.lib = lib
 
     def block_k(self, s: int, density: float) -> int:
@@ -99,11 +112,23 @@ class Oracle:
     def round_bf16(self, x: float) -> float:
         return float(self.lib.oracle_round_bf16(float(x)))
 
-    def quantize(self, x: float, lo: float, hi: float) -> int:
-        return int(self.lib.oracle_quantize(x, lo, hi))
+    def quantize(self, x: float, lo: float, hi: float, bits: int = 4) -> int:
+        return int(self.lib.oracle_quantize(x, lo, hi, bits))
 
-    def dequantize(self, code: int, lo: float, hi: float) -> float:
-        return float(self.lib.oracle_dequantize(code, lo, hi))
+    def quantize_randomized(self, x: float, lo: float, hi: float, xi: float, bits: int = 4) -> int:
+        return int(self.lib.oracle_quantize_randomized(x, lo, hi, bits, xi))
+
+    def dequantize(self, code: int, lo: float, hi: float, bits: int = 4) -> float:
+        return float(self.lib.oracle_dequantize(code, lo, hi, bits))
+
+    def philox4x32_10(self, ctr, key) -> tuple:
+        c = (ctypes.c_uint32 * 4)(*[int(x) & 0xFFFFFFFF for x in ctr])
+        out = (ctypes.c_uint32 * 4)()
+        self.lib.oracle_philox4x32_10(c, int(key[0]) & 0xFFFFFFFF, int(key[1]) & 0xFFFFFFFF, out)
+        return tuple(int(x) for x in out)
+
+    def uniform_xi(self, seed: int, tensor: int, t: int, i: int) -> float:
+        return float(self.lib.oracle_uniform_xi(int(seed), int(tensor), int(t), int(i)))
 
     def tensor(self, n: int, **kw) -> "TensorState":
         return TensorState(self, n, **kw)
@@ -116,12 +141,15 @@ class TensorState:
                  bucket: int = 64, window: int = 10, density: float = 0.01,
                  value_bf16: bool = True, param_bf16: bool = False,
                  beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
-                 weight_decay: float = 0.0):
+                 weight_decay: float = 0.0, ef_bits: int = 4, rounding: int = 0,
+                 seed: int = 0, tensor: int = 0):
         self.o = oracle
         self.cfg = _Cfg(n=n, block=block, bucket=bucket, window=window,
                         value_bf16=int(value_bf16), param_bf16=int(param_bf16),
-                        pad_=0, density=density, beta1=beta1, beta2=beta2,
-                        eps=eps, weight_decay=weight_decay)
+                        ef_bits=int(ef_bits), density=density, beta1=beta1, beta2=beta2,
+                        eps=eps, weight_decay=weight_decay, rounding=int(rounding),
+                        tensor=int(tensor), seed=int(seed))
+        self.ef_bits = int(ef_bits)
         lib = oracle.lib
         c = ctypes.byref(self.cfg)
         self.n = n
@@ -129,7 +157,7 @@ class TensorState:
         self.nbuckets = int(lib.oracle_num_buckets(c))
         self.K = int(lib.oracle_row_width(c))
         self.k_full = oracle.block_k(block, density)
-        self.ef = np.zeros((n + 1) // 2, np.uint8)
+        self.ef = np.zeros(n if ef_bits == 8 else (n + 1) // 2, np.uint8)
         self.delta = np.zeros(self.nbuckets, np.float32)
         self.Delta = np.zeros(self.nbuckets, np.float32)
         self.win_idx = np.zeros((window, self.K), np.uint16)
@@ -154,7 +182,9 @@ class TensorState:
         return self.win_idx[row, lo:lo + k].copy(), self.win_val[row, lo:lo + k].copy()
 
     def codes(self) -> np.ndarray:
-        """The 4-bit codes, one per element."""
+        """The codes, one per element."""
+        if self.ef_bits == 8:
+            return self.ef.copy()
         c = np.empty(2 * self.ef.size, np.uint8)
         c[0::2] = self.ef & 0x0F
         c[1::2] = self.ef >> 4

@@ -10,7 +10,10 @@
  *   - Section 3.1 (Top-K applied per block of B_d elements with
  *     block-relative indices; per-bucket quantization metadata delta/Delta;
  *     the 4-bit error feedback stored two codes per byte),
- *   - Algorithm 4 (decoupled weight decay (1 - eta*lambda) * theta).
+ *   - Algorithm 4 (decoupled weight decay (1 - eta*lambda) * theta),
+ *   - Lemma 1 (Section 4: the randomized-rounding quantizer of the error
+ *     feedback, floor((x - delta)/u + xi) with xi ~ U[0, 1)), as an option
+ *     beside the round-to-nearest Q of Algorithm 2; b = 4 or 8 bits.
  *
  * Only the test suite, the smoke check and the benchmark's CPU-baseline leg
  * load this library.  It shares no code, header or table with the HIP path.
@@ -32,6 +35,13 @@
  *     entries in ascending index order with their signed values;
  *   - Q rounds half-to-even; a bucket whose max equals its min encodes every
  *     element as 0, and Q^-1 of any code in such a bucket is its min;
+ *   - the randomized Q draws xi for element i of tensor j at step t from
+ *     Philox4x32-10 (Salmon et al., "Parallel Random Numbers: As Easy as
+ *     1, 2, 3", SC 2011): key = the 64-bit seed, counter = (i/4 low word,
+ *     i/4 high word, j, t); word i mod 4 of the output, w, gives
+ *     xi = (w >> 8) * 2^-24; the code is floor(y + xi) taken exactly (not
+ *     after rounding the sum) for y = fl(fl(x - delta)/u), clamped to
+ *     [0, 2^b - 1];
  *   - the window row written at step s is row (s-1) mod m; in AdamStats it
  *     carries the weight beta^(t-s), so the newest row has exponent 0 and the
  *     oldest m-1 (Section 3, "Dynamic Statistics");
@@ -43,6 +53,7 @@
  * Data layout (the oracle's own):
  *   theta[n], grad[n]     binary32 values (bf16 values held exactly)
  *   ef[(n+1)/2]           4-bit codes, element 2j in the low nibble
+ *   ef[n]                 (b = 8) one code per byte
  *   delta[nb], Delta[nb]  bucket min / max, nb = ceil(n / B_q)
  *   win_idx[m*K]          window indices, row-major (m rows of K entries);
  *   win_val[m*K]          window values (bf16-rounded when value_bf16);
@@ -54,19 +65,20 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define EF_BITS 4
-#define EF_LEVELS 15.0f /* 2^b - 1 for b = 4 */
-
 typedef struct {
   int64_t n;          /* elements in the tensor                          */
   int32_t block;      /* B_d: Top-K block size                           */
-  int32_t bucket;     /* B_q: quantization bucket size (divides B_d)     */
+  int32_t bucket;     /* B_q: quantization bucket size (divides B_d, or  */
+                      /* any size when a step covers the whole tensor)   */
   int32_t window;     /* m: rows in the sliding window                   */
   int32_t value_bf16; /* 1: window values stored as bf16, 0: binary32    */
   int32_t param_bf16; /* 1: parameters stored as bf16, 0: binary32       */
-  int32_t pad_;
+  int32_t ef_bits;    /* b: 4 or 8                                       */
   double density;     /* k/d in (0, 1]                                   */
   double beta1, beta2, eps, weight_decay;
+  int32_t rounding;   /* 0: nearest (Algorithm 2), 1: randomized (Lemma 1) */
+  int32_t tensor;     /* j: the tensor's number, part of the random counter */
+  uint64_t seed;      /* key of the random stream                        */
 } oracle_cfg;
 
 /* ---------------------------------------------------------------------- */
@@ -126,34 +138,89 @@ static float round_to_bf16(double x) {
 }
 
 /* ---------------------------------------------------------------------- */
-/* Q and Q^-1 (Algorithm 2) for b = 4, binary32                            */
+/* Q and Q^-1 (Algorithm 2; Lemma 1), binary32, L = 2^b - 1 levels         */
 /* ---------------------------------------------------------------------- */
 
 /* Q^-1: x = x_Q * u + delta with u = (Delta - delta) / (2^b - 1). */
-static float dequantize(unsigned code, float lo, float hi) {
-  float u = (hi - lo) / EF_LEVELS;
+static float dequantize(unsigned code, float lo, float hi, float levels) {
+  float u = (hi - lo) / levels;
   float scaled = (float)code * u;
   return scaled + lo;
 }
 
-/* Q: x_Q = round((x - delta) / u), rounding half to even, kept in [0, 15];
+/* Q: x_Q = round((x - delta) / u), rounding half to even, kept in [0, L];
  * a bucket with u == 0 encodes 0. */
-static unsigned quantize(float x, float lo, float hi) {
-  float u = (hi - lo) / EF_LEVELS;
+static unsigned quantize(float x, float lo, float hi, float levels) {
+  float u = (hi - lo) / levels;
   if (u == 0.0f) return 0u;
   float y = (x - lo) / u;
   float r = nearbyintf(y);
   if (r < 0.0f) r = 0.0f;
-  if (r > EF_LEVELS) r = EF_LEVELS;
+  if (r > levels) r = levels;
   return (unsigned)r;
 }
 
-static unsigned get_code(const uint8_t* ef, int64_t i) {
+/* Randomized Q (Lemma 1): x_Q = floor((x - delta) / u + xi), kept in
+ * [0, L]; a bucket with u == 0 encodes 0.  xi = w * 2^-24 for a 24-bit
+ * integer w, and the floor of the exact sum y + xi is floor(y) + 1 exactly
+ * when w + floor(2^24 * frac(y)) >= 2^24 (frac(y) and its scaling are exact
+ * in binary32); rounding the sum first would move y's just below an integer
+ * up with a probability of up to one ulp. */
+static unsigned quantize_randomized(float x, float lo, float hi, float levels, uint32_t w24) {
+  float u = (hi - lo) / levels;
+  if (u == 0.0f) return 0u;
+  float y = (x - lo) / u;
+  float fy = floorf(y);
+  float f = y - fy;
+  uint32_t fr = (uint32_t)floorf(f * 16777216.0f);
+  float r = fy + ((w24 + fr >= (1u << 24)) ? 1.0f : 0.0f);
+  if (r < 0.0f) r = 0.0f;
+  if (r > levels) r = levels;
+  return (unsigned)r;
+}
+
+/* Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC 2011): ten rounds of
+ * two 32x32 -> 64-bit products with the round keys, the key advancing by
+ * the Weyl constants between rounds. */
+static void philox4x32_10(const uint32_t ctr[4], uint32_t k0, uint32_t k1, uint32_t out[4]) {
+  uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * x0;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * x2;
+    const uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+    const uint32_t y1 = (uint32_t)p1;
+    const uint32_t y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+    const uint32_t y3 = (uint32_t)p0;
+    x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+  }
+  out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* The 24-bit integer w of xi = w * 2^-24 for element i of tensor j at step
+ * t: xi is uniform on [0, 1) in steps of 2^-24. */
+static uint32_t uniform_w24(uint64_t seed, int32_t j, int64_t t, int64_t i) {
+  const uint64_t quad = (uint64_t)i >> 2;
+  const uint32_t ctr[4] = {(uint32_t)quad, (uint32_t)(quad >> 32), (uint32_t)j, (uint32_t)t};
+  uint32_t out[4];
+  philox4x32_10(ctr, (uint32_t)seed, (uint32_t)(seed >> 32), out);
+  return out[i & 3] >> 8;
+}
+
+static unsigned get_code(const uint8_t* ef, int64_t i, int bits) {
+  if (bits == 8) return ef[i];
   uint8_t byte = ef[i >> 1];
   return (i & 1) ? (unsigned)(byte >> 4) : (unsigned)(byte & 0x0F);
 }
 
-static void put_code(uint8_t* ef, int64_t i, unsigned code) {
+static void put_code(uint8_t* ef, int64_t i, unsigned code, int bits) {
+  if (bits == 8) {
+    ef[i] = (uint8_t)code;
+    return;
+  }
   uint8_t byte = ef[i >> 1];
   if (i & 1) byte = (uint8_t)((byte & 0x0F) | (code << 4));
   else       byte = (uint8_t)((byte & 0xF0) | code);
@@ -237,11 +304,14 @@ int oracle_step(const oracle_cfg* c, int64_t t, double lr, float* theta,
                 const float* grad, uint8_t* ef, float* delta, float* Delta,
                 uint16_t* win_idx, float* win_val, int64_t q0, int64_t q1) {
   if (t < 1 || c->window < 1 || c->block < 1 || c->bucket < 1 ||
-      c->block % c->bucket != 0)
+      (c->ef_bits != 4 && c->ef_bits != 8) || (c->rounding != 0 && c->rounding != 1))
     return -1;
   const int64_t nblk = oracle_num_blocks(c);
   if (q1 > nblk) q1 = nblk;
   if (q0 < 0 || q0 >= q1) return 0;
+  /* a bucket that does not lie inside one block needs the whole tensor */
+  if (c->block % c->bucket != 0 && (q0 != 0 || q1 != nblk)) return -1;
+  const float levels = (float)((1 << c->ef_bits) - 1);
   const int64_t lo = q0 * c->block;
   int64_t hi = q1 * c->block;
   if (hi > c->n) hi = c->n;
@@ -254,7 +324,7 @@ int oracle_step(const oracle_cfg* c, int64_t t, double lr, float* theta,
   /* Accumulator: a = g + Q^-1(e, delta, Delta). */
   for (int64_t i = lo; i < hi; ++i) {
     const int64_t b = i / c->bucket;
-    a[i - lo] = grad[i] + dequantize(get_code(ef, i), delta[b], Delta[b]);
+    a[i - lo] = grad[i] + dequantize(get_code(ef, i, c->ef_bits), delta[b], Delta[b], levels);
   }
 
   for (int64_t q = q0; q < q1; ++q) {
@@ -286,7 +356,12 @@ int oracle_step(const oracle_cfg* c, int64_t t, double lr, float* theta,
     const int64_t b = b0 / c->bucket;
     delta[b] = mn;
     Delta[b] = mx;
-    for (int64_t i = b0; i < b1; ++i) put_code(ef, i, quantize(a[i - lo], mn, mx));
+    for (int64_t i = b0; i < b1; ++i) {
+      const unsigned code = c->rounding
+          ? quantize_randomized(a[i - lo], mn, mx, levels, uniform_w24(c->seed, c->tensor, t, i))
+          : quantize(a[i - lo], mn, mx, levels);
+      put_code(ef, i, code, c->ef_bits);
+    }
   }
 
   /* m-hat, v-hat = AdamStats over the window (binary64), then the update
@@ -310,5 +385,19 @@ int oracle_step(const oracle_cfg* c, int64_t t, double lr, float* theta,
 
 /* Exposed for the tests: binary32 -> bf16 rounding and the codec. */
 float oracle_round_bf16(double x) { return round_to_bf16(x); }
-float oracle_dequantize(unsigned code, float lo, float hi) { return dequantize(code, lo, hi); }
-unsigned oracle_quantize(float x, float lo, float hi) { return quantize(x, lo, hi); }
+float oracle_dequantize(unsigned code, float lo, float hi, int bits) {
+  return dequantize(code, lo, hi, (float)((1 << bits) - 1));
+}
+unsigned oracle_quantize(float x, float lo, float hi, int bits) {
+  return quantize(x, lo, hi, (float)((1 << bits) - 1));
+}
+/* xi must lie on the 2^-24 grid of [0, 1). */
+unsigned oracle_quantize_randomized(float x, float lo, float hi, int bits, float xi) {
+  return quantize_randomized(x, lo, hi, (float)((1 << bits) - 1), (uint32_t)(xi * 16777216.0f));
+}
+void oracle_philox4x32_10(const uint32_t ctr[4], uint32_t k0, uint32_t k1, uint32_t out[4]) {
+  philox4x32_10(ctr, k0, k1, out);
+}
+float oracle_uniform_xi(uint64_t seed, int32_t j, int64_t t, int64_t i) {
+  return (float)uniform_w24(seed, j, t, i) * 0x1p-24f;
+}

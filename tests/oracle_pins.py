@@ -23,6 +23,15 @@ What pins what:
     (1 - eta*lambda)*theta elsewhere (Algorithm 4).
   - bf16 rounding: torch's CPU float32 -> bfloat16 conversion (RNE), and a
     binary64 double-rounding case.
+  - Randomized Q (Lemma 1): E[x_hat] = x, checked by averaging over xi on
+    the midpoints of 256 equal cells of [0, 1) and, through whole steps, over
+    300 seeds; every draw is one of the two grid points around x; the
+    bucket's min and max are exact; the lemma's norm bound per bucket.
+  - The random stream: the published known-answer vectors of Philox4x32-10
+    (Salmon et al., SC 2011); xi on the 2^-24 grid of [0, 1), uniform
+    (mean and a 16-bin chi-square), changing with seed, tensor and step.
+  - 8-bit codes: the half-step bound with 255 levels, ties to even, max ->
+    255, and the step's reconstruction bound.
 """
 from __future__ import annotations
 
@@ -47,10 +56,10 @@ def _brute_topk(x: np.ndarray, k: int) -> list[int]:
     return sorted(order[:k])
 
 
-def _decode(codes, lo, hi, bucket):
-    """Q^-1 per element in binary32 (x_Q * u + delta, u = (Delta-delta)/15)."""
+def _decode(codes, lo, hi, bucket, levels=15):
+    """Q^-1 per element in binary32 (x_Q * u + delta, u = (Delta-delta)/L)."""
     b = np.arange(codes.size) // bucket
-    u = ((hi[b] - lo[b]) / np.float32(15)).astype(np.float32)
+    u = ((hi[b] - lo[b]) / np.float32(levels)).astype(np.float32)
     return (codes.astype(np.float32) * u).astype(np.float32) + lo[b]
 
 
@@ -100,6 +109,149 @@ def check_quantizer(o) -> None:
         slack = 4 * float(_ulp(max(abs(lo), abs(hi))))
         for x, c in zip(xs, codes):
             assert abs(o.dequantize(c, lo, hi) - float(x)) <= u / 2 + slack, (x, lo, hi)
+
+
+def check_quantizer_8bit(o) -> None:
+    # 255 levels: lo = 0, hi = 255 gives u = 1, half steps round to even
+    for x, want in [(0.5, 0), (1.5, 2), (2.5, 2), (100.5, 100), (254.5, 254), (255.0, 255),
+                    (17.49, 17), (17.51, 18)]:
+        assert o.quantize(x, 0.0, 255.0, 8) == want, (x, want)
+    rng = np.random.default_rng(25)
+    for _ in range(200):
+        lo, hi = np.sort(rng.standard_normal(2).astype(np.float32) * np.float32(10.0 ** rng.integers(-6, 3)))
+        lo, hi = float(lo), float(hi)
+        u = (hi - lo) / 255.0
+        assert o.quantize(lo, lo, hi, 8) == 0 and o.dequantize(0, lo, hi, 8) == lo
+        if hi > lo:
+            assert o.quantize(hi, lo, hi, 8) == 255
+        xs = np.sort(rng.uniform(lo, hi, 64).astype(np.float32))
+        codes = [o.quantize(float(x), lo, hi, 8) for x in xs]
+        assert all(0 <= c <= 255 for c in codes)
+        assert all(a <= b for a, b in zip(codes, codes[1:])), "codes not monotone"
+        slack = 4 * float(_ulp(max(abs(lo), abs(hi))))
+        for x, c in zip(xs, codes):
+            assert abs(o.dequantize(c, lo, hi, 8) - float(x)) <= u / 2 + slack, (x, lo, hi)
+
+
+# Published known-answer vectors of Philox4x32-10 (counter, key -> output),
+# from the Random123 distribution that accompanies Salmon et al. (SC 2011).
+PHILOX_KAT = [
+    ((0, 0, 0, 0), (0, 0), (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+    ((0xFFFFFFFF,) * 4, (0xFFFFFFFF,) * 2, (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+    ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+     (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1)),
+]
+
+
+def check_philox_kat(o) -> None:
+    for ctr, key, want in PHILOX_KAT:
+        assert o.philox4x32_10(ctr, key) == want, (ctr, key)
+
+
+def check_uniform_stream(o) -> None:
+    seed = 0x0123456789ABCDEF
+    # element i of tensor j at step t: top 24 bits of word i mod 4 of the
+    # block at counter (i/4 low, i/4 high, j, t), key = the seed's two words
+    for j, t, i in [(0, 1, 0), (3, 7, 5), (2, 2, 2 ** 33 + 6), (1, 1, 4095)]:
+        out = o.philox4x32_10(((i >> 2) & 0xFFFFFFFF, i >> 34, j, t), (seed & 0xFFFFFFFF, seed >> 32))
+        assert o.uniform_xi(seed, j, t, i) == (out[i & 3] >> 8) * 2.0 ** -24, (j, t, i)
+    xs = np.array([o.uniform_xi(seed, 0, 1, i) for i in range(40000)])
+    assert xs.min() >= 0.0 and xs.max() < 1.0
+    assert np.array_equal(xs * 2 ** 24, np.floor(xs * 2 ** 24)), "not on the 2^-24 grid"
+    assert abs(xs.mean() - 0.5) < 5 * math.sqrt(1 / 12 / xs.size)
+    counts = np.bincount((xs * 16).astype(np.int64), minlength=16)
+    chi2 = float(((counts - xs.size / 16) ** 2 / (xs.size / 16)).sum())
+    assert chi2 < 44.3, chi2      # 15 degrees of freedom, upper 0.01% point
+    base = [o.uniform_xi(seed, 0, 1, i) for i in range(64)]
+    assert base != [o.uniform_xi(seed, 0, 2, i) for i in range(64)], "step not in the counter"
+    assert base != [o.uniform_xi(seed, 1, 1, i) for i in range(64)], "tensor not in the counter"
+    assert base != [o.uniform_xi(seed + 1, 0, 1, i) for i in range(64)]
+    assert base != [o.uniform_xi(seed + (1 << 32), 0, 1, i) for i in range(64)]
+
+
+def check_randomized_quantizer(o) -> None:
+    rng = np.random.default_rng(21)
+    K = 256
+    xis = [(k + 0.5) / K for k in range(K)]
+    for bits in (4, 8):
+        L = 2 ** bits - 1
+        for _ in range(30):
+            lo, hi = np.sort(rng.standard_normal(2).astype(np.float32) * np.float32(10.0 ** rng.integers(-4, 2)))
+            lo, hi = float(lo), float(hi)
+            u = (hi - lo) / L
+            slack = 8 * float(_ulp(max(abs(lo), abs(hi))))
+            for x in rng.uniform(lo, hi, 6).astype(np.float32):
+                codes = [o.quantize_randomized(float(x), lo, hi, xi, bits) for xi in xis]
+                assert all(0 <= c <= L for c in codes)
+                assert max(codes) - min(codes) <= 1, "a draw away from the two grid points around x"
+                mean = float(np.mean([o.dequantize(c, lo, hi, bits) for c in codes]))
+                assert abs(mean - float(x)) <= u / K + slack, ("biased", bits, float(x), lo, hi, mean)
+            assert all(o.quantize_randomized(lo, lo, hi, xi, bits) == 0 for xi in (0.0, 0.5, 1 - 2 ** -24))
+            if hi > lo:
+                assert o.quantize_randomized(hi, lo, hi, 0.5, bits) == L
+    # xi = 0 truncates; a grid point stays put for any xi below 1
+    assert o.quantize_randomized(2.3, 0.0, 15.0, 0.0) == 2
+    assert o.quantize_randomized(2.3, 0.0, 15.0, 0.75) == 3
+    assert o.quantize_randomized(2.0, 0.0, 15.0, 1 - 2 ** -24) == 2
+    assert o.quantize(3.0, 3.0, 3.0) == 0 and o.quantize_randomized(3.0, 3.0, 3.0, 0.9) == 0
+
+
+def check_randomized_ef_unbiased(o) -> None:
+    """Whole steps with randomized Q: averaged over seeds, the decoded error
+    feedback after step 1 is the residual a - T_k(a) (Lemma 1), and each
+    bucket meets the lemma's norm bound."""
+    rng = np.random.default_rng(23)
+    n, block, bucket, S = 512, 256, 64, 300
+    g = rng.standard_normal(n).astype(np.float32)
+    for bits in (4, 8):
+        L = 2 ** bits - 1
+        acc = np.zeros(n)
+        codes0 = None
+        for seed in range(S):
+            st = o.tensor(n, block=block, bucket=bucket, density=0.05, window=2, rounding=1,
+                          seed=seed, tensor=3, ef_bits=bits)
+            st.step(np.zeros(n, np.float32), g, 1, 1e-3)
+            dec = _decode(st.codes(), st.delta, st.Delta, bucket, L).astype(np.float64)
+            acc += dec
+            codes0 = st.codes() if codes0 is None else codes0
+            r = g.astype(np.float64).copy()
+            for q in range(st.nblocks):
+                idx, _ = st.window_entries(0, q)
+                r[q * block + idx.astype(np.int64)] = 0.0
+            for b0 in range(0, n, bucket):
+                x, xh = r[b0:b0 + bucket], dec[b0:b0 + bucket]
+                lo, hi = x.min(), x.max()
+                bound = math.sqrt(bucket - 2) / L * (hi - lo) / math.sqrt(hi * hi + lo * lo)
+                assert np.linalg.norm(xh - x) <= bound * np.linalg.norm(x) * (1 + 1e-5), (bits, seed, b0)
+        bidx = np.arange(n) // bucket
+        u = (st.Delta[bidx].astype(np.float64) - st.delta[bidx]) / L
+        assert np.all(np.abs(acc / S - r) <= 6 * u / (2 * math.sqrt(S)) + 1e-6), bits
+        other = o.tensor(n, block=block, bucket=bucket, density=0.05, window=2, rounding=1,
+                         seed=0, tensor=4, ef_bits=bits)
+        other.step(np.zeros(n, np.float32), g, 1, 1e-3)
+        assert not np.array_equal(other.codes(), codes0), "tensor number not in the stream"
+
+
+def check_reconstruction_8bit(o) -> None:
+    rng = np.random.default_rng(26)
+    n, block, bucket = 2000, 256, 32
+    st = o.tensor(n, block=block, bucket=bucket, density=0.02, window=3, ef_bits=8)
+    theta = np.zeros(n, np.float32)
+    for t in range(1, 5):
+        g = rng.standard_normal(n).astype(np.float32)
+        a = (g + _decode(st.codes(), st.delta, st.Delta, bucket, 255)).astype(np.float32)
+        st.step(theta, g, t, 1e-3)
+        rec = _decode(st.codes(), st.delta, st.Delta, bucket, 255).astype(np.float64)
+        bidx = np.arange(n) // bucket
+        bound = (st.Delta[bidx].astype(np.float64) - st.delta[bidx]) / 255 / 2
+        bound += 4 * _ulp(np.maximum(np.abs(st.delta[bidx]), np.abs(st.Delta[bidx])))
+        row = st.row_of_step(t)
+        for q in range(st.nblocks):
+            idx, val = st.window_entries(row, q)
+            i = q * block + idx.astype(np.int64)
+            rec[i] += val
+            bound[i] += np.abs(val.astype(np.float64) - a[i]) + _ulp(a[i])
+        assert np.all(np.abs(rec - a) <= bound), t
 
 
 def check_topk_bruteforce(o) -> None:
@@ -360,4 +512,10 @@ ALL_CHECKS = [
     check_decay_exponents,
     check_untouched_and_sparsity,
     check_weight_decay,
+    check_quantizer_8bit,
+    check_philox_kat,
+    check_uniform_stream,
+    check_randomized_quantizer,
+    check_randomized_ef_unbiased,
+    check_reconstruction_8bit,
 ]

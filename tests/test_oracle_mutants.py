@@ -27,19 +27,32 @@ MUTANTS = [
     ("round half up", "float r = nearbyintf(y);", "float r = floorf(y + 0.5f);"),
     ("truncating quantizer", "float r = nearbyintf(y);", "float r = floorf(y);"),
     ("decode sign", "return scaled + lo;", "return scaled - lo;"),
-    ("decode level 16", "#define EF_LEVELS 15.0f", "#define EF_LEVELS 16.0f"),
+    ("decode level 16", "const float levels = (float)((1 << c->ef_bits) - 1);",
+     "const float levels = (float)(1 << c->ef_bits);"),
     ("min and max swapped", "if (a[i - lo] < mn) mn = a[i - lo];", "if (a[i - lo] > mn) mn = a[i - lo];"),
     ("update sign", "(double)theta[i] * decay - lr * upd", "(double)theta[i] * decay + lr * upd"),
     ("eps inside sqrt", "mh[i - lo] / (c->eps + sqrt(vh[i - lo]))", "mh[i - lo] / sqrt(c->eps + vh[i - lo])"),
     ("second moment not squared", "(squared ? v * v : v)", "(squared ? v : v)"),
     ("decay sign", "1.0 - lr * c->weight_decay", "1.0 + lr * c->weight_decay"),
     ("bf16 keeps 9 bits", "int q = e - 8;", "int q = e - 9;"),
-    ("accumulator ignores EF", "a[i - lo] = grad[i] + dequantize(get_code(ef, i), delta[b], Delta[b]);",
+    ("accumulator ignores EF",
+     "a[i - lo] = grad[i] + dequantize(get_code(ef, i, c->ef_bits), delta[b], Delta[b], levels);",
      "a[i - lo] = grad[i];"),
     ("nibbles swapped", "return (i & 1) ? (unsigned)(byte >> 4) : (unsigned)(byte & 0x0F);",
      "return (i & 1) ? (unsigned)(byte & 0x0F) : (unsigned)(byte >> 4);"),
     ("beta1 for both moments", "adam_stats(c, t, c->beta2, 1,", "adam_stats(c, t, c->beta1, 1,"),
     ("k rounds down", "double x = ceil(density * (double)s - 1e-9);", "double x = floor(density * (double)s);"),
+    ("philox multiplier", "(uint64_t)0xD2511F53u * x0", "(uint64_t)0xD2511F55u * x0"),
+    ("philox key bump", "k0 += 0x9E3779B9u;", "k0 += 0x9E3779BBu;"),
+    ("philox nine rounds", "round < 10", "round < 9"),
+    ("xi from the low bits", "return out[i & 3] >> 8;", "return out[i & 3] & 0xFFFFFFu;"),
+    ("xi ignores the step", "(uint32_t)j, (uint32_t)t}", "(uint32_t)j, 0u}"),
+    ("randomized rounds to nearest", "float r = fy + ((w24 + fr >= (1u << 24)) ? 1.0f : 0.0f);",
+     "float r = nearbyintf(y);"),
+    ("randomized rounds up", "float r = fy + ((w24 + fr >= (1u << 24)) ? 1.0f : 0.0f);",
+     "float r = fy + (f > 0.0f ? 1.0f : 0.0f);"),
+    ("randomized ignores the fraction", "(w24 + fr >= (1u << 24))", "(w24 >= (1u << 23))"),
+    ("8-bit codes read as nibbles", "if (bits == 8) return ef[i];", "if (bits == 8) return ef[i] & 0x0F;"),
 ]
 
 
