@@ -65,7 +65,20 @@ enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
  *   weight_decay lambda of the decoupled decay theta *= (1 - eta*lambda)
  *                (Algorithm 4); >= 0.
  *   window       m, rows in the sliding window, 1..64.
- *   ef_bits      b, bits per EF code; only 4 is implemented.
+ *   ef_bits      b, bits per EF code: 4 (the paper's choice, Section 3.1) or
+ *                8 (a wider code for the same buckets).  8 needs
+ *                topk_block <= 4096.
+ *   ef_rounding  how Q rounds: MICROADAM_ROUND_NEAREST (Algorithm 2, half to
+ *                even) or MICROADAM_ROUND_RANDOMIZED (Lemma 1: floor((x -
+ *                delta)/u + xi), xi ~ U[0, 1), which makes Q unbiased); the
+ *                latter needs topk_block <= 4096.
+ *   seed         key of the randomized rounding's random stream: element i
+ *                of tensor j at step t draws xi = (w >> 8) * 2^-24 from word
+ *                i mod 4 of Philox4x32-10 (Salmon et al., SC 2011) at counter
+ *                (i/4 low word, i/4 high word, j, t) under the key (seed low
+ *                word, seed high word); j is the tensor's position in the
+ *                numels list of microadam_init.  The floor is taken of the
+ *                exact sum.  Unused with NEAREST.
  *   ef_bucket    B_q, elements sharing one (delta, Delta) pair; a power of
  *                two in [8, 512] dividing topk_block.
  *   topk_block   B_d, Top-K block size; a multiple of ef_bucket, at most
@@ -76,6 +89,9 @@ enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
  *                MICROADAM_F32 (lossless window values, for checking the
  *                moment rebuild).
  */
+/* Rounding of the error-feedback quantizer. */
+enum { MICROADAM_ROUND_NEAREST = 0, MICROADAM_ROUND_RANDOMIZED = 1 };
+
 typedef struct microadam_config {
   double density;
   double beta1;
@@ -88,7 +104,8 @@ typedef struct microadam_config {
   int32_t ef_bucket;
   int32_t topk_block;
   int32_t window_value_dtype;
-  int32_t reserved; /* must be 0 */
+  int32_t ef_rounding;
+  uint64_t seed;
 } microadam_config;
 
 typedef struct microadam_handle_s* microadam_handle;
@@ -106,7 +123,8 @@ typedef struct microadam_handle_s* microadam_handle;
  *
  *   EF codes   B_d/2 bytes per block: element 2j of the block in the low
  *              nibble of byte j, element 2j+1 in the high nibble (nibbles
- *              past the block's elements are 0).
+ *              past the block's elements are 0).  With ef_bits = 8, B_d
+ *              bytes per block, element i in byte i.
  *   stats      B_d/B_q pairs of float32 (delta, Delta) per block = (min,
  *              max) of the bucket's residual; pair b covers the block's
  *              elements [b*B_q, (b+1)*B_q); pairs past its elements are

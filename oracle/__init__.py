@@ -56,6 +56,7 @@ class _Cfg(ctypes.Structure):
         ("rounding", ctypes.c_int32),
         ("tensor", ctypes.c_int32),
         ("seed", ctypes.c_uint64),
+        ("offset", ctypes.c_int64),
     ]
 
 
@@ -142,13 +143,13 @@ class TensorState:
                  value_bf16: bool = True, param_bf16: bool = False,
                  beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
                  weight_decay: float = 0.0, ef_bits: int = 4, rounding: int = 0,
-                 seed: int = 0, tensor: int = 0):
+                 seed: int = 0, tensor: int = 0, offset: int = 0):
         self.o = oracle
         self.cfg = _Cfg(n=n, block=block, bucket=bucket, window=window,
                         value_bf16=int(value_bf16), param_bf16=int(param_bf16),
                         ef_bits=int(ef_bits), density=density, beta1=beta1, beta2=beta2,
                         eps=eps, weight_decay=weight_decay, rounding=int(rounding),
-                        tensor=int(tensor), seed=int(seed))
+                        tensor=int(tensor), seed=int(seed), offset=int(offset))
         self.ef_bits = int(ef_bits)
         lib = oracle.lib
         c = ctypes.byref(self.cfg)

@@ -79,6 +79,8 @@ typedef struct {
   int32_t rounding;   /* 0: nearest (Algorithm 2), 1: randomized (Lemma 1) */
   int32_t tensor;     /* j: the tensor's number, part of the random counter */
   uint64_t seed;      /* key of the random stream                        */
+  int64_t offset;     /* number of this state's element 0 in its tensor  */
+                      /* (part of the random counter; 0 for a tensor)    */
 } oracle_cfg;
 
 /* ---------------------------------------------------------------------- */
@@ -358,7 +360,7 @@ int oracle_step(const oracle_cfg* c, int64_t t, double lr, float* theta,
     Delta[b] = mx;
     for (int64_t i = b0; i < b1; ++i) {
       const unsigned code = c->rounding
-          ? quantize_randomized(a[i - lo], mn, mx, levels, uniform_w24(c->seed, c->tensor, t, i))
+          ? quantize_randomized(a[i - lo], mn, mx, levels, uniform_w24(c->seed, c->tensor, t, c->offset + i))
           : quantize(a[i - lo], mn, mx, levels);
       put_code(ef, i, code, c->ef_bits);
     }

@@ -28,6 +28,8 @@ MICROADAM_ERR_NO_MEMORY = -6
 
 MICROADAM_F32 = 0
 MICROADAM_BF16 = 1
+MICROADAM_ROUND_NEAREST = 0
+MICROADAM_ROUND_RANDOMIZED = 1
 
 
 class microadam_config(ctypes.Structure):
@@ -43,7 +45,8 @@ class microadam_config(ctypes.Structure):
         ("ef_bucket", ctypes.c_int32),
         ("topk_block", ctypes.c_int32),
         ("window_value_dtype", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("ef_rounding", ctypes.c_int32),
+        ("seed", ctypes.c_uint64),
     ]
 
 
@@ -132,10 +135,11 @@ def _check(rc: int, where: str) -> None:
 
 def make_config(density=0.01, beta1=0.9, beta2=0.999, eps=1e-8, lr=1e-4, weight_decay=0.0,
                 window=10, ef_bits=4, ef_bucket=64, topk_block=4096,
-                window_value_dtype=MICROADAM_BF16) -> microadam_config:
+                window_value_dtype=MICROADAM_BF16, ef_rounding=MICROADAM_ROUND_NEAREST,
+                seed=0) -> microadam_config:
     """A microadam_config; defaults are the paper's fine-tuning settings."""
     return microadam_config(density, beta1, beta2, eps, lr, weight_decay, window, ef_bits,
-                            ef_bucket, topk_block, window_value_dtype, 0)
+                            ef_bucket, topk_block, window_value_dtype, ef_rounding, seed)
 
 
 def _i64_array(xs: Sequence[int]):

@@ -60,7 +60,7 @@ int validate_config(const microadam_config* c) {
   if (c->window > microadam::kMaxWindow)
     return fail(MICROADAM_ERR_UNSUPPORTED, "window above 64 is not supported");
   if (c->ef_bits < 1 || c->ef_bits > 16) return fail(MICROADAM_ERR_INVALID_ARG, "ef_bits out of range");
-  if (c->ef_bits != 4) return fail(MICROADAM_ERR_UNSUPPORTED, "only ef_bits = 4 is implemented");
+  if (c->ef_bits != 4 && c->ef_bits != 8) return fail(MICROADAM_ERR_UNSUPPORTED, "ef_bits must be 4 or 8");
   if (c->ef_bucket < 2) return fail(MICROADAM_ERR_INVALID_ARG, "ef_bucket must be >= 2");
   if (!is_pow2(c->ef_bucket) || c->ef_bucket < 8 || c->ef_bucket > 512)
     return fail(MICROADAM_ERR_UNSUPPORTED, "ef_bucket must be a power of two in [8, 512]");
@@ -73,7 +73,10 @@ int validate_config(const microadam_config* c) {
     return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block must be a multiple of 16");
   if (c->window_value_dtype != MICROADAM_BF16 && c->window_value_dtype != MICROADAM_F32)
     return fail(MICROADAM_ERR_INVALID_ARG, "window_value_dtype must be BF16 or F32");
-  if (c->reserved != 0) return fail(MICROADAM_ERR_INVALID_ARG, "reserved must be 0");
+  if (c->ef_rounding != MICROADAM_ROUND_NEAREST && c->ef_rounding != MICROADAM_ROUND_RANDOMIZED)
+    return fail(MICROADAM_ERR_INVALID_ARG, "ef_rounding must be NEAREST or RANDOMIZED");
+  if ((c->ef_bits != 4 || c->ef_rounding != MICROADAM_ROUND_NEAREST) && c->topk_block > 4096)
+    return fail(MICROADAM_ERR_UNSUPPORTED, "8-bit or randomized error feedback needs topk_block <= 4096");
   return MICROADAM_OK;
 }
 
@@ -103,7 +106,7 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
   const int64_t B = c->topk_block, Bq = c->ef_bucket, m = c->window;
   const int64_t eb = entry_bytes(c);
   const int32_t k_full = (int32_t)block_k(B, c->density);
-  pl.ef_stride = (uint64_t)B / 2;
+  pl.ef_stride = (uint64_t)B * (uint64_t)c->ef_bits / 8;
   pl.stats_stride = (uint64_t)(B / Bq) * 8;
   // whole 128-byte lines per record, so that a row can be written as whole
   // lines without touching another block's record; blocks above 4096 add a
@@ -245,6 +248,9 @@ void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& 
   p.eps = (float)c.eps;
   p.c1 = (float)((1.0 - c.beta1) / (1.0 - std::pow(c.beta1, (double)t)));
   p.c2 = (float)((1.0 - c.beta2) / (1.0 - std::pow(c.beta2, (double)t)));
+  p.ef_mode = (c.ef_bits == 8 ? 1 : 0) | (c.ef_rounding == MICROADAM_ROUND_RANDOMIZED ? 2 : 0);
+  p.seed_lo = (uint32_t)c.seed;
+  p.seed_hi = (uint32_t)(c.seed >> 32);
 }
 
 int check_handle(microadam_handle h) {

@@ -31,7 +31,7 @@ struct TensorDesc {
 inline int threads_for_block(int block) { return block <= 1024 ? 64 : 256; }
 
 // State layout: three planes indexed by the global block number gb.
-//   EF codes       ef_plane    + gb * B_d/2
+//   EF codes       ef_plane    + gb * B_d*b/8 (b = 4 or 8 bits per code)
 //   (min, max)     stats_plane + gb * (B_d/B_q) * 8
 //   window rows    win_plane   + gb * win_stride (m * k_full * entry_bytes
 //                  rounded up to whole 128-byte lines)
@@ -56,6 +56,8 @@ struct StepParams {
   int32_t k_full;                // entries per row of a full block (all tensors)
   int32_t decay_is_one;          // weight_decay * lr == 0
   float lr, decay, eps, c1, c2;
+  int32_t ef_mode;               // code format: bit 0 8-bit codes, bit 1 randomized rounding
+  uint32_t seed_lo, seed_hi;     // key of the randomized rounding's stream
 };
 
 // Launchers (defined in microadam_kernels.hip).  Return hipSuccess or the

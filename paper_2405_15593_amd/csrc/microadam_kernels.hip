@@ -107,6 +107,50 @@ __device__ __forceinline__ float div15(float d) {
   return __builtin_fmaf(e, r, q0);
 }
 
+// Error-feedback code formats (a template parameter of the select kernel):
+// bit 0: 8-bit codes, one byte per element (else 4-bit, two per byte);
+// bit 1: randomized rounding (Lemma 1) instead of round-to-nearest.
+constexpr int kEf8 = 1, kEfRandom = 2;
+
+// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel Random Numbers: As
+// Easy as 1, 2, 3", SC 2011): ten rounds of two 32x32 -> 64-bit products
+// with the round keys; the key advances by the Weyl constants between rounds
+// (the key words are wave-uniform and stay in scalar registers).
+__device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c[0]), lo0 = 0xD2511F53u * c[0];
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c[2]), lo1 = 0xCD9E8D57u * c[2];
+    c = u32x4{hi1 ^ c[1] ^ k0, lo1, hi0 ^ c[3] ^ k1, lo0};
+  }
+  return c;
+}
+
+// Randomized code (Lemma 1): floor(y + xi) for y = (x - lo)/u (IEEE
+// division) and xi = w24 * 2^-24, taken exactly: floor(y) + 1 when w24 +
+// floor(2^24 * frac(y)) >= 2^24 (the fraction and its scaling are exact);
+// clamped to [0, L].  u != 0.
+__device__ __forceinline__ uint32_t code_randomized(float x, float lo, float u, float levels, uint32_t w24) {
+  const float y = (x - lo) / u;
+  const float fy = __builtin_floorf(y);
+  const float f = y - fy;
+  const uint32_t fr = (uint32_t)__builtin_floorf(f * 16777216.0f);
+  float r = fy + ((w24 + fr >= (1u << 24)) ? 1.0f : 0.0f);
+  r = __builtin_fminf(__builtin_fmaxf(r, 0.0f), levels);
+  return (uint32_t)r;
+}
+
+// Quantization step of a bucket: (max - min) / L, correctly rounded.
+template <int EFM>
+__device__ __forceinline__ float ef_step(float d) {
+  if constexpr (EFM & kEf8) return d / 255.0f;
+  else return div15(d);
+}
+
 // Byte n of x as a float (v_cvt_f32_ubyte{n}); the compiler does not form
 // these from shifts and masks of packed nibbles.
 template <int N>
@@ -278,6 +322,7 @@ struct Block {
   TensorDesc desc;
   int s;                  // valid elements
   int kq;                 // window entries per row
+  uint32_t j;             // tensor number
 };
 
 __device__ __forceinline__ Block locate(const StepParams& p, int64_t gb) {
@@ -289,6 +334,7 @@ __device__ __forceinline__ Block locate(const StepParams& p, int64_t gb) {
   b.e0 = (int64_t)q * p.block;
   b.s = last ? b.desc.s_last : p.block;
   b.kq = last ? b.desc.k_last : b.desc.k_full;
+  b.j = j;
   return b;
 }
 
@@ -371,25 +417,36 @@ __device__ __forceinline__ uint32_t lane_prefix(uint32_t c, uint32_t& total) {
 // [eb, eb + EPL) of its block as NV = EPL/8 vectors of 8.  LB: its buckets
 // are the lane or groups of lanes (B_q >= EPL); else buckets of whole
 // vectors inside the lane.
-template <int EPL, bool LB, bool GBF16>
+template <int EPL, bool LB, bool GBF16, int EFM = 0>
 struct LaneIn {
   static constexpr int NV = EPL / 8;
+  static constexpr int CW = (EFM & kEf8) ? 2 : 1;  // code words per vector
   u32x2 st[LB ? 1 : NV];  // bucket (min, max) pairs: one, or one per vector
-  uint32_t cw[NV];        // codes of vector v: element e in bits [4e, 4e + 4)
+  uint32_t cw[NV * CW];   // codes of vector v: 4-bit, element e in bits [4e, 4e + 4)
+                          // of word v; 8-bit, byte e & 3 of word 2v + e/4
   Raw8<GBF16> graw[NV];   // gradient
 };
 
 // Bucket pairs and codes of the lane.  `wide`: 16-byte code accesses (the
 // block fills every lane of the kernel), else 8-byte ones (B_d is a multiple
 // of 16, so no access then straddles the end of the block's codes).
-template <int EPL, bool LB, bool GBF16>
-__device__ __forceinline__ void lane_load_state(LaneIn<EPL, LB, GBF16>& in, Rsrc re, Rsrc rs, uint32_t eb, int bl,
-                                                bool wide) {
+template <int EPL, bool LB, bool GBF16, int EFM>
+__device__ __forceinline__ void lane_load_state(LaneIn<EPL, LB, GBF16, EFM>& in, Rsrc re, Rsrc rs, uint32_t eb,
+                                                int bl, bool wide) {
   constexpr int NV = EPL / 8;
 #pragma unroll
   for (int v = 0; v < (LB ? 1 : NV); ++v)
     in.st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, 0);
-  if (NV > 2 && wide) {
+  if constexpr (EFM & kEf8) {
+    // 16 codes per 16-byte access; B_d is a multiple of 16, so an access lies
+    // wholly inside or wholly past the block's codes
+#pragma unroll
+    for (int q = 0; q < NV / 2; ++q) {
+      const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(re, eb + 16 * q, 0, 0);
+#pragma unroll
+      for (int h = 0; h < 4; ++h) in.cw[4 * q + h] = t[h];
+    }
+  } else if (NV > 2 && wide) {
 #pragma unroll
     for (int q = 0; q < NV / 4; ++q) {
       const u32x4 t = __builtin_amdgcn_raw_buffer_load_b128(re, (eb >> 1) + 16 * q, 0, 0);
@@ -406,33 +463,39 @@ __device__ __forceinline__ void lane_load_state(LaneIn<EPL, LB, GBF16>& in, Rsrc
   }
 }
 
-template <int EPL, bool LB, bool GBF16>
-__device__ __forceinline__ void lane_load_grad(LaneIn<EPL, LB, GBF16>& in, Rsrc rg, uint32_t eb) {
+template <int EPL, bool LB, bool GBF16, int EFM>
+__device__ __forceinline__ void lane_load_grad(LaneIn<EPL, LB, GBF16, EFM>& in, Rsrc rg, uint32_t eb) {
 #pragma unroll
   for (int v = 0; v < EPL / 8; ++v) in.graw[v] = load8<GBF16>(rg, eb + 8 * v);
 }
 
 // a = g + Q^-1(e) (Algorithm 1; Algorithm 2, Q^-1).  rem: the lane's
 // elements below the end of the block, [0, rem); the others are 0.
-template <int EPL, bool LB, bool GBF16>
-__device__ __forceinline__ void lane_decode(const LaneIn<EPL, LB, GBF16>& in, float (&a)[EPL / 8][8], int rem,
+template <int EPL, bool LB, bool GBF16, int EFM>
+__device__ __forceinline__ void lane_decode(const LaneIn<EPL, LB, GBF16, EFM>& in, float (&a)[EPL / 8][8], int rem,
                                             bool full) {
   constexpr int NV = EPL / 8;
   {
     float lo0 = 0.0f, u0 = 0.0f;
     if constexpr (LB) {
       lo0 = __uint_as_float(in.st[0][0]);
-      u0 = div15(__uint_as_float(in.st[0][1]) - lo0);
+      u0 = ef_step<EFM>(__uint_as_float(in.st[0][1]) - lo0);
     }
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const float lo = LB ? lo0 : __uint_as_float(in.st[v][0]);
-      const float u = LB ? u0 : div15(__uint_as_float(in.st[v][1]) - lo);
-      const uint32_t ev = in.cw[v] & 0x0F0F0F0Fu, od = (in.cw[v] >> 4) & 0x0F0F0F0Fu;
+      const float u = LB ? u0 : ef_step<EFM>(__uint_as_float(in.st[v][1]) - lo);
       float g[8], c[8];
       unpack8<GBF16>(in.graw[v], g);
-      c[0] = ubyte<0>(ev); c[2] = ubyte<1>(ev); c[4] = ubyte<2>(ev); c[6] = ubyte<3>(ev);
-      c[1] = ubyte<0>(od); c[3] = ubyte<1>(od); c[5] = ubyte<2>(od); c[7] = ubyte<3>(od);
+      if constexpr (EFM & kEf8) {
+        const uint32_t w0 = in.cw[2 * v], w1 = in.cw[2 * v + 1];
+        c[0] = ubyte<0>(w0); c[1] = ubyte<1>(w0); c[2] = ubyte<2>(w0); c[3] = ubyte<3>(w0);
+        c[4] = ubyte<0>(w1); c[5] = ubyte<1>(w1); c[6] = ubyte<2>(w1); c[7] = ubyte<3>(w1);
+      } else {
+        const uint32_t ev = in.cw[v] & 0x0F0F0F0Fu, od = (in.cw[v] >> 4) & 0x0F0F0F0Fu;
+        c[0] = ubyte<0>(ev); c[2] = ubyte<1>(ev); c[4] = ubyte<2>(ev); c[6] = ubyte<3>(ev);
+        c[1] = ubyte<0>(od); c[3] = ubyte<1>(od); c[5] = ubyte<2>(od); c[7] = ubyte<3>(od);
+      }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float sc = c[e] * u;
@@ -462,15 +525,27 @@ __device__ __forceinline__ void lane_vmax(const float (&a)[EPL / 8][8], float (&
   }
 }
 
-// e = Q(a with a[I] = 0) (Algorithm 1; Algorithm 2, Q; Section 3.1): zeroes
-// the kept elements (|a| > T, and |a| == T up to index i_last; every
-// |a| >= T when notie), computes the bucket (min, max) pairs and the codes,
-// and stores both.
-template <int EPL, bool LB>
+// Where the randomized quantizer's xi come from: element i of tensor j at
+// step t takes word i mod 4 of Philox4x32-10 at counter (i/4 low, i/4 high,
+// j, t) under the 64-bit seed, and xi = (word >> 8) * 2^-24.
+struct EfStream {
+  int64_t e0;      // first element of the block in its tensor
+  uint32_t j, t;   // tensor number, step
+  uint32_t k0, k1; // seed, low and high word
+};
+
+// e = Q(a with a[I] = 0) (Algorithm 1; Algorithm 2, Q; Section 3.1; with
+// kEfRandom the randomized Q of Lemma 1): zeroes the kept elements (|a| >
+// T, and |a| == T up to index i_last; every |a| >= T when notie), computes
+// the bucket (min, max) pairs and the codes, and stores both.
+template <int EPL, bool LB, int EFM = 0>
 __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint32_t T, bool notie,
                                                     uint32_t i_last, uint32_t eb, int s, int rem, bool full, int bl,
-                                                    bool wide, Rsrc re, Rsrc rs) {
+                                                    bool wide, Rsrc re, Rsrc rs, const EfStream& rs_ef = {}) {
   constexpr int NV = EPL / 8;
+  constexpr bool EF8 = (EFM & kEf8) != 0;
+  constexpr int CW = EF8 ? 2 : 1;
+  constexpr float L = EF8 ? 255.0f : 15.0f;
   constexpr int lg = EPL == 16 ? 4 : EPL == 32 ? 5 : 6;
   // kept elements: |a| > T, and |a| == T up to index i_last; without ties
   // at the threshold that is |a| >= T (a wave-uniform case).  With ties the
@@ -551,7 +626,7 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
       }
     }
   }
-  uint32_t wv[NV];
+  uint32_t wv[NV * CW];
   {
     float uq = 0.0f, mnq = 0.0f;
 #pragma unroll
@@ -560,39 +635,84 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
         mn[v] = mn[v] + 0.0f;  // a bucket bound of -0 is stored as +0
         mx[v] = mx[v] + 0.0f;
         mnq = mn[v];
-        uq = div15(mx[v] - mn[v]);
+        uq = ef_step<EFM>(mx[v] - mn[v]);
       }
-      // Codes from two products that bracket the quotient: v_rcp is within
-      // 1 ulp for these u, so r_lo < 1/u < r_hi and
-      // rint((x-min)*r_lo) <= rint((x-min)/u) <= rint((x-min)*r_hi).  Where
-      // the two agree (all but a few elements in a million) the code is
-      // exact; elsewhere it is recomputed with an IEEE division.
       const float uv = uq, mnv = mnq;
-      const float rcp = __builtin_amdgcn_rcpf(uv);
-      const float r_lo = __uint_as_float(__float_as_uint(rcp) - 2u);
-      const float r_hi = __uint_as_float(__float_as_uint(rcp) + 2u);
-      uint32_t d1e = 0, d1o = 0, d2e = 0, d2o = 0;
+      uint32_t w[CW];
+      if constexpr ((EFM & kEfRandom) != 0) {
+        // two Philox blocks give the xi of the vector's 8 elements (the
+        // vector starts at a multiple of 8 within the tensor)
+        const uint64_t quad = (uint64_t)(rs_ef.e0 + eb + 8 * v) >> 2;
+        uint32_t w24[8];
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        const float ye = a[v][2 * h] - mnv, yo = a[v][2 * h + 1] - mnv;
-        const float p1e = ye * r_lo, p1o = yo * r_lo;
-        const float p2e = ye * r_hi, p2o = yo * r_hi;
-        d1e = __builtin_amdgcn_cvt_pk_u8_f32(p1e, h, d1e);  // round half to even, clamp to [0, 255]
-        d1o = __builtin_amdgcn_cvt_pk_u8_f32(p1o, h, d1o);
-        d2e = __builtin_amdgcn_cvt_pk_u8_f32(p2e, h, d2e);
-        d2o = __builtin_amdgcn_cvt_pk_u8_f32(p2o, h, d2o);
-      }
-      uint32_t w = d1e | (d1o << 4);
-      const bool exact_u = uv >= 0x1p-125f && uv <= 0x1p+125f;
-      if (!exact_u | (d1e != d2e) | (d1o != d2o)) {
-        w = 0;
+        for (int h = 0; h < 2; ++h) {
+          const uint64_t qh = quad + h;
+          const u32x4 r = philox4x32_10(u32x4{(uint32_t)qh, (uint32_t)(qh >> 32), rs_ef.j, rs_ef.t}, rs_ef.k0,
+                                        rs_ef.k1);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) w24[4 * h + i] = r[i] >> 8;
+        }
+#pragma unroll
+        for (int c = 0; c < CW; ++c) w[c] = 0;
         if (uv != 0.0f) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const float y = a[v][e] - mnv;
-            float rr = __builtin_rintf(y / uv);
-            rr = __builtin_fminf(__builtin_fmaxf(rr, 0.0f), 15.0f);
-            w |= (uint32_t)rr << (4 * e);
+            const uint32_t code = code_randomized(a[v][e], mnv, uv, L, w24[e]);
+            if constexpr (EF8) w[e >> 2] |= code << (8 * (e & 3));
+            else w[0] |= code << (4 * e);
+          }
+        }
+      } else {
+        // Codes from two products that bracket the quotient: v_rcp is within
+        // 1 ulp for these u, so r_lo < 1/u < r_hi and
+        // rint((x-min)*r_lo) <= rint((x-min)/u) <= rint((x-min)*r_hi).  Where
+        // the two agree (all but a few elements in a million) the code is
+        // exact; elsewhere it is recomputed with an IEEE division.
+        const float rcp = __builtin_amdgcn_rcpf(uv);
+        const float r_lo = __uint_as_float(__float_as_uint(rcp) - 2u);
+        const float r_hi = __uint_as_float(__float_as_uint(rcp) + 2u);
+        bool agree;
+        if constexpr (EF8) {
+          uint32_t d1a = 0, d1b = 0, d2a = 0, d2b = 0;
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            const float ya = a[v][h] - mnv, yb = a[v][4 + h] - mnv;
+            d1a = __builtin_amdgcn_cvt_pk_u8_f32(ya * r_lo, h, d1a);  // round half to even, clamp to [0, 255]
+            d1b = __builtin_amdgcn_cvt_pk_u8_f32(yb * r_lo, h, d1b);
+            d2a = __builtin_amdgcn_cvt_pk_u8_f32(ya * r_hi, h, d2a);
+            d2b = __builtin_amdgcn_cvt_pk_u8_f32(yb * r_hi, h, d2b);
+          }
+          w[0] = d1a;
+          w[CW - 1] = d1b;
+          agree = (d1a == d2a) & (d1b == d2b);
+        } else {
+          uint32_t d1e = 0, d1o = 0, d2e = 0, d2o = 0;
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            const float ye = a[v][2 * h] - mnv, yo = a[v][2 * h + 1] - mnv;
+            const float p1e = ye * r_lo, p1o = yo * r_lo;
+            const float p2e = ye * r_hi, p2o = yo * r_hi;
+            d1e = __builtin_amdgcn_cvt_pk_u8_f32(p1e, h, d1e);  // round half to even, clamp to [0, 255]
+            d1o = __builtin_amdgcn_cvt_pk_u8_f32(p1o, h, d1o);
+            d2e = __builtin_amdgcn_cvt_pk_u8_f32(p2e, h, d2e);
+            d2o = __builtin_amdgcn_cvt_pk_u8_f32(p2o, h, d2o);
+          }
+          w[0] = d1e | (d1o << 4);
+          agree = (d1e == d2e) & (d1o == d2o);
+        }
+        const bool exact_u = uv >= 0x1p-125f && uv <= 0x1p+125f;
+        if (!exact_u | !agree) {
+#pragma unroll
+          for (int c = 0; c < CW; ++c) w[c] = 0;
+          if (uv != 0.0f) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float y = a[v][e] - mnv;
+              float rr = __builtin_rintf(y / uv);
+              rr = __builtin_fminf(__builtin_fmaxf(rr, 0.0f), L);
+              if constexpr (EF8) w[e >> 2] |= (uint32_t)rr << (8 * (e & 3));
+              else w[0] |= (uint32_t)rr << (4 * e);
+            }
           }
         }
       }
@@ -600,13 +720,22 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
         const int r = opaque_v(rem);
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          if (8 * v + e >= r) w &= ~(0xFu << (4 * e));
+          if (8 * v + e >= r) {
+            if constexpr (EF8) w[e >> 2] &= ~(0xFFu << (8 * (e & 3)));
+            else w[0] &= ~(0xFu << (4 * e));
+          }
       }
-      wv[v] = w;
+#pragma unroll
+      for (int c = 0; c < CW; ++c) wv[CW * v + c] = w[c];
     }
   }
   if ((int)eb < s) {
-    if (NV > 2 && wide) {
+    if constexpr (EF8) {
+#pragma unroll
+      for (int q = 0; q < NV / 2; ++q)
+        __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]}, re,
+                                               eb + 16 * q, 0, 0);
+    } else if (NV > 2 && wide) {
 #pragma unroll
       for (int q = 0; q < NV / 4; ++q)
         __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]}, re,
@@ -632,7 +761,7 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
   }
 }
 
-template <int EPL, bool LB, bool GBF16, bool VF32>
+template <int EPL, bool LB, bool GBF16, bool VF32, int EFM>
 __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
 select_kernel(StepParams p, int64_t first) {
   constexpr int NV = EPL / 8;
@@ -653,10 +782,11 @@ select_kernel(StepParams p, int64_t first) {
   // The block's EF codes and bucket pairs are addressed by gb alone, so their
   // loads go out before the tensor lookup that the gradient needs.
   const uint32_t nbk = (uint32_t)(p.block >> bl);
-  const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * (p.block >> 1), (uint32_t)(p.block >> 1));
+  const uint32_t ef_bytes = (EFM & kEf8) ? (uint32_t)p.block : (uint32_t)(p.block >> 1);
+  const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * ef_bytes, ef_bytes);
   const Rsrc rs = make_rsrc(p.state + p.stats_plane + (uint64_t)gb * nbk * 8, nbk * 8);
   const bool wide = p.block == CAP;
-  LaneIn<EPL, LB, GBF16> in;
+  LaneIn<EPL, LB, GBF16, EFM> in;
   lane_load_state(in, re, rs, eb, bl, wide);
   const Block b = locate(p, gb);
   const int s = b.s, kq = b.kq;
@@ -966,7 +1096,8 @@ select_kernel(StepParams p, int64_t first) {
   }
 
   // ---------------------------------------------- 4. e = Q(a with a[I] = 0)
-  lane_quantize_store<EPL, LB>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs);
+  lane_quantize_store<EPL, LB, EFM>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs,
+                                    EfStream{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi});
 }
 
 // ================================================ select, blocks above 4096
@@ -1597,11 +1728,12 @@ update_kernel(StepParams p, int64_t first_block, float* mhat, float* vhat) {
   }
 }
 
-template <int EPL, bool LB, bool GB, bool VF>
+template <int EPL, bool LB, bool GB, bool VF, int EFM>
 hipError_t launch_select_t(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
   if (count <= 0) return hipSuccess;
   const size_t lds = select_lds_words() * 4;
-  hipLaunchKernelGGL((select_kernel<EPL, LB, GB, VF>), dim3((uint32_t)count), dim3(kWave), lds, stream, p, first);
+  hipLaunchKernelGGL((select_kernel<EPL, LB, GB, VF, EFM>), dim3((uint32_t)count), dim3(kWave), lds, stream, p,
+                     first);
   return hipGetLastError();
 }
 
@@ -1648,20 +1780,36 @@ hipError_t launch_update_large(const StepParams& p, int64_t first, int64_t count
   return hipGetLastError();
 }
 
-template <int EPL, bool GB, bool VF>
+template <int EPL, bool GB, bool VF, int EFM>
 hipError_t launch_select_e(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
   // whole buckets per lane (B_q >= EPL) or buckets of whole vectors
-  if ((1 << p.bucket_log2) >= EPL) return launch_select_t<EPL, true, GB, VF>(p, first, count, stream);
-  return launch_select_t<EPL, false, GB, VF>(p, first, count, stream);
+  if ((1 << p.bucket_log2) >= EPL) return launch_select_t<EPL, true, GB, VF, EFM>(p, first, count, stream);
+  return launch_select_t<EPL, false, GB, VF, EFM>(p, first, count, stream);
+}
+
+// Blocks above 4096 elements take the multi-wave kernel, which has the
+// default code format only (the host rejects the others there).
+template <bool GB, bool VF, int EFM>
+hipError_t launch_select_d(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  if (p.block > kSubBlock) {
+    if constexpr (EFM != 0) return hipErrorInvalidValue;
+    else return launch_select_large<GB, VF>(p, first, count, stream);
+  }
+  switch (select_epl(p.block)) {
+    case 16: return launch_select_e<16, GB, VF, EFM>(p, first, count, stream);
+    case 32: return launch_select_e<32, GB, VF, EFM>(p, first, count, stream);
+    default: return launch_select_e<64, GB, VF, EFM>(p, first, count, stream);
+  }
 }
 
 template <bool GB, bool VF>
-hipError_t launch_select_d(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
-  if (p.block > kSubBlock) return launch_select_large<GB, VF>(p, first, count, stream);
-  switch (select_epl(p.block)) {
-    case 16: return launch_select_e<16, GB, VF>(p, first, count, stream);
-    case 32: return launch_select_e<32, GB, VF>(p, first, count, stream);
-    default: return launch_select_e<64, GB, VF>(p, first, count, stream);
+hipError_t launch_select_f(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  switch (p.ef_mode) {
+    case 0: return launch_select_d<GB, VF, 0>(p, first, count, stream);
+    case kEf8: return launch_select_d<GB, VF, kEf8>(p, first, count, stream);
+    case kEfRandom: return launch_select_d<GB, VF, kEfRandom>(p, first, count, stream);
+    case kEf8 | kEfRandom: return launch_select_d<GB, VF, kEf8 | kEfRandom>(p, first, count, stream);
+    default: return hipErrorInvalidValue;
   }
 }
 
@@ -1723,10 +1871,10 @@ size_t step_lds_bytes(int block, int k_full, int value_f32) {
 hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
                          hipStream_t stream) {
   if (grad_bf16)
-    return value_f32 ? launch_select_d<true, true>(p, first, count, stream)
-                     : launch_select_d<true, false>(p, first, count, stream);
-  return value_f32 ? launch_select_d<false, true>(p, first, count, stream)
-                   : launch_select_d<false, false>(p, first, count, stream);
+    return value_f32 ? launch_select_f<true, true>(p, first, count, stream)
+                     : launch_select_f<true, false>(p, first, count, stream);
+  return value_f32 ? launch_select_f<false, true>(p, first, count, stream)
+                   : launch_select_f<false, false>(p, first, count, stream);
 }
 
 hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, int64_t first, int64_t count,

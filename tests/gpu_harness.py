@@ -1,8 +1,9 @@
 """Drives libmicroadam (through its C ABI binding) and the CPU oracle on the
 same seeded inputs and compares them after every step.
 
-Bit-exact: the 4-bit EF codes, the bucket (delta, Delta) pairs and every live
-window row (indices and bf16 / float32 values).  Within tolerance: the
+Bit-exact: the EF codes (4- or 8-bit, nearest or randomized rounding), the
+bucket (delta, Delta) pairs and every live window row (indices and bf16 /
+float32 values).  Within tolerance: the
 parameters and the window moments, which the kernel computes in binary32 and
 the oracle in binary64.  Tolerances (relative, per element):
   parameters  |x - y| <= tol * max(|y|, lr)   tol 1e-5 for float32 storage,
@@ -38,14 +39,17 @@ class Unit:
         self.j, self.q0, self.q1 = j, q0, q1
         self.e0 = q0 * block
         self.e1 = min(numel, q1 * block)
-        self.state = o.tensor(self.e1 - self.e0, block=block, **okw)
+        # the randomized rounding's stream is keyed by the tensor number and
+        # the element's place in the whole tensor
+        self.state = o.tensor(self.e1 - self.e0, block=block, tensor=j, offset=self.e0, **okw)
 
 
 class GpuOracleRun:
     def __init__(self, numels, *, param_dtype=torch.float32, grad_dtype=torch.float32,
                  grad_dist="normal", grad_scale=1.0, lr=1e-3, seed=0, sample=None,
                  density=0.01, window=10, bucket=64, block=4096, value_f32=False,
-                 beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, ranges=1, device="cuda"):
+                 beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, ranges=1, ef_bits=4,
+                 ef_rounding=0, ef_seed=0, device="cuda"):
         self.numels = list(numels)
         self.lr = lr
         self.device = torch.device(device)
@@ -54,8 +58,9 @@ class GpuOracleRun:
         self.block, self.bucket, self.window = block, bucket, window
         self.cfg = ma.make_config(density=density, beta1=beta1, beta2=beta2, eps=eps, lr=lr,
                                   weight_decay=weight_decay, window=window, ef_bucket=bucket,
-                                  topk_block=block,
+                                  topk_block=block, ef_bits=ef_bits, ef_rounding=ef_rounding, seed=ef_seed,
                                   window_value_dtype=ma.MICROADAM_F32 if value_f32 else ma.MICROADAM_BF16)
+        self.ef_bits = ef_bits
         self.params = [wl.draw(n, "normal", 0.02, seed + 7919 * (j + 1), self.device, param_dtype)
                        for j, n in enumerate(self.numels)]
         self.opt = ma.MicroAdam(self.params, self.cfg)
@@ -64,7 +69,7 @@ class GpuOracleRun:
         self.o = oracle.default()
         okw = dict(bucket=bucket, window=window, density=density, value_bf16=not value_f32,
                    param_bf16=param_dtype == torch.bfloat16, beta1=beta1, beta2=beta2, eps=eps,
-                   weight_decay=weight_decay)
+                   weight_decay=weight_decay, ef_bits=ef_bits, rounding=ef_rounding, seed=ef_seed)
         self.value_f32 = value_f32
         self.units: list[Unit] = []
         for j, n in enumerate(self.numels):
@@ -114,6 +119,10 @@ class GpuOracleRun:
         parts, raw = [], None
         for q in range(u.q0, u.q1):
             n = self._block_elems(lay, q)
+            if self.ef_bits == 8:
+                raw = self._read(lay.ef_plane + lay.block_number(q) * lay.ef_stride, n)
+                parts.append(raw.copy())
+                continue
             raw = self._read(lay.ef_plane + lay.block_number(q) * lay.ef_stride, (n + 1) // 2)
             c = np.empty(2 * raw.size, np.uint8)
             c[0::2] = raw & 0x0F
@@ -156,7 +165,7 @@ class GpuOracleRun:
             bad = np.nonzero(codes != st.codes())[0]
             assert bad.size == 0, (f"EF codes differ: tensor {u.j} block {u.q0} t={t}: "
                                    f"first at element {bad[0]}: gpu {codes[bad[0]]} oracle {st.codes()[bad[0]]}")
-            if (u.e1 - u.e0) % 2 == 1:
+            if self.ef_bits == 4 and (u.e1 - u.e0) % 2 == 1:
                 assert (raw[-1] >> 4) == 0, "odd tail nibble not zero"
             lo, hi = self.gpu_stats(u)
             assert np.array_equal(lo.view(np.uint32), st.delta.view(np.uint32)), f"delta differs t={t} tensor {u.j}"

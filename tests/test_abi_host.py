@@ -72,6 +72,15 @@ def test_state_bytes_tails_and_f32(lib):
     assert got2 == sum(pad(5 * x) for x in per_block)
 
 
+def test_state_bytes_8bit_codes(lib):
+    cfg = ma.make_config(density=0.01, window=3, ef_bucket=16, topk_block=256, ef_bits=8,
+                         ef_rounding=ma.MICROADAM_ROUND_RANDOMIZED, seed=7)
+    n = 1001            # 4 blocks of 256 (k 3): one code byte per element
+    pad = lambda x: -(-x // 256) * 256
+    per_block = (256, 16 * 8, 128)
+    assert ma.microadam_state_bytes(cfg, [n]) == sum(pad(4 * x) for x in per_block)
+
+
 def test_state_bytes_large_blocks(lib):
     """Blocks above 4096 elements (the flat 1.5e9 workload's B_d = 65536,
     k = 3277, m = 20, B_q = 128): each window record holds the m rows and an
@@ -96,8 +105,11 @@ BAD = [
     (dict(weight_decay=-1.0), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(window=0), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(window=65), ma.MICROADAM_ERR_UNSUPPORTED),
-    (dict(ef_bits=8), ma.MICROADAM_ERR_UNSUPPORTED),
+    (dict(ef_bits=6), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bits=0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(ef_bits=8, topk_block=8192), ma.MICROADAM_ERR_UNSUPPORTED),
+    (dict(ef_rounding=1, topk_block=8192), ma.MICROADAM_ERR_UNSUPPORTED),
+    (dict(ef_rounding=2), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(ef_bucket=48), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bucket=1), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(topk_block=4000, ef_bucket=64), ma.MICROADAM_ERR_INVALID_ARG),

@@ -54,6 +54,20 @@ CASES = {
     "block20000_bucket16": (dict(numels=[20000 * 2 + 777, 5000], block=20000, bucket=16,
                                  density=0.02, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
                                  window=4), 6),
+    # error-feedback formats beyond the paper's default: 8-bit codes, and the
+    # randomized rounding of Lemma 1 (Philox stream keyed by seed, tensor,
+    # step and element), bit-exact against the oracle
+    "ef8_nearest_tails": (dict(numels=[4096 * 2 + 768, 1001, 64, 5], param_dtype=bf16, grad_dtype=bf16,
+                               grad_scale=1e-3, window=4, ef_bits=8), 6),
+    "ef8_bucket8_block1024": (dict(numels=[5000, 1024], block=1024, bucket=8, density=0.01, window=3,
+                                   ef_bits=8), 5),
+    "randomized_4bit": (dict(numels=[4096 * 3 + 200, 333, 4096], grad_dist="student_t4", window=3,
+                             ef_rounding=1, ef_seed=12345), 6),
+    "randomized_8bit_block256": (dict(numels=[3000, 77], block=256, bucket=16, density=0.05, window=3,
+                                      ef_bits=8, ef_rounding=1, ef_seed=99), 5),
+    "randomized_block2048_bf16": (dict(numels=[9000], block=2048, bucket=32, window=3, param_dtype=bf16,
+                                       grad_dtype=bf16, grad_scale=1e-3, ef_rounding=1,
+                                       ef_seed=2 ** 40 + 3), 4),
 }
 
 
@@ -164,3 +178,20 @@ def test_flat_1p5e9_ties_sampled():
     """One 1.5e9-element bf16 tensor, B_d = 65536, k = 3277, m = 20,
     B_q = 128, Student-t(2) gradients snapped to 64 magnitudes; 5 steps."""
     _workload_sampled("flat1p5b_ties_bf16", 5, 4999, (4,))
+
+
+def test_randomized_sampled_offsets():
+    """Randomized rounding on 2000 full 4096-blocks of one tensor plus a
+    second tensor, sampled blocks: the stream's element numbers count from
+    the start of each tensor, not of the sampled block."""
+    print("[parity] randomized rounding, sampled blocks", flush=True)
+
+    def sample(j, nb):
+        return sorted({0, 1, nb - 1, *range(0, nb, 37)})
+
+    run = GpuOracleRun([4096 * 2000 + 55, 4096 * 3], grad_dtype=bf16, param_dtype=bf16, grad_scale=1e-3,
+                       lr=1e-4, density=0.01, window=4, bucket=64, block=4096, sample=sample,
+                       ef_rounding=1, ef_seed=0xDEADBEEF12345)
+    for t in range(5):
+        run.step(check_moments=t == 4)
+    run.opt.close()
