@@ -79,9 +79,13 @@ enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
  *                word, seed high word); j is the tensor's position in the
  *                numels list of microadam_init.  The floor is taken of the
  *                exact sum.  Unused with NEAREST.
- *   ef_bucket    B_q, elements sharing one (delta, Delta) pair; a power of
- *                two in [8, 512] dividing topk_block.
- *   topk_block   B_d, Top-K block size; a multiple of ef_bucket, at most
+ *   ef_bucket    B_q, elements sharing one (delta, Delta) pair: a power of
+ *                two in [8, 512] dividing topk_block (buckets inside blocks),
+ *                or any size >= topk_block (buckets of each tensor's
+ *                elements [c*B_q, (c+1)*B_q), spanning blocks; Section 3.1
+ *                names 100K), which needs topk_block <= 4096 and runs the
+ *                quantization as a second pass over the block.
+ *   topk_block   B_d, Top-K block size; at most
  *                65536 (block-relative indices are uint16).  This build
  *                implements multiples of 16 and returns
  *                MICROADAM_ERR_UNSUPPORTED for other valid sizes.
@@ -128,7 +132,13 @@ typedef struct microadam_handle_s* microadam_handle;
  *   stats      B_d/B_q pairs of float32 (delta, Delta) per block = (min,
  *              max) of the bucket's residual; pair b covers the block's
  *              elements [b*B_q, (b+1)*B_q); pairs past its elements are
- *              unused.
+ *              unused.  With buckets spanning blocks (ef_bucket >= B_d and
+ *              not a power of two in [8, 512] dividing B_d) the buckets are
+ *              the tensor's elements [c*B_q, (c+1)*B_q), and their pairs
+ *              live in two tables of bucket_table_bytes: the pair of bucket
+ *              c written at step t is at stats_plane + (t mod 2) *
+ *              bucket_table_bytes + 8*c (stats_stride is 0).  A plane of 16
+ *              bytes per block of partial (min, max) pairs follows them.
  *   window     m*k_full*entry_bytes per block, rounded up to a multiple
  *              of 128 bytes (the stride): row r (the row written at
  *              step s is r = (s-1) mod m) starts at r*k_q*entry_bytes within
@@ -157,6 +167,7 @@ typedef struct microadam_layout {
   uint64_t ef_plane, ef_stride;
   uint64_t stats_plane, stats_stride;
   uint64_t window_plane, window_stride;
+  uint64_t bucket_table_bytes; /* buckets spanning blocks: see stats above; else 0 */
 } microadam_layout;
 
 /*

@@ -67,6 +67,7 @@ class microadam_layout(ctypes.Structure):
         ("stats_stride", ctypes.c_uint64),
         ("window_plane", ctypes.c_uint64),
         ("window_stride", ctypes.c_uint64),
+        ("bucket_table_bytes", ctypes.c_uint64),
     ]
 
     def block_number(self, q: int) -> int:

@@ -45,6 +45,15 @@ int64_t block_k(int64_t s, double density) {
 
 bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
+// Buckets of B_q >= B_d elements that are not the block-local kind (a power
+// of two in [8, 512] dividing B_d): each tensor's buckets restart at its
+// element 0, so a bucket may hold several blocks and a block may straddle two.
+bool buckets_span_blocks(const microadam_config* c) {
+  const bool local = is_pow2(c->ef_bucket) && c->ef_bucket >= 8 && c->ef_bucket <= 512 && c->topk_block > 0 &&
+                     c->topk_block % c->ef_bucket == 0;
+  return !local && c->ef_bucket >= c->topk_block;
+}
+
 int validate_config(const microadam_config* c) {
   if (!c) return fail(MICROADAM_ERR_INVALID_ARG, "config is NULL");
   if (!(c->density > 0.0 && c->density <= 1.0))
@@ -62,15 +71,19 @@ int validate_config(const microadam_config* c) {
   if (c->ef_bits < 1 || c->ef_bits > 16) return fail(MICROADAM_ERR_INVALID_ARG, "ef_bits out of range");
   if (c->ef_bits != 4 && c->ef_bits != 8) return fail(MICROADAM_ERR_UNSUPPORTED, "ef_bits must be 4 or 8");
   if (c->ef_bucket < 2) return fail(MICROADAM_ERR_INVALID_ARG, "ef_bucket must be >= 2");
-  if (!is_pow2(c->ef_bucket) || c->ef_bucket < 8 || c->ef_bucket > 512)
-    return fail(MICROADAM_ERR_UNSUPPORTED, "ef_bucket must be a power of two in [8, 512]");
   if (c->topk_block < 1) return fail(MICROADAM_ERR_INVALID_ARG, "topk_block must be >= 1");
   if (c->topk_block > microadam::kMaxBlock)
     return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block above 65536 does not fit uint16 indices");
-  if (c->topk_block % c->ef_bucket != 0)
-    return fail(MICROADAM_ERR_INVALID_ARG, "topk_block must be a multiple of ef_bucket");
+  if (!buckets_span_blocks(c)) {
+    if (!is_pow2(c->ef_bucket) || c->ef_bucket < 8 || c->ef_bucket > 512)
+      return fail(MICROADAM_ERR_UNSUPPORTED, "ef_bucket must be a power of two in [8, 512], or >= topk_block");
+    if (c->topk_block % c->ef_bucket != 0)
+      return fail(MICROADAM_ERR_INVALID_ARG, "topk_block must be a multiple of ef_bucket");
+  }
   if (c->topk_block % 16 != 0)
     return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block must be a multiple of 16");
+  if (buckets_span_blocks(c) && c->topk_block > 4096)
+    return fail(MICROADAM_ERR_UNSUPPORTED, "buckets of topk_block or more elements need topk_block <= 4096");
   if (c->window_value_dtype != MICROADAM_BF16 && c->window_value_dtype != MICROADAM_F32)
     return fail(MICROADAM_ERR_INVALID_ARG, "window_value_dtype must be BF16 or F32");
   if (c->ef_rounding != MICROADAM_ROUND_NEAREST && c->ef_rounding != MICROADAM_ROUND_RANDOMIZED)
@@ -82,6 +95,7 @@ int validate_config(const microadam_config* c) {
 
 struct TensorPlan {
   int64_t numel, num_blocks, num_buckets, num_full, first_block, last_block;
+  int64_t first_bucket;  // buckets spanning blocks: bucket 0's place in the tables
   int32_t k_full, k_last, s_last;
 };
 
@@ -91,6 +105,12 @@ struct Planes {
   uint64_t ef, stats, win, total;
   uint64_t ef_stride, stats_stride, win_stride;  // bytes per block
   int64_t n_full, n_blocks;
+  // buckets spanning blocks: two tables of n_buckets (delta, Delta) pairs
+  // (table_bytes each) in the stats plane, and a partials plane of 16 bytes
+  // per block
+  bool big = false;
+  int64_t n_buckets = 0;
+  uint64_t table_bytes = 0, partial = 0;
 };
 
 int entry_bytes(const microadam_config* c) { return c->window_value_dtype == MICROADAM_F32 ? 8 : 4; }
@@ -106,8 +126,10 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
   const int64_t B = c->topk_block, Bq = c->ef_bucket, m = c->window;
   const int64_t eb = entry_bytes(c);
   const int32_t k_full = (int32_t)block_k(B, c->density);
+  pl.big = buckets_span_blocks(c);
+  pl.n_buckets = 0;
   pl.ef_stride = (uint64_t)B * (uint64_t)c->ef_bits / 8;
-  pl.stats_stride = (uint64_t)(B / Bq) * 8;
+  pl.stats_stride = pl.big ? 0 : (uint64_t)(B / Bq) * 8;
   // whole 128-byte lines per record, so that a row can be written as whole
   // lines without touching another block's record; blocks above 4096 add a
   // table of m * ceil(B_d/4096) uint32 segment starts behind the rows
@@ -127,6 +149,8 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
     p.k_full = k_full;
     p.s_last = (int32_t)(d - (p.num_blocks - 1) * B);
     p.k_last = (int32_t)block_k(p.s_last, c->density);
+    p.first_bucket = pl.big ? pl.n_buckets : 0;
+    if (pl.big) pl.n_buckets += p.num_buckets;
     full += p.num_full;
     out.push_back(p);
   }
@@ -138,7 +162,13 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
   pl.n_blocks = next;
   pl.ef = 0;
   pl.stats = align_up(pl.ef + nb * pl.ef_stride);
-  pl.win = align_up(pl.stats + nb * pl.stats_stride);
+  if (pl.big) {
+    pl.table_bytes = (uint64_t)pl.n_buckets * 8;
+    pl.partial = align_up(pl.stats + 2 * pl.table_bytes);
+    pl.win = align_up(pl.partial + nb * 16);
+  } else {
+    pl.win = align_up(pl.stats + nb * pl.stats_stride);
+  }
   pl.total = align_up(pl.win + nb * pl.win_stride);
   return MICROADAM_OK;
 }
@@ -251,6 +281,13 @@ void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& 
   p.ef_mode = (c.ef_bits == 8 ? 1 : 0) | (c.ef_rounding == MICROADAM_ROUND_RANDOMIZED ? 2 : 0);
   p.seed_lo = (uint32_t)c.seed;
   p.seed_hi = (uint32_t)(c.seed >> 32);
+  if (h->planes.big) {
+    p.big_bucket = c.ef_bucket;
+    p.total_buckets = h->planes.n_buckets;
+    p.table_bytes = h->planes.table_bytes;
+    p.partial_plane = h->planes.partial;
+  }
+  p.n_tensors = (int32_t)h->plans.size();
 }
 
 int check_handle(microadam_handle h) {
@@ -307,6 +344,8 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   const int nt = threads_for_block(cfg->topk_block);
   if (total_blocks * (int64_t)nt >= ((int64_t)1 << 32) || total_blocks >= ((int64_t)1 << 31))
     return fail(MICROADAM_ERR_UNSUPPORTED, "too many Top-K blocks for one launch");
+  if (pl.big && (total_blocks >= ((int64_t)1 << 28) || pl.table_bytes >= ((uint64_t)1 << 32)))
+    return fail(MICROADAM_ERR_UNSUPPORTED, "too many blocks or buckets for buckets spanning blocks");
 
   microadam_handle h = new (std::nothrow) microadam_handle_s;
   if (!h) return fail(MICROADAM_ERR_NO_MEMORY, "handle allocation failed");
@@ -316,7 +355,8 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   h->param_bf16 = param_dtype == MICROADAM_BF16;
   h->grad_bf16 = grad_dtype == MICROADAM_BF16;
   h->value_f32 = cfg->window_value_dtype == MICROADAM_F32;
-  while ((1 << h->bucket_log2) < cfg->ef_bucket) ++h->bucket_log2;
+  if (!pl.big)
+    while ((1 << h->bucket_log2) < cfg->ef_bucket) ++h->bucket_log2;
   h->state = (uint8_t*)state;
   h->state_bytes = state_bytes;
   h->total_blocks = total_blocks;
@@ -370,6 +410,8 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
     d.k_last = p.k_last;
     d.s_last = p.s_last;
     d.num_full = (int32_t)p.num_full;
+    d.first_bucket = p.first_bucket;
+    d.num_buckets = h->planes.big ? p.num_buckets : 0;
     for (TableSlot& t : h->slots) t.h[j] = d;
   }
   hipStream_t s = (hipStream_t)stream;
@@ -440,9 +482,25 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
   StepParams p;
   fill_constants(h, t, lr, p);
   const bool prof = h->profiling;
-  const int R = h->ranges;
+  // buckets spanning blocks tie blocks together through the bucket tables,
+  // so such a step always runs as one range
+  const int R = h->planes.big ? 1 : h->ranges;
   auto rec = [&](int i, hipStream_t st) { return prof ? hipEventRecord(h->ev[i], st) : hipSuccess; };
-  if (R == 1) {
+  if (h->planes.big) {
+    // select with per-block partials, the bucket reduction, the quantization
+    // of the residual, then the update
+    if ((e = rec(0, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    e = microadam::launch_select_partials(p, h->grad_bf16, h->value_f32, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
+    e = microadam::launch_bucket_reduce(p, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the bucket reduction");
+    e = microadam::launch_requant(p, h->grad_bf16, h->value_f32, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the quantization kernel");
+    if ((e = rec(1, s)) != hipSuccess || (e = rec(2, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    e = microadam::launch_update(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
+    if ((e = rec(3, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  } else if (R == 1) {
     if ((e = rec(0, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     e = microadam::launch_select(p, h->grad_bf16, h->value_f32, 0, h->total_blocks, s);
     if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
@@ -516,8 +574,9 @@ int microadam_tensor_layout(microadam_handle h, int32_t tensor, microadam_layout
   out->last_block = p.last_block;
   out->ef_plane = h->planes.ef;
   out->ef_stride = h->planes.ef_stride;
-  out->stats_plane = h->planes.stats;
+  out->stats_plane = h->planes.big ? h->planes.stats + (uint64_t)p.first_bucket * 8 : h->planes.stats;
   out->stats_stride = h->planes.stats_stride;
+  out->bucket_table_bytes = h->planes.table_bytes;
   out->window_plane = h->planes.win;
   out->window_stride = h->planes.win_stride;
   return MICROADAM_OK;

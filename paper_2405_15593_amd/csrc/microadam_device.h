@@ -24,6 +24,8 @@ struct TensorDesc {
   int32_t k_last;         // entries per window row, last block
   int32_t s_last;         // elements in the last block
   int32_t num_full;       // full blocks
+  int64_t first_bucket;   // buckets spanning blocks: the tensor's bucket 0 in the table
+  int64_t num_buckets;    // its buckets (0 with buckets inside blocks)
 };
 
 // Threads per workgroup for a Top-K block of B_d elements (each thread owns
@@ -58,7 +60,21 @@ struct StepParams {
   float lr, decay, eps, c1, c2;
   int32_t ef_mode;               // code format: bit 0 8-bit codes, bit 1 randomized rounding
   uint32_t seed_lo, seed_hi;     // key of the randomized rounding's stream
+  // buckets spanning blocks (big_bucket = B_q > 0; else 0): the pairs of all
+  // tensors' buckets in two tables of table_bytes at stats_plane (step t
+  // fills table t mod 2), and per block two (min, max) partials at
+  // partial_plane + gb * 16
+  int64_t big_bucket;
+  int64_t total_buckets;
+  uint64_t table_bytes, partial_plane;
+  int32_t n_tensors;
 };
+
+// Steps with buckets spanning blocks: the per-block partials, their reduction
+// into the new bucket table, and the quantization of the residual with it.
+hipError_t launch_select_partials(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream);
+hipError_t launch_bucket_reduce(const StepParams& p, hipStream_t stream);
+hipError_t launch_requant(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream);
 
 // Launchers (defined in microadam_kernels.hip).  Return hipSuccess or the
 // launch error.  Each takes the global blocks [first, first + count); the

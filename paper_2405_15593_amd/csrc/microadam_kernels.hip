@@ -198,6 +198,8 @@ __device__ __forceinline__ TensorDesc load_desc(const __attribute__((address_spa
   r.k_last = d->k_last;
   r.s_last = d->s_last;
   r.num_full = d->num_full;
+  r.first_bucket = d->first_bucket;
+  r.num_buckets = d->num_buckets;
   return r;
 }
 
@@ -427,16 +429,26 @@ struct LaneIn {
   Raw8<GBF16> graw[NV];   // gradient
 };
 
+// Code values of vector v as floats (4-bit: nibbles, 8-bit: bytes).
+template <int EFM>
+__device__ __forceinline__ void unpack_codes(const uint32_t* cw, int v, float (&c)[8]) {
+  if constexpr (EFM & kEf8) {
+    const uint32_t w0 = cw[2 * v], w1 = cw[2 * v + 1];
+    c[0] = ubyte<0>(w0); c[1] = ubyte<1>(w0); c[2] = ubyte<2>(w0); c[3] = ubyte<3>(w0);
+    c[4] = ubyte<0>(w1); c[5] = ubyte<1>(w1); c[6] = ubyte<2>(w1); c[7] = ubyte<3>(w1);
+  } else {
+    const uint32_t ev = cw[v] & 0x0F0F0F0Fu, od = (cw[v] >> 4) & 0x0F0F0F0Fu;
+    c[0] = ubyte<0>(ev); c[2] = ubyte<1>(ev); c[4] = ubyte<2>(ev); c[6] = ubyte<3>(ev);
+    c[1] = ubyte<0>(od); c[3] = ubyte<1>(od); c[5] = ubyte<2>(od); c[7] = ubyte<3>(od);
+  }
+}
+
 // Bucket pairs and codes of the lane.  `wide`: 16-byte code accesses (the
 // block fills every lane of the kernel), else 8-byte ones (B_d is a multiple
 // of 16, so no access then straddles the end of the block's codes).
 template <int EPL, bool LB, bool GBF16, int EFM>
-__device__ __forceinline__ void lane_load_state(LaneIn<EPL, LB, GBF16, EFM>& in, Rsrc re, Rsrc rs, uint32_t eb,
-                                                int bl, bool wide) {
+__device__ __forceinline__ void lane_load_codes(LaneIn<EPL, LB, GBF16, EFM>& in, Rsrc re, uint32_t eb, bool wide) {
   constexpr int NV = EPL / 8;
-#pragma unroll
-  for (int v = 0; v < (LB ? 1 : NV); ++v)
-    in.st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, 0);
   if constexpr (EFM & kEf8) {
     // 16 codes per 16-byte access; B_d is a multiple of 16, so an access lies
     // wholly inside or wholly past the block's codes
@@ -464,6 +476,16 @@ __device__ __forceinline__ void lane_load_state(LaneIn<EPL, LB, GBF16, EFM>& in,
 }
 
 template <int EPL, bool LB, bool GBF16, int EFM>
+__device__ __forceinline__ void lane_load_state(LaneIn<EPL, LB, GBF16, EFM>& in, Rsrc re, Rsrc rs, uint32_t eb,
+                                                int bl, bool wide) {
+  constexpr int NV = EPL / 8;
+#pragma unroll
+  for (int v = 0; v < (LB ? 1 : NV); ++v)
+    in.st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, 0);
+  lane_load_codes(in, re, eb, wide);
+}
+
+template <int EPL, bool LB, bool GBF16, int EFM>
 __device__ __forceinline__ void lane_load_grad(LaneIn<EPL, LB, GBF16, EFM>& in, Rsrc rg, uint32_t eb) {
 #pragma unroll
   for (int v = 0; v < EPL / 8; ++v) in.graw[v] = load8<GBF16>(rg, eb + 8 * v);
@@ -487,15 +509,7 @@ __device__ __forceinline__ void lane_decode(const LaneIn<EPL, LB, GBF16, EFM>& i
       const float u = LB ? u0 : ef_step<EFM>(__uint_as_float(in.st[v][1]) - lo);
       float g[8], c[8];
       unpack8<GBF16>(in.graw[v], g);
-      if constexpr (EFM & kEf8) {
-        const uint32_t w0 = in.cw[2 * v], w1 = in.cw[2 * v + 1];
-        c[0] = ubyte<0>(w0); c[1] = ubyte<1>(w0); c[2] = ubyte<2>(w0); c[3] = ubyte<3>(w0);
-        c[4] = ubyte<0>(w1); c[5] = ubyte<1>(w1); c[6] = ubyte<2>(w1); c[7] = ubyte<3>(w1);
-      } else {
-        const uint32_t ev = in.cw[v] & 0x0F0F0F0Fu, od = (in.cw[v] >> 4) & 0x0F0F0F0Fu;
-        c[0] = ubyte<0>(ev); c[2] = ubyte<1>(ev); c[4] = ubyte<2>(ev); c[6] = ubyte<3>(ev);
-        c[1] = ubyte<0>(od); c[3] = ubyte<1>(od); c[5] = ubyte<2>(od); c[7] = ubyte<3>(od);
-      }
+      unpack_codes<EFM>(in.cw, v, c);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float sc = c[e] * u;
@@ -505,6 +519,69 @@ __device__ __forceinline__ void lane_decode(const LaneIn<EPL, LB, GBF16, EFM>& i
     }
   }
   if (!full) {  // elements past the end of the tensor are 0 and never kept
+    const int r = opaque_v(rem);
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (8 * v + e >= r) a[v][e] = 0.0f;
+  }
+}
+
+// ------------------------------------------- buckets spanning Top-K blocks
+// With buckets of B_q >= B_d elements (Section 3.1 mentions B_q = 100K) a
+// bucket holds several blocks and a block may straddle two buckets.  The
+// (delta, Delta) pairs of a tensor's buckets live in two tables: step t
+// decodes with table (t-1) mod 2 and fills table t mod 2.  The select kernel
+// then writes, per block, the (min, max) of the residual in each of its (at
+// most two) buckets; a reduction turns them into the new table, and a second
+// pass over the block quantizes the residual with it.
+
+// The lane's two buckets: its elements [0, sp) lie in the first, the rest
+// in the next.  `table`: the pairs of step t's decode (0) or of step t (1).
+struct LqBuckets {
+  u32x2 st[2];
+  int sp;
+};
+
+__device__ __forceinline__ LqBuckets lq_buckets(const StepParams& p, const Block& b, uint32_t eb, int epl,
+                                                int table) {
+  const int64_t bq = p.big_bucket;
+  const int64_t el = b.e0 + eb;  // tensor element of the lane's first element
+  const int64_t bk = el / bq;
+  const int64_t sp = (bk + 1) * bq - el;
+  const uint64_t t = (uint64_t)((p.t - 1 + table) & 1);
+  const Rsrc rt = make_rsrc(p.state + p.stats_plane + t * p.table_bytes + (uint64_t)b.desc.first_bucket * 8,
+                            (uint32_t)(b.desc.num_buckets * 8));
+  LqBuckets r;
+  r.st[0] = __builtin_amdgcn_raw_buffer_load_b64(rt, (uint32_t)(bk * 8), 0, 0);
+  r.st[1] = __builtin_amdgcn_raw_buffer_load_b64(rt, (uint32_t)(bk * 8 + 8), 0, 0);  // past the end: 0
+  r.sp = sp < epl ? (int)sp : epl;
+  return r;
+}
+
+// a = g + Q^-1(e) with the lane's two buckets (the arithmetic of lane_decode).
+template <int EPL, bool GBF16, int EFM>
+__device__ __forceinline__ void lane_decode_lq(const LaneIn<EPL, true, GBF16, EFM>& in, const LqBuckets& bk,
+                                               float (&a)[EPL / 8][8], int rem, bool full) {
+  constexpr int NV = EPL / 8;
+  const float lo0 = __uint_as_float(bk.st[0][0]), u0 = ef_step<EFM>(__uint_as_float(bk.st[0][1]) - lo0);
+  const float lo1 = __uint_as_float(bk.st[1][0]), u1 = ef_step<EFM>(__uint_as_float(bk.st[1][1]) - lo1);
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    float g[8], c[8];
+    unpack8<GBF16>(in.graw[v], g);
+    unpack_codes<EFM>(in.cw, v, c);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const bool second = 8 * v + e >= bk.sp;
+      const float lo = second ? lo1 : lo0, u = second ? u1 : u0;
+      const float sc = c[e] * u;
+      const float d = sc + lo;
+      a[v][e] = g[e] + d;
+    }
+  }
+  if (!full) {
     const int r = opaque_v(rem);
 #pragma unroll
     for (int v = 0; v < NV; ++v)
@@ -534,19 +611,125 @@ struct EfStream {
   uint32_t k0, k1; // seed, low and high word
 };
 
-// e = Q(a with a[I] = 0) (Algorithm 1; Algorithm 2, Q; Section 3.1; with
-// kEfRandom the randomized Q of Lemma 1): zeroes the kept elements (|a| >
-// T, and |a| == T up to index i_last; every |a| >= T when notie), computes
-// the bucket (min, max) pairs and the codes, and stores both.
-template <int EPL, bool LB, int EFM = 0>
-__device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint32_t T, bool notie,
-                                                    uint32_t i_last, uint32_t eb, int s, int rem, bool full, int bl,
-                                                    bool wide, Rsrc re, Rsrc rs, const EfStream& rs_ef = {}) {
-  constexpr int NV = EPL / 8;
+// Codes of one vector of 8 elements x against one bucket (lower bound mnv,
+// quantization step uv): 4-bit codes in w[0], element e in bits [4e, 4e + 4);
+// 8-bit codes in w[0], w[1], element e in byte e & 3 of word e / 4.  quad:
+// the tensor element number of x[0], divided by 4 (the randomized rounding's
+// counter).
+template <int EFM>
+__device__ __forceinline__ void vector_codes(const float (&x)[8], float mnv, float uv, uint64_t quad,
+                                             const EfStream& st, uint32_t (&w)[(EFM & kEf8) ? 2 : 1]) {
   constexpr bool EF8 = (EFM & kEf8) != 0;
   constexpr int CW = EF8 ? 2 : 1;
   constexpr float L = EF8 ? 255.0f : 15.0f;
-  constexpr int lg = EPL == 16 ? 4 : EPL == 32 ? 5 : 6;
+  if constexpr ((EFM & kEfRandom) != 0) {
+    // two Philox blocks give the xi of the vector's 8 elements (the
+    // vector starts at a multiple of 8 within the tensor)
+    uint32_t w24[8];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint64_t qh = quad + h;
+      const u32x4 r = philox4x32_10(u32x4{(uint32_t)qh, (uint32_t)(qh >> 32), st.j, st.t}, st.k0, st.k1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w24[4 * h + i] = r[i] >> 8;
+    }
+#pragma unroll
+    for (int c = 0; c < CW; ++c) w[c] = 0;
+    if (uv != 0.0f) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t code = code_randomized(x[e], mnv, uv, L, w24[e]);
+        if constexpr (EF8) w[e >> 2] |= code << (8 * (e & 3));
+        else w[0] |= code << (4 * e);
+      }
+    }
+  } else {
+    // Codes from two products that bracket the quotient: v_rcp is within
+    // 1 ulp for these u, so r_lo < 1/u < r_hi and
+    // rint((x-min)*r_lo) <= rint((x-min)/u) <= rint((x-min)*r_hi).  Where
+    // the two agree (all but a few elements in a million) the code is
+    // exact; elsewhere it is recomputed with an IEEE division.
+    const float rcp = __builtin_amdgcn_rcpf(uv);
+    const float r_lo = __uint_as_float(__float_as_uint(rcp) - 2u);
+    const float r_hi = __uint_as_float(__float_as_uint(rcp) + 2u);
+    bool agree;
+    if constexpr (EF8) {
+      uint32_t d1a = 0, d1b = 0, d2a = 0, d2b = 0;
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const float ya = x[h] - mnv, yb = x[4 + h] - mnv;
+        d1a = __builtin_amdgcn_cvt_pk_u8_f32(ya * r_lo, h, d1a);  // round half to even, clamp to [0, 255]
+        d1b = __builtin_amdgcn_cvt_pk_u8_f32(yb * r_lo, h, d1b);
+        d2a = __builtin_amdgcn_cvt_pk_u8_f32(ya * r_hi, h, d2a);
+        d2b = __builtin_amdgcn_cvt_pk_u8_f32(yb * r_hi, h, d2b);
+      }
+      w[0] = d1a;
+      w[CW - 1] = d1b;
+      agree = (d1a == d2a) & (d1b == d2b);
+    } else {
+      uint32_t d1e = 0, d1o = 0, d2e = 0, d2o = 0;
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const float ye = x[2 * h] - mnv, yo = x[2 * h + 1] - mnv;
+        const float p1e = ye * r_lo, p1o = yo * r_lo;
+        const float p2e = ye * r_hi, p2o = yo * r_hi;
+        d1e = __builtin_amdgcn_cvt_pk_u8_f32(p1e, h, d1e);  // round half to even, clamp to [0, 255]
+        d1o = __builtin_amdgcn_cvt_pk_u8_f32(p1o, h, d1o);
+        d2e = __builtin_amdgcn_cvt_pk_u8_f32(p2e, h, d2e);
+        d2o = __builtin_amdgcn_cvt_pk_u8_f32(p2o, h, d2o);
+      }
+      w[0] = d1e | (d1o << 4);
+      agree = (d1e == d2e) & (d1o == d2o);
+    }
+    const bool exact_u = uv >= 0x1p-125f && uv <= 0x1p+125f;
+    if (!exact_u | !agree) {
+#pragma unroll
+      for (int c = 0; c < CW; ++c) w[c] = 0;
+      if (uv != 0.0f) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float y = x[e] - mnv;
+          float rr = __builtin_rintf(y / uv);
+          rr = __builtin_fminf(__builtin_fmaxf(rr, 0.0f), L);
+          if constexpr (EF8) w[e >> 2] |= (uint32_t)rr << (8 * (e & 3));
+          else w[0] |= (uint32_t)rr << (4 * e);
+        }
+      }
+    }
+  }
+}
+
+// Stores a lane's codes (the layout of vector_codes, vector after vector).
+// `wide`: 16-byte accesses for 4-bit codes (the block fills every lane of the
+// kernel); 8-bit codes always take them, since B_d is a multiple of 16 and an
+// access then lies wholly inside or wholly past the block's codes.
+template <int EPL, int EFM>
+__device__ __forceinline__ void lane_store_codes(const uint32_t (&wv)[(EPL / 8) * ((EFM & kEf8) ? 2 : 1)],
+                                                 uint32_t eb, bool wide, Rsrc re) {
+  constexpr int NV = EPL / 8;
+  if constexpr ((EFM & kEf8) != 0) {
+#pragma unroll
+    for (int q = 0; q < NV / 2; ++q)
+      __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]}, re,
+                                             eb + 16 * q, 0, 0);
+  } else if (NV > 2 && wide) {
+#pragma unroll
+    for (int q = 0; q < NV / 4; ++q)
+      __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]}, re,
+                                             (eb >> 1) + 16 * q, 0, 0);
+  } else {
+#pragma unroll
+    for (int q = 0; q < NV / 2; ++q)
+      __builtin_amdgcn_raw_buffer_store_b64(u32x2{wv[2 * q], wv[2 * q + 1]}, re, (eb >> 1) + 8 * q, 0, 0);
+  }
+}
+
+// a[I] = 0 (Algorithm 1): the kept elements are |a| > T, and |a| == T up to
+// index i_last; every |a| >= T when notie.
+template <int EPL>
+__device__ __forceinline__ void lane_zero_kept(float (&a)[EPL / 8][8], uint32_t T, bool notie, uint32_t i_last,
+                                               uint32_t eb) {
+  constexpr int NV = EPL / 8;
   // kept elements: |a| > T, and |a| == T up to index i_last; without ties
   // at the threshold that is |a| >= T (a wave-uniform case).  With ties the
   // kept elements equal to T are zeroed first, and the rest are those
@@ -575,6 +758,21 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
 #pragma unroll
       for (int e = 0; e < 8; ++e) a[v][e] = (__builtin_fabsf(a[v][e]) >= tk) ? 0.0f : a[v][e];
   }
+}
+
+// e = Q(a with a[I] = 0) (Algorithm 1; Algorithm 2, Q; Section 3.1; with
+// kEfRandom the randomized Q of Lemma 1): zeroes the kept elements (|a| >
+// T, and |a| == T up to index i_last; every |a| >= T when notie), computes
+// the bucket (min, max) pairs and the codes, and stores both.
+template <int EPL, bool LB, int EFM = 0>
+__device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint32_t T, bool notie,
+                                                    uint32_t i_last, uint32_t eb, int s, int rem, bool full, int bl,
+                                                    bool wide, Rsrc re, Rsrc rs, const EfStream& rs_ef = {}) {
+  constexpr int NV = EPL / 8;
+  constexpr bool EF8 = (EFM & kEf8) != 0;
+  constexpr int CW = EF8 ? 2 : 1;
+  constexpr int lg = EPL == 16 ? 4 : EPL == 32 ? 5 : 6;
+  lane_zero_kept<EPL>(a, T, notie, i_last, eb);
   // bucket min / max: per vector, then over the vectors of a bucket inside
   // the lane, then over the lanes of a bucket
   float mn[NV], mx[NV];
@@ -639,83 +837,7 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
       }
       const float uv = uq, mnv = mnq;
       uint32_t w[CW];
-      if constexpr ((EFM & kEfRandom) != 0) {
-        // two Philox blocks give the xi of the vector's 8 elements (the
-        // vector starts at a multiple of 8 within the tensor)
-        const uint64_t quad = (uint64_t)(rs_ef.e0 + eb + 8 * v) >> 2;
-        uint32_t w24[8];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const uint64_t qh = quad + h;
-          const u32x4 r = philox4x32_10(u32x4{(uint32_t)qh, (uint32_t)(qh >> 32), rs_ef.j, rs_ef.t}, rs_ef.k0,
-                                        rs_ef.k1);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) w24[4 * h + i] = r[i] >> 8;
-        }
-#pragma unroll
-        for (int c = 0; c < CW; ++c) w[c] = 0;
-        if (uv != 0.0f) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const uint32_t code = code_randomized(a[v][e], mnv, uv, L, w24[e]);
-            if constexpr (EF8) w[e >> 2] |= code << (8 * (e & 3));
-            else w[0] |= code << (4 * e);
-          }
-        }
-      } else {
-        // Codes from two products that bracket the quotient: v_rcp is within
-        // 1 ulp for these u, so r_lo < 1/u < r_hi and
-        // rint((x-min)*r_lo) <= rint((x-min)/u) <= rint((x-min)*r_hi).  Where
-        // the two agree (all but a few elements in a million) the code is
-        // exact; elsewhere it is recomputed with an IEEE division.
-        const float rcp = __builtin_amdgcn_rcpf(uv);
-        const float r_lo = __uint_as_float(__float_as_uint(rcp) - 2u);
-        const float r_hi = __uint_as_float(__float_as_uint(rcp) + 2u);
-        bool agree;
-        if constexpr (EF8) {
-          uint32_t d1a = 0, d1b = 0, d2a = 0, d2b = 0;
-#pragma unroll
-          for (int h = 0; h < 4; ++h) {
-            const float ya = a[v][h] - mnv, yb = a[v][4 + h] - mnv;
-            d1a = __builtin_amdgcn_cvt_pk_u8_f32(ya * r_lo, h, d1a);  // round half to even, clamp to [0, 255]
-            d1b = __builtin_amdgcn_cvt_pk_u8_f32(yb * r_lo, h, d1b);
-            d2a = __builtin_amdgcn_cvt_pk_u8_f32(ya * r_hi, h, d2a);
-            d2b = __builtin_amdgcn_cvt_pk_u8_f32(yb * r_hi, h, d2b);
-          }
-          w[0] = d1a;
-          w[CW - 1] = d1b;
-          agree = (d1a == d2a) & (d1b == d2b);
-        } else {
-          uint32_t d1e = 0, d1o = 0, d2e = 0, d2o = 0;
-#pragma unroll
-          for (int h = 0; h < 4; ++h) {
-            const float ye = a[v][2 * h] - mnv, yo = a[v][2 * h + 1] - mnv;
-            const float p1e = ye * r_lo, p1o = yo * r_lo;
-            const float p2e = ye * r_hi, p2o = yo * r_hi;
-            d1e = __builtin_amdgcn_cvt_pk_u8_f32(p1e, h, d1e);  // round half to even, clamp to [0, 255]
-            d1o = __builtin_amdgcn_cvt_pk_u8_f32(p1o, h, d1o);
-            d2e = __builtin_amdgcn_cvt_pk_u8_f32(p2e, h, d2e);
-            d2o = __builtin_amdgcn_cvt_pk_u8_f32(p2o, h, d2o);
-          }
-          w[0] = d1e | (d1o << 4);
-          agree = (d1e == d2e) & (d1o == d2o);
-        }
-        const bool exact_u = uv >= 0x1p-125f && uv <= 0x1p+125f;
-        if (!exact_u | !agree) {
-#pragma unroll
-          for (int c = 0; c < CW; ++c) w[c] = 0;
-          if (uv != 0.0f) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const float y = a[v][e] - mnv;
-              float rr = __builtin_rintf(y / uv);
-              rr = __builtin_fminf(__builtin_fmaxf(rr, 0.0f), L);
-              if constexpr (EF8) w[e >> 2] |= (uint32_t)rr << (8 * (e & 3));
-              else w[0] |= (uint32_t)rr << (4 * e);
-            }
-          }
-        }
-      }
+      vector_codes<EFM>(a[v], mnv, uv, (uint64_t)(rs_ef.e0 + eb + 8 * v) >> 2, rs_ef, w);
       if (!full) {
         const int r = opaque_v(rem);
 #pragma unroll
@@ -730,21 +852,7 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
     }
   }
   if ((int)eb < s) {
-    if constexpr (EF8) {
-#pragma unroll
-      for (int q = 0; q < NV / 2; ++q)
-        __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]}, re,
-                                               eb + 16 * q, 0, 0);
-    } else if (NV > 2 && wide) {
-#pragma unroll
-      for (int q = 0; q < NV / 4; ++q)
-        __builtin_amdgcn_raw_buffer_store_b128(u32x4{wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]}, re,
-                                               (eb >> 1) + 16 * q, 0, 0);
-    } else {
-#pragma unroll
-      for (int q = 0; q < NV / 2; ++q)
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{wv[2 * q], wv[2 * q + 1]}, re, (eb >> 1) + 8 * q, 0, 0);
-    }
+    lane_store_codes<EPL, EFM>(wv, eb, wide, re);
     if constexpr (LB) {
       if ((eb & ((1u << bl) - 1)) == 0)
         __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[0]), __float_as_uint(mx[0])}, rs,
@@ -761,9 +869,10 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
   }
 }
 
-template <int EPL, bool LB, bool GBF16, bool VF32, int EFM>
+template <int EPL, bool LB, bool GBF16, bool VF32, int EFM, bool LQ = false>
 __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
 select_kernel(StepParams p, int64_t first) {
+  static_assert(!LQ || (EPL == 64 && LB && (EFM & kEfRandom) == 0), "buckets spanning blocks: 64 per lane");
   constexpr int NV = EPL / 8;
   constexpr int CAP = kWave * EPL;
   using E = Entry<VF32>;
@@ -787,8 +896,11 @@ select_kernel(StepParams p, int64_t first) {
   const Rsrc rs = make_rsrc(p.state + p.stats_plane + (uint64_t)gb * nbk * 8, nbk * 8);
   const bool wide = p.block == CAP;
   LaneIn<EPL, LB, GBF16, EFM> in;
-  lane_load_state(in, re, rs, eb, bl, wide);
+  if constexpr (LQ) lane_load_codes(in, re, eb, wide);
+  else lane_load_state(in, re, rs, eb, bl, wide);
   const Block b = locate(p, gb);
+  LqBuckets lqb = {};
+  if constexpr (LQ) lqb = lq_buckets(p, b, eb, EPL, 0);
   const int s = b.s, kq = b.kq;
   const bool full = s == CAP;
   const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + b.e0 * (GBF16 ? 2 : 4), vec_bytes<GBF16>(s));
@@ -809,7 +921,8 @@ select_kernel(StepParams p, int64_t first) {
   // ---------------------------------------------- 1. a = g + Q^-1(e)
   float a[NV][8];
   const int rem = s - (int)eb;  // this lane's elements below the end of the block: [0, rem)
-  lane_decode(in, a, rem, full);
+  if constexpr (LQ) lane_decode_lq(in, lqb, a, rem, full);
+  else lane_decode(in, a, rem, full);
 
   // ---------------------------------------------- 2. Top-K threshold
   float vmax[NV];
@@ -1096,8 +1209,187 @@ select_kernel(StepParams p, int64_t first) {
   }
 
   // ---------------------------------------------- 4. e = Q(a with a[I] = 0)
-  lane_quantize_store<EPL, LB, EFM>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs,
-                                    EfStream{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi});
+  if constexpr (LQ) {
+    lane_zero_kept<EPL>(a, T, notie, i_last, eb);
+    lane_partials<EPL>(a, p, b, eb, rem, gb);
+  } else {
+    lane_quantize_store<EPL, LB, EFM>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs,
+                                      EfStream{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi});
+  }
+}
+
+// Per block and bucket, the (min, max) of the residual (elements past the
+// block's end excluded; an empty part gives (+inf, -inf)): pairs for the
+// block's first bucket and for the next one, written by lane 0.
+template <int EPL>
+__device__ __forceinline__ void lane_partials(const float (&a)[EPL / 8][8], const StepParams& p, const Block& b,
+                                              uint32_t eb, int rem, int64_t gb) {
+  constexpr int NV = EPL / 8;
+  const int64_t bq = p.big_bucket;
+  const int64_t split = ((b.e0 / bq) + 1) * bq - b.e0;  // block element where the next bucket starts
+  const int64_t ls = split - (int64_t)eb;
+  const int lsplit = ls < 0 ? 0 : ls > EPL ? EPL : (int)ls;
+  const int r = opaque_v(rem);
+  float mn0 = __builtin_inff(), mx0 = -__builtin_inff(), mn1 = __builtin_inff(), mx1 = -__builtin_inff();
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int i = 8 * v + e;
+      const float x = a[v][e];
+      if (i < r) {
+        if (i < lsplit) {
+          mn0 = __builtin_fminf(mn0, x);
+          mx0 = __builtin_fmaxf(mx0, x);
+        } else {
+          mn1 = __builtin_fminf(mn1, x);
+          mx1 = __builtin_fmaxf(mx1, x);
+        }
+      }
+    }
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    mn0 = __builtin_fminf(mn0, __shfl_xor(mn0, d, kWave));
+    mx0 = __builtin_fmaxf(mx0, __shfl_xor(mx0, d, kWave));
+    mn1 = __builtin_fminf(mn1, __shfl_xor(mn1, d, kWave));
+    mx1 = __builtin_fmaxf(mx1, __shfl_xor(mx1, d, kWave));
+  }
+  if (thread_id() == 0) {
+    const Rsrc rp = make_rsrc(p.state + p.partial_plane + (uint64_t)gb * 16, 16);
+    __builtin_amdgcn_raw_buffer_store_b128(
+        u32x4{__float_as_uint(mn0), __float_as_uint(mx0), __float_as_uint(mn1), __float_as_uint(mx1)}, rp, 0, 0, 0);
+  }
+}
+
+// One thread per bucket of the step (all tensors): the (min, max) over the
+// partials of the blocks it covers, -0 stored as +0, into table t mod 2.
+__global__ void __launch_bounds__(256) bucket_reduce_kernel(StepParams p) {
+  const int64_t cg = (int64_t)block_id() * 256 + thread_id();
+  if (cg >= p.total_buckets) return;
+  const __attribute__((address_space(4))) TensorDesc* td = constant_ptr(p.tensors);
+  int lo = 0, hi = p.n_tensors - 1;  // the last tensor whose buckets start at or before cg
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (td[mid].first_bucket <= cg) lo = mid;
+    else hi = mid - 1;
+  }
+  const TensorDesc d = load_desc(td + lo);
+  const int64_t bq = p.big_bucket, B = p.block;
+  const int64_t c = cg - d.first_bucket;
+  const int64_t e_lo = c * bq;
+  const int64_t e_hi = e_lo + bq < d.numel ? e_lo + bq : d.numel;
+  const int64_t q_lo = e_lo / B, q_hi = (e_hi - 1) / B;
+  const Rsrc rp = make_rsrc(p.state + p.partial_plane, (uint32_t)(p.total_blocks * 16));
+  float mn = __builtin_inff(), mx = -__builtin_inff();
+  for (int64_t q = q_lo; q <= q_hi; ++q) {
+    const int64_t gb = q == d.num_blocks - 1 ? d.last_block : d.first_block + q;
+    const uint32_t part = (q * B) / bq == c ? 0u : 8u;  // the block's first bucket, or its second
+    const u32x2 pr = __builtin_amdgcn_raw_buffer_load_b64(rp, (uint32_t)(gb * 16) + part, 0, 0);
+    mn = __builtin_fminf(mn, __uint_as_float(pr[0]));
+    mx = __builtin_fmaxf(mx, __uint_as_float(pr[1]));
+  }
+  mn = mn + 0.0f;  // a bucket bound of -0 is stored as +0
+  mx = mx + 0.0f;
+  const uint64_t t = (uint64_t)(p.t & 1);
+  float* out = (float*)(p.state + p.stats_plane + t * p.table_bytes) + 2 * cg;
+  out[0] = mn;
+  out[1] = mx;
+}
+
+// e = Q(a with a[I] = 0) for buckets spanning blocks (Algorithm 1; Algorithm
+// 2, Q; Lemma 1 with kEfRandom): recomputes a = g + Q^-1(e) exactly as the
+// select kernel did (same codes, same pairs), zeroes the elements of the
+// block's new window row, and quantizes with the new pairs.  One wave per
+// block, 64 elements per lane.
+template <bool GBF16, bool VF32, int EFM>
+__global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
+requant_kernel(StepParams p, int64_t first) {
+  constexpr int EPL = 64, NV = EPL / 8, CAP = kWave * EPL;
+  constexpr int CW = (EFM & kEf8) ? 2 : 1;
+  using E = Entry<VF32>;
+  __shared__ uint32_t kept[CAP / 32];  // bit i: element i is in the new row
+
+  const int lane = thread_id();
+  const uint32_t eb = (uint32_t)lane * EPL;
+  const int64_t gb = first + block_id();
+  const uint32_t ef_bytes = (EFM & kEf8) ? (uint32_t)p.block : (uint32_t)(p.block >> 1);
+  const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * ef_bytes, ef_bytes);
+  const bool wide = p.block == CAP;
+  LaneIn<EPL, true, GBF16, EFM> in;
+  lane_load_codes(in, re, eb, wide);
+  const Block b = locate(p, gb);
+  const int s = b.s, kq = b.kq;
+  const bool full = s == CAP;
+  const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + b.e0 * (GBF16 ? 2 : 4), vec_bytes<GBF16>(s));
+  lane_load_grad(in, rg, eb);
+  const LqBuckets old_b = lq_buckets(p, b, eb, EPL, 0), new_b = lq_buckets(p, b, eb, EPL, 1);
+
+  kept[lane] = 0u;
+  kept[lane + kWave] = 0u;
+  wave_sync();
+  const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
+  const uint32_t row0 = (uint32_t)p.new_slot * kq;
+  for (int j = lane; j < kq; j += kWave) {
+    const uint32_t i = E::idx(E::load(rw, row0 + j));
+    atomicOr(&kept[(i >> 5) & (CAP / 32 - 1)], 1u << (i & 31));
+  }
+  wave_sync();
+
+  float a[NV][8];
+  const int rem = s - (int)eb;
+  lane_decode_lq(in, old_b, a, rem, full);
+  const uint32_t k0 = kept[2 * lane], k1 = kept[2 * lane + 1];  // this lane's 64 elements
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int i = 8 * v + e;
+      const uint32_t bit = i < 32 ? (k0 >> i) & 1u : (k1 >> (i - 32)) & 1u;
+      if (bit) a[v][e] = 0.0f;
+    }
+
+  const float lo0 = __uint_as_float(new_b.st[0][0]), u0 = ef_step<EFM>(__uint_as_float(new_b.st[0][1]) - lo0);
+  const float lo1 = __uint_as_float(new_b.st[1][0]), u1 = ef_step<EFM>(__uint_as_float(new_b.st[1][1]) - lo1);
+  const EfStream st{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi};
+  uint32_t wv[NV * CW];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const uint64_t quad = (uint64_t)(b.e0 + eb + 8 * v) >> 2;
+    uint32_t w[CW];
+    const int cut = new_b.sp - 8 * v;  // elements [0, cut) of the vector in the first bucket
+    if (cut >= 8) {
+      vector_codes<EFM>(a[v], lo0, u0, quad, st, w);
+    } else if (cut <= 0) {
+      vector_codes<EFM>(a[v], lo1, u1, quad, st, w);
+    } else {
+      uint32_t w1[CW];
+      vector_codes<EFM>(a[v], lo0, u0, quad, st, w);
+      vector_codes<EFM>(a[v], lo1, u1, quad, st, w1);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (e >= cut) {
+          if constexpr (EFM & kEf8) {
+            const uint32_t m = 0xFFu << (8 * (e & 3));
+            w[e >> 2] = (w[e >> 2] & ~m) | (w1[e >> 2] & m);
+          } else {
+            const uint32_t m = 0xFu << (4 * e);
+            w[0] = (w[0] & ~m) | (w1[0] & m);
+          }
+        }
+    }
+    if (!full) {
+      const int r = opaque_v(rem);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (8 * v + e >= r) {
+          if constexpr (EFM & kEf8) w[e >> 2] &= ~(0xFFu << (8 * (e & 3)));
+          else w[0] &= ~(0xFu << (4 * e));
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < CW; ++c) wv[CW * v + c] = w[c];
+  }
+  if ((int)eb < s) lane_store_codes<EPL, EFM>(wv, eb, wide, re);
 }
 
 // ================================================ select, blocks above 4096
@@ -1856,6 +2148,38 @@ hipError_t launch_export(const StepParams& p, int64_t first_block, int64_t block
   return hipGetLastError();
 }
 
+template <bool GB, bool VF, int EF8>
+hipError_t launch_select_partials_t(const StepParams& p, hipStream_t stream) {
+  const size_t lds = select_lds_words() * 4;
+  hipLaunchKernelGGL((select_kernel<64, true, GB, VF, EF8, true>), dim3((uint32_t)p.total_blocks), dim3(kWave), lds,
+                     stream, p, (int64_t)0);
+  return hipGetLastError();
+}
+
+template <bool GB, bool VF>
+hipError_t launch_select_partials_d(const StepParams& p, hipStream_t stream) {
+  return (p.ef_mode & kEf8) ? launch_select_partials_t<GB, VF, kEf8>(p, stream)
+                            : launch_select_partials_t<GB, VF, 0>(p, stream);
+}
+
+template <bool GB, bool VF, int EFM>
+hipError_t launch_requant_t(const StepParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL((requant_kernel<GB, VF, EFM>), dim3((uint32_t)p.total_blocks), dim3(kWave), 0, stream, p,
+                     (int64_t)0);
+  return hipGetLastError();
+}
+
+template <bool GB, bool VF>
+hipError_t launch_requant_d(const StepParams& p, hipStream_t stream) {
+  switch (p.ef_mode) {
+    case 0: return launch_requant_t<GB, VF, 0>(p, stream);
+    case kEf8: return launch_requant_t<GB, VF, kEf8>(p, stream);
+    case kEfRandom: return launch_requant_t<GB, VF, kEfRandom>(p, stream);
+    case kEf8 | kEfRandom: return launch_requant_t<GB, VF, kEf8 | kEfRandom>(p, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
 
 size_t step_lds_bytes(int block, int k_full, int value_f32) {
@@ -1910,6 +2234,27 @@ hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_
                      : launch_export<64, false>(p, first_block, num_blocks, mhat, vhat, stream);
   return value_f32 ? launch_export<256, true>(p, first_block, num_blocks, mhat, vhat, stream)
                    : launch_export<256, false>(p, first_block, num_blocks, mhat, vhat, stream);
+}
+
+hipError_t launch_select_partials(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream) {
+  if (p.total_blocks <= 0) return hipSuccess;
+  if (grad_bf16)
+    return value_f32 ? launch_select_partials_d<true, true>(p, stream) : launch_select_partials_d<true, false>(p, stream);
+  return value_f32 ? launch_select_partials_d<false, true>(p, stream) : launch_select_partials_d<false, false>(p, stream);
+}
+
+hipError_t launch_bucket_reduce(const StepParams& p, hipStream_t stream) {
+  if (p.total_buckets <= 0) return hipSuccess;
+  const uint32_t grid = (uint32_t)((p.total_buckets + 255) / 256);
+  hipLaunchKernelGGL(bucket_reduce_kernel, dim3(grid), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_requant(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream) {
+  if (p.total_blocks <= 0) return hipSuccess;
+  if (grad_bf16)
+    return value_f32 ? launch_requant_d<true, true>(p, stream) : launch_requant_d<true, false>(p, stream);
+  return value_f32 ? launch_requant_d<false, true>(p, stream) : launch_requant_d<false, false>(p, stream);
 }
 
 }  // namespace microadam

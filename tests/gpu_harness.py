@@ -132,6 +132,12 @@ class GpuOracleRun:
 
     def gpu_stats(self, u: Unit):
         lay = self.opt.layout(u.j)
+        if lay.bucket_table_bytes:
+            # buckets spanning blocks: the tensor's pairs in the table of step t
+            assert u.q0 == 0 and u.q1 == lay.num_blocks, "buckets spanning blocks need whole tensors"
+            off = lay.stats_plane + (self.t % 2) * lay.bucket_table_bytes
+            raw = self._read(off, 8 * lay.num_buckets).view(np.float32).reshape(-1, 2)
+            return raw[:, 0].copy(), raw[:, 1].copy()
         lo, hi = [], []
         for q in range(u.q0, u.q1):
             nb = -(-self._block_elems(lay, q) // self.bucket)

@@ -81,6 +81,17 @@ def test_state_bytes_8bit_codes(lib):
     assert ma.microadam_state_bytes(cfg, [n]) == sum(pad(4 * x) for x in per_block)
 
 
+def test_state_bytes_buckets_spanning_blocks(lib):
+    cfg = ma.make_config(density=0.01, window=3, ef_bucket=100000, topk_block=4096)
+    numels = [4096 * 30 + 1000, 250000]   # 31 and 62 blocks; 2 and 3 buckets
+    pad = lambda x: -(-x // 256) * 256
+    blocks, buckets = 31 + 62, 2 + 3
+    rec = -(-3 * 41 * 4 // 128) * 128    # 3 rows of 41 four-byte entries, whole lines
+    # 4-bit codes, two tables of (delta, Delta) pairs, per-block partials, window
+    want = pad(blocks * 2048) + pad(2 * buckets * 8) + pad(blocks * 16) + pad(blocks * rec)
+    assert ma.microadam_state_bytes(cfg, numels) == want
+
+
 def test_state_bytes_large_blocks(lib):
     """Blocks above 4096 elements (the flat 1.5e9 workload's B_d = 65536,
     k = 3277, m = 20, B_q = 128): each window record holds the m rows and an
@@ -110,6 +121,8 @@ BAD = [
     (dict(ef_bits=8, topk_block=8192), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_rounding=1, topk_block=8192), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_rounding=2), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(ef_bucket=100000, topk_block=8192), ma.MICROADAM_ERR_UNSUPPORTED),
+    (dict(ef_bucket=1000, topk_block=4096), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bucket=48), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bucket=1), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(topk_block=4000, ef_bucket=64), ma.MICROADAM_ERR_INVALID_ARG),

@@ -68,6 +68,14 @@ CASES = {
     "randomized_block2048_bf16": (dict(numels=[9000], block=2048, bucket=32, window=3, param_dtype=bf16,
                                        grad_dtype=bf16, grad_scale=1e-3, ef_rounding=1,
                                        ef_seed=2 ** 40 + 3), 4),
+    # buckets spanning Top-K blocks (B_q >= B_d; Section 3.1 names 100K):
+    # per-block partials, a bucket reduction and a second quantization pass
+    "big_bucket_100k": (dict(numels=[4096 * 30 + 1000, 250000, 5000], bucket=100000, window=3,
+                             param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3), 5),
+    "big_bucket_8bit_randomized": (dict(numels=[50000, 3000], block=1024, bucket=10000, window=3,
+                                        density=0.02, ef_bits=8, ef_rounding=1, ef_seed=5), 5),
+    "big_bucket_equals_block": (dict(numels=[4096 * 5 + 17, 900], bucket=4096, window=2,
+                                     grad_dist="student_t4"), 4),
 }
 
 
