@@ -83,16 +83,23 @@ def _blocks(w, n):
     return nb, k_total
 
 
-def select_bytes(w) -> int:
+def select_bytes(w, ef_bits: int = 4, bucket: int | None = None) -> int:
     """Algorithmic HBM bytes of one select launch: gradient read, EF codes
-    read and written (ceil(n/2) B each way), bucket (delta, Delta) read and
+    read and written (ceil(n*b/8) B each way), bucket (delta, Delta) read and
     written (8 B per bucket each way), one window row written (4 B per kept
-    bf16 entry)."""
+    bf16 entry).  With buckets spanning blocks (bucket >= the block) the
+    second pass reads the gradient, the codes and the new row again, and each
+    block writes and the reduction reads 16 B of partials."""
     sg = w.grad_dtype.itemsize
+    bucket = bucket or w.bucket
+    span = bucket >= w.block and not (bucket <= 512 and w.block % bucket == 0)
     total = 0
     for n in w.numels:
-        _, k_total = _blocks(w, n)
-        total += n * sg + 2 * ((n + 1) // 2) + 2 * 8 * (-(-n // w.bucket)) + 4 * k_total
+        nb, k_total = _blocks(w, n)
+        codes = -(-n * ef_bits // 8)
+        total += n * sg + 2 * codes + 2 * 8 * (-(-n // bucket)) + 4 * k_total
+        if span:
+            total += n * sg + codes + 4 * k_total + 2 * 16 * nb
     return total
 
 
@@ -171,6 +178,11 @@ def main() -> int:
     ap.add_argument("--cpu-blocks", type=int, default=10000, help="0 disables the CPU baseline")
     ap.add_argument("--ranges", type=int, default=1,
                     help="block ranges per step (each range's update overlaps the next selects)")
+    ap.add_argument("--ef-bits", type=int, default=4, choices=(4, 8), help="bits per EF code")
+    ap.add_argument("--ef-rounding", default="nearest", choices=("nearest", "randomized"),
+                    help="EF quantizer rounding (randomized: Lemma 1)")
+    ap.add_argument("--ef-bucket", type=int, default=0,
+                    help="EF bucket size (0: the workload's; >= topk_block: buckets spanning blocks)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device-to-device copy three times (the known-size "
                          "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
@@ -203,8 +215,10 @@ def main() -> int:
     grad_sets = [wl.grads_for_step(w, s, dev) for s in (1, 2)]
     torch.cuda.synchronize()
     print("[bench] inputs resident", file=sys.stderr, flush=True)
-    cfg = ma.make_config(density=w.density, window=w.window, ef_bucket=w.bucket,
-                         topk_block=w.block, lr=w.lr)
+    bucket = args.ef_bucket or w.bucket
+    rounding = ma.MICROADAM_ROUND_RANDOMIZED if args.ef_rounding == "randomized" else ma.MICROADAM_ROUND_NEAREST
+    cfg = ma.make_config(density=w.density, window=w.window, ef_bucket=bucket, topk_block=w.block, lr=w.lr,
+                         ef_bits=args.ef_bits, ef_rounding=rounding, seed=1234)
     opt = ma.MicroAdam(params, cfg)
     opt.set_ranges(args.ranges)
 
@@ -225,7 +239,7 @@ def main() -> int:
     wall = time.perf_counter() - wall0
     sel_ms = sum(k[0] for k in kernel_ms) / len(kernel_ms)
     upd_ms = sum(k[1] for k in kernel_ms) / len(kernel_ms)
-    sel_b = select_bytes(w)
+    sel_b = select_bytes(w, args.ef_bits, bucket)
     upd_b = sum(update_bytes(w, t) for t in range(t_first, t_first + args.steps)) / args.steps
     kernels = {
         "select_kernel": {"ms": sel_ms, "bytes": sel_b, "gbs": sel_b / sel_ms / 1e6},
@@ -233,7 +247,8 @@ def main() -> int:
     }
     dominant = max(kernels, key=lambda k: kernels[k]["ms"])
     dk = kernels[dominant]
-    traffic, traffic_note = read_traffic(dominant, w.name)
+    default_ef = args.ef_bits == 4 and args.ef_rounding == "nearest" and bucket == w.bucket
+    traffic, traffic_note = read_traffic(dominant, w.name) if default_ef else (None, "counters taken with the default EF")
     print(f"[bench] kernel ms per step (select, update): "
           f"{[(round(a, 3), round(b, 3)) for a, b in kernel_ms]}", file=sys.stderr, flush=True)
 
@@ -262,7 +277,8 @@ def main() -> int:
             "grad_dtype": "bf16" if w.grad_dtype.itemsize == 2 else "f32",
             "grad_dist": w.grad_dist, "topk_block": w.block, "density": w.density,
             "k_per_block": block_k(w.block, w.density), "window": w.window,
-            "ef_bits": 4, "ef_bucket": w.bucket, "steps_timed": [t_first, t_first + args.steps - 1],
+            "ef_bits": args.ef_bits, "ef_rounding": args.ef_rounding, "ef_bucket": bucket,
+            "steps_timed": [t_first, t_first + args.steps - 1],
             "window_full": t_first > w.window, "ranges": args.ranges,
         },
         "kernels": kernels,

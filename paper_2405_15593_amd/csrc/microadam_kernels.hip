@@ -123,9 +123,10 @@ __device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1
       k0 += 0x9E3779B9u;
       k1 += 0xBB67AE85u;
     }
-    const uint32_t hi0 = __umulhi(0xD2511F53u, c[0]), lo0 = 0xD2511F53u * c[0];
-    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c[2]), lo1 = 0xCD9E8D57u * c[2];
-    c = u32x4{hi1 ^ c[1] ^ k0, lo1, hi0 ^ c[3] ^ k1, lo0};
+    // one 32x32 -> 64-bit multiply each (v_mad_u64_u32)
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c[0];
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c[2];
+    c = u32x4{(uint32_t)(p1 >> 32) ^ c[1] ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c[3] ^ k1, (uint32_t)p0};
   }
   return c;
 }
@@ -142,6 +143,13 @@ __device__ __forceinline__ uint32_t code_randomized(float x, float lo, float u, 
   float r = fy + ((w24 + fr >= (1u << 24)) ? 1.0f : 0.0f);
   r = __builtin_fminf(__builtin_fmaxf(r, 0.0f), levels);
   return (uint32_t)r;
+}
+
+// Round-to-nearest code (Algorithm 2, Q): rint((x - lo)/u) with an IEEE
+// division, clamped to [0, L].  u != 0.
+__device__ __forceinline__ uint32_t code_nearest(float x, float lo, float u, float levels) {
+  const float r = __builtin_rintf((x - lo) / u);
+  return (uint32_t)__builtin_fminf(__builtin_fmaxf(r, 0.0f), levels);
 }
 
 // Quantization step of a bucket: (max - min) / L, correctly rounded.
@@ -611,6 +619,18 @@ struct EfStream {
   uint32_t k0, k1; // seed, low and high word
 };
 
+// The 24-bit integers w of xi = w * 2^-24 for the 8 elements starting at
+// tensor element 4*quad (two Philox blocks).
+__device__ __forceinline__ void philox_w24(uint64_t quad, const EfStream& st, uint32_t (&w24)[8]) {
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint64_t qh = quad + h;
+    const u32x4 r = philox4x32_10(u32x4{(uint32_t)qh, (uint32_t)(qh >> 32), st.j, st.t}, st.k0, st.k1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w24[4 * h + i] = r[i] >> 8;
+  }
+}
+
 // Codes of one vector of 8 elements x against one bucket (lower bound mnv,
 // quantization step uv): 4-bit codes in w[0], element e in bits [4e, 4e + 4);
 // 8-bit codes in w[0], w[1], element e in byte e & 3 of word e / 4.  quad:
@@ -623,16 +643,9 @@ __device__ __forceinline__ void vector_codes(const float (&x)[8], float mnv, flo
   constexpr int CW = EF8 ? 2 : 1;
   constexpr float L = EF8 ? 255.0f : 15.0f;
   if constexpr ((EFM & kEfRandom) != 0) {
-    // two Philox blocks give the xi of the vector's 8 elements (the
-    // vector starts at a multiple of 8 within the tensor)
+    // the vector starts at a multiple of 8 within the tensor
     uint32_t w24[8];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const uint64_t qh = quad + h;
-      const u32x4 r = philox4x32_10(u32x4{(uint32_t)qh, (uint32_t)(qh >> 32), st.j, st.t}, st.k0, st.k1);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) w24[4 * h + i] = r[i] >> 8;
-    }
+    philox_w24(quad, st, w24);
 #pragma unroll
     for (int c = 0; c < CW; ++c) w[c] = 0;
     if (uv != 0.0f) {
@@ -866,6 +879,49 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
                                                 (e0 >> bl) * 8, 0, 0);
       }
     }
+  }
+}
+
+// Per block and bucket, the (min, max) of the residual (elements past the
+// block's end excluded; an empty part gives (+inf, -inf)): pairs for the
+// block's first bucket and for the next one, written by lane 0.
+template <int EPL>
+__device__ __forceinline__ void lane_partials(const float (&a)[EPL / 8][8], const StepParams& p, const Block& b,
+                                              uint32_t eb, int rem, int64_t gb) {
+  constexpr int NV = EPL / 8;
+  const int64_t bq = p.big_bucket;
+  const int64_t split = ((b.e0 / bq) + 1) * bq - b.e0;  // block element where the next bucket starts
+  const int64_t ls = split - (int64_t)eb;
+  const int lsplit = ls < 0 ? 0 : ls > EPL ? EPL : (int)ls;
+  const int r = opaque_v(rem);
+  float mn0 = __builtin_inff(), mx0 = -__builtin_inff(), mn1 = __builtin_inff(), mx1 = -__builtin_inff();
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int i = 8 * v + e;
+      const float x = a[v][e];
+      if (i < r) {
+        if (i < lsplit) {
+          mn0 = __builtin_fminf(mn0, x);
+          mx0 = __builtin_fmaxf(mx0, x);
+        } else {
+          mn1 = __builtin_fminf(mn1, x);
+          mx1 = __builtin_fmaxf(mx1, x);
+        }
+      }
+    }
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    mn0 = __builtin_fminf(mn0, __shfl_xor(mn0, d, kWave));
+    mx0 = __builtin_fmaxf(mx0, __shfl_xor(mx0, d, kWave));
+    mn1 = __builtin_fminf(mn1, __shfl_xor(mn1, d, kWave));
+    mx1 = __builtin_fmaxf(mx1, __shfl_xor(mx1, d, kWave));
+  }
+  if (thread_id() == 0) {
+    const Rsrc rp = make_rsrc(p.state + p.partial_plane + (uint64_t)gb * 16, 16);
+    __builtin_amdgcn_raw_buffer_store_b128(
+        u32x4{__float_as_uint(mn0), __float_as_uint(mx0), __float_as_uint(mn1), __float_as_uint(mx1)}, rp, 0, 0, 0);
   }
 }
 
@@ -1218,49 +1274,6 @@ select_kernel(StepParams p, int64_t first) {
   }
 }
 
-// Per block and bucket, the (min, max) of the residual (elements past the
-// block's end excluded; an empty part gives (+inf, -inf)): pairs for the
-// block's first bucket and for the next one, written by lane 0.
-template <int EPL>
-__device__ __forceinline__ void lane_partials(const float (&a)[EPL / 8][8], const StepParams& p, const Block& b,
-                                              uint32_t eb, int rem, int64_t gb) {
-  constexpr int NV = EPL / 8;
-  const int64_t bq = p.big_bucket;
-  const int64_t split = ((b.e0 / bq) + 1) * bq - b.e0;  // block element where the next bucket starts
-  const int64_t ls = split - (int64_t)eb;
-  const int lsplit = ls < 0 ? 0 : ls > EPL ? EPL : (int)ls;
-  const int r = opaque_v(rem);
-  float mn0 = __builtin_inff(), mx0 = -__builtin_inff(), mn1 = __builtin_inff(), mx1 = -__builtin_inff();
-#pragma unroll
-  for (int v = 0; v < NV; ++v)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int i = 8 * v + e;
-      const float x = a[v][e];
-      if (i < r) {
-        if (i < lsplit) {
-          mn0 = __builtin_fminf(mn0, x);
-          mx0 = __builtin_fmaxf(mx0, x);
-        } else {
-          mn1 = __builtin_fminf(mn1, x);
-          mx1 = __builtin_fmaxf(mx1, x);
-        }
-      }
-    }
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    mn0 = __builtin_fminf(mn0, __shfl_xor(mn0, d, kWave));
-    mx0 = __builtin_fmaxf(mx0, __shfl_xor(mx0, d, kWave));
-    mn1 = __builtin_fminf(mn1, __shfl_xor(mn1, d, kWave));
-    mx1 = __builtin_fmaxf(mx1, __shfl_xor(mx1, d, kWave));
-  }
-  if (thread_id() == 0) {
-    const Rsrc rp = make_rsrc(p.state + p.partial_plane + (uint64_t)gb * 16, 16);
-    __builtin_amdgcn_raw_buffer_store_b128(
-        u32x4{__float_as_uint(mn0), __float_as_uint(mx0), __float_as_uint(mn1), __float_as_uint(mx1)}, rp, 0, 0, 0);
-  }
-}
-
 // One thread per bucket of the step (all tensors): the (min, max) over the
 // partials of the blocks it covers, -0 stored as +0, into table t mod 2.
 __global__ void __launch_bounds__(256) bucket_reduce_kernel(StepParams p) {
@@ -1351,40 +1364,26 @@ requant_kernel(StepParams p, int64_t first) {
   const float lo0 = __uint_as_float(new_b.st[0][0]), u0 = ef_step<EFM>(__uint_as_float(new_b.st[0][1]) - lo0);
   const float lo1 = __uint_as_float(new_b.st[1][0]), u1 = ef_step<EFM>(__uint_as_float(new_b.st[1][1]) - lo1);
   const EfStream st{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi};
+  constexpr float L = (EFM & kEf8) ? 255.0f : 15.0f;
   uint32_t wv[NV * CW];
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
-    const uint64_t quad = (uint64_t)(b.e0 + eb + 8 * v) >> 2;
+    // each element against its own bucket's pair, with an IEEE division
+    uint32_t w24[8] = {};
+    if constexpr ((EFM & kEfRandom) != 0) philox_w24((uint64_t)(b.e0 + eb + 8 * v) >> 2, st, w24);
     uint32_t w[CW];
-    const int cut = new_b.sp - 8 * v;  // elements [0, cut) of the vector in the first bucket
-    if (cut >= 8) {
-      vector_codes<EFM>(a[v], lo0, u0, quad, st, w);
-    } else if (cut <= 0) {
-      vector_codes<EFM>(a[v], lo1, u1, quad, st, w);
-    } else {
-      uint32_t w1[CW];
-      vector_codes<EFM>(a[v], lo0, u0, quad, st, w);
-      vector_codes<EFM>(a[v], lo1, u1, quad, st, w1);
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (e >= cut) {
-          if constexpr (EFM & kEf8) {
-            const uint32_t m = 0xFFu << (8 * (e & 3));
-            w[e >> 2] = (w[e >> 2] & ~m) | (w1[e >> 2] & m);
-          } else {
-            const uint32_t m = 0xFu << (4 * e);
-            w[0] = (w[0] & ~m) | (w1[0] & m);
-          }
-        }
-    }
-    if (!full) {
-      const int r = opaque_v(rem);
+    for (int c = 0; c < CW; ++c) w[c] = 0;
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (8 * v + e >= r) {
-          if constexpr (EFM & kEf8) w[e >> 2] &= ~(0xFFu << (8 * (e & 3)));
-          else w[0] &= ~(0xFu << (4 * e));
-        }
+    for (int e = 0; e < 8; ++e) {
+      const bool second = 8 * v + e >= new_b.sp;
+      const float lo = second ? lo1 : lo0, u = second ? u1 : u0;
+      uint32_t code = 0;
+      if (u != 0.0f)
+        code = (EFM & kEfRandom) ? code_randomized(a[v][e], lo, u, L, w24[e]) : code_nearest(a[v][e], lo, u, L);
+      if (8 * v + e >= rem) code = 0;  // past the block's end
+      if constexpr (EFM & kEf8) w[e >> 2] |= code << (8 * (e & 3));
+      else w[0] |= code << (4 * e);
     }
 #pragma unroll
     for (int c = 0; c < CW; ++c) wv[CW * v + c] = w[c];
