@@ -116,7 +116,7 @@ struct Planes {
 int entry_bytes(const microadam_config* c) { return c->window_value_dtype == MICROADAM_F32 ? 8 : 4; }
 
 // Full blocks are numbered first, tensor by tensor; the ragged last blocks
-// follow, so that the kernels see one run of equal blocks.
+// follow, so that the full blocks form one range of equal blocks.
 int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
               std::vector<TensorPlan>& out, Planes& pl) {
   if (n < 1) return fail(MICROADAM_ERR_INVALID_ARG, "n_tensors must be >= 1");

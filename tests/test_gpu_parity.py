@@ -150,20 +150,20 @@ def test_c5_shape_block65536_forced_ties():
     run.opt.close()
 
 
-def _workload_sampled(name, steps, every, check_at, lr=1e-4):
+def _workload_sampled(name, steps, every, check_at, lr=1e-4, **ef):
     """A parameter list of the benchmark workloads at full size, in the
     launch configuration bench.py times; the oracle checks every tensor's
     first and last block and every `every`-th block in between."""
     from paper_2405_15593_amd.workloads import WORKLOADS
     w = WORKLOADS[name]
-    print(f"[parity] {name} sampled, {len(w.numels)} tensors, d={w.d}, {steps} steps", flush=True)
+    print(f"[parity] {name} sampled, {len(w.numels)} tensors, d={w.d}, {steps} steps {ef}", flush=True)
 
     def sample(j, nb):
         return sorted({0, nb - 1, *range(0, nb, every)})
 
     run = GpuOracleRun(w.numels, param_dtype=w.param_dtype, grad_dtype=w.grad_dtype,
                        grad_dist=w.grad_dist, grad_scale=w.grad_scale, lr=lr, density=w.density,
-                       window=w.window, bucket=w.bucket, block=w.block, sample=sample)
+                       window=w.window, bucket=w.bucket, block=w.block, sample=sample, **ef)
     for t in range(steps):
         run.step(check_moments=t in check_at)
         print(f"[parity] {name} step {t + 1} checked", flush=True)
@@ -175,6 +175,13 @@ def test_llama2_7b_bf16_sampled_window_full():
     bf16 parameters, Student-t(4) gradients), 12 steps so that the window of
     10 is full and wraps, as in the timed steps."""
     _workload_sampled("llama2_7b_bf16", 12, 499, (0, 11))
+
+
+def test_llama2_7b_bf16_randomized_8bit_sampled():
+    """The Llama-2-7B list with 8-bit codes and randomized rounding (291
+    tensor numbers and element numbers up to 1.3e8 in the random stream),
+    4 steps, every 997th block."""
+    _workload_sampled("llama2_7b_bf16", 4, 997, (3,), ef_bits=8, ef_rounding=1, ef_seed=20240523)
 
 
 def test_llama2_13b_bf16_sampled():
