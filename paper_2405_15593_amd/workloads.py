@@ -46,7 +46,7 @@ class Workload:
     shapes: list[tuple[int, ...]]
     param_dtype: torch.dtype
     grad_dtype: torch.dtype
-    grad_dist: str              # "normal", "student_t4", "student_t2_snapped64"
+    grad_dist: str              # a distribution name of draw()
     grad_scale: float
     block: int = 4096
     density: float = 0.01
@@ -114,6 +114,14 @@ def draw(n: int, dist: str, scale: float, seed: int, device, dtype) -> torch.Ten
             j = j.clamp(0, 63)
             x = torch.sign(x) * torch.exp2((j - 40) / 4)
             x = torch.where(x == 0, torch.exp2(torch.tensor(-10.0, device=device)), x)
+    elif dist == "zeros":
+        x = torch.zeros_like(z)
+    elif dist == "constant":
+        x = torch.ones_like(z)
+    elif dist == "signs":          # +1 or -1: every |x| ties
+        x = torch.where(z < 0, -1.0, 1.0)
+    elif dist == "sparse_spikes":  # about 1 in 200 elements nonzero, the rest exact zeros
+        x = torch.where(z.abs() > 2.807, z, torch.zeros_like(z))
     else:
         raise ValueError(dist)
     return (x * scale).to(dtype)

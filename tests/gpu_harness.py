@@ -49,7 +49,7 @@ class GpuOracleRun:
                  grad_dist="normal", grad_scale=1.0, lr=1e-3, seed=0, sample=None,
                  density=0.01, window=10, bucket=64, block=4096, value_f32=False,
                  beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, ranges=1, ef_bits=4,
-                 ef_rounding=0, ef_seed=0, device="cuda"):
+                 ef_rounding=0, ef_seed=0, degenerate=False, device="cuda"):
         self.numels = list(numels)
         self.lr = lr
         self.device = torch.device(device)
@@ -61,6 +61,7 @@ class GpuOracleRun:
                                   topk_block=block, ef_bits=ef_bits, ef_rounding=ef_rounding, seed=ef_seed,
                                   window_value_dtype=ma.MICROADAM_F32 if value_f32 else ma.MICROADAM_BF16)
         self.ef_bits = ef_bits
+        self.degenerate = degenerate  # inputs whose codes, rows or updates may all be zero
         self.params = [wl.draw(n, "normal", 0.02, seed + 7919 * (j + 1), self.device, param_dtype)
                        for j, n in enumerate(self.numels)]
         self.opt = ma.MicroAdam(self.params, self.cfg)
@@ -186,9 +187,10 @@ class GpuOracleRun:
                     assert np.array_equal(gv.view(np.uint32), ov.view(np.uint32)), (
                         f"window values differ: tensor {u.j} block {u.q0 + qq} row of step {s} at t={t}")
         # the comparison must have looked at real data
-        assert nonzero_vals > 0, "no window value compared"
-        if self.cfg.density < 1.0:
-            assert nonzero_codes > 0, "no EF code compared"
+        if not self.degenerate:
+            assert nonzero_vals > 0, "no window value compared"
+            if self.cfg.density < 1.0:
+                assert nonzero_codes > 0, "no EF code compared"
 
     def check_params(self):
         tol = 2e-2 if self.params[0].dtype == torch.bfloat16 else 1e-5
@@ -201,7 +203,7 @@ class GpuOracleRun:
             bad = np.nonzero(np.abs(got - ref) > lim)[0]
             assert bad.size == 0, (f"params differ: tensor {u.j} block {u.q0} element {bad[0]}: "
                                    f"gpu {got[bad[0]]!r} oracle {ref[bad[0]]!r}")
-        assert changed > 0, "the step changed no parameter"
+        assert changed > 0 or self.degenerate, "the step changed no parameter"
 
     def check_moments(self, t):
         b1, b2 = self.betas

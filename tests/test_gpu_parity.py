@@ -68,6 +68,20 @@ CASES = {
     "randomized_block2048_bf16": (dict(numels=[9000], block=2048, bucket=32, window=3, param_dtype=bf16,
                                        grad_dtype=bf16, grad_scale=1e-3, ef_rounding=1,
                                        ef_seed=2 ** 40 + 3), 4),
+    # degenerate inputs: all-zero gradients (every |a| ties at 0, the rows
+    # hold zeros, every bucket has max = min), a constant gradient (ties
+    # everywhere, the residual is constant so u = 0 after the first step),
+    # gradients of +-1 (ties of mixed sign), and isolated spikes among exact
+    # zeros (zeros tie below the threshold)
+    "zero_grad": (dict(numels=[4096 + 100, 33], grad_dist="zeros", window=3, degenerate=True), 4),
+    "constant_grad": (dict(numels=[4096 * 2 + 300], grad_dist="constant", grad_scale=0.25, window=3,
+                           param_dtype=bf16, grad_dtype=bf16, degenerate=True), 5),
+    "sign_grad": (dict(numels=[4096 + 1000, 200], grad_dist="signs", grad_scale=1e-2, window=3,
+                       degenerate=True), 5),
+    "sparse_spikes": (dict(numels=[4096 * 3, 777], grad_dist="sparse_spikes", density=0.02, window=4,
+                           degenerate=True), 6),
+    "zero_grad_randomized_8bit": (dict(numels=[2048 + 48], block=1024, bucket=16, grad_dist="zeros",
+                                       window=2, ef_bits=8, ef_rounding=1, ef_seed=3, degenerate=True), 3),
     # buckets spanning Top-K blocks (B_q >= B_d; Section 3.1 names 100K):
     # per-block partials, a bucket reduction and a second quantization pass
     "big_bucket_100k": (dict(numels=[4096 * 30 + 1000, 250000, 5000], bucket=100000, window=3,
