@@ -1584,31 +1584,36 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
 // One workgroup of 256 threads per 4096-element sub-block j of a block
 // (thread tid: the sub-block's elements 16*tid + [0, 16)).  The live rows'
 // entries of sub-block j are the segments the select kernel recorded; they are
-// staged in LDS in batches of kStageLarge, oldest row first, and one wave
-// rebuilds z1 = sum beta1^r V and z2 = sum beta2^r V^2 from them in that
-// order (Algorithm 2, AdamStats).  Every thread then turns its own 16
+// staged in LDS, oldest row first, in batches of stage_large entries, and
+// one wave rebuilds z1 = sum beta1^r V and z2 = sum beta2^r V^2 from them in
+// that order (Algorithm 2, AdamStats).  Every thread then turns its own 16
 // elements' sums into the update (an element without entries has sums 0 and
 // a decrement of 0) and applies it (Algorithm 1; Algorithm 4).
-constexpr int kStageLarge = 2048;
+// 4608 staged entries (2304 with binary32 values) hold the live entries of a
+// sub-block at the 1.5e9 workload's density 5% and m = 20 (about 4100) in one
+// batch, and keep three workgroups per compute unit.
+template <bool VF>
+constexpr int stage_large() { return VF ? 2304 : 4608; }
 
 template <bool VF>
 constexpr size_t update_large_lds_bytes() {
-  return (size_t)2 * (kSubBlock + kWave) * 4 + (size_t)3 * kWave * 4 + (size_t)kStageLarge * (VF ? 8 : 4);
+  return (size_t)2 * (kSubBlock + kWave) * 4 + (size_t)3 * kWave * 4 + 16 + (size_t)stage_large<VF>() * (VF ? 8 : 4);
 }
 
 template <bool PBF16, bool VF32, bool EXPORT>
 __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t first_block, int32_t nsub,
                                                            float* mhat, float* vhat) {
-  constexpr int NT = 256;
+  constexpr int NT = 256, STAGE = stage_large<VF32>();
   using E = Entry<VF32>;
   using ET = typename E::T;
   extern __shared__ __align__(16) uint32_t smem[];
-  float* const z1 = (float*)smem;                // [kSubBlock] + sink words
+  float* const z1 = (float*)smem;                         // [kSubBlock] + sink words
   float* const z2 = z1 + kSubBlock + kWave;
   uint32_t* const seg_lo = (uint32_t*)(z2 + kSubBlock + kWave);  // [kWave] by row age
   uint32_t* const seg_n = seg_lo + kWave;
-  uint32_t* const seg_at = seg_n + kWave;       // position of the row's first entry in the staged order
-  ET* const stage = (ET*)(seg_at + kWave);       // [kStageLarge]
+  uint32_t* const seg_at = seg_n + kWave;  // position of the row's first entry in the staged order
+  uint32_t* const misc = seg_at + kWave;   // [4]: the entry total
+  ET* const stage = (ET*)(misc + 4);       // [STAGE]
 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
   const int64_t wg = block_id();
@@ -1621,81 +1626,153 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
   const int kq = g.kq, m = p.window, n_live = p.n_live;
   const int slot0 = (p.new_slot + 1 + m - n_live) % m;  // oldest live row first
   const int nsub_blk = (p.block + kSubBlock - 1) / kSubBlock;  // table entries per row
+  const uint32_t eb = (uint32_t)tid * 16;
 
-  // the live rows' segments of sub-block j (row age r = 0 is the oldest)
+  // the parameters go out first; their latency hides behind the rebuild
+  const int es = PBF16 ? 2 : 4;
+  const Rsrc rp = make_rsrc((const void*)(g.base + (uint64_t)lo * es), vec_bytes<PBF16>(s));
+  Raw8<PBF16> th[2];
+  if (!EXPORT) {
+#pragma unroll
+    for (int v = 0; v < 2; ++v) th[v] = load8<PBF16>(rp, eb + 8 * v);
+  }
+
+  // the live rows' segments of sub-block j (row age r = 0 is the oldest),
+  // their starts in the staged order by a scan over wave 0's lanes
   constexpr uint32_t EB = VF32 ? 8u : 4u;
   const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
   const uint32_t table = (uint32_t)m * p.k_full * EB;
-  if (tid < n_live) {
-    const int slot = (slot0 + tid) % m;
-    const uint32_t a0 = __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)slot * nsub_blk + j) * 4, 0, 0);
-    const uint32_t a1 = j + 1 < nsub_blk
-                            ? __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)slot * nsub_blk + j + 1) * 4, 0, 0)
-                            : (uint32_t)kq;
-    seg_lo[tid] = (uint32_t)slot * kq + a0;  // entry number in the record
-    seg_n[tid] = a1 - a0;
+  uint32_t my_at = 0, my_n = 0;  // wave 0, lane r: row r's first staged position and entry count
+  if (wave == 0) {
+    uint32_t n = 0, start = 0;
+    if (lane < n_live) {
+      const int slot = (slot0 + lane) % m;
+      const uint32_t a0 = __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)slot * nsub_blk + j) * 4, 0, 0);
+      const uint32_t a1 = j + 1 < nsub_blk
+                              ? __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)slot * nsub_blk + j + 1) * 4, 0, 0)
+                              : (uint32_t)kq;
+      start = (uint32_t)slot * kq + a0;  // entry number in the record
+      n = a1 - a0;
+    }
+    uint32_t inc = n;  // inclusive prefix over lanes
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      const uint32_t o = __shfl_up(inc, d, kWave);
+      if (lane >= d) inc += o;
+    }
+    seg_lo[lane] = start;
+    seg_n[lane] = n;
+    seg_at[lane] = inc - n;
+    my_at = inc - n;
+    my_n = n;
+    if (lane == kWave - 1) misc[0] = inc;
   }
   {
     const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      *(float4*)(z1 + tid * 16 + 4 * q) = zero;
-      *(float4*)(z2 + tid * 16 + 4 * q) = zero;
+      *(float4*)(z1 + eb + 4 * q) = zero;
+      *(float4*)(z2 + eb + 4 * q) = zero;
     }
   }
   lds_sync();
-  uint32_t total = 0;
-  for (int r = 0; r < n_live; ++r) total += seg_n[r];
-  if (tid == 0) {
-    uint32_t at = 0;
-    for (int r = 0; r < n_live; ++r) {
-      seg_at[r] = at;
-      at += seg_n[r];
-    }
-  }
-  lds_sync();
+  const uint32_t total = misc[0];
 
   const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
   const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
   const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
-  for (uint32_t b0 = 0; b0 < total; b0 += kStageLarge) {
-    const uint32_t b1 = total - b0 < (uint32_t)kStageLarge ? total : b0 + kStageLarge;
-    // stage the entries [b0, b1) of the concatenated segments
-    for (int r = 0; r < n_live; ++r) {
-      const uint32_t at = seg_at[r], n = seg_n[r];
-      const uint32_t x0 = at > b0 ? at : b0, x1 = at + n < b1 ? at + n : b1;
-      for (uint32_t x = x0 + tid; x < x1; x += NT) stage[x - b0] = E::load(rw, seg_lo[r] + (x - at));
+  for (uint32_t b0 = 0; b0 < total; b0 += STAGE) {
+    const uint32_t b1 = total - b0 < (uint32_t)STAGE ? total : b0 + STAGE;
+    // stage the entries [b0, b1) of the concatenated segments: every thread
+    // issues the loads of its positions b0 + tid + NT*i together (the row of
+    // a position by binary search over the rows' first positions), then
+    // writes them to LDS
+    {
+      constexpr int PER = STAGE / NT;
+      ET ld[PER];
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const uint32_t x = b0 + tid + NT * i;
+        int r = 0;
+        for (int half = 32; half > 0; half >>= 1)
+          if (r + half < n_live && seg_at[r + half] <= x) r += half;
+        const uint32_t entry = x < b1 ? seg_lo[r] + (x - seg_at[r]) : 0u;
+        ld[i] = E::load(rw, entry);
+      }
+#pragma unroll
+      for (int i = 0; i < PER; ++i)
+        if (b0 + tid + NT * i < b1) stage[tid + NT * i] = ld[i];
     }
     lds_sync();
     if (wave == 0) {
-      // row by row, oldest first, 64 entries at a time: the entries of one
-      // row have distinct indices, so each chunk reads, adds and writes its
-      // words (lanes without an entry work on the sink words)
+      // row by row, oldest first.  The entries of one row have distinct
+      // indices, so up to 4 chunks of 64 of a row read their words
+      // together, then add and write them (lanes without an entry work on
+      // the sink words); the next row's reads follow this row's writes.
+      // The rows' positions come from wave 0's registers, and the staged
+      // entries of the next row's first chunks are read before this row's
+      // words are written.
+      ET nxt[4];
+      auto read_group = [&](uint32_t x, uint32_t x1, ET (&e)[4]) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const uint32_t xc = x + c * kWave + lane;
+          e[c] = stage[xc < x1 ? xc - b0 : 0];
+        }
+      };
+      auto row_span = [&](int r, uint32_t& x0, uint32_t& x1) {
+        const uint32_t at = (uint32_t)__builtin_amdgcn_readlane((int)my_at, r);
+        const uint32_t n = (uint32_t)__builtin_amdgcn_readlane((int)my_n, r);
+        x0 = at > b0 ? at : b0;
+        x1 = at + n < b1 ? at + n : b1;
+      };
+      // one group of up to 4 chunks of a row: positions [x, x + 256) below x1
+      auto process = [&](uint32_t x, uint32_t x1, const ET (&e)[4], float w1, float w2) {
+        uint32_t zp[4];
+        float v[4], a1[4], a2[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const bool have = x + c * kWave + lane < x1;
+          const uint32_t i = E::idx(e[c]) - (uint32_t)lo;
+          zp[c] = have && i < (uint32_t)s ? i : (uint32_t)(kSubBlock + lane);
+          v[c] = E::val(e[c]);
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          a1[c] = z1[zp[c]];
+          a2[c] = z2[zp[c]];
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          z1[zp[c]] = a1[c] + w1 * v[c];
+          z2[zp[c]] = a2[c] + w2 * (v[c] * v[c]);
+        }
+      };
+      uint32_t nx0 = 0, nx1 = 0;
+      row_span(0, nx0, nx1);
+      read_group(nx0, nx1, nxt);
       for (int r = 0; r < n_live; ++r) {
-        const uint32_t at = seg_at[r], n = seg_n[r];
-        const uint32_t x0 = at > b0 ? at : b0, x1 = at + n < b1 ? at + n : b1;
+        const uint32_t x0 = nx0, x1 = nx1;
+        ET cur[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cur[c] = nxt[c];
+        if (r + 1 < n_live) {
+          row_span(r + 1, nx0, nx1);
+          read_group(nx0, nx1, nxt);
+        }
         const int age = n_live - 1 - r;
         const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), age));
         const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), age));
-        for (uint32_t x = x0; x < x1; x += kWave) {
-          const bool have = x + lane < x1;
-          const ET e = stage[have ? x + lane - b0 : 0];
-          const uint32_t i = E::idx(e) - (uint32_t)lo;
-          const uint32_t zp = have && i < (uint32_t)s ? i : (uint32_t)(kSubBlock + lane);
-          const float v = E::val(e);
-          const float x1v = w1 * v, x2v = w2 * (v * v);
-          const float a1 = z1[zp], a2 = z2[zp];
-          z1[zp] = a1 + x1v;
-          z2[zp] = a2 + x2v;
+        process(x0, x1, cur, w1, w2);
+        for (uint32_t x = x0 + 4 * kWave; x < x1; x += 4 * kWave) {  // rows of more than 256 entries
+          ET e[4];
+          read_group(x, x1, e);
+          process(x, x1, e, w1, w2);
         }
       }
     }
     lds_sync();
   }
-
-  // every thread: its 16 elements
-  const uint32_t eb = (uint32_t)tid * 16;
-  if ((int)eb >= s) return;
   float s1[16], s2[16];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -1704,6 +1781,9 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
     s1[4 * q] = u1.x; s1[4 * q + 1] = u1.y; s1[4 * q + 2] = u1.z; s1[4 * q + 3] = u1.w;
     s2[4 * q] = u2.x; s2[4 * q + 1] = u2.y; s2[4 * q + 2] = u2.z; s2[4 * q + 3] = u2.w;
   }
+
+  // every thread: its 16 elements
+  if ((int)eb >= s) return;
   if (EXPORT) {
 #pragma unroll
     for (int e = 0; e < 16; ++e)
@@ -1713,14 +1793,11 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
       }
     return;
   }
-  const int es = PBF16 ? 2 : 4;
-  const Rsrc rp = make_rsrc((const void*)(g.base + (uint64_t)lo * es), vec_bytes<PBF16>(s));
   const bool full = s == kSubBlock;
 #pragma unroll
   for (int v = 0; v < 2; ++v) {
-    const Raw8<PBF16> th = load8<PBF16>(rp, eb + 8 * v);
     float thf[8], out[8];
-    unpack8<PBF16>(th, thf);
+    unpack8<PBF16>(th[v], thf);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float mh = p.c1 * s1[8 * v + e];
