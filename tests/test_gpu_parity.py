@@ -80,6 +80,16 @@ CASES = {
                        degenerate=True), 5),
     "sparse_spikes": (dict(numels=[4096 * 3, 777], grad_dist="sparse_spikes", density=0.02, window=4,
                            degenerate=True), 6),
+    # the same at blocks above 4096: a constant gradient over a 65536-block
+    # (the search never narrows to few keys) with a 4000-element tail (it
+    # starts narrowed), spikes among zeros (the threshold is 0) and signs
+    "block65536_constant_grad": (dict(numels=[65536 + 4000], block=65536, bucket=128, density=0.05,
+                                      grad_dist="constant", grad_scale=0.25, window=3, param_dtype=bf16,
+                                      grad_dtype=bf16, degenerate=True), 4),
+    "block16384_sparse_spikes": (dict(numels=[16384 * 2 + 500], block=16384, density=0.02, window=3,
+                                      grad_dist="sparse_spikes", degenerate=True), 4),
+    "block8192_sign_grad": (dict(numels=[8192 + 3000], block=8192, grad_dist="signs", grad_scale=1e-2,
+                                 window=3, degenerate=True), 4),
     "zero_grad_randomized_8bit": (dict(numels=[2048 + 48], block=1024, bucket=16, grad_dist="zeros",
                                        window=2, ef_bits=8, ef_rounding=1, ef_seed=3, degenerate=True), 3),
     # buckets spanning Top-K blocks (B_q >= B_d; Section 3.1 names 100K):
