@@ -1931,7 +1931,6 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
   constexpr uint32_t EB = VF32 ? 8u : 4u;
   const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
   const uint32_t table = (uint32_t)m * p.k_full * EB;
-  uint32_t my_at = 0, my_n = 0;  // wave 0, lane r: row r's first staged position and entry count
   if (wave == 0) {
     uint32_t n = 0, start = 0;
     if (lane < n_live) {
@@ -1952,8 +1951,6 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
     seg_lo[lane] = start;
     seg_n[lane] = n;
     seg_at[lane] = inc - n;
-    my_at = inc - n;
-    my_n = n;
     if (lane == kWave - 1) misc[0] = inc;
   }
   {
@@ -1993,74 +1990,27 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
         if (b0 + tid + NT * i < b1) stage[tid + NT * i] = ld[i];
     }
     lds_sync();
-    if (wave == 0) {
-      // row by row, oldest first.  The entries of one row have distinct
-      // indices, so up to 4 chunks of 64 of a row read their words
-      // together, then add and write them (lanes without an entry work on
-      // the sink words); the next row's reads follow this row's writes.
-      // The rows' positions come from wave 0's registers, and the staged
-      // entries of the next row's first chunks are read before this row's
-      // words are written.
-      ET nxt[4];
-      auto read_group = [&](uint32_t x, uint32_t x1, ET (&e)[4]) {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const uint32_t xc = x + c * kWave + lane;
-          e[c] = stage[xc < x1 ? xc - b0 : 0];
-        }
-      };
-      auto row_span = [&](int r, uint32_t& x0, uint32_t& x1) {
-        const uint32_t at = (uint32_t)__builtin_amdgcn_readlane((int)my_at, r);
-        const uint32_t n = (uint32_t)__builtin_amdgcn_readlane((int)my_n, r);
-        x0 = at > b0 ? at : b0;
-        x1 = at + n < b1 ? at + n : b1;
-      };
-      // one group of up to 4 chunks of a row: positions [x, x + 256) below x1
-      auto process = [&](uint32_t x, uint32_t x1, const ET (&e)[4], float w1, float w2) {
-        uint32_t zp[4];
-        float v[4], a1[4], a2[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const bool have = x + c * kWave + lane < x1;
-          const uint32_t i = E::idx(e[c]) - (uint32_t)lo;
-          zp[c] = have && i < (uint32_t)s ? i : (uint32_t)(kSubBlock + lane);
-          v[c] = E::val(e[c]);
-        }
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          a1[c] = z1[zp[c]];
-          a2[c] = z2[zp[c]];
-        }
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          z1[zp[c]] = a1[c] + w1 * v[c];
-          z2[zp[c]] = a2[c] + w2 * (v[c] * v[c]);
-        }
-      };
-      uint32_t nx0 = 0, nx1 = 0;
-      row_span(0, nx0, nx1);
-      read_group(nx0, nx1, nxt);
-      for (int r = 0; r < n_live; ++r) {
-        const uint32_t x0 = nx0, x1 = nx1;
-        ET cur[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) cur[c] = nxt[c];
-        if (r + 1 < n_live) {
-          row_span(r + 1, nx0, nx1);
-          read_group(nx0, nx1, nxt);
-        }
-        const int age = n_live - 1 - r;
-        const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), age));
-        const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), age));
-        process(x0, x1, cur, w1, w2);
-        for (uint32_t x = x0 + 4 * kWave; x < x1; x += 4 * kWave) {  // rows of more than 256 entries
-          ET e[4];
-          read_group(x, x1, e);
-          process(x, x1, e, w1, w2);
-        }
+    // row by row, oldest first, the whole workgroup on one row: a row's
+    // entries have distinct indices, so its read-add-writes never meet; a
+    // barrier orders them before the next row's (the summation order per
+    // element is the rows' order, as with one wave)
+    for (int r = 0; r < n_live; ++r) {
+      const uint32_t at = seg_at[r], n = seg_n[r];
+      const uint32_t x0 = at > b0 ? at : b0, x1 = at + n < b1 ? at + n : b1;
+      const int age = n_live - 1 - r;
+      const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), age));
+      const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), age));
+      for (uint32_t x = x0 + (uint32_t)tid; x < x1; x += NT) {
+        const ET e = stage[x - b0];
+        const uint32_t i = E::idx(e) - (uint32_t)lo;
+        const uint32_t zp = i < (uint32_t)s ? i : (uint32_t)(kSubBlock + lane);
+        const float v = E::val(e);
+        const float a1 = z1[zp], a2 = z2[zp];
+        z1[zp] = a1 + w1 * v;
+        z2[zp] = a2 + w2 * (v * v);
       }
+      lds_sync();
     }
-    lds_sync();
   }
   float s1[16], s2[16];
 #pragma unroll
