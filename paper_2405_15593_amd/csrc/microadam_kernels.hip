@@ -1883,6 +1883,9 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
 // batch, and keep three workgroups per compute unit.
 template <bool VF>
 constexpr int stage_large() { return VF ? 2304 : 4608; }
+// Live rows up to which the update reads a sub-block's entries straight into
+// registers (when no row holds more than 256 of them).
+constexpr int kFastRows = 24;
 
 template <bool VF>
 constexpr size_t update_large_lds_bytes() {
@@ -1901,7 +1904,7 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
   uint32_t* const seg_lo = (uint32_t*)(z2 + kSubBlock + kWave);  // [kWave] by row age
   uint32_t* const seg_n = seg_lo + kWave;
   uint32_t* const seg_at = seg_n + kWave;  // position of the row's first entry in the staged order
-  uint32_t* const misc = seg_at + kWave;   // [4]: the entry total
+  uint32_t* const misc = seg_at + kWave;   // [4]: the entry total, the longest segment
   ET* const stage = (ET*)(misc + 4);       // [STAGE]
 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
@@ -1942,16 +1945,21 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
       start = (uint32_t)slot * kq + a0;  // entry number in the record
       n = a1 - a0;
     }
-    uint32_t inc = n;  // inclusive prefix over lanes
+    uint32_t inc = n, big = n;  // inclusive prefix over lanes; the longest segment
 #pragma unroll
     for (int d = 1; d < kWave; d <<= 1) {
       const uint32_t o = __shfl_up(inc, d, kWave);
       if (lane >= d) inc += o;
+      const uint32_t b2 = __shfl_xor(big, d, kWave);
+      big = b2 > big ? b2 : big;
     }
     seg_lo[lane] = start;
     seg_n[lane] = n;
     seg_at[lane] = inc - n;
-    if (lane == kWave - 1) misc[0] = inc;
+    if (lane == kWave - 1) {
+      misc[0] = inc;
+      misc[1] = big;
+    }
   }
   {
     const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -1967,6 +1975,36 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
   const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
   const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
   const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
+  // one workgroup-wide read-add-write of a row's entry per thread (the
+  // entries of a row have distinct indices)
+  auto add_entry = [&](ET e, float w1, float w2) {
+    const uint32_t i = E::idx(e) - (uint32_t)lo;
+    const uint32_t zp = i < (uint32_t)s ? i : (uint32_t)(kSubBlock + lane);
+    const float v = E::val(e);
+    const float a1 = z1[zp], a2 = z2[zp];
+    z1[zp] = a1 + w1 * v;
+    z2[zp] = a2 + w2 * (v * v);
+  };
+  if (n_live <= kFastRows && misc[1] <= (uint32_t)NT) {
+    // every live row holds at most NT entries of the sub-block: thread t
+    // loads entry t of every row at once, then the rows are added oldest
+    // first from registers, a barrier between rows
+    ET ld[kFastRows];
+#pragma unroll
+    for (int r = 0; r < kFastRows; ++r)
+      if (r < n_live && (uint32_t)tid < seg_n[r]) ld[r] = E::load(rw, seg_lo[r] + (uint32_t)tid);
+#pragma unroll
+    for (int r = 0; r < kFastRows; ++r) {
+      const uint32_t n = r < n_live ? seg_n[r] : 0u;
+      if (n != 0) {  // (uniform)
+        const int age = n_live - 1 - r;
+        const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), age));
+        const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), age));
+        if ((uint32_t)tid < n) add_entry(ld[r], w1, w2);
+        lds_sync();
+      }
+    }
+  } else
   for (uint32_t b0 = 0; b0 < total; b0 += STAGE) {
     const uint32_t b1 = total - b0 < (uint32_t)STAGE ? total : b0 + STAGE;
     // stage the entries [b0, b1) of the concatenated segments: every thread
@@ -2000,15 +2038,7 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
       const int age = n_live - 1 - r;
       const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), age));
       const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), age));
-      for (uint32_t x = x0 + (uint32_t)tid; x < x1; x += NT) {
-        const ET e = stage[x - b0];
-        const uint32_t i = E::idx(e) - (uint32_t)lo;
-        const uint32_t zp = i < (uint32_t)s ? i : (uint32_t)(kSubBlock + lane);
-        const float v = E::val(e);
-        const float a1 = z1[zp], a2 = z2[zp];
-        z1[zp] = a1 + w1 * v;
-        z2[zp] = a2 + w2 * (v * v);
-      }
+      for (uint32_t x = x0 + (uint32_t)tid; x < x1; x += NT) add_entry(stage[x - b0], w1, w2);
       lds_sync();
     }
   }

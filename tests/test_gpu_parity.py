@@ -54,6 +54,11 @@ CASES = {
     "block20000_bucket16": (dict(numels=[20000 * 2 + 777, 5000], block=20000, bucket=16,
                                  density=0.02, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
                                  window=4), 6),
+    # the large-block update's two ways of reading the window: more than 24
+    # live rows, and rows of more than 256 entries per 4096-element sub-block
+    "block8192_window30": (dict(numels=[8192 * 2 + 300], block=8192, density=0.02, window=30,
+                                param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3), 28),
+    "block8192_dense_rows": (dict(numels=[8192 + 4100], block=8192, density=0.1, window=4), 6),
     # error-feedback formats beyond the paper's default: 8-bit codes, and the
     # randomized rounding of Lemma 1 (Philox stream keyed by seed, tensor,
     # step and element), bit-exact against the oracle
