@@ -1872,15 +1872,16 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
 // ================================================ update, blocks above 4096
 // One workgroup of 256 threads per 4096-element sub-block j of a block
 // (thread tid: the sub-block's elements 16*tid + [0, 16)).  The live rows'
-// entries of sub-block j are the segments the select kernel recorded; they are
-// staged in LDS, oldest row first, in batches of stage_large entries, and
-// one wave rebuilds z1 = sum beta1^r V and z2 = sum beta2^r V^2 from them in
-// that order (Algorithm 2, AdamStats).  Every thread then turns its own 16
-// elements' sums into the update (an element without entries has sums 0 and
-// a decrement of 0) and applies it (Algorithm 1; Algorithm 4).
-// 4608 staged entries (2304 with binary32 values) hold the live entries of a
-// sub-block at the 1.5e9 workload's density 5% and m = 20 (about 4100) in one
-// batch, and keep three workgroups per compute unit.
+// entries of sub-block j are the segments the select kernel recorded.  The
+// workgroup rebuilds z1 = sum beta1^r V and z2 = sum beta2^r V^2 one row at a
+// time, oldest first (Algorithm 2, AdamStats), from registers when every row
+// holds at most 256 of the sub-block's entries (and at most kFastRows rows are
+// live), else from LDS, where they are staged in batches of stage_large
+// entries.  Every thread then turns its own 16 elements' sums into the update
+// (an element without entries has sums 0 and a decrement of 0) and applies it
+// (Algorithm 1; Algorithm 4).  4608 staged entries (2304 with binary32
+// values) hold the live entries of a sub-block at density 5% and m = 20
+// (about 4100) in one batch, and keep three workgroups per compute unit.
 template <bool VF>
 constexpr int stage_large() { return VF ? 2304 : 4608; }
 // Live rows up to which the update reads a sub-block's entries straight into
