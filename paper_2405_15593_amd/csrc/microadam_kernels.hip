@@ -1399,14 +1399,14 @@ requant_kernel(StepParams p, int64_t first) {
 // k keys lie at or above hi, at least k at or above lo, and the at most
 // 8 keys per thread between them are gathered in LDS, so every bit costs a
 // few comparisons per thread and one barrier; once at most 256 keys remain
-// undecided they are gathered again and wave 0 finishes alone.  The bracket
-// is read off a sample of 1024 keys (a 16-ary search, one digit per wave,
-// one barrier per 4 bits) and checked by one counting pass; when the check
-// fails (an unlucky sample, large tie groups) a bitwise search over every
-// element narrows it instead.  The new row is written in element order, and for each
-// sub-block the position in the row of its first entry goes to the record's
-// segment table, behind the m rows, where the update finds the entries of one
-// sub-block.
+// undecided they are gathered again and the waves finish 4 bits per barrier
+// (a 16-ary search, one digit per wave).  The bracket is read off a sample of
+// 1024 keys (16-ary in the same way) and checked by one counting pass; when
+// the check fails (an unlucky sample, large tie groups) a bitwise search over
+// every element narrows it instead.  The new row is written in element order,
+// and for each sub-block the position in the row of its first entry goes to
+// the record's segment table, behind the m rows, where the update finds the
+// entries of one sub-block.
 constexpr int kSubBlock = 4096;
 constexpr int kCandPerThread = 8;
 template <bool B>
@@ -1440,8 +1440,8 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   uint32_t* const pre = cnt + 2 * NW;   // [2][NW] per-wave totals of the two element-order scans
   uint32_t* const two = pre + 2 * NW;   // [2][NW] per-wave counts of a bracket pass
   uint32_t* const misc = two + 2 * NW;  // [4]
-  uint32_t* const dig = misc + 4;       // [2][2][16] sample counts per digit, two searches
-  uint32_t* const last = dig + 64;      // [256] the keys wave 0 finishes with
+  uint32_t* const dig = misc + 4;       // [2][32] counts per digit, alternating between rounds
+  uint32_t* const last = dig + 64;      // [256] the last undecided keys
   uint32_t* const region = last + 256;  // the sample, then the gathered keys
 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
