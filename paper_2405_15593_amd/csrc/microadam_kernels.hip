@@ -1879,11 +1879,11 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
 // live), else from LDS, where they are staged in batches of stage_large
 // entries.  Every thread then turns its own 16 elements' sums into the update
 // (an element without entries has sums 0 and a decrement of 0) and applies it
-// (Algorithm 1; Algorithm 4).  4608 staged entries (2304 with binary32
-// values) hold the live entries of a sub-block at density 5% and m = 20
-// (about 4100) in one batch, and keep three workgroups per compute unit.
+// (Algorithm 1; Algorithm 4).  The staging batch is small (1024 entries, 512
+// with binary32 values: 37 KB of LDS in all), so that four workgroups fit a
+// compute unit for the register path, which uses no staging.
 template <bool VF>
-constexpr int stage_large() { return VF ? 2304 : 4608; }
+constexpr int stage_large() { return VF ? 512 : 1024; }
 // Live rows up to which the update reads a sub-block's entries straight into
 // registers (when no row holds more than 256 of them).
 constexpr int kFastRows = 24;
