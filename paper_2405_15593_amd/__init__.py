@@ -166,9 +166,11 @@ def microadam_init(cfg: microadam_config, numels: Sequence[int], param_dtype: in
 
 def microadam_step(h: int, param_ptrs: Sequence[int], grad_ptrs: Sequence[int],
                    lr: float = math.nan, stream: int = 0) -> None:
+    """`param_ptrs` / `grad_ptrs`: sequences of device addresses, or ctypes
+    arrays of c_void_p built once and passed again (no per-call copy)."""
     n = len(param_ptrs)
-    P = (ctypes.c_void_p * n)(*param_ptrs)
-    G = (ctypes.c_void_p * len(grad_ptrs))(*grad_ptrs)
+    P = param_ptrs if isinstance(param_ptrs, ctypes.Array) else (ctypes.c_void_p * n)(*param_ptrs)
+    G = grad_ptrs if isinstance(grad_ptrs, ctypes.Array) else (ctypes.c_void_p * len(grad_ptrs))(*grad_ptrs)
     _check(load().microadam_step(ctypes.c_void_p(h), P, G, n, float(lr), ctypes.c_void_p(stream)),
            "microadam_step")
 
@@ -239,6 +241,7 @@ class MicroAdam:
         assert self.params, "no parameters"
         self.cfg = cfg if cfg is not None else make_config(**cfg_kw)
         dt = {torch.float32: MICROADAM_F32, torch.bfloat16: MICROADAM_BF16}
+        self._dtype_code = dt
         self.param_dtype = dt[self.params[0].dtype]
         for p in self.params:
             assert p.is_cuda and p.is_contiguous() and dt[p.dtype] == self.param_dtype
@@ -251,6 +254,9 @@ class MicroAdam:
         self.grad_dtype = None
         self.handle = None
         self.ranges = 1
+        # the addresses of the last checked call, and their ctypes arrays
+        self._pp, self._gp = None, None
+        self._parr = self._garr = None
 
     def _stream(self) -> int:
         import torch
@@ -281,11 +287,25 @@ class MicroAdam:
     def step(self, grads, lr: float | None = None) -> None:
         grads = list(grads)
         assert len(grads) == len(self.params)
-        for g, p in zip(grads, self.params):
-            assert g.is_contiguous() and g.numel() == p.numel() and g.device == p.device
-        self._ensure(grads)
-        microadam_step(self.handle, [p.data_ptr() for p in self.params],
-                       [g.data_ptr() for g in grads], math.nan if lr is None else lr,
+        gp = [g.data_ptr() for g in grads]
+        if gp != self._gp:
+            for g, p in zip(grads, self.params):
+                assert g.is_contiguous() and g.numel() == p.numel() and g.device == p.device
+            self._ensure(grads)
+            self._garr = (ctypes.c_void_p * len(gp))(*gp)
+            self._gp = gp
+        else:
+            # the addresses of the last checked call (so the same device);
+            # the sizes are checked again
+            assert [g.numel() for g in grads] == self.numels
+        gdt = grads[0].dtype
+        assert all(g.dtype is gdt for g in grads) and self._dtype_code.get(gdt) == self.grad_dtype, \
+            "gradients of one dtype, the one of the first step"
+        pp = [p.data_ptr() for p in self.params]
+        if pp != self._pp:
+            self._parr = (ctypes.c_void_p * len(pp))(*pp)
+            self._pp = pp
+        microadam_step(self.handle, self._parr, self._garr, math.nan if lr is None else lr,
                        self._stream())
 
     @property
