@@ -16,9 +16,10 @@ alternate between steps.
 Prints one JSON line.  `roofline` describes the dominant (longer) kernel:
 `achieved` is its algorithmic HBM bytes per launch (select_bytes /
 update_bytes) over its mean duration, timed with HIP events that the library
-records on the launch stream around each kernel.  `traffic` comes from the
-committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary of that kernel when it
-was taken on the current kernel source, else null.  `cpu_baseline` times the
+records on the launch stream around each kernel of the timed steps (read once
+after them).  `traffic` comes from the committed rocprofv3 FETCH_SIZE /
+WRITE_SIZE summary of that kernel when it was taken on the current kernel
+source, else null.  `cpu_baseline` times the
 CPU oracle on a sample of the same workload's blocks on this host.
 """
 from __future__ import annotations
@@ -229,16 +230,18 @@ def main() -> int:
 
     opt.set_profiling(True)
     t_first = opt.t + 1
-    kernel_ms = []
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     for i in range(args.steps):
         opt.step(grad_sets[(args.warmup + i) % 2])
-        kernel_ms.append(opt.kernel_times())
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    sel_ms = sum(k[0] for k in kernel_ms) / len(kernel_ms)
-    upd_ms = sum(k[1] for k in kernel_ms) / len(kernel_ms)
+    # the library's events around every launch of the timed steps, read once
+    # after them (no synchronization between steps)
+    sel_tot, upd_tot, n_timed = opt.kernel_times_total()
+    assert n_timed == args.steps, (n_timed, args.steps)
+    sel_ms = sel_tot / n_timed
+    upd_ms = upd_tot / n_timed
     sel_b = select_bytes(w, args.ef_bits, bucket)
     upd_b = sum(update_bytes(w, t) for t in range(t_first, t_first + args.steps)) / args.steps
     kernels = {
@@ -249,8 +252,8 @@ def main() -> int:
     dk = kernels[dominant]
     default_ef = args.ef_bits == 4 and args.ef_rounding == "nearest" and bucket == w.bucket
     traffic, traffic_note = read_traffic(dominant, w.name) if default_ef else (None, "counters taken with the default EF")
-    print(f"[bench] kernel ms per step (select, update): "
-          f"{[(round(a, 3), round(b, 3)) for a, b in kernel_ms]}", file=sys.stderr, flush=True)
+    print(f"[bench] mean kernel ms per step (select, update) over {n_timed} steps: "
+          f"{round(sel_ms, 3), round(upd_ms, 3)}", file=sys.stderr, flush=True)
 
     cpu = None
     if args.cpu_blocks > 0:

@@ -232,12 +232,12 @@ int microadam_tensor_layout(microadam_handle h, int32_t tensor,
 int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat,
                             float* vhat, void* stream);
 
-/* Static name of an error code. */
 /*
  * Profiling.  With profiling on (off after init), every microadam_step
  * records HIP events on its stream around its two kernels.  Events are
  * created on the first call that turns profiling on, with the init device
- * current.
+ * current.  Every call that turns it on starts a new total for
+ * microadam_kernel_times_total.
  */
 int microadam_set_profiling(microadam_handle h, int32_t on);
 
@@ -251,6 +251,19 @@ int microadam_set_profiling(microadam_handle h, int32_t on);
  * until that step is done.  out_ms: 2 host floats.
  */
 int microadam_kernel_times(microadam_handle h, float* out_ms);
+
+/*
+ * Summed kernel durations of every step profiled since profiling was last
+ * switched on (or since the previous call of this function), without
+ * synchronizing between steps: out_ms[0] = select, out_ms[1] = update, in
+ * milliseconds (summed as microadam_kernel_times reports one step), and
+ * *out_steps = the number of steps they cover; the totals then restart at 0.
+ * The library keeps each profiled step's events in a ring of four sets and
+ * reads a set when it is needed again, four profiled steps later.  Blocks
+ * until the steps counted are done.  out_ms: 2 host floats; out_steps: one
+ * host int64.  Errors: MICROADAM_ERR_INVALID_ARG for NULL outputs.
+ */
+int microadam_kernel_times_total(microadam_handle h, float* out_ms, int64_t* out_steps);
 
 /*
  * Splits every following step into `ranges` consecutive ranges of Top-K

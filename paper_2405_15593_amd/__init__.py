@@ -80,7 +80,8 @@ EXPORTS = (
     "microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
     "microadam_get_step", "microadam_set_step", "microadam_tensor_layout",
     "microadam_debug_moments", "microadam_set_profiling", "microadam_kernel_times",
-    "microadam_set_ranges", "microadam_error_string", "microadam_last_error",
+    "microadam_kernel_times_total", "microadam_set_ranges", "microadam_error_string",
+    "microadam_last_error",
 )
 
 
@@ -114,6 +115,7 @@ def load(path: str = LIBRARY):
     lib.microadam_debug_moments.argtypes = [vp, i32, vp, vp, vp]
     lib.microadam_set_profiling.argtypes = [vp, i32]
     lib.microadam_kernel_times.argtypes = [vp, P(ctypes.c_float)]
+    lib.microadam_kernel_times_total.argtypes = [vp, P(ctypes.c_float), P(i64)]
     lib.microadam_set_ranges.argtypes = [vp, i32]
     lib.microadam_error_string.argtypes = [ctypes.c_int]
     lib.microadam_error_string.restype = ctypes.c_char_p
@@ -121,7 +123,8 @@ def load(path: str = LIBRARY):
     lib.microadam_last_error.restype = ctypes.c_char_p
     for f in ("microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
               "microadam_set_step", "microadam_tensor_layout", "microadam_debug_moments",
-              "microadam_set_profiling", "microadam_kernel_times", "microadam_set_ranges"):
+              "microadam_set_profiling", "microadam_kernel_times", "microadam_kernel_times_total",
+              "microadam_set_ranges"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -212,6 +215,16 @@ def microadam_kernel_times(h: int) -> tuple:
     out = (ctypes.c_float * 2)()
     _check(load().microadam_kernel_times(ctypes.c_void_p(h), out), "microadam_kernel_times")
     return float(out[0]), float(out[1])
+
+
+def microadam_kernel_times_total(h: int) -> tuple:
+    """(select ms, update ms, steps): durations summed over the steps profiled
+    since profiling was switched on or since the previous call."""
+    out = (ctypes.c_float * 2)()
+    n = ctypes.c_int64()
+    _check(load().microadam_kernel_times_total(ctypes.c_void_p(h), out, ctypes.byref(n)),
+           "microadam_kernel_times_total")
+    return float(out[0]), float(out[1]), int(n.value)
 
 
 def microadam_set_ranges(h: int, ranges: int) -> None:
@@ -329,6 +342,11 @@ class MicroAdam:
     def kernel_times(self) -> tuple:
         """(select ms, update ms) of the last step taken with profiling on."""
         return microadam_kernel_times(self.handle)
+
+    def kernel_times_total(self) -> tuple:
+        """(select ms, update ms, steps) summed over the steps profiled since
+        profiling was switched on or since the previous call."""
+        return microadam_kernel_times_total(self.handle)
 
     def set_ranges(self, ranges: int) -> None:
         """Split each step into block ranges whose updates overlap the next

@@ -209,8 +209,16 @@ struct microadam_handle_s {
   hipEvent_t step_done = nullptr;     // last launch of this handle finished
   bool profiling = false;
   int32_t timed = 0;                  // block ranges of the last step if it recorded events
-  // per block range: select start, select end, update start, update end
-  hipEvent_t ev[4 * kMaxRanges] = {};
+  // A ring of event sets for the profiled steps; per block range: select
+  // start, select end, update start, update end.  A set holds a step whose
+  // durations are not yet in the totals while pending[slot] > 0 (its ranges).
+  static constexpr int kProfSlots = 4;
+  hipEvent_t ev[kProfSlots][4 * kMaxRanges] = {};
+  int32_t pending[kProfSlots] = {};
+  int32_t prof_slot = 0;              // set of the last profiled step
+  int64_t prof_count = 0;             // profiled steps since profiling was switched on
+  double total_ms[2] = {0.0, 0.0};    // summed durations of the steps folded so far
+  int64_t total_steps = 0;
   int32_t ranges = 1;                 // block ranges a step is split into
   hipStream_t aux = nullptr;          // runs the updates of a split step
   hipEvent_t range_done[kMaxRanges] = {};  // select of range i finished
@@ -237,14 +245,46 @@ void release(microadam_handle h) {
     (void)hipStreamSynchronize(h->aux);
     (void)hipStreamDestroy(h->aux);
   }
-  for (hipEvent_t& e : h->ev)
-    if (e) (void)hipEventDestroy(e);
+  for (auto& set : h->ev)
+    for (hipEvent_t& e : set)
+      if (e) (void)hipEventDestroy(e);
   for (hipEvent_t& e : h->range_done)
     if (e) (void)hipEventDestroy(e);
   if (h->aux_done) (void)hipEventDestroy(h->aux_done);
   if (h->d_block_tensor) (void)hipFree(h->d_block_tensor);
   if (h->d_wpow) (void)hipFree(h->d_wpow);
   delete h;
+}
+
+// Durations of the steps recorded in event set `slot` (select, update; summed
+// over the step's ranges), waiting for them.
+hipError_t slot_times(microadam_handle h, int slot, int32_t ranges, float* out_ms) {
+  hipError_t e;
+  out_ms[0] = out_ms[1] = 0.0f;
+  for (int i = 0; i < ranges; ++i) {
+    hipEvent_t* ev = h->ev[slot] + 4 * i;
+    float a = 0.0f, b = 0.0f;
+    if ((e = hipEventSynchronize(ev[1])) != hipSuccess || (e = hipEventSynchronize(ev[3])) != hipSuccess ||
+        (e = hipEventElapsedTime(&a, ev[0], ev[1])) != hipSuccess ||
+        (e = hipEventElapsedTime(&b, ev[2], ev[3])) != hipSuccess)
+      return e;
+    out_ms[0] += a;
+    out_ms[1] += b;
+  }
+  return hipSuccess;
+}
+
+// Adds the durations of the step pending in event set `slot` to the totals.
+hipError_t fold_slot(microadam_handle h, int slot) {
+  if (h->pending[slot] <= 0) return hipSuccess;
+  float ms[2];
+  const hipError_t e = slot_times(h, slot, h->pending[slot], ms);
+  if (e != hipSuccess) return e;
+  h->total_ms[0] += ms[0];
+  h->total_ms[1] += ms[1];
+  ++h->total_steps;
+  h->pending[slot] = 0;
+  return hipSuccess;
 }
 
 // Per-step constants, derived in binary64 and rounded once to binary32: the
@@ -485,7 +525,11 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
   // buckets spanning blocks tie blocks together through the bucket tables,
   // so such a step always runs as one range
   const int R = h->planes.big ? 1 : h->ranges;
-  auto rec = [&](int i, hipStream_t st) { return prof ? hipEventRecord(h->ev[i], st) : hipSuccess; };
+  // a profiled step takes the next event set of the ring, first adding the
+  // step it held (steps ago, so normally done) to the totals
+  const int pslot = prof ? (int)(h->prof_count % microadam_handle_s::kProfSlots) : 0;
+  if (prof && (e = fold_slot(h, pslot)) != hipSuccess) return hip_fail(e, "reading the kernel timers");
+  auto rec = [&](int i, hipStream_t st) { return prof ? hipEventRecord(h->ev[pslot][i], st) : hipSuccess; };
   if (h->planes.big) {
     // select with per-block partials, the bucket reduction, the quantization
     // of the residual, then the update
@@ -533,6 +577,11 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
     if ((e = hipStreamWaitEvent(s, h->aux_done, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
   }
   h->timed = prof ? R : 0;
+  if (prof) {
+    h->pending[pslot] = R;
+    h->prof_slot = pslot;
+    ++h->prof_count;
+  }
   if ((e = hipEventRecord(h->step_done, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   h->t = t;
   return MICROADAM_OK;
@@ -608,13 +657,22 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat, flo
 int microadam_set_profiling(microadam_handle h, int32_t on) {
   int rc = check_handle(h);
   if (rc) return rc;
-  if (on && !h->ev[0]) {
+  if (on && !h->ev[microadam_handle_s::kProfSlots - 1][4 * kMaxRanges - 1]) {
     rc = check_device(h);
     if (rc) return rc;
-    for (hipEvent_t& e : h->ev) {
-      const hipError_t err = hipEventCreate(&e);
-      if (err != hipSuccess) return hip_fail(err, "hipEventCreate");
-    }
+    for (auto& set : h->ev)
+      for (hipEvent_t& e : set) {
+        if (e) continue;
+        const hipError_t err = hipEventCreate(&e);
+        if (err != hipSuccess) return hip_fail(err, "hipEventCreate");
+      }
+  }
+  if (on) {  // a new total starts; steps not yet added to the old one are dropped
+    for (int32_t& n : h->pending) n = 0;
+    h->prof_count = 0;
+    h->total_ms[0] = h->total_ms[1] = 0.0;
+    h->total_steps = 0;
+    h->timed = 0;
   }
   h->profiling = on != 0;
   return MICROADAM_OK;
@@ -627,15 +685,23 @@ int microadam_kernel_times(microadam_handle h, float* out_ms) {
   if (!h->timed) return fail(MICROADAM_ERR_INVALID_ARG, "the last step was not profiled");
   hipError_t e;
   if ((e = hipEventSynchronize(h->step_done)) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
-  out_ms[0] = out_ms[1] = 0.0f;
-  for (int i = 0; i < h->timed; ++i) {
-    float a = 0.0f, b = 0.0f;
-    if ((e = hipEventElapsedTime(&a, h->ev[4 * i], h->ev[4 * i + 1])) != hipSuccess ||
-        (e = hipEventElapsedTime(&b, h->ev[4 * i + 2], h->ev[4 * i + 3])) != hipSuccess)
-      return hip_fail(e, "hipEventElapsedTime");
-    out_ms[0] += a;
-    out_ms[1] += b;
+  if ((e = slot_times(h, h->prof_slot, h->timed, out_ms)) != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+  return MICROADAM_OK;
+}
+
+int microadam_kernel_times_total(microadam_handle h, float* out_ms, int64_t* out_steps) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  if (!out_ms || !out_steps) return fail(MICROADAM_ERR_INVALID_ARG, "out_ms or out_steps is NULL");
+  for (int k = 0; k < microadam_handle_s::kProfSlots; ++k) {
+    const hipError_t e = fold_slot(h, k);
+    if (e != hipSuccess) return hip_fail(e, "reading the kernel timers");
   }
+  out_ms[0] = (float)h->total_ms[0];
+  out_ms[1] = (float)h->total_ms[1];
+  *out_steps = h->total_steps;
+  h->total_ms[0] = h->total_ms[1] = 0.0;
+  h->total_steps = 0;
   return MICROADAM_OK;
 }
 
