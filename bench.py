@@ -199,7 +199,8 @@ def main() -> int:
         return 0
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
-              "(the MicroAdam step needs no communication; see DESIGN.md for sharding)",
+              "(the step is block-local: each GPU would step its own shard of the blocks, "
+              "with no communication inside the step)",
               file=sys.stderr)
         return 2
 
