@@ -54,6 +54,17 @@ CASES = {
     "block20000_bucket16": (dict(numels=[20000 * 2 + 777, 5000], block=20000, bucket=16,
                                  density=0.02, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
                                  window=4), 6),
+    # the large-block search's branches: k above the bracket's capacity of 8
+    # keys per thread (B_d = 32768, density 20%: the bitwise fallback), a
+    # density so low that the sample gives no upper bound (B_d = 16384, k = 33),
+    # and binary32 window values at B_d = 65536
+    "block32768_density20": (dict(numels=[32768 + 5000], block=32768, density=0.2, window=3,
+                                  grad_dist="student_t4"), 4),
+    "block16384_k33": (dict(numels=[16384 * 2 + 700], block=16384, density=0.002, window=3,
+                            grad_dist="student_t4", param_dtype=bf16, grad_dtype=bf16,
+                            grad_scale=1e-3), 4),
+    "block65536_f32_values": (dict(numels=[65536 + 9000], block=65536, density=0.01, window=2,
+                                   value_f32=True), 3),
     # the large-block update's two ways of reading the window: more than 24
     # live rows, and rows of more than 256 entries per 4096-element sub-block
     "block8192_window30": (dict(numels=[8192 * 2 + 300], block=8192, density=0.02, window=30,
