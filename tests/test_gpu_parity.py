@@ -65,6 +65,9 @@ CASES = {
                             grad_scale=1e-3), 4),
     "block65536_f32_values": (dict(numels=[65536 + 9000], block=65536, density=0.01, window=2,
                                    value_f32=True), 3),
+    # a step split into 3 block ranges with the large-block kernels
+    "block16384_ranges3": (dict(numels=[16384 * 3 + 500, 9000], block=16384, density=0.02, window=3,
+                                ranges=3), 4),
     # the large-block update's two ways of reading the window: more than 24
     # live rows, and rows of more than 256 entries per 4096-element sub-block
     "block8192_window30": (dict(numels=[8192 * 2 + 300], block=8192, density=0.02, window=30,
