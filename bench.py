@@ -37,8 +37,11 @@ sys.path.insert(0, ROOT)
 
 METRIC = "MicroAdam step params/sec + achieved HBM GB/s (% peak), Llama-2-7B shape"
 HBM_PEAK_GBS = 8000.0
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2405_15593_amd", "csrc", f)
-                  for f in ("microadam_kernels.hip", "microadam_device.h")]
+CSRC = os.path.join(ROOT, "paper_2405_15593_amd", "csrc")
+# the device code: every HIP source and header of the library (the host-only
+# API file excluded)
+KERNEL_SOURCES = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
+                        if f.endswith((".hip", ".h")))
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -177,8 +180,6 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama2_7b_bf16")
     ap.add_argument("--cpu-blocks", type=int, default=10000, help="0 disables the CPU baseline")
-    ap.add_argument("--ranges", type=int, default=1,
-                    help="block ranges per step (each range's update overlaps the next selects)")
     ap.add_argument("--ef-bits", type=int, default=4, choices=(4, 8), help="bits per EF code")
     ap.add_argument("--ef-rounding", default="nearest", choices=("nearest", "randomized"),
                     help="EF quantizer rounding (randomized: Lemma 1)")
@@ -222,7 +223,6 @@ def main() -> int:
     cfg = ma.make_config(density=w.density, window=w.window, ef_bucket=bucket, topk_block=w.block, lr=w.lr,
                          ef_bits=args.ef_bits, ef_rounding=rounding, seed=1234)
     opt = ma.MicroAdam(params, cfg)
-    opt.set_ranges(args.ranges)
 
     for i in range(args.warmup):
         opt.step(grad_sets[i % 2])
@@ -283,7 +283,7 @@ def main() -> int:
             "k_per_block": block_k(w.block, w.density), "window": w.window,
             "ef_bits": args.ef_bits, "ef_rounding": args.ef_rounding, "ef_bucket": bucket,
             "steps_timed": [t_first, t_first + args.steps - 1],
-            "window_full": t_first > w.window, "ranges": args.ranges,
+            "window_full": t_first > w.window,
         },
         "kernels": kernels,
         "step_hbm_gbs": (sel_b + upd_b) / (sel_ms + upd_ms) / 1e6,

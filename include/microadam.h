@@ -60,7 +60,8 @@ enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
  *   density      k/d in (0, 1].  A Top-K block of s elements keeps
  *                k_s = min(s, max(1, ceil(density * s - 1e-9))) entries.
  *   beta1,beta2  moment decay rates in [0, 1).
- *   eps          added to sqrt(v-hat) in the update (Algorithm 1); >= 0.
+ *   eps          added to sqrt(v-hat) in the update (Algorithm 1); > 0 (an
+ *                element without window entries then takes a zero step).
  *   lr           default step size eta (microadam_step may override it).
  *   weight_decay lambda of the decoupled decay theta *= (1 - eta*lambda)
  *                (Algorithm 4); >= 0.
@@ -245,10 +246,8 @@ int microadam_set_profiling(microadam_handle h, int32_t on);
  * Durations in milliseconds of the kernels of the last step, which must have
  * been taken with profiling on: out_ms[0] = select (EF decode, block Top-K,
  * new window row, EF re-quantisation), out_ms[1] = update (moment rebuild
- * from the window and parameter update).  A step split into block ranges
- * (microadam_set_ranges) reports the sum over its ranges of each kernel's
- * launch durations; those of the two kernels then overlap in time.  Blocks
- * until that step is done.  out_ms: 2 host floats.
+ * from the window and parameter update).  Blocks until that step is done.
+ * out_ms: 2 host floats.
  */
 int microadam_kernel_times(microadam_handle h, float* out_ms);
 
@@ -264,20 +263,6 @@ int microadam_kernel_times(microadam_handle h, float* out_ms);
  * host int64.  Errors: MICROADAM_ERR_INVALID_ARG for NULL outputs.
  */
 int microadam_kernel_times_total(microadam_handle h, float* out_ms, int64_t* out_steps);
-
-/*
- * Splits every following step into `ranges` consecutive ranges of Top-K
- * blocks, 1 <= ranges <= 32 (1 after init).  The result of a step does not
- * depend on it: blocks share no state, and the update of a block reads only
- * what its own select wrote (Algorithm 1 works on each block alone).  With
- * ranges > 1 the update of range i runs on a stream the library owns
- * (created here on the first such call, with the init device current, at
- * default priority) while the selects of the later ranges run on the step's
- * stream; the step's stream waits for the last update, so work queued on it
- * afterwards sees the whole step.  Errors: MICROADAM_ERR_INVALID_ARG for
- * ranges out of bounds.
- */
-int microadam_set_ranges(microadam_handle h, int32_t ranges);
 
 const char* microadam_error_string(int code);
 

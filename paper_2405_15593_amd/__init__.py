@@ -80,7 +80,7 @@ EXPORTS = (
     "microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
     "microadam_get_step", "microadam_set_step", "microadam_tensor_layout",
     "microadam_debug_moments", "microadam_set_profiling", "microadam_kernel_times",
-    "microadam_kernel_times_total", "microadam_set_ranges", "microadam_error_string",
+    "microadam_kernel_times_total", "microadam_error_string",
     "microadam_last_error",
 )
 
@@ -116,15 +116,13 @@ def load(path: str = LIBRARY):
     lib.microadam_set_profiling.argtypes = [vp, i32]
     lib.microadam_kernel_times.argtypes = [vp, P(ctypes.c_float)]
     lib.microadam_kernel_times_total.argtypes = [vp, P(ctypes.c_float), P(i64)]
-    lib.microadam_set_ranges.argtypes = [vp, i32]
     lib.microadam_error_string.argtypes = [ctypes.c_int]
     lib.microadam_error_string.restype = ctypes.c_char_p
     lib.microadam_last_error.argtypes = []
     lib.microadam_last_error.restype = ctypes.c_char_p
     for f in ("microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
               "microadam_set_step", "microadam_tensor_layout", "microadam_debug_moments",
-              "microadam_set_profiling", "microadam_kernel_times", "microadam_kernel_times_total",
-              "microadam_set_ranges"):
+              "microadam_set_profiling", "microadam_kernel_times", "microadam_kernel_times_total"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -227,10 +225,6 @@ def microadam_kernel_times_total(h: int) -> tuple:
     return float(out[0]), float(out[1]), int(n.value)
 
 
-def microadam_set_ranges(h: int, ranges: int) -> None:
-    _check(load().microadam_set_ranges(ctypes.c_void_p(h), int(ranges)), "microadam_set_ranges")
-
-
 def microadam_error_string(code: int) -> str:
     return load().microadam_error_string(code).decode()
 
@@ -266,7 +260,6 @@ class MicroAdam:
         self.state_view = self.state[off:off + nbytes]
         self.grad_dtype = None
         self.handle = None
-        self.ranges = 1
         # the addresses of the last checked call, and their ctypes arrays
         self._pp, self._gp = None, None
         self._parr = self._garr = None
@@ -284,8 +277,6 @@ class MicroAdam:
         self.handle = microadam_init(self.cfg, self.numels, self.param_dtype, self.grad_dtype,
                                      self.state_view.data_ptr(), self.state_view.numel(),
                                      self._stream())
-        if self.ranges != 1:
-            microadam_set_ranges(self.handle, self.ranges)
 
     def restore(self, state, t: int, grads) -> None:
         """Creates the handle for gradients like `grads`, then loads a saved
@@ -347,13 +338,6 @@ class MicroAdam:
         """(select ms, update ms, steps) summed over the steps profiled since
         profiling was switched on or since the previous call."""
         return microadam_kernel_times_total(self.handle)
-
-    def set_ranges(self, ranges: int) -> None:
-        """Split each step into block ranges whose updates overlap the next
-        ranges' selects (same results); applied from the next step on."""
-        if self.handle is not None:
-            microadam_set_ranges(self.handle, ranges)
-        self.ranges = int(ranges)
 
     def close(self) -> None:
         if self.handle is not None:

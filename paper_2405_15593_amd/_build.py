@@ -1,6 +1,9 @@
-"""Builds libmicroadam.so (HIP for gfx950) in-tree with hipcc."""
+"""Builds libmicroadam.so (HIP for gfx950) in-tree with hipcc: every source
+of csrc/ is compiled to an object file in parallel, then linked."""
 from __future__ import annotations
 
+import concurrent.futures as cf
+import glob
 import os
 import subprocess
 
@@ -9,11 +12,11 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libmicroadam.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("microadam_kernels.hip", "microadam_api.cpp")]
+OBJDIR = os.path.join(PKG, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+COMPILE_FLAGS = [
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # one rounding per written operation: results that decide integers
     # (EF codes, Top-K) must not depend on FMA contraction
     "-ffp-contract=off",
@@ -24,19 +27,38 @@ FLAGS = [
     "-Xarch_device", "-fno-honor-nans", "-Xarch_device", "-mno-amdgpu-ieee",
     "-Wall", "-Wno-unused-function",
     "-I", INCLUDE, "-I", CSRC,
-    "-Wl,-rpath,/opt/rocm/lib",
 ]
+LINK_FLAGS = ["--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,-rpath,/opt/rocm/lib"]
 
 
-def build(verbose: bool = False) -> str:
-    """Compiles every HIP/C++ source of the library; always rebuilds."""
+def sources() -> list[str]:
+    return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
+
+
+def _compile(src: str) -> str:
+    obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
+    cmd = [HIPCC, *COMPILE_FLAGS, "-x", "hip", "-c", src, "-o", obj + ".tmp"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {os.path.basename(src)} ({res.returncode}):\n{res.stderr[-6000:]}")
+    os.replace(obj + ".tmp", obj)
+    return obj
+
+
+def build(verbose: bool = False, jobs: int | None = None) -> str:
+    """Compiles every HIP/C++ source of the library (always) and links it."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    srcs = sources()
+    jobs = jobs or min(len(srcs), os.cpu_count() or 4, 16)
+    with cf.ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(_compile, srcs))
     tmp = LIBRARY + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-x", "hip", SOURCES[0], "-x", "hip", SOURCES[1], "-o", tmp]
+    cmd = [HIPCC, *LINK_FLAGS, *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{res.stderr[-6000:]}")
+        raise RuntimeError(f"link failed ({res.returncode}):\n{res.stderr[-6000:]}")
     os.replace(tmp, LIBRARY)
     return LIBRARY
 

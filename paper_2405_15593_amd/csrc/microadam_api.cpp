@@ -60,8 +60,8 @@ int validate_config(const microadam_config* c) {
     return fail(MICROADAM_ERR_INVALID_ARG, "density must be in (0, 1]");
   if (!(c->beta1 >= 0.0 && c->beta1 < 1.0) || !(c->beta2 >= 0.0 && c->beta2 < 1.0))
     return fail(MICROADAM_ERR_INVALID_ARG, "beta1 and beta2 must be in [0, 1)");
-  if (!(c->eps >= 0.0) || !std::isfinite(c->eps))
-    return fail(MICROADAM_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if (!(c->eps > 0.0) || !std::isfinite(c->eps))
+    return fail(MICROADAM_ERR_INVALID_ARG, "eps must be finite and > 0");
   if (!std::isfinite(c->lr)) return fail(MICROADAM_ERR_INVALID_ARG, "lr must be finite");
   if (!(c->weight_decay >= 0.0) || !std::isfinite(c->weight_decay))
     return fail(MICROADAM_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
@@ -188,7 +188,6 @@ struct TableSlot {
 };
 
 constexpr int kTableSlots = 4;
-constexpr int kMaxRanges = 32;
 
 struct microadam_handle_s {
   microadam_config cfg;
@@ -208,21 +207,17 @@ struct microadam_handle_s {
   int current = -1;                   // slot used by the last step
   hipEvent_t step_done = nullptr;     // last launch of this handle finished
   bool profiling = false;
-  int32_t timed = 0;                  // block ranges of the last step if it recorded events
-  // A ring of event sets for the profiled steps; per block range: select
-  // start, select end, update start, update end.  A set holds a step whose
-  // durations are not yet in the totals while pending[slot] > 0 (its ranges).
+  bool timed = false;                 // the last step recorded events
+  // A ring of event sets for the profiled steps: select start, select end,
+  // update start, update end.  A set holds a step whose durations are not
+  // yet in the totals while pending[slot] is set.
   static constexpr int kProfSlots = 4;
-  hipEvent_t ev[kProfSlots][4 * kMaxRanges] = {};
-  int32_t pending[kProfSlots] = {};
+  hipEvent_t ev[kProfSlots][4] = {};
+  bool pending[kProfSlots] = {};
   int32_t prof_slot = 0;              // set of the last profiled step
   int64_t prof_count = 0;             // profiled steps since profiling was switched on
   double total_ms[2] = {0.0, 0.0};    // summed durations of the steps folded so far
   int64_t total_steps = 0;
-  int32_t ranges = 1;                 // block ranges a step is split into
-  hipStream_t aux = nullptr;          // runs the updates of a split step
-  hipEvent_t range_done[kMaxRanges] = {};  // select of range i finished
-  hipEvent_t aux_done = nullptr;      // every update of the last split step finished
 };
 
 namespace {
@@ -241,49 +236,37 @@ void release(microadam_handle h) {
     if (t.d) (void)hipFree(t.d);
     if (t.h) (void)hipHostFree(t.h);
   }
-  if (h->aux) {
-    (void)hipStreamSynchronize(h->aux);
-    (void)hipStreamDestroy(h->aux);
-  }
   for (auto& set : h->ev)
     for (hipEvent_t& e : set)
       if (e) (void)hipEventDestroy(e);
-  for (hipEvent_t& e : h->range_done)
-    if (e) (void)hipEventDestroy(e);
-  if (h->aux_done) (void)hipEventDestroy(h->aux_done);
   if (h->d_block_tensor) (void)hipFree(h->d_block_tensor);
   if (h->d_wpow) (void)hipFree(h->d_wpow);
   delete h;
 }
 
-// Durations of the steps recorded in event set `slot` (select, update; summed
-// over the step's ranges), waiting for them.
-hipError_t slot_times(microadam_handle h, int slot, int32_t ranges, float* out_ms) {
+// Durations of the step recorded in event set `slot` (select, update),
+// waiting for them.
+hipError_t slot_times(microadam_handle h, int slot, float* out_ms) {
   hipError_t e;
+  const hipEvent_t* ev = h->ev[slot];
   out_ms[0] = out_ms[1] = 0.0f;
-  for (int i = 0; i < ranges; ++i) {
-    hipEvent_t* ev = h->ev[slot] + 4 * i;
-    float a = 0.0f, b = 0.0f;
-    if ((e = hipEventSynchronize(ev[1])) != hipSuccess || (e = hipEventSynchronize(ev[3])) != hipSuccess ||
-        (e = hipEventElapsedTime(&a, ev[0], ev[1])) != hipSuccess ||
-        (e = hipEventElapsedTime(&b, ev[2], ev[3])) != hipSuccess)
-      return e;
-    out_ms[0] += a;
-    out_ms[1] += b;
-  }
+  if ((e = hipEventSynchronize(ev[1])) != hipSuccess || (e = hipEventSynchronize(ev[3])) != hipSuccess ||
+      (e = hipEventElapsedTime(&out_ms[0], ev[0], ev[1])) != hipSuccess ||
+      (e = hipEventElapsedTime(&out_ms[1], ev[2], ev[3])) != hipSuccess)
+    return e;
   return hipSuccess;
 }
 
 // Adds the durations of the step pending in event set `slot` to the totals.
 hipError_t fold_slot(microadam_handle h, int slot) {
-  if (h->pending[slot] <= 0) return hipSuccess;
+  if (!h->pending[slot]) return hipSuccess;
   float ms[2];
-  const hipError_t e = slot_times(h, slot, h->pending[slot], ms);
+  const hipError_t e = slot_times(h, slot, ms);
   if (e != hipSuccess) return e;
   h->total_ms[0] += ms[0];
   h->total_ms[1] += ms[1];
   ++h->total_steps;
-  h->pending[slot] = 0;
+  h->pending[slot] = false;
   return hipSuccess;
 }
 
@@ -522,63 +505,32 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
   StepParams p;
   fill_constants(h, t, lr, p);
   const bool prof = h->profiling;
-  // buckets spanning blocks tie blocks together through the bucket tables,
-  // so such a step always runs as one range
-  const int R = h->planes.big ? 1 : h->ranges;
   // a profiled step takes the next event set of the ring, first adding the
   // step it held (steps ago, so normally done) to the totals
   const int pslot = prof ? (int)(h->prof_count % microadam_handle_s::kProfSlots) : 0;
   if (prof && (e = fold_slot(h, pslot)) != hipSuccess) return hip_fail(e, "reading the kernel timers");
-  auto rec = [&](int i, hipStream_t st) { return prof ? hipEventRecord(h->ev[pslot][i], st) : hipSuccess; };
+  auto rec = [&](int i) { return prof ? hipEventRecord(h->ev[pslot][i], s) : hipSuccess; };
+  if ((e = rec(0)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if (h->planes.big) {
     // select with per-block partials, the bucket reduction, the quantization
-    // of the residual, then the update
-    if ((e = rec(0, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    // of the residual
     e = microadam::launch_select_partials(p, h->grad_bf16, h->value_f32, s);
     if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
     e = microadam::launch_bucket_reduce(p, s);
     if (e != hipSuccess) return hip_fail(e, "launching the bucket reduction");
     e = microadam::launch_requant(p, h->grad_bf16, h->value_f32, s);
     if (e != hipSuccess) return hip_fail(e, "launching the quantization kernel");
-    if ((e = rec(1, s)) != hipSuccess || (e = rec(2, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    e = microadam::launch_update(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
-    if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
-    if ((e = rec(3, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  } else if (R == 1) {
-    if ((e = rec(0, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  } else {
     e = microadam::launch_select(p, h->grad_bf16, h->value_f32, 0, h->total_blocks, s);
     if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
-    if ((e = rec(1, s)) != hipSuccess || (e = rec(2, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    e = microadam::launch_update(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
-    if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
-    if ((e = rec(3, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  } else {
-    // Range i's update runs on the auxiliary stream after range i's select,
-    // beside the selects of the ranges after it; the caller's stream waits
-    // for the last update before anything it runs next.
-    auto first_of = [&](int i) { return h->total_blocks * i / R; };
-    for (int i = 0; i < R; ++i) {
-      if ((e = rec(4 * i, s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-      e = microadam::launch_select(p, h->grad_bf16, h->value_f32, first_of(i), first_of(i + 1) - first_of(i), s);
-      if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
-      if ((e = rec(4 * i + 1, s)) != hipSuccess || (e = hipEventRecord(h->range_done[i], s)) != hipSuccess)
-        return hip_fail(e, "hipEventRecord");
-    }
-    for (int i = 0; i < R; ++i) {
-      if ((e = hipStreamWaitEvent(h->aux, h->range_done[i], 0)) != hipSuccess)
-        return hip_fail(e, "hipStreamWaitEvent");
-      if ((e = rec(4 * i + 2, h->aux)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-      e = microadam::launch_update(p, h->param_bf16, h->value_f32, first_of(i), first_of(i + 1) - first_of(i),
-                                   h->aux);
-      if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
-      if ((e = rec(4 * i + 3, h->aux)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    }
-    if ((e = hipEventRecord(h->aux_done, h->aux)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    if ((e = hipStreamWaitEvent(s, h->aux_done, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
   }
-  h->timed = prof ? R : 0;
+  if ((e = rec(1)) != hipSuccess || (e = rec(2)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  e = microadam::launch_update(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
+  if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
+  if ((e = rec(3)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  h->timed = prof;
   if (prof) {
-    h->pending[pslot] = R;
+    h->pending[pslot] = true;
     h->prof_slot = pslot;
     ++h->prof_count;
   }
@@ -657,7 +609,7 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat, flo
 int microadam_set_profiling(microadam_handle h, int32_t on) {
   int rc = check_handle(h);
   if (rc) return rc;
-  if (on && !h->ev[microadam_handle_s::kProfSlots - 1][4 * kMaxRanges - 1]) {
+  if (on && !h->ev[microadam_handle_s::kProfSlots - 1][3]) {
     rc = check_device(h);
     if (rc) return rc;
     for (auto& set : h->ev)
@@ -668,11 +620,11 @@ int microadam_set_profiling(microadam_handle h, int32_t on) {
       }
   }
   if (on) {  // a new total starts; steps not yet added to the old one are dropped
-    for (int32_t& n : h->pending) n = 0;
+    for (bool& n : h->pending) n = false;
     h->prof_count = 0;
     h->total_ms[0] = h->total_ms[1] = 0.0;
     h->total_steps = 0;
-    h->timed = 0;
+    h->timed = false;
   }
   h->profiling = on != 0;
   return MICROADAM_OK;
@@ -685,7 +637,7 @@ int microadam_kernel_times(microadam_handle h, float* out_ms) {
   if (!h->timed) return fail(MICROADAM_ERR_INVALID_ARG, "the last step was not profiled");
   hipError_t e;
   if ((e = hipEventSynchronize(h->step_done)) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
-  if ((e = slot_times(h, h->prof_slot, h->timed, out_ms)) != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+  if ((e = slot_times(h, h->prof_slot, out_ms)) != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
   return MICROADAM_OK;
 }
 
@@ -702,28 +654,6 @@ int microadam_kernel_times_total(microadam_handle h, float* out_ms, int64_t* out
   *out_steps = h->total_steps;
   h->total_ms[0] = h->total_ms[1] = 0.0;
   h->total_steps = 0;
-  return MICROADAM_OK;
-}
-
-int microadam_set_ranges(microadam_handle h, int32_t ranges) {
-  int rc = check_handle(h);
-  if (rc) return rc;
-  if (ranges < 1 || ranges > kMaxRanges) return fail(MICROADAM_ERR_INVALID_ARG, "ranges must be in [1, 32]");
-  if (ranges > 1 && !h->aux) {
-    rc = check_device(h);
-    if (rc) return rc;
-    // events first, the stream last: a handle with `aux` set has them all
-    hipError_t e;
-    if (!h->aux_done && (e = hipEventCreateWithFlags(&h->aux_done, hipEventDisableTiming)) != hipSuccess)
-      return hip_fail(e, "hipEventCreate");
-    for (hipEvent_t& ev : h->range_done)
-      if (!ev && (e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess)
-        return hip_fail(e, "hipEventCreate");
-    // default priority, like every other stream of the library
-    if ((e = hipStreamCreateWithFlags(&h->aux, hipStreamNonBlocking)) != hipSuccess)
-      return hip_fail(e, "hipStreamCreate");
-  }
-  h->ranges = ranges;
   return MICROADAM_OK;
 }
 

@@ -71,15 +71,16 @@ struct StepParams {
 };
 
 // Steps with buckets spanning blocks: the per-block partials, their reduction
-// into the new bucket table, and the quantization of the residual with it.
+// into the new bucket table, and the quantization of the residual with it
+// (k_span.hip).
 hipError_t launch_select_partials(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream);
 hipError_t launch_bucket_reduce(const StepParams& p, hipStream_t stream);
 hipError_t launch_requant(const StepParams& p, int grad_bf16, int value_f32, hipStream_t stream);
 
-// Launchers (defined in microadam_kernels.hip).  Return hipSuccess or the
-// launch error.  Each takes the global blocks [first, first + count); the
-// update of a block must follow its select, and blocks share nothing, so a
-// step may run as several ranges, each range's update after its select.
+// Launchers (microadam_launch.hip dispatches to the kernel translation
+// units).  Return hipSuccess or the launch error.  Each takes the global
+// blocks [first, first + count); the update of a block must follow its
+// select, and blocks share nothing.
 hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
                          hipStream_t stream);
 hipError_t launch_update(const StepParams& p, int param_bf16, int value_f32, int64_t first, int64_t count,
@@ -90,5 +91,30 @@ hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_
 
 // Dynamic LDS bytes the kernels need (the larger of the two step kernels).
 size_t step_lds_bytes(int block, int k_full, int value_f32);
+
+// Per translation unit: the one-wave select for blocks of up to 4096
+// elements in each error-feedback format (k_select_{near,rand}{4,8}.hip),
+// the multi-wave select (k_select_large.hip), and the updates and moment
+// exports (k_update.hip, k_update_large.hip).
+hipError_t launch_select_near4(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                               hipStream_t stream);
+hipError_t launch_select_near8(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                               hipStream_t stream);
+hipError_t launch_select_rand4(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                               hipStream_t stream);
+hipError_t launch_select_rand8(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                               hipStream_t stream);
+hipError_t launch_select_large_blocks(const StepParams& p, int grad_bf16, int value_f32, int64_t first,
+                                      int64_t count, hipStream_t stream);
+hipError_t launch_update_blocks(const StepParams& p, int param_bf16, int value_f32, int64_t first, int64_t count,
+                                hipStream_t stream);
+hipError_t launch_update_large_blocks(const StepParams& p, int param_bf16, int value_f32, int64_t first,
+                                      int64_t count, hipStream_t stream);
+hipError_t launch_moments_blocks(const StepParams& p, int64_t first_block, int64_t num_blocks, float* mhat,
+                                 float* vhat, int value_f32, hipStream_t stream);
+hipError_t launch_moments_large_blocks(const StepParams& p, int64_t first_block, int64_t num_blocks, float* mhat,
+                                       float* vhat, int value_f32, hipStream_t stream);
+size_t update_lds_max(int nt);
+size_t update_large_lds();
 
 }  // namespace microadam

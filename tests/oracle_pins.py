@@ -23,6 +23,15 @@ What pins what:
     (1 - eta*lambda)*theta elsewhere (Algorithm 4).
   - bf16 rounding: torch's CPU float32 -> bfloat16 conversion (RNE), and a
     binary64 double-rounding case.
+  - bf16 parameters (Algorithm 1's update stored in bf16): the t = 1 closed
+    form rounded once from binary64 (round to odd into binary32, then torch's
+    RNE), including a value placed just off a bf16 midpoint so that a
+    rounding through binary32 gives the other neighbour.
+  - Buckets spanning Top-K blocks (Section 3.1 names buckets of 100K): the
+    buckets are each tensor's element ranges [c*B_q, (c+1)*B_q), whatever the
+    block size; after step 1 every bucket's (min, max) and codes are those of
+    the residual over that range (numpy), and the reconstruction and Lemma 1
+    norm bounds hold through several steps.
   - Randomized Q (Lemma 1): E[x_hat] = x, checked by averaging over xi on
     the midpoints of 256 equal cells of [0, 1) and, through whole steps, over
     300 seeds; every draw is one of the two grid points around x; the
@@ -48,6 +57,22 @@ def _bf16(x) -> np.ndarray:
     """float32 -> bf16 (round-half-to-even) by torch's CPU conversion."""
     t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
     return t.to(torch.bfloat16).to(torch.float32).numpy()
+
+
+def _bf16_from_f64(x) -> np.ndarray:
+    """binary64 -> bf16 with one rounding (half to even): round to odd into
+    binary32 (truncate toward zero, then set the last bit when inexact), then
+    torch's binary32 -> bf16 conversion.  Rounding to odd into a format with
+    at least two more bits than the target makes the second rounding the
+    correct one (Boldo and Melquiond, IEEE Trans. Computers 57(4), 2008).
+    (torch's own float64 -> bfloat16 goes through binary32 with two roundings
+    to nearest, which is what the pins must tell apart.)"""
+    x = np.asarray(x, np.float64)
+    f = x.astype(np.float32)
+    over = np.abs(f.astype(np.float64)) > np.abs(x)
+    f = np.where(over, np.nextafter(f, np.float32(0)), f).astype(np.float32)
+    inexact = (f.astype(np.float64) != x).astype(np.uint32)
+    return _bf16((f.view(np.uint32) | inexact).view(np.float32))
 
 
 def _brute_topk(x: np.ndarray, k: int) -> list[int]:
@@ -498,6 +523,150 @@ def check_weight_decay(o) -> None:
     assert not np.array_equal(theta[live], want[live])
 
 
+def check_first_step_closed_form_bf16(o) -> None:
+    """bf16 parameters: at t = 1, m-hat = V and v-hat = V^2, so every kept
+    entry moves to theta_0 - eta*V/(eps + |V|), rounded once from the exact
+    value to bf16; every other entry keeps its bits (lambda = 0)."""
+    # the helper itself on two double-rounding traps
+    assert _bf16_from_f64([1.0 + 2.0 ** -8 + 2.0 ** -40])[0] == 1.0 + 2.0 ** -7
+    assert _bf16_from_f64([1.0 - 2.0 ** -9 - 2.0 ** -35])[0] == 1.0 - 2.0 ** -8
+    rng = np.random.default_rng(27)
+    n, block = 2000, 256
+    cases = [
+        # random bf16 parameters and gradients, the eps of Appendix B
+        (_bf16(rng.standard_normal(n) * 0.02), (rng.standard_normal(n) * 1e-3).astype(np.float32),
+         1e-3, EPS),
+        # eps = 2^-100 (eps + |V| == |V| exactly for these V) and positive V:
+        # a kept entry moves by exactly eta, and eta = 2^-9 + 2^-35 puts
+        # 1 - eta just below the bf16 midpoint 1 - 2^-9, where one rounding
+        # gives 1 - 2^-8 and a rounding through binary32 (onto the midpoint,
+        # then to even) gives 1.0
+        (np.ones(n, np.float32), (np.abs(rng.standard_normal(n)) + 0.1).astype(np.float32),
+         2.0 ** -9 + 2.0 ** -35, 2.0 ** -100),
+    ]
+    for ci, (theta0, g, lr, eps) in enumerate(cases):
+        st = o.tensor(n, block=block, bucket=32, density=0.02, window=5, param_bf16=True, eps=eps)
+        theta = theta0.copy()
+        st.step(theta, g, 1, lr)
+        kept = np.zeros(n, bool)
+        want = theta0.astype(np.float64)
+        for q in range(st.nblocks):
+            idx, val = st.window_entries(0, q)
+            i = q * block + idx.astype(np.int64)
+            kept[i] = True
+            V = val.astype(np.float64)
+            want[i] = theta0[i].astype(np.float64) - lr * (V / (eps + np.abs(V)))
+        want = _bf16_from_f64(want)
+        assert np.array_equal(theta.view(np.uint32), want.view(np.uint32)), ci
+        assert np.array_equal(theta[~kept].view(np.uint32), theta0[~kept].view(np.uint32)), ci
+        if ci == 1:
+            assert np.all(theta[kept] == np.float32(1.0 - 2.0 ** -8))
+
+
+# (n, B_d, B_q) with buckets that are not inside blocks: larger than the
+# block and not a multiple of it, a multiple of it, and one bucket holding
+# the whole tensor
+SPANNING = [(1001, 64, 200), (640, 64, 192), (3000, 128, 1000), (300, 32, 100000)]
+
+
+def _check_bucket_codes(st, r, bucket, levels=15):
+    """delta/Delta of every bucket (tensor elements [c*B_q, (c+1)*B_q)) are
+    the min/max of the residual r there; min -> code 0, max -> the top code,
+    every element within half a step."""
+    codes = st.codes()
+    dec = _decode(codes, st.delta, st.Delta, bucket, levels).astype(np.float64)
+    assert st.nbuckets == -(-r.size // bucket)
+    for b in range(st.nbuckets):
+        x = r[b * bucket:(b + 1) * bucket]
+        lo, hi = np.float32(x.min()) + np.float32(0), np.float32(x.max()) + np.float32(0)
+        assert st.delta[b].view(np.uint32) == lo.view(np.uint32), b
+        assert st.Delta[b].view(np.uint32) == hi.view(np.uint32), b
+        c = codes[b * bucket:(b + 1) * bucket]
+        assert c[np.argmin(x)] == 0, b
+        if hi > lo:
+            assert c[np.argmax(x)] == levels, b
+        u = (float(hi) - float(lo)) / levels
+        slack = 4 * float(_ulp(max(abs(lo), abs(hi))))
+        assert np.all(np.abs(dec[b * bucket:(b + 1) * bucket] - x) <= u / 2 + slack), b
+
+
+def check_spanning_buckets_first_step(o) -> None:
+    """Buckets spanning blocks, step 1: e = Q(g with g[I] = 0) with each
+    tensor's buckets counted from its element 0."""
+    rng = np.random.default_rng(28)
+    for n, block, bucket in SPANNING:
+        g = rng.standard_normal(n).astype(np.float32)
+        st = o.tensor(n, block=block, bucket=bucket, density=0.05, window=3)
+        st.step(np.zeros(n, np.float32), g, 1, 1e-3)
+        r = g.copy()
+        for q in range(st.nblocks):
+            idx, _ = st.window_entries(0, q)
+            assert list(idx) == _brute_topk(g[q * block:(q + 1) * block], st.block_k(q))
+            r[q * block + idx.astype(np.int64)] = 0.0
+        _check_bucket_codes(st, r, bucket)
+
+
+def check_spanning_buckets_reconstruction(o) -> None:
+    """Buckets spanning blocks over five steps: each step's accumulator a_t
+    (decoded with the previous step's pairs) equals the next EF decoded with
+    the new pairs plus the kept entries, within half a step (plus the bf16
+    rounding of the kept values)."""
+    rng = np.random.default_rng(29)
+    for n, block, bucket in SPANNING:
+        st = o.tensor(n, block=block, bucket=bucket, density=0.05, window=3)
+        theta = np.zeros(n, np.float32)
+        for t in range(1, 6):
+            g = rng.standard_normal(n).astype(np.float32)
+            a = (g + _decode(st.codes(), st.delta, st.Delta, bucket)).astype(np.float32)
+            st.step(theta, g, t, 1e-3)
+            r = a.copy()
+            row = st.row_of_step(t)
+            extra = np.zeros(n)
+            for q in range(st.nblocks):
+                idx, val = st.window_entries(row, q)
+                i = q * block + idx.astype(np.int64)
+                assert list(idx) == _brute_topk(a[q * block:(q + 1) * block], st.block_k(q)), (n, t, q)
+                r[i] = 0.0
+                extra[i] = np.abs(val.astype(np.float64) - a[i]) + _ulp(a[i])
+            _check_bucket_codes(st, r, bucket)
+            rec = _decode(st.codes(), st.delta, st.Delta, bucket).astype(np.float64)
+            for q in range(st.nblocks):
+                idx, val = st.window_entries(row, q)
+                rec[q * block + idx.astype(np.int64)] += val
+            bidx = np.arange(n) // bucket
+            bound = (st.Delta[bidx].astype(np.float64) - st.delta[bidx]) / 15 / 2
+            bound += 4 * _ulp(np.maximum(np.abs(st.delta[bidx]), np.abs(st.Delta[bidx]))) + extra
+            assert np.all(np.abs(rec - a) <= bound), (n, t)
+
+
+def check_spanning_buckets_lemma1(o) -> None:
+    """Randomized rounding with buckets spanning blocks: every bucket of the
+    first step's error feedback meets Lemma 1's norm bound, and the decoded
+    EF averaged over seeds is the residual."""
+    rng = np.random.default_rng(30)
+    n, block, bucket, S = 700, 64, 200, 120
+    g = rng.standard_normal(n).astype(np.float32)
+    acc = np.zeros(n)
+    for seed in range(S):
+        st = o.tensor(n, block=block, bucket=bucket, density=0.05, window=2, rounding=1, seed=seed, tensor=1)
+        st.step(np.zeros(n, np.float32), g, 1, 1e-3)
+        dec = _decode(st.codes(), st.delta, st.Delta, bucket).astype(np.float64)
+        acc += dec
+        r = g.astype(np.float64).copy()
+        for q in range(st.nblocks):
+            idx, _ = st.window_entries(0, q)
+            r[q * block + idx.astype(np.int64)] = 0.0
+        for b0 in range(0, n, bucket):
+            x, xh = r[b0:b0 + bucket], dec[b0:b0 + bucket]
+            lo, hi = x.min(), x.max()
+            assert st.delta[b0 // bucket] == np.float32(lo) and st.Delta[b0 // bucket] == np.float32(hi)
+            bound = math.sqrt(x.size - 2) / 15 * (hi - lo) / math.sqrt(hi * hi + lo * lo)
+            assert np.linalg.norm(xh - x) <= bound * np.linalg.norm(x) * (1 + 1e-5), (seed, b0)
+    bidx = np.arange(n) // bucket
+    u = (st.Delta[bidx].astype(np.float64) - st.delta[bidx]) / 15
+    assert np.all(np.abs(acc / S - r) <= 6 * u / (2 * math.sqrt(S)) + 1e-6)
+
+
 ALL_CHECKS = [
     check_round_bf16,
     check_quantizer,
@@ -518,4 +687,8 @@ ALL_CHECKS = [
     check_randomized_quantizer,
     check_randomized_ef_unbiased,
     check_reconstruction_8bit,
+    check_first_step_closed_form_bf16,
+    check_spanning_buckets_first_step,
+    check_spanning_buckets_reconstruction,
+    check_spanning_buckets_lemma1,
 ]

@@ -112,6 +112,7 @@ BAD = [
     (dict(beta1=1.0), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(beta2=-0.1), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(eps=-1.0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(eps=0.0), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(lr=math.inf), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(weight_decay=-1.0), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(window=0), ma.MICROADAM_ERR_INVALID_ARG),
@@ -173,8 +174,7 @@ def test_null_handle_calls(lib):
     for f, args in [(ma.microadam_get_step, (0,)), (ma.microadam_set_step, (0, 1)),
                     (ma.microadam_tensor_layout, (0, 0)), (ma.microadam_debug_moments, (0, 0, 1, 1)),
                     (ma.microadam_step, (0, [1], [1])), (ma.microadam_set_profiling, (0, True)),
-                    (ma.microadam_kernel_times, (0,)), (ma.microadam_kernel_times_total, (0,)),
-                    (ma.microadam_set_ranges, (0, 4))]:
+                    (ma.microadam_kernel_times, (0,)), (ma.microadam_kernel_times_total, (0,))]:
         with pytest.raises(ma.MicroAdamError) as e:
             f(*args)
         assert e.value.code == ma.MICROADAM_ERR_INVALID_ARG

@@ -53,6 +53,13 @@ MUTANTS = [
      "float r = fy + (f > 0.0f ? 1.0f : 0.0f);"),
     ("randomized ignores the fraction", "(w24 + fr >= (1u << 24))", "(w24 >= (1u << 23))"),
     ("8-bit codes read as nibbles", "if (bits == 8) return ef[i];", "if (bits == 8) return ef[i] & 0x0F;"),
+    ("param_bf16 ignored", "theta[i] = c->param_bf16 ? round_to_bf16(nt) : (float)nt;", "theta[i] = (float)nt;"),
+    ("theta rounded through binary32", "theta[i] = c->param_bf16 ? round_to_bf16(nt) : (float)nt;",
+     "theta[i] = c->param_bf16 ? round_to_bf16((double)(float)nt) : (float)nt;"),
+    ("decode bucket relative to the block", "const int64_t b = i / c->bucket;",
+     "const int64_t b = (i / c->block) * ((c->block + c->bucket - 1) / c->bucket) + (i % c->block) / c->bucket;"),
+    ("buckets restart at each block", "int64_t b1 = b0 + c->bucket;",
+     "int64_t b1 = b0 + c->bucket; if ((b1 - 1) / c->block != b0 / c->block) b1 = (b0 / c->block + 1) * c->block;"),
 ]
 
 
