@@ -251,19 +251,19 @@ select_kernel(StepParams p, int64_t first) {
   }
   if (general) {
     // Exact bitwise search over every element (ties, large k, many
-    // candidates): the largest T with #{key >= T} >= k.  Keys are |a| as
-    // integers (bits & 0x7FFFFFFF), a total order that agrees with |a| on
-    // finite values and puts a NaN above infinity, so the counts below stay
-    // consistent for any input and exactly k entries are kept.
+    // candidates): the largest T with #{key >= T} >= k.  Keys are compared
+    // as |a| against the float with the same bits (the same order for
+    // finite values; the thresholds tried never exceed +inf's bits).
     uint32_t t = 0;
     bool exact = false;
     for (int bit = 30; bit >= 0 && !exact; --bit) {
       const uint32_t c = t | (1u << bit);
+      const float cf = __uint_as_float(c);
       uint32_t n = 0;
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) n += popc(ballot(key_of(a[v][e]) >= c));
+        for (int e = 0; e < 8; ++e) n += popc(ballot(__builtin_fabsf(a[v][e]) >= cf));
         __builtin_amdgcn_sched_barrier(0);  // bounds the masks in flight
       }
       if (n >= (uint32_t)kq) {
@@ -272,25 +272,25 @@ select_kernel(StepParams p, int64_t first) {
       }
     }
     T = t;
-    // kept: with an exact count key >= t; else key > t, and key == t for the
+    // kept: with an exact count |a| >= t; else |a| > t, and |a| == t for the
     // first `need` such elements in element order
     uint32_t sel_l = 0;
-    const uint32_t tv = (uint32_t)opaque_v((int)t);
     if (exact) {
       notie = true;
+      const float tf = opaque_f(__uint_as_float(t));
 #pragma unroll
       for (int v = 0; v < NV; ++v)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sel_l += key_of(a[v][e]) >= tv ? 1u : 0u;
+        for (int e = 0; e < 8; ++e) sel_l += __builtin_fabsf(a[v][e]) >= tf ? 1u : 0u;
     } else {
+      const float tf = opaque_f(__uint_as_float(t));
       uint32_t ngt_l = 0, neq_l = 0;
 #pragma unroll
       for (int v = 0; v < NV; ++v)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const uint32_t kk = key_of(a[v][e]);
-          ngt_l += kk > tv ? 1u : 0u;
-          neq_l += kk == tv ? 1u : 0u;
+          ngt_l += __builtin_fabsf(a[v][e]) > tf ? 1u : 0u;
+          neq_l += __builtin_fabsf(a[v][e]) == tf ? 1u : 0u;
         }
       uint32_t ngt = 0;
 #pragma unroll
@@ -304,42 +304,45 @@ select_kernel(StepParams p, int64_t first) {
       const bool mine = eq_pre < need && eq_pre + neq_l >= need;
       uint32_t my_last = 0;
       if (mine) {
+        const float tf2 = opaque_f(tf);
         uint32_t r = eq_pre;
 #pragma unroll
         for (int v = 0; v < NV; ++v)
 #pragma unroll
           for (int e = 0; e < 8; ++e)
-            if (key_of(a[v][e]) == tv) {
+            if (__builtin_fabsf(a[v][e]) == tf2) {
               if (r == need - 1) my_last = eb + 8 * v + e;
               ++r;
             }
       }
-      // (the counts are consistent, so exactly one lane has `mine`; the
-      // guard keeps the read defined regardless)
+      // With finite keys exactly one lane has `mine`.  A NaN reaches no
+      // threshold, so with fewer than k non-NaN keys none may have it: the
+      // guard keeps the read defined, and the stores below stay in the row.
       const uint64_t mm = ballot(mine);
       i_last = mm ? __builtin_amdgcn_readlane(my_last, (int)__builtin_ctzll(mm)) : 0u;
       const int last_here = (int)i_last - (int)eb;
+      const float tf3 = opaque_f(tf);
 #pragma unroll
       for (int v = 0; v < NV; ++v)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const uint32_t kk = key_of(a[v][e]);
-          sel_l += ((kk > tv) | ((kk == tv) & (8 * v + e <= last_here))) ? 1u : 0u;
+          const float ab = __builtin_fabsf(a[v][e]);
+          sel_l += ((ab > tf3) | ((ab == tf3) & (8 * v + e <= last_here))) ? 1u : 0u;
         }
     }
-    // the kept elements of this lane, stored in element order (positions
-    // past the row's k entries are never written)
+    // the kept elements of this lane, stored in element order
     uint32_t pos = 0;
 #pragma unroll
     for (int b2 = 0; b2 < 7; ++b2) pos += lanes_below(ballot((sel_l >> b2) & 1u)) << b2;
     if (sel_l) {
+      const float tf = opaque_f(__uint_as_float(t));
       const int last_here = notie ? (int)kWave * EPL : (int)i_last - (int)eb;
 #pragma unroll
       for (int v = 0; v < NV; ++v)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const uint32_t kk = key_of(a[v][e]);
-          if ((kk > tv) | ((kk == tv) & (8 * v + e <= last_here))) {
+          const float ab = __builtin_fabsf(a[v][e]);
+          if ((ab > tf) | ((ab == tf) & (8 * v + e <= last_here))) {
             if (pos < (uint32_t)kq) E::store(rw, row0 + pos, E::make(eb + 8 * v + e, a[v][e]));
             ++pos;
           }
