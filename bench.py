@@ -5,22 +5,24 @@ Default workload: the Llama-2-7B parameter list (291 tensors, 6,738,415,616
 bf16 parameters), bf16 gradients 1e-3 * Student-t(4), Top-K block 4096 at
 density 1% (k = 41), window m = 10, 4-bit EF with bucket 64, lr 1e-4.
 
-One step = one call of microadam_step over all 291 tensors: two kernel
-launches, select (EF decode, block Top-K, new window row, EF re-quantisation)
-then update (moment rebuild from the window, parameter update).  The W
-warm-up steps fill the window (W >= m gives steady state); the K timed steps
-run back to back, bracketed by device synchronisation.  Inputs are resident
-in HBM before timing starts: two gradient sets are generated up front and
-alternate between steps.
+One step = one call of microadam_step over all 291 tensors.  For this
+workload it is one fused kernel launch (EF decode, block Top-K, new window
+row, EF re-quantisation, moment rebuild from the window, parameter update);
+configurations outside the fused kernel's limits run a select and an update
+kernel.  The W warm-up steps fill the window (W >= m gives steady state); the
+K timed steps run back to back, bracketed by device synchronisation.  Inputs
+are resident in HBM before timing starts: two gradient sets are generated up
+front and alternate between steps.
 
-Prints one JSON line.  `roofline` describes the dominant (longer) kernel:
-`achieved` is its algorithmic HBM bytes per launch (select_bytes /
-update_bytes) over its mean duration, timed with HIP events that the library
-records on the launch stream around each kernel of the timed steps (read once
-after them).  `traffic` comes from the committed rocprofv3 FETCH_SIZE /
-WRITE_SIZE summary of that kernel when it was taken on the current kernel
-source, else null.  `cpu_baseline` times the
-CPU oracle on a sample of the same workload's blocks on this host.
+Prints one JSON line.  `roofline` describes the dominant (longest) kernel:
+`achieved` is its algorithmic HBM bytes per launch (fused_bytes, or
+select_bytes / update_bytes) over its mean duration, timed with HIP events
+that the library records on the launch stream around each kernel of the timed
+steps (read once after them).  `traffic` comes from the committed rocprofv3
+FETCH_SIZE / WRITE_SIZE summary of that kernel when it was taken on the
+current kernel source, else null.  `cpu_baseline` times the CPU oracle, as it
+stands, on this host's cores (one process per core, each on its own sample of
+the workload's blocks) and reports the single-core rate beside it.
 """
 from __future__ import annotations
 
@@ -119,8 +121,14 @@ def update_bytes(w, t: int) -> int:
     return total
 
 
-def step_bytes(w, t: int) -> int:
-    return select_bytes(w) + update_bytes(w, t)
+def fused_bytes(w, t: int, ef_bits: int = 4) -> int:
+    """Algorithmic HBM bytes of one fused step launch at step t: the select's
+    bytes and the update's, less the new row's read (it stays on chip)."""
+    total = select_bytes(w, ef_bits) + update_bytes(w, t)
+    for n in w.numels:
+        _, k_total = _blocks(w, n)
+        total -= 4 * k_total
+    return total
 
 
 def read_traffic(kernel: str, workload: str):
@@ -142,35 +150,73 @@ def read_traffic(kernel: str, workload: str):
         return None, "malformed traffic summary"
 
 
-def cpu_baseline(w, blocks: int, seed: int = 0) -> dict:
-    """The CPU oracle (single-threaded, as it stands) on `blocks` Top-K blocks
-    of the workload's shape, run for m + 2 steps; the last three steps (window
-    full) are timed."""
+def _oracle_worker(args) -> tuple:
+    """One CPU-baseline worker: the oracle, as it stands (single-threaded C),
+    on `blocks` Top-K blocks of the workload's shape run as one tensor for
+    m + 2 steps; returns (parameters, seconds) of the last three steps (window
+    full).  Blocks are independent, so the workers' blocks are a sample of the
+    workload's."""
+    wname, blocks, seed = args
     import numpy as np
-    import torch
     import oracle
+    from paper_2405_15593_amd import workloads as wl
+    w = wl.WORKLOADS[wname]
     o = oracle.default()
     n = blocks * w.block
     st = o.tensor(n, block=w.block, bucket=w.bucket, window=w.window, density=w.density,
-                  value_bf16=True, param_bf16=True)
+                  value_bf16=True, param_bf16=w.param_dtype.itemsize == 2)
     rng = np.random.default_rng(seed)
-    theta = (rng.standard_normal(n) * w.param_std).astype(np.float32)
-    theta = torch.from_numpy(theta).to(torch.bfloat16).float().numpy()
-    steps = w.window + 2
-    timed_steps = 3
-    timed = 0.0
+
+    def bf16(x):   # round to bf16 (nearest, ties to even) in numpy
+        b = x.astype(np.float32).view(np.uint32)
+        b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
+        return b.view(np.float32)
+
+    theta = bf16(rng.standard_normal(n) * w.param_std)
+    steps, timed_steps, timed = w.window + 2, 3, 0.0
     for t in range(1, steps + 1):
-        g = (rng.standard_t(4, n) * w.grad_scale).astype(np.float32)
-        g = torch.from_numpy(g).to(torch.bfloat16).float().numpy()
+        g = bf16(rng.standard_t(4, n) * w.grad_scale)
         t0 = time.perf_counter()
         st.step(theta, g, t, w.lr)
         dt = time.perf_counter() - t0
         if t > steps - timed_steps:
             timed += dt
-    rate = timed_steps * n / timed
-    return {"value": rate, "unit": "params/s", "cores": 1, "kind": "oracle",
-            "sample": (f"{blocks} blocks of {w.block} ({n} params) of the same shape, bf16, steps "
-                       f"{steps - timed_steps + 1}-{steps} (window full) timed: {timed:.2f} s")}
+    return timed_steps * n, timed
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, blocks_per_worker: int, workers: int) -> dict:
+    """The CPU oracle on this host's cores: one worker first alone (the
+    single-core rate), then `workers` at once in separate processes (started
+    fresh, so they share nothing with this GPU process), each on its own
+    blocks; the rate is all workers' parameters over the slowest worker's
+    time."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
+    ctx = mp.get_context("spawn")
+    with cf.ProcessPoolExecutor(max_workers=workers, mp_context=ctx) as ex:
+        n1, t1 = ex.submit(_oracle_worker, (w.name, blocks_per_worker, 1000)).result()
+        res = list(ex.map(_oracle_worker, [(w.name, blocks_per_worker, 1001 + i) for i in range(workers)]))
+    params = sum(r[0] for r in res)
+    wall = max(r[1] for r in res)
+    rate = params / wall
+    return {"value": rate, "unit": "params/s", "cores": workers, "kind": "oracle",
+            "single_core_value": n1 / t1, "nproc": os.cpu_count(), "cpu_model": cpu_model(),
+            "extrapolated": True,
+            "sample": (f"{workers} processes x {blocks_per_worker} blocks of {w.block} "
+                       f"({workers * blocks_per_worker * w.block} params, "
+                       f"{100.0 * workers * blocks_per_worker * w.block / w.d:.2f}% of the workload) of the same "
+                       f"shape, bf16, steps {w.window}-{w.window + 2} (window full) timed; "
+                       f"the slowest worker took {wall:.2f} s; one full step extrapolated: {w.d / rate:.1f} s")}
 
 
 def main() -> int:
@@ -179,12 +225,17 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama2_7b_bf16")
-    ap.add_argument("--cpu-blocks", type=int, default=10000, help="0 disables the CPU baseline")
+    ap.add_argument("--cpu-blocks", type=int, default=1000,
+                    help="Top-K blocks per CPU-baseline worker (0 disables the CPU baseline)")
+    ap.add_argument("--cpu-workers", type=int, default=0,
+                    help="CPU-baseline processes (0: the cores this process may use, at most 16)")
     ap.add_argument("--ef-bits", type=int, default=4, choices=(4, 8), help="bits per EF code")
     ap.add_argument("--ef-rounding", default="nearest", choices=("nearest", "randomized"),
                     help="EF quantizer rounding (randomized: Lemma 1)")
     ap.add_argument("--ef-bucket", type=int, default=0,
                     help="EF bucket size (0: the workload's; >= topk_block: buckets spanning blocks)")
+    ap.add_argument("--fused", type=int, default=0, choices=(0, 1),
+                    help="1: run each step as the one fused kernel where the configuration allows")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 4 GiB device-to-device copy three times (the known-size "
                          "kernel that scales rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
@@ -221,7 +272,7 @@ def main() -> int:
     bucket = args.ef_bucket or w.bucket
     rounding = ma.MICROADAM_ROUND_RANDOMIZED if args.ef_rounding == "randomized" else ma.MICROADAM_ROUND_NEAREST
     cfg = ma.make_config(density=w.density, window=w.window, ef_bucket=bucket, topk_block=w.block, lr=w.lr,
-                         ef_bits=args.ef_bits, ef_rounding=rounding, seed=1234)
+                         ef_bits=args.ef_bits, ef_rounding=rounding, seed=1234, fused=args.fused)
     opt = ma.MicroAdam(params, cfg)
 
     for i in range(args.warmup):
@@ -241,25 +292,32 @@ def main() -> int:
     # after them (no synchronization between steps)
     sel_tot, upd_tot, n_timed = opt.kernel_times_total()
     assert n_timed == args.steps, (n_timed, args.steps)
-    sel_ms = sel_tot / n_timed
-    upd_ms = upd_tot / n_timed
-    sel_b = select_bytes(w, args.ef_bits, bucket)
-    upd_b = sum(update_bytes(w, t) for t in range(t_first, t_first + args.steps)) / args.steps
-    kernels = {
-        "select_kernel": {"ms": sel_ms, "bytes": sel_b, "gbs": sel_b / sel_ms / 1e6},
-        "update_kernel": {"ms": upd_ms, "bytes": upd_b, "gbs": upd_b / upd_ms / 1e6},
-    }
+    steps_t = range(t_first, t_first + args.steps)
+    if opt.step_kernels == 1:
+        ms = sel_tot / n_timed
+        b = sum(fused_bytes(w, t, args.ef_bits) for t in steps_t) / args.steps
+        kernels = {"step_kernel": {"ms": ms, "bytes": b, "gbs": b / ms / 1e6}}
+    else:
+        sel_ms, upd_ms = sel_tot / n_timed, upd_tot / n_timed
+        sel_b = select_bytes(w, args.ef_bits, bucket)
+        upd_b = sum(update_bytes(w, t) for t in steps_t) / args.steps
+        kernels = {
+            "select_kernel": {"ms": sel_ms, "bytes": sel_b, "gbs": sel_b / sel_ms / 1e6},
+            "update_kernel": {"ms": upd_ms, "bytes": upd_b, "gbs": upd_b / upd_ms / 1e6},
+        }
     dominant = max(kernels, key=lambda k: kernels[k]["ms"])
     dk = kernels[dominant]
     default_ef = args.ef_bits == 4 and args.ef_rounding == "nearest" and bucket == w.bucket
     traffic, traffic_note = read_traffic(dominant, w.name) if default_ef else (None, "counters taken with the default EF")
-    print(f"[bench] mean kernel ms per step (select, update) over {n_timed} steps: "
-          f"{round(sel_ms, 3), round(upd_ms, 3)}", file=sys.stderr, flush=True)
+    print(f"[bench] mean kernel ms per step over {n_timed} steps: "
+          f"{ {k: round(v['ms'], 3) for k, v in kernels.items()} }", file=sys.stderr, flush=True)
 
     cpu = None
     if args.cpu_blocks > 0:
-        print(f"[bench] CPU oracle baseline on {args.cpu_blocks} blocks", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, args.cpu_blocks)
+        workers = args.cpu_workers or min(16, len(os.sched_getaffinity(0)))
+        print(f"[bench] CPU oracle baseline: {workers} processes x {args.cpu_blocks} blocks", file=sys.stderr,
+              flush=True)
+        cpu = cpu_baseline(w, args.cpu_blocks, workers)
 
     ms_per_step = wall / args.steps * 1e3
     out = {
@@ -286,7 +344,8 @@ def main() -> int:
             "window_full": t_first > w.window,
         },
         "kernels": kernels,
-        "step_hbm_gbs": (sel_b + upd_b) / (sel_ms + upd_ms) / 1e6,
+        "step_kernels": opt.step_kernels,
+        "step_hbm_gbs": sum(k["bytes"] for k in kernels.values()) / sum(k["ms"] for k in kernels.values()) / 1e6,
         "roofline": {
             "bound": "hbm",
             "kernel": dominant,

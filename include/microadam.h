@@ -93,6 +93,13 @@ enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
  *   window_value_dtype  MICROADAM_BF16 (the paper's choice, Section 3.2) or
  *                MICROADAM_F32 (lossless window values, for checking the
  *                moment rebuild).
+ *   fused        0: every step runs a select kernel (EF decode, block Top-K,
+ *                new row, re-quantization) and then an update kernel (moment
+ *                rebuild, parameter update), the faster form on MI355X; 1:
+ *                where the configuration allows (see microadam_step_kernels),
+ *                all of a step in one fused kernel, one workgroup per block.
+ *                Both give the same results.
+ *   reserved     0.
  */
 /* Rounding of the error-feedback quantizer. */
 enum { MICROADAM_ROUND_NEAREST = 0, MICROADAM_ROUND_RANDOMIZED = 1 };
@@ -111,6 +118,8 @@ typedef struct microadam_config {
   int32_t window_value_dtype;
   int32_t ef_rounding;
   uint64_t seed;
+  int32_t fused;
+  int32_t reserved;
 } microadam_config;
 
 typedef struct microadam_handle_s* microadam_handle;
@@ -200,7 +209,7 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels,
 
 /*
  * One MicroAdam step (Algorithm 1 with the decay of Algorithm 4) over all
- * tensors, as one kernel launch on `stream`.  params[j] (updated in place)
+ * tensors, queued on `stream` (microadam_step_kernels launches).  params[j] (updated in place)
  * and grads[j] (read only) are device pointers to numels[j] contiguous
  * elements of the init dtypes, 16-byte aligned.  lr: the step size eta for
  * this step, or NaN to use cfg.lr.  The step counter t advances by one.
@@ -234,8 +243,18 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat,
                             float* vhat, void* stream);
 
 /*
+ * Kernel launches per microadam_step (fixed at init), or a negative error
+ * code: 1 where the step runs as one fused kernel (cfg.fused = 1, Top-K
+ * blocks of 2049 to 4096 elements, at most 128 entries per row, m *
+ * ceil(k/64) <= 16, parameters and gradients of one dtype, buckets inside
+ * blocks); 2 (select, then update) otherwise; 4 with buckets spanning blocks
+ * (select, bucket reduction, quantization, update).
+ */
+int microadam_step_kernels(microadam_handle h);
+
+/*
  * Profiling.  With profiling on (off after init), every microadam_step
- * records HIP events on its stream around its two kernels.  Events are
+ * records HIP events on its stream around its kernels.  Events are
  * created on the first call that turns profiling on, with the init device
  * current.  Every call that turns it on starts a new total for
  * microadam_kernel_times_total.
@@ -246,7 +265,8 @@ int microadam_set_profiling(microadam_handle h, int32_t on);
  * Durations in milliseconds of the kernels of the last step, which must have
  * been taken with profiling on: out_ms[0] = select (EF decode, block Top-K,
  * new window row, EF re-quantisation), out_ms[1] = update (moment rebuild
- * from the window and parameter update).  Blocks until that step is done.
+ * from the window and parameter update); for a fused step (see
+ * microadam_step_kernels) out_ms[0] is the fused kernel and out_ms[1] is 0.  Blocks until that step is done.
  * out_ms: 2 host floats.
  */
 int microadam_kernel_times(microadam_handle h, float* out_ms);

@@ -47,6 +47,8 @@ class microadam_config(ctypes.Structure):
         ("window_value_dtype", ctypes.c_int32),
         ("ef_rounding", ctypes.c_int32),
         ("seed", ctypes.c_uint64),
+        ("fused", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
 
@@ -79,7 +81,7 @@ class microadam_layout(ctypes.Structure):
 EXPORTS = (
     "microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
     "microadam_get_step", "microadam_set_step", "microadam_tensor_layout",
-    "microadam_debug_moments", "microadam_set_profiling", "microadam_kernel_times",
+    "microadam_debug_moments", "microadam_step_kernels", "microadam_set_profiling", "microadam_kernel_times",
     "microadam_kernel_times_total", "microadam_error_string",
     "microadam_last_error",
 )
@@ -113,6 +115,7 @@ def load(path: str = LIBRARY):
     lib.microadam_set_step.argtypes = [vp, i64]
     lib.microadam_tensor_layout.argtypes = [vp, i32, P(microadam_layout)]
     lib.microadam_debug_moments.argtypes = [vp, i32, vp, vp, vp]
+    lib.microadam_step_kernels.argtypes = [vp]
     lib.microadam_set_profiling.argtypes = [vp, i32]
     lib.microadam_kernel_times.argtypes = [vp, P(ctypes.c_float)]
     lib.microadam_kernel_times_total.argtypes = [vp, P(ctypes.c_float), P(i64)]
@@ -122,7 +125,8 @@ def load(path: str = LIBRARY):
     lib.microadam_last_error.restype = ctypes.c_char_p
     for f in ("microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
               "microadam_set_step", "microadam_tensor_layout", "microadam_debug_moments",
-              "microadam_set_profiling", "microadam_kernel_times", "microadam_kernel_times_total"):
+              "microadam_step_kernels", "microadam_set_profiling", "microadam_kernel_times",
+              "microadam_kernel_times_total"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -138,10 +142,10 @@ def _check(rc: int, where: str) -> None:
 def make_config(density=0.01, beta1=0.9, beta2=0.999, eps=1e-8, lr=1e-4, weight_decay=0.0,
                 window=10, ef_bits=4, ef_bucket=64, topk_block=4096,
                 window_value_dtype=MICROADAM_BF16, ef_rounding=MICROADAM_ROUND_NEAREST,
-                seed=0) -> microadam_config:
+                seed=0, fused=0) -> microadam_config:
     """A microadam_config; defaults are the paper's fine-tuning settings."""
     return microadam_config(density, beta1, beta2, eps, lr, weight_decay, window, ef_bits,
-                            ef_bucket, topk_block, window_value_dtype, ef_rounding, seed)
+                            ef_bucket, topk_block, window_value_dtype, ef_rounding, seed, int(fused), 0)
 
 
 def _i64_array(xs: Sequence[int]):
@@ -202,6 +206,13 @@ def microadam_debug_moments(h: int, tensor: int, mhat_ptr: int, vhat_ptr: int, s
     _check(load().microadam_debug_moments(ctypes.c_void_p(h), tensor, ctypes.c_void_p(mhat_ptr),
                                           ctypes.c_void_p(vhat_ptr), ctypes.c_void_p(stream)),
            "microadam_debug_moments")
+
+
+def microadam_step_kernels(h: int) -> int:
+    n = load().microadam_step_kernels(ctypes.c_void_p(h))
+    if n < 0:
+        _check(n, "microadam_step_kernels")
+    return int(n)
 
 
 def microadam_set_profiling(h: int, on: bool) -> None:
@@ -326,6 +337,11 @@ class MicroAdam:
         v = torch.empty(n, dtype=torch.float32, device=self.device)
         microadam_debug_moments(self.handle, j, m.data_ptr(), v.data_ptr(), self._stream())
         return m, v
+
+    @property
+    def step_kernels(self) -> int:
+        """Kernel launches per step: 1 (fused), 2 (select, update) or 4."""
+        return microadam_step_kernels(self.handle)
 
     def set_profiling(self, on: bool = True) -> None:
         microadam_set_profiling(self.handle, on)

@@ -41,7 +41,7 @@ struct LargeLds {
 };
 
 template <int NW, bool LB, bool GBF16, bool VF32>
-__global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, int64_t first) {
+__global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, int64_t first, int64_t count) {
   constexpr int EPL = 64, NV = 8, NT = NW * kWave, CAP = NT * EPL, R = kCandPerThread, NC = NT * R;
   constexpr int SPT = kSamples / NT, SPL = kSamples / kWave;  // samples per thread; per lane
   constexpr int DPW = 16 / NW;                                  // sample digits per wave
@@ -59,7 +59,7 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
   const uint32_t eb = (uint32_t)tid * EPL;
   const int bl = p.bucket_log2;
-  const int64_t gb = first + block_id();
+  const int64_t gb = first + xcd_block(block_id(), count);
 
   const uint32_t nbk = (uint32_t)(p.block >> bl);
   const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * (p.block >> 1), (uint32_t)(p.block >> 1));
@@ -496,10 +496,10 @@ hipError_t launch_select_large_t(const StepParams& p, int64_t first, int64_t cou
   const size_t lds = LargeLds<NW>::words() * 4;
   if ((1 << p.bucket_log2) >= 64)
     hipLaunchKernelGGL((select_large_kernel<NW, true, GB, VF>), dim3((uint32_t)count), dim3(NW * kWave), lds, stream,
-                       p, first);
+                       p, first, count);
   else
     hipLaunchKernelGGL((select_large_kernel<NW, false, GB, VF>), dim3((uint32_t)count), dim3(NW * kWave), lds,
-                       stream, p, first);
+                       stream, p, first, count);
   return hipGetLastError();
 }
 

@@ -47,7 +47,7 @@ __global__ void __launch_bounds__(256) bucket_reduce_kernel(StepParams p) {
 // block, 64 elements per lane.
 template <bool GBF16, bool VF32, int EFM>
 __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
-requant_kernel(StepParams p, int64_t first) {
+requant_kernel(StepParams p, int64_t first, int64_t count) {
   constexpr int EPL = 64, NV = EPL / 8, CAP = kWave * EPL;
   constexpr int CW = (EFM & kEf8) ? 2 : 1;
   using E = Entry<VF32>;
@@ -55,7 +55,7 @@ requant_kernel(StepParams p, int64_t first) {
 
   const int lane = thread_id();
   const uint32_t eb = (uint32_t)lane * EPL;
-  const int64_t gb = first + block_id();
+  const int64_t gb = first + xcd_block(block_id(), count);
   const uint32_t ef_bytes = (EFM & kEf8) ? (uint32_t)p.block : (uint32_t)(p.block >> 1);
   const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * ef_bytes, ef_bytes);
   const bool wide = p.block == CAP;
@@ -126,7 +126,7 @@ template <bool GB, bool VF, int EF8>
 hipError_t launch_select_partials_t(const StepParams& p, hipStream_t stream) {
   const size_t lds = select_lds_words() * 4;
   hipLaunchKernelGGL((select_kernel<64, true, GB, VF, EF8, true>), dim3((uint32_t)p.total_blocks), dim3(kWave), lds,
-                     stream, p, (int64_t)0);
+                     stream, p, (int64_t)0, p.total_blocks);
   return hipGetLastError();
 }
 
@@ -139,7 +139,7 @@ hipError_t launch_select_partials_d(const StepParams& p, hipStream_t stream) {
 template <bool GB, bool VF, int EFM>
 hipError_t launch_requant_t(const StepParams& p, hipStream_t stream) {
   hipLaunchKernelGGL((requant_kernel<GB, VF, EFM>), dim3((uint32_t)p.total_blocks), dim3(kWave), 0, stream, p,
-                     (int64_t)0);
+                     (int64_t)0, p.total_blocks);
   return hipGetLastError();
 }
 

@@ -61,7 +61,7 @@ constexpr int update_waves_per_eu() {
 
 template <int NT, bool PBF16, bool VF32, bool EXPORT, int KC, bool ONE>
 __global__ void __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(update_waves_per_eu<NT, VF32, KC, ONE>())))
-update_kernel(StepParams p, int64_t first_block, float* mhat, float* vhat) {
+update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, float* vhat) {
   static_assert(!ONE || !EXPORT, "one accumulator: parameter update only");
   constexpr int NW = NT / kWave;
   constexpr int CAP = NT * kLaneElems;
@@ -80,7 +80,7 @@ update_kernel(StepParams p, int64_t first_block, float* mhat, float* vhat) {
   // oldest live row first: the row written at step s is slot (s-1) mod m
   const int slot0 = (p.new_slot + 1 + m - n_live) % m;
 
-  const Span u = span_of(p, (int32_t)(first_block + block_id()), PBF16 ? 2 : 4);
+  const Span u = span_of(p, (int32_t)(first_block + xcd_block(block_id(), count)), PBF16 ? 2 : 4);
   const int s = u.s, kq = u.kq;
   const int leader = u.gb & (NW - 1);
   const int R = (kq + kWave - 1) / kWave;
@@ -302,7 +302,7 @@ hipError_t launch_update_k(const StepParams& p, int64_t first, int64_t count, hi
   if (count <= 0) return hipSuccess;
   const size_t lds = update_lds_bytes<NT, VF, KC, ONE>();
   hipLaunchKernelGGL((update_kernel<NT, PB, VF, false, KC, ONE>), dim3((uint32_t)count), dim3(NT), lds, stream, p,
-                     first, (float*)nullptr, (float*)nullptr);
+                     first, count, (float*)nullptr, (float*)nullptr);
   return hipGetLastError();
 }
 
@@ -328,7 +328,7 @@ hipError_t launch_export(const StepParams& p, int64_t first_block, int64_t block
   if (blocks <= 0) return hipSuccess;
   const size_t lds = update_lds_bytes<NT, VF, 16, false>();
   hipLaunchKernelGGL((update_kernel<NT, false, VF, true, 16, false>), dim3((uint32_t)blocks), dim3(NT), lds, stream,
-                     p, first_block, mh, vh);
+                     p, first_block, blocks, mh, vh);
   return hipGetLastError();
 }
 

@@ -30,7 +30,7 @@ constexpr size_t update_large_lds_bytes() {
 }
 
 template <bool PBF16, bool VF32, bool EXPORT>
-__global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t first_block, int32_t nsub,
+__global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t first_block, int64_t count, int32_t nsub,
                                                            float* mhat, float* vhat) {
   constexpr int NT = 256, STAGE = stage_large<VF32>();
   using E = Entry<VF32>;
@@ -45,7 +45,7 @@ __global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t
   ET* const stage = (ET*)(misc + 4);       // [STAGE]
 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
-  const int64_t wg = block_id();
+  const int64_t wg = xcd_block(block_id(), count * nsub);
   const int32_t gb = (int32_t)(first_block + wg / nsub);
   const int j = (int)(wg % nsub);
   const Span g = span_of(p, gb, PBF16 ? 2 : 4);
@@ -229,7 +229,7 @@ hipError_t launch_update_large(const StepParams& p, int64_t first, int64_t count
   if (count <= 0) return hipSuccess;
   const int32_t nsub = (p.block + kSubBlock - 1) / kSubBlock;
   hipLaunchKernelGGL((update_large_kernel<PB, VF, EXPORT>), dim3((uint32_t)(count * nsub)), dim3(256),
-                     update_large_lds_bytes<VF>(), stream, p, first, nsub, mh, vh);
+                     update_large_lds_bytes<VF>(), stream, p, first, count, nsub, mh, vh);
   return hipGetLastError();
 }
 

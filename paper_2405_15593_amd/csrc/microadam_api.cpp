@@ -88,6 +88,8 @@ int validate_config(const microadam_config* c) {
     return fail(MICROADAM_ERR_INVALID_ARG, "window_value_dtype must be BF16 or F32");
   if (c->ef_rounding != MICROADAM_ROUND_NEAREST && c->ef_rounding != MICROADAM_ROUND_RANDOMIZED)
     return fail(MICROADAM_ERR_INVALID_ARG, "ef_rounding must be NEAREST or RANDOMIZED");
+  if (c->fused != 0 && c->fused != 1) return fail(MICROADAM_ERR_INVALID_ARG, "fused must be 0 or 1");
+  if (c->reserved != 0) return fail(MICROADAM_ERR_INVALID_ARG, "reserved must be 0");
   if ((c->ef_bits != 4 || c->ef_rounding != MICROADAM_ROUND_NEAREST) && c->topk_block > 4096)
     return fail(MICROADAM_ERR_UNSUPPORTED, "8-bit or randomized error feedback needs topk_block <= 4096");
   return MICROADAM_OK;
@@ -195,6 +197,7 @@ struct microadam_handle_s {
   Planes planes;
   int32_t param_bf16 = 0, grad_bf16 = 0, value_f32 = 0;
   int32_t bucket_log2 = 0;
+  bool fused = false;                 // steps run as the one fused kernel
   uint8_t* state = nullptr;
   uint64_t state_bytes = 0;
   int64_t t = 0;
@@ -388,6 +391,16 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
     release(h);
     return fail(MICROADAM_ERR_UNSUPPORTED, "k per block too large for the LDS budget");
   }
+  {
+    // one fused kernel per step when asked for and where a block fits one
+    // 256-thread workgroup and its new row and live rows fit the kernel's
+    // LDS; else a select and an update kernel (or four launches with buckets
+    // spanning blocks)
+    const int32_t kf = h->plans[0].k_full;
+    const int32_t parts = (kf + 63) / 64;
+    h->fused = cfg->fused == 1 && !pl.big && cfg->topk_block > 2048 && cfg->topk_block <= 4096 && kf <= microadam::kFusedMaxK &&
+               cfg->window * parts <= microadam::kFusedMaxChunks && h->param_bf16 == h->grad_bf16;
+  }
 
   hipError_t e = hipGetDevice(&h->device);
   if (e != hipSuccess) { release(h); return hip_fail(e, "hipGetDevice"); }
@@ -511,7 +524,10 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
   if (prof && (e = fold_slot(h, pslot)) != hipSuccess) return hip_fail(e, "reading the kernel timers");
   auto rec = [&](int i) { return prof ? hipEventRecord(h->ev[pslot][i], s) : hipSuccess; };
   if ((e = rec(0)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  if (h->planes.big) {
+  if (h->fused) {
+    e = microadam::launch_step(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the step kernel");
+  } else if (h->planes.big) {
     // select with per-block partials, the bucket reduction, the quantization
     // of the residual
     e = microadam::launch_select_partials(p, h->grad_bf16, h->value_f32, s);
@@ -525,8 +541,10 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
     if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
   }
   if ((e = rec(1)) != hipSuccess || (e = rec(2)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  e = microadam::launch_update(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
-  if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
+  if (!h->fused) {
+    e = microadam::launch_update(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
+  }
   if ((e = rec(3)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   h->timed = prof;
   if (prof) {
@@ -604,6 +622,12 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat, flo
     e = microadam::launch_moments(p, tp.last_block, 1, mhat, vhat, h->value_f32, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "launching the moment kernel");
   return MICROADAM_OK;
+}
+
+int microadam_step_kernels(microadam_handle h) {
+  int rc = check_handle(h);
+  if (rc) return rc;
+  return h->fused ? 1 : h->planes.big ? 4 : 2;
 }
 
 int microadam_set_profiling(microadam_handle h, int32_t on) {

@@ -63,6 +63,20 @@ __device__ __forceinline__ float opaque_f(float x) {
 __device__ __forceinline__ int thread_id() { return (int)__builtin_amdgcn_workitem_id_x(); }
 __device__ __forceinline__ int64_t block_id() { return (int64_t)__builtin_amdgcn_workgroup_id_x(); }
 
+// Block handled by workgroup w of a launch over n blocks.  Workgroups are
+// dispatched to the eight XCDs (each with its own L2) in turn, so XCD x runs
+// w = x, x + 8, x + 16, ...; this gives each XCD one contiguous range of
+// blocks instead (a bijection of [0, n)): neighbouring blocks, whose state
+// records may share cache lines, then meet in the same L2.
+#ifndef MICROADAM_XCD_MAP
+#define MICROADAM_XCD_MAP 1
+#endif
+__device__ __forceinline__ int64_t xcd_block(int64_t w, int64_t n) {
+  if (!MICROADAM_XCD_MAP) return w;
+  const int64_t x = w & 7, j = w >> 3, q = n >> 3, r = n & 7;
+  return x * q + (x < r ? x : r) + j;
+}
+
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float x) {
   return __builtin_bit_cast(

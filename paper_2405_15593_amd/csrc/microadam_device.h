@@ -117,4 +117,22 @@ hipError_t launch_moments_large_blocks(const StepParams& p, int64_t first_block,
 size_t update_lds_max(int nt);
 size_t update_large_lds();
 
+// The fused step (step_kernel.h, k_step_{near,rand}{4,8}.hip): every stage of
+// a block in one workgroup, for blocks of 2049 to 4096 elements with at most
+// kFusedMaxK entries per row, live rows of at most kFusedMaxChunks chunks of
+// 64 entries, and parameters and gradients of one dtype (`bf16`).
+constexpr int kFusedMaxK = 128;
+constexpr int kFusedMaxChunks = 16;
+hipError_t launch_step(const StepParams& p, int bf16, int value_f32, int64_t first, int64_t count,
+                       hipStream_t stream);
+hipError_t launch_step_near4(const StepParams& p, int bf16, int value_f32, int64_t first, int64_t count,
+                             hipStream_t stream);
+hipError_t launch_step_near8(const StepParams& p, int bf16, int value_f32, int64_t first, int64_t count,
+                             hipStream_t stream);
+hipError_t launch_step_rand4(const StepParams& p, int bf16, int value_f32, int64_t first, int64_t count,
+                             hipStream_t stream);
+hipError_t launch_step_rand8(const StepParams& p, int bf16, int value_f32, int64_t first, int64_t count,
+                             hipStream_t stream);
+size_t fused_lds_bytes(int value_f32);
+
 }  // namespace microadam

@@ -1,6 +1,6 @@
 // Host-side dispatch of a step's launches to the kernel translation units by
 // block size and error-feedback format.
-#include "microadam_common.h"
+#include "step_kernel.h"
 
 namespace microadam {
 
@@ -27,6 +27,22 @@ hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, int6
     case 1: return launch_select_near8(p, grad_bf16, value_f32, first, count, stream);
     case 2: return launch_select_rand4(p, grad_bf16, value_f32, first, count, stream);
     case 3: return launch_select_rand8(p, grad_bf16, value_f32, first, count, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+size_t fused_lds_bytes(int value_f32) {
+  return (value_f32 ? step_kernel_lds_words<true>() : step_kernel_lds_words<false>()) * 4;
+}
+
+hipError_t launch_step(const StepParams& p, int bf16, int value_f32, int64_t first, int64_t count,
+                       hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  switch (p.ef_mode) {
+    case 0: return launch_step_near4(p, bf16, value_f32, first, count, stream);
+    case 1: return launch_step_near8(p, bf16, value_f32, first, count, stream);
+    case 2: return launch_step_rand4(p, bf16, value_f32, first, count, stream);
+    case 3: return launch_step_rand8(p, bf16, value_f32, first, count, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -10,7 +10,7 @@ namespace {
 
 template <int EPL, bool LB, bool GBF16, bool VF32, int EFM, bool LQ = false>
 __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
-select_kernel(StepParams p, int64_t first) {
+select_kernel(StepParams p, int64_t first, int64_t count) {
   static_assert(!LQ || (EPL == 64 && LB && (EFM & kEfRandom) == 0), "buckets spanning blocks: 64 per lane");
   constexpr int NV = EPL / 8;
   constexpr int CAP = kWave * EPL;
@@ -25,7 +25,7 @@ select_kernel(StepParams p, int64_t first) {
   const int lane = thread_id();
   const uint32_t eb = (uint32_t)lane * EPL;  // first element of this lane
   const int bl = p.bucket_log2;
-  const int64_t gb = first + block_id();
+  const int64_t gb = first + xcd_block(block_id(), count);
 
   // The block's EF codes and bucket pairs are addressed by gb alone, so their
   // loads go out before the tensor lookup that the gradient needs.
@@ -365,7 +365,7 @@ hipError_t launch_select_t(const StepParams& p, int64_t first, int64_t count, hi
   if (count <= 0) return hipSuccess;
   const size_t lds = select_lds_words() * 4;
   hipLaunchKernelGGL((select_kernel<EPL, LB, GB, VF, EFM>), dim3((uint32_t)count), dim3(kWave), lds, stream, p,
-                     first);
+                     first, count);
   return hipGetLastError();
 }
 

@@ -59,7 +59,7 @@ class GpuOracleRun:
                  grad_dist="normal", grad_scale=1.0, lr=1e-3, seed=0, sample=None,
                  density=0.01, window=10, bucket=64, block=4096, value_f32=False,
                  beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, ef_bits=4,
-                 ef_rounding=0, ef_seed=0, degenerate=False, device="cuda"):
+                 ef_rounding=0, ef_seed=0, degenerate=False, fused=0, device="cuda"):
         self.numels = list(numels)
         self.lr = lr
         self.device = torch.device(device)
@@ -69,6 +69,7 @@ class GpuOracleRun:
         self.cfg = ma.make_config(density=density, beta1=beta1, beta2=beta2, eps=eps, lr=lr,
                                   weight_decay=weight_decay, window=window, ef_bucket=bucket,
                                   topk_block=block, ef_bits=ef_bits, ef_rounding=ef_rounding, seed=ef_seed,
+                                  fused=fused,
                                   window_value_dtype=ma.MICROADAM_F32 if value_f32 else ma.MICROADAM_BF16)
         self.ef_bits = ef_bits
         self.degenerate = degenerate  # inputs whose codes, rows or updates may all be zero

@@ -113,6 +113,7 @@ BAD = [
     (dict(beta2=-0.1), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(eps=-1.0), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(eps=0.0), ma.MICROADAM_ERR_INVALID_ARG),
+    (dict(fused=2), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(lr=math.inf), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(weight_decay=-1.0), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(window=0), ma.MICROADAM_ERR_INVALID_ARG),

@@ -120,17 +120,41 @@ CASES = {
                                         density=0.02, ef_bits=8, ef_rounding=1, ef_seed=5), 5),
     "big_bucket_equals_block": (dict(numels=[4096 * 5 + 17, 900], bucket=4096, window=2,
                                      grad_dist="student_t4"), 4),
+    # the fused step kernel (blocks of 2049 to 4096 elements, k <= 128,
+    # m * ceil(k/64) <= 16, one dtype): its cooperative exact search on tie
+    # groups at the threshold (k = 123) and on +-1 signs, the largest
+    # staging (window 8 with k = 128: 16 chunks), 8-bit and randomized codes,
+    # buckets of 8 (two per thread) and 16, and blocks of 3008 elements
+    "fused_ties_k123": (dict(numels=[4096 * 3 + 200], grad_dist="student_t2_snapped64", grad_scale=1e-3,
+                             param_dtype=bf16, grad_dtype=bf16, density=0.03, window=5), 6),
+    "fused_signs": (dict(numels=[4096 * 2 + 1000], grad_dist="signs", grad_scale=1e-2, window=3,
+                         degenerate=True), 4),
+    "fused_k128_window8": (dict(numels=[4096 * 2 + 3000], density=0.03125, window=8, param_dtype=bf16,
+                                grad_dtype=bf16, grad_scale=1e-3), 10),
+    "fused_randomized_8bit": (dict(numels=[4096 * 3 + 100, 5000], grad_dist="student_t4", window=3, ef_bits=8,
+                                   ef_rounding=1, ef_seed=77), 5),
+    "fused_bucket8": (dict(numels=[4096 * 2 + 40], bucket=8, window=3, param_dtype=bf16, grad_dtype=bf16,
+                           grad_scale=1e-3), 4),
+    "fused_bucket16_randomized": (dict(numels=[4096 + 900], bucket=16, window=4, ef_rounding=1, ef_seed=3), 5),
+    "fused_block3008": (dict(numels=[3008 * 4 + 7], block=3008, bucket=8, density=0.02, window=4), 6),
 }
 
+# configurations the one-kernel fused step takes (with fused=1)
+FUSED = {"bf16_tails", "f32_student_t", "f32_window_values", "bucket512", "weight_decay", "window_one",
+         "zero_grad", "constant_grad", "sign_grad", "sparse_spikes", "ef8_nearest_tails", "randomized_4bit",
+         *[k for k in CASES if k.startswith("fused_")]}
 
-@pytest.mark.parametrize("name", list(CASES))
-def test_parity(name):
+
+@pytest.mark.parametrize("name,fused", [(k, 0) for k in CASES] + [(k, 1) for k in CASES if k in FUSED])
+def test_parity(name, fused):
     kw, steps = CASES[name]
     kw = dict(kw)
     numels = kw.pop("numels")
-    print(f"[parity] {name} numels={numels} {kw} steps={steps}", flush=True)
-    run = GpuOracleRun(numels, **kw)
-    for _ in range(steps):
+    print(f"[parity] {name} fused={fused} numels={numels} {kw} steps={steps}", flush=True)
+    run = GpuOracleRun(numels, fused=fused, **kw)
+    run.step()
+    assert (run.opt.step_kernels == 1) == (fused == 1 and name in FUSED), (name, run.opt.step_kernels)
+    for _ in range(steps - 1):
         run.step(check_moments=run.t % 2 == 0 or steps < 8)
     _report(run, name)
 
@@ -219,6 +243,12 @@ def test_llama2_7b_bf16_sampled_window_full():
     bf16 parameters, Student-t(4) gradients), 12 steps so that the window of
     10 is full and wraps, as in the timed steps."""
     _workload_sampled("llama2_7b_bf16", 12, 499, (0, 11))
+
+
+def test_llama2_7b_bf16_sampled_fused():
+    """The Llama-2-7B list through the fused one-kernel step (fused=1), 12
+    steps, every 997th block."""
+    _workload_sampled("llama2_7b_bf16", 12, 997, (0, 11), fused=1)
 
 
 def test_llama2_7b_bf16_randomized_8bit_sampled():
