@@ -284,6 +284,29 @@ int microadam_kernel_times(microadam_handle h, float* out_ms);
  */
 int microadam_kernel_times_total(microadam_handle h, float* out_ms, int64_t* out_steps);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): step t
+ * (>= 1) of the tensor list numels[0..n_tensors) on a caller-owned state
+ * buffer laid out as microadam_init lays it out for the same cfg and numels
+ * (>= microadam_state_bytes bytes, 256-byte aligned), holding the state
+ * after step t - 1: all zero bytes before step 1, which the caller provides.
+ * No handle is used and nothing is allocated: the tensor table and window
+ * weights go to a static device array of the library, at most 4096 tensors
+ * (393 KB; every GPU the library runs on holds its own copy until the
+ * process ends), and the kernels are those of microadam_step, with the same
+ * results.  params, grads, lr, stream as for microadam_step; param_dtype and
+ * grad_dtype as for microadam_init.  Calls that overlap on one GPU (other
+ * streams, other host threads) race on the shared array, and each call
+ * overwrites what the last one left there; calls on one stream are ordered.
+ * Errors: MICROADAM_ERR_UNSUPPORTED for more than 4096 tensors, else those
+ * of microadam_init and microadam_step; nothing is queued on failure.
+ */
+int microadam_step_noalloc(const microadam_config* cfg, const int64_t* numels, int32_t n_tensors,
+                           int32_t param_dtype, int32_t grad_dtype, void* state, uint64_t state_bytes,
+                           int64_t t, void* const* params, const void* const* grads, double lr,
+                           void* stream);
+
 const char* microadam_error_string(int code);
 
 /* The calling thread's most recent error message ("" if none). */

@@ -33,9 +33,10 @@ CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
 
 def build(source: str = SOURCE, out: str = LIBRARY) -> str:
     """Compile the oracle with gcc (no FMA contraction, no fast-math)."""
-    cmd = ["gcc", *CFLAGS, "-o", out + ".tmp", source, "-lm"]
+    tmp = f"{out}.{os.getpid()}.tmp"  # concurrent builds (test workers) do not share a temporary
+    cmd = ["gcc", *CFLAGS, "-o", tmp, source, "-lm"]
     subprocess.run(cmd, check=True)
-    os.replace(out + ".tmp", out)
+    os.replace(tmp, out)
     return out
 
 

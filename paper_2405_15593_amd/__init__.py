@@ -82,7 +82,7 @@ EXPORTS = (
     "microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
     "microadam_get_step", "microadam_set_step", "microadam_tensor_layout",
     "microadam_debug_moments", "microadam_step_kernels", "microadam_set_profiling", "microadam_kernel_times",
-    "microadam_kernel_times_total", "microadam_error_string",
+    "microadam_kernel_times_total", "microadam_step_noalloc", "microadam_error_string",
     "microadam_last_error",
 )
 
@@ -116,6 +116,8 @@ def load(path: str = LIBRARY):
     lib.microadam_tensor_layout.argtypes = [vp, i32, P(microadam_layout)]
     lib.microadam_debug_moments.argtypes = [vp, i32, vp, vp, vp]
     lib.microadam_step_kernels.argtypes = [vp]
+    lib.microadam_step_noalloc.argtypes = [P(microadam_config), P(i64), i32, i32, i32, vp, u64, i64, P(vp), P(vp),
+                                           ctypes.c_double, vp]
     lib.microadam_set_profiling.argtypes = [vp, i32]
     lib.microadam_kernel_times.argtypes = [vp, P(ctypes.c_float)]
     lib.microadam_kernel_times_total.argtypes = [vp, P(ctypes.c_float), P(i64)]
@@ -126,7 +128,7 @@ def load(path: str = LIBRARY):
     for f in ("microadam_state_bytes", "microadam_init", "microadam_step", "microadam_destroy",
               "microadam_set_step", "microadam_tensor_layout", "microadam_debug_moments",
               "microadam_step_kernels", "microadam_set_profiling", "microadam_kernel_times",
-              "microadam_kernel_times_total"):
+              "microadam_kernel_times_total", "microadam_step_noalloc"):
         getattr(lib, f).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -178,6 +180,17 @@ def microadam_step(h: int, param_ptrs: Sequence[int], grad_ptrs: Sequence[int],
     G = grad_ptrs if isinstance(grad_ptrs, ctypes.Array) else (ctypes.c_void_p * len(grad_ptrs))(*grad_ptrs)
     _check(load().microadam_step(ctypes.c_void_p(h), P, G, n, float(lr), ctypes.c_void_p(stream)),
            "microadam_step")
+
+
+def microadam_step_noalloc(cfg: microadam_config, numels: Sequence[int], param_dtype: int, grad_dtype: int,
+                           state_ptr: int, state_bytes: int, t: int, param_ptrs: Sequence[int],
+                           grad_ptrs: Sequence[int], lr: float = math.nan, stream: int = 0) -> None:
+    n = len(numels)
+    P = (ctypes.c_void_p * n)(*param_ptrs)
+    G = (ctypes.c_void_p * n)(*grad_ptrs)
+    _check(load().microadam_step_noalloc(ctypes.byref(cfg), _i64_array(numels), n, param_dtype, grad_dtype,
+                                         ctypes.c_void_p(state_ptr), state_bytes, int(t), P, G, float(lr),
+                                         ctypes.c_void_p(stream)), "microadam_step_noalloc")
 
 
 def microadam_destroy(h: int) -> None:

@@ -4,8 +4,11 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstddef>
 #include <cstdint>
+#include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -18,16 +21,21 @@ using microadam::TensorDesc;
 
 namespace {
 
-thread_local std::string g_last_error;
+// The calling thread's last error message, in a fixed buffer (reporting an
+// error allocates nothing).
+thread_local char g_last_error[512];
 
-int fail(int code, const std::string& msg) {
-  g_last_error = msg;
+int fail(int code, const char* msg) {
+  std::snprintf(g_last_error, sizeof(g_last_error), "%s", msg);
   return code;
 }
 
 int hip_fail(hipError_t e, const char* what) {
-  return fail(MICROADAM_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  std::snprintf(g_last_error, sizeof(g_last_error), "%s: %s", what, hipGetErrorString(e));
+  return MICROADAM_ERR_HIP;
 }
+
+void clear_error() { g_last_error[0] = '\0'; }
 
 constexpr uint64_t kAlign = 256;
 constexpr size_t kMaxLds = 65536;        // dynamic LDS budget per workgroup
@@ -99,6 +107,7 @@ struct TensorPlan {
   int64_t numel, num_blocks, num_buckets, num_full, first_block, last_block;
   int64_t first_bucket;  // buckets spanning blocks: bucket 0's place in the tables
   int32_t k_full, k_last, s_last;
+  int32_t ragged_before;  // tensors before this one that end in a ragged block
 };
 
 // Byte offsets of the three state planes; every block owns a record of fixed
@@ -119,12 +128,10 @@ int entry_bytes(const microadam_config* c) { return c->window_value_dtype == MIC
 
 // Full blocks are numbered first, tensor by tensor; the ragged last blocks
 // follow, so that the full blocks form one range of equal blocks.
-int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
-              std::vector<TensorPlan>& out, Planes& pl) {
+// out: n entries (host memory of the caller; nothing is allocated here).
+int make_plan(const microadam_config* c, const int64_t* numels, int32_t n, TensorPlan* out, Planes& pl) {
   if (n < 1) return fail(MICROADAM_ERR_INVALID_ARG, "n_tensors must be >= 1");
   if (!numels) return fail(MICROADAM_ERR_INVALID_ARG, "numels is NULL");
-  out.clear();
-  out.reserve((size_t)n);
   const int64_t B = c->topk_block, Bq = c->ef_bucket, m = c->window;
   const int64_t eb = entry_bytes(c);
   const int32_t k_full = (int32_t)block_k(B, c->density);
@@ -154,11 +161,14 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
     p.first_bucket = pl.big ? pl.n_buckets : 0;
     if (pl.big) pl.n_buckets += p.num_buckets;
     full += p.num_full;
-    out.push_back(p);
+    out[j] = p;
   }
   int64_t next = full;
-  for (TensorPlan& p : out)
+  for (int32_t j = 0; j < n; ++j) {
+    TensorPlan& p = out[j];
+    p.ragged_before = (int32_t)(next - full);
     p.last_block = p.num_full < p.num_blocks ? next++ : p.first_block + p.num_blocks - 1;
+  }
   const uint64_t nb = (uint64_t)next;
   pl.n_full = full;
   pl.n_blocks = next;
@@ -176,6 +186,139 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n,
 }
 
 using microadam::threads_for_block;
+
+// Launch limits of a plan (blocks per launch; buckets spanning blocks).
+int check_launch_size(const microadam_config* cfg, const Planes& pl) {
+  const int64_t total_blocks = pl.n_blocks;
+  const int nt = threads_for_block(cfg->topk_block);
+  if (total_blocks * (int64_t)nt >= ((int64_t)1 << 32) || total_blocks >= ((int64_t)1 << 31))
+    return fail(MICROADAM_ERR_UNSUPPORTED, "too many Top-K blocks for one launch");
+  if (pl.big && (total_blocks >= ((int64_t)1 << 28) || pl.table_bytes >= ((uint64_t)1 << 32)))
+    return fail(MICROADAM_ERR_UNSUPPORTED, "too many blocks or buckets for buckets spanning blocks");
+  return MICROADAM_OK;
+}
+
+// One fused kernel per step when asked for and where a block fits one
+// 256-thread workgroup and its new row and live rows fit the kernel's LDS;
+// else a select and an update kernel (or four launches with buckets
+// spanning blocks).
+bool use_fused(const microadam_config* cfg, const Planes& pl, int32_t k_full, int32_t param_bf16,
+               int32_t grad_bf16) {
+  const int32_t parts = (k_full + 63) / 64;
+  return cfg->fused == 1 && !pl.big && cfg->topk_block > 2048 && cfg->topk_block <= 4096 &&
+         k_full <= microadam::kFusedMaxK && cfg->window * parts <= microadam::kFusedMaxChunks &&
+         param_bf16 == grad_bf16;
+}
+
+int32_t bucket_log2_of(const microadam_config* cfg, const Planes& pl) {
+  int32_t b = 0;
+  if (!pl.big)
+    while ((1 << b) < cfg->ef_bucket) ++b;
+  return b;
+}
+
+// The kernels' view of tensor j (the param and grad addresses are set per step).
+TensorDesc desc_of(const TensorPlan& p, const Planes& pl) {
+  TensorDesc d;
+  std::memset(&d, 0, sizeof(d));
+  d.numel = p.numel;
+  d.first_block = p.first_block;
+  d.num_blocks = p.num_blocks;
+  d.last_block = p.last_block;
+  d.k_full = p.k_full;
+  d.k_last = p.k_last;
+  d.s_last = p.s_last;
+  d.num_full = (int32_t)p.num_full;
+  d.first_bucket = p.first_bucket;
+  d.num_buckets = pl.big ? p.num_buckets : 0;
+  d.ragged_before = p.ragged_before;
+  return d;
+}
+
+// beta1^r and beta2^r, r < m, from binary64 rounded once (Algorithm 2).
+void window_weights(const microadam_config* cfg, float* w) {
+  for (int r = 0; r < 2 * microadam::kMaxWindow; ++r) w[r] = 0.0f;
+  for (int r = 0; r < cfg->window; ++r) {
+    w[r] = (float)std::pow(cfg->beta1, (double)r);
+    w[microadam::kMaxWindow + r] = (float)std::pow(cfg->beta2, (double)r);
+  }
+}
+
+// Per-step constants, derived in binary64 and rounded once to binary32: the
+// bias corrections (1 - beta)/(1 - beta^t) of AdamStats (Algorithm 2) and the
+// decay factor 1 - eta*lambda (Algorithm 4).  The window weights beta^r live
+// in a device table (`wpow`).
+void fill_step_params(const microadam_config& c, const Planes& pl, int32_t k_full, int32_t n_tensors,
+                      int32_t bucket_log2, int64_t t, double lr, const TensorDesc* tensors,
+                      const uint32_t* block_tensor, const float* wpow, uint8_t* state, StepParams& p) {
+  const int m = c.window;
+  std::memset(&p, 0, sizeof(p));
+  p.tensors = tensors;
+  p.block_tensor = block_tensor;
+  p.wpow = wpow;
+  p.state = state;
+  p.ef_plane = pl.ef;
+  p.stats_plane = pl.stats;
+  p.win_plane = pl.win;
+  p.win_stride = pl.win_stride;
+  p.t = t;
+  p.total_blocks = pl.n_blocks;
+  p.n_full = pl.n_full;
+  p.block = c.topk_block;
+  p.bucket_log2 = bucket_log2;
+  p.window = m;
+  p.n_live = (int32_t)(t < m ? t : m);
+  p.new_slot = (int32_t)((t - 1) % m);
+  p.k_full = k_full;
+  p.lr = (float)lr;
+  p.decay = (float)(1.0 - lr * c.weight_decay);
+  p.decay_is_one = (lr * c.weight_decay == 0.0) ? 1 : 0;
+  p.eps = (float)c.eps;
+  p.c1 = (float)((1.0 - c.beta1) / (1.0 - std::pow(c.beta1, (double)t)));
+  p.c2 = (float)((1.0 - c.beta2) / (1.0 - std::pow(c.beta2, (double)t)));
+  p.ef_mode = (c.ef_bits == 8 ? 1 : 0) | (c.ef_rounding == MICROADAM_ROUND_RANDOMIZED ? 2 : 0);
+  p.seed_lo = (uint32_t)c.seed;
+  p.seed_hi = (uint32_t)(c.seed >> 32);
+  if (pl.big) {
+    p.big_bucket = c.ef_bucket;
+    p.total_buckets = pl.n_buckets;
+    p.table_bytes = pl.table_bytes;
+    p.partial_plane = pl.partial;
+  }
+  p.n_tensors = n_tensors;
+}
+
+// Queues the launches of one step on `s`; rec(i) records profiling event i
+// (0: start, 1, 2: between the select and the update, 3: end).
+template <typename Rec>
+int queue_step(const StepParams& p, bool fused, bool big, int32_t param_bf16, int32_t grad_bf16,
+               int32_t value_f32, hipStream_t s, Rec rec) {
+  hipError_t e;
+  if ((e = rec(0)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if (fused) {
+    e = microadam::launch_step(p, param_bf16, value_f32, 0, p.total_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the step kernel");
+  } else if (big) {
+    // select with per-block partials, the bucket reduction, the quantization
+    // of the residual
+    e = microadam::launch_select_partials(p, grad_bf16, value_f32, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
+    e = microadam::launch_bucket_reduce(p, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the bucket reduction");
+    e = microadam::launch_requant(p, grad_bf16, value_f32, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the quantization kernel");
+  } else {
+    e = microadam::launch_select(p, grad_bf16, value_f32, 0, p.total_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
+  }
+  if ((e = rec(1)) != hipSuccess || (e = rec(2)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if (!fused) {
+    e = microadam::launch_update(p, param_bf16, value_f32, 0, p.total_blocks, s);
+    if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
+  }
+  if ((e = rec(3)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  return MICROADAM_OK;
+}
 
 }  // namespace
 
@@ -273,47 +416,11 @@ hipError_t fold_slot(microadam_handle h, int slot) {
   return hipSuccess;
 }
 
-// Per-step constants, derived in binary64 and rounded once to binary32: the
-// bias corrections (1 - beta)/(1 - beta^t) of AdamStats (Algorithm 2) and the
-// decay factor 1 - eta*lambda (Algorithm 4).  The window weights beta^r live
-// in a device table filled at init.
+// Per-step constants of a handle's step t.
 void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& p) {
-  const microadam_config& c = h->cfg;
-  const int m = c.window;
-  std::memset(&p, 0, sizeof(p));
-  p.tensors = h->current >= 0 ? h->slots[h->current].d : nullptr;
-  p.block_tensor = h->d_block_tensor;
-  p.wpow = h->d_wpow;
-  p.state = h->state;
-  p.ef_plane = h->planes.ef;
-  p.stats_plane = h->planes.stats;
-  p.win_plane = h->planes.win;
-  p.win_stride = h->planes.win_stride;
-  p.t = t;
-  p.total_blocks = h->total_blocks;
-  p.n_full = h->planes.n_full;
-  p.block = c.topk_block;
-  p.bucket_log2 = h->bucket_log2;
-  p.window = m;
-  p.n_live = (int32_t)(t < m ? t : m);
-  p.new_slot = (int32_t)((t - 1) % m);
-  p.k_full = h->plans.empty() ? 0 : h->plans[0].k_full;
-  p.lr = (float)lr;
-  p.decay = (float)(1.0 - lr * c.weight_decay);
-  p.decay_is_one = (lr * c.weight_decay == 0.0) ? 1 : 0;
-  p.eps = (float)c.eps;
-  p.c1 = (float)((1.0 - c.beta1) / (1.0 - std::pow(c.beta1, (double)t)));
-  p.c2 = (float)((1.0 - c.beta2) / (1.0 - std::pow(c.beta2, (double)t)));
-  p.ef_mode = (c.ef_bits == 8 ? 1 : 0) | (c.ef_rounding == MICROADAM_ROUND_RANDOMIZED ? 2 : 0);
-  p.seed_lo = (uint32_t)c.seed;
-  p.seed_hi = (uint32_t)(c.seed >> 32);
-  if (h->planes.big) {
-    p.big_bucket = c.ef_bucket;
-    p.total_buckets = h->planes.n_buckets;
-    p.table_bytes = h->planes.table_bytes;
-    p.partial_plane = h->planes.partial;
-  }
-  p.n_tensors = (int32_t)h->plans.size();
+  fill_step_params(h->cfg, h->planes, h->plans.empty() ? 0 : h->plans[0].k_full, (int32_t)h->plans.size(),
+                   h->bucket_log2, t, lr, h->current >= 0 ? h->slots[h->current].d : nullptr, h->d_block_tensor,
+                   h->d_wpow, h->state, p);
 }
 
 int check_handle(microadam_handle h) {
@@ -339,9 +446,10 @@ int microadam_state_bytes(const microadam_config* cfg, const int64_t* numels, in
   if (!out_bytes) return fail(MICROADAM_ERR_INVALID_ARG, "out_bytes is NULL");
   int rc = validate_config(cfg);
   if (rc) return rc;
-  std::vector<TensorPlan> plans;
+  if (n_tensors < 1) return fail(MICROADAM_ERR_INVALID_ARG, "n_tensors must be >= 1");
+  std::vector<TensorPlan> plans((size_t)n_tensors);
   Planes pl;
-  rc = make_plan(cfg, numels, n_tensors, plans, pl);
+  rc = make_plan(cfg, numels, n_tensors, plans.data(), pl);
   if (rc) return rc;
   *out_bytes = pl.total;
   return MICROADAM_OK;
@@ -357,21 +465,19 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   if ((param_dtype != MICROADAM_F32 && param_dtype != MICROADAM_BF16) ||
       (grad_dtype != MICROADAM_F32 && grad_dtype != MICROADAM_BF16))
     return fail(MICROADAM_ERR_INVALID_ARG, "param_dtype / grad_dtype must be F32 or BF16");
-  std::vector<TensorPlan> plans;
+  if (n_tensors < 1) return fail(MICROADAM_ERR_INVALID_ARG, "n_tensors must be >= 1");
+  std::vector<TensorPlan> plans((size_t)n_tensors);
   Planes pl;
-  rc = make_plan(cfg, numels, n_tensors, plans, pl);
+  rc = make_plan(cfg, numels, n_tensors, plans.data(), pl);
   if (rc) return rc;
   const uint64_t total = pl.total;
   if (!state) return fail(MICROADAM_ERR_INVALID_ARG, "state is NULL");
   if ((uintptr_t)state % kAlign) return fail(MICROADAM_ERR_INVALID_ARG, "state must be 256-byte aligned");
   if (state_bytes < total)
     return fail(MICROADAM_ERR_STATE_SIZE, "state buffer smaller than microadam_state_bytes");
+  rc = check_launch_size(cfg, pl);
+  if (rc) return rc;
   const int64_t total_blocks = pl.n_blocks;
-  const int nt = threads_for_block(cfg->topk_block);
-  if (total_blocks * (int64_t)nt >= ((int64_t)1 << 32) || total_blocks >= ((int64_t)1 << 31))
-    return fail(MICROADAM_ERR_UNSUPPORTED, "too many Top-K blocks for one launch");
-  if (pl.big && (total_blocks >= ((int64_t)1 << 28) || pl.table_bytes >= ((uint64_t)1 << 32)))
-    return fail(MICROADAM_ERR_UNSUPPORTED, "too many blocks or buckets for buckets spanning blocks");
 
   microadam_handle h = new (std::nothrow) microadam_handle_s;
   if (!h) return fail(MICROADAM_ERR_NO_MEMORY, "handle allocation failed");
@@ -381,8 +487,7 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   h->param_bf16 = param_dtype == MICROADAM_BF16;
   h->grad_bf16 = grad_dtype == MICROADAM_BF16;
   h->value_f32 = cfg->window_value_dtype == MICROADAM_F32;
-  if (!pl.big)
-    while ((1 << h->bucket_log2) < cfg->ef_bucket) ++h->bucket_log2;
+  h->bucket_log2 = bucket_log2_of(cfg, pl);
   h->state = (uint8_t*)state;
   h->state_bytes = state_bytes;
   h->total_blocks = total_blocks;
@@ -391,16 +496,7 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
     release(h);
     return fail(MICROADAM_ERR_UNSUPPORTED, "k per block too large for the LDS budget");
   }
-  {
-    // one fused kernel per step when asked for and where a block fits one
-    // 256-thread workgroup and its new row and live rows fit the kernel's
-    // LDS; else a select and an update kernel (or four launches with buckets
-    // spanning blocks)
-    const int32_t kf = h->plans[0].k_full;
-    const int32_t parts = (kf + 63) / 64;
-    h->fused = cfg->fused == 1 && !pl.big && cfg->topk_block > 2048 && cfg->topk_block <= 4096 && kf <= microadam::kFusedMaxK &&
-               cfg->window * parts <= microadam::kFusedMaxChunks && h->param_bf16 == h->grad_bf16;
-  }
+  h->fused = use_fused(cfg, pl, h->plans[0].k_full, h->param_bf16, h->grad_bf16);
 
   hipError_t e = hipGetDevice(&h->device);
   if (e != hipSuccess) { release(h); return hip_fail(e, "hipGetDevice"); }
@@ -412,12 +508,8 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
     return hip_fail(e, "allocating the block table");
   }
   {
-    // beta1^r and beta2^r, r < m, from binary64 rounded once (Algorithm 2)
-    float w[2 * microadam::kMaxWindow] = {};
-    for (int r = 0; r < cfg->window; ++r) {
-      w[r] = (float)std::pow(cfg->beta1, (double)r);
-      w[microadam::kMaxWindow + r] = (float)std::pow(cfg->beta2, (double)r);
-    }
+    float w[2 * microadam::kMaxWindow];
+    window_weights(cfg, w);
     if ((e = hipMemcpy(h->d_wpow, w, sizeof(w), hipMemcpyHostToDevice)) != hipSuccess) {
       release(h);
       return hip_fail(e, "uploading the window weights");
@@ -436,18 +528,7 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
     const TensorPlan& p = h->plans[j];
     for (int64_t b = 0; b < p.num_full; ++b) bt[(size_t)(p.first_block + b)] = (uint32_t)j;
     bt[(size_t)p.last_block] = (uint32_t)j;
-    TensorDesc d;
-    std::memset(&d, 0, sizeof(d));
-    d.numel = p.numel;
-    d.first_block = p.first_block;
-    d.num_blocks = p.num_blocks;
-    d.last_block = p.last_block;
-    d.k_full = p.k_full;
-    d.k_last = p.k_last;
-    d.s_last = p.s_last;
-    d.num_full = (int32_t)p.num_full;
-    d.first_bucket = p.first_bucket;
-    d.num_buckets = h->planes.big ? p.num_buckets : 0;
+    const TensorDesc d = desc_of(p, h->planes);
     for (TableSlot& t : h->slots) t.h[j] = d;
   }
   hipStream_t s = (hipStream_t)stream;
@@ -460,7 +541,7 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
     return hip_fail(e, "clearing the state buffer");
   }
   *out = h;
-  g_last_error.clear();
+  clear_error();
   return MICROADAM_OK;
 }
 
@@ -523,29 +604,8 @@ int microadam_step(microadam_handle h, void* const* params, const void* const* g
   const int pslot = prof ? (int)(h->prof_count % microadam_handle_s::kProfSlots) : 0;
   if (prof && (e = fold_slot(h, pslot)) != hipSuccess) return hip_fail(e, "reading the kernel timers");
   auto rec = [&](int i) { return prof ? hipEventRecord(h->ev[pslot][i], s) : hipSuccess; };
-  if ((e = rec(0)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  if (h->fused) {
-    e = microadam::launch_step(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
-    if (e != hipSuccess) return hip_fail(e, "launching the step kernel");
-  } else if (h->planes.big) {
-    // select with per-block partials, the bucket reduction, the quantization
-    // of the residual
-    e = microadam::launch_select_partials(p, h->grad_bf16, h->value_f32, s);
-    if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
-    e = microadam::launch_bucket_reduce(p, s);
-    if (e != hipSuccess) return hip_fail(e, "launching the bucket reduction");
-    e = microadam::launch_requant(p, h->grad_bf16, h->value_f32, s);
-    if (e != hipSuccess) return hip_fail(e, "launching the quantization kernel");
-  } else {
-    e = microadam::launch_select(p, h->grad_bf16, h->value_f32, 0, h->total_blocks, s);
-    if (e != hipSuccess) return hip_fail(e, "launching the select kernel");
-  }
-  if ((e = rec(1)) != hipSuccess || (e = rec(2)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  if (!h->fused) {
-    e = microadam::launch_update(p, h->param_bf16, h->value_f32, 0, h->total_blocks, s);
-    if (e != hipSuccess) return hip_fail(e, "launching the update kernel");
-  }
-  if ((e = rec(3)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  rc = queue_step(p, h->fused, h->planes.big, h->param_bf16, h->grad_bf16, h->value_f32, s, rec);
+  if (rc) return rc;
   h->timed = prof;
   if (prof) {
     h->pending[pslot] = true;
@@ -681,6 +741,111 @@ int microadam_kernel_times_total(microadam_handle h, float* out_ms, int64_t* out
   return MICROADAM_OK;
 }
 
+}  // extern "C"
+
+// ------------------------------------------------- the no-allocation step
+namespace {
+constexpr int32_t kNoAllocMaxTensors = 4096;
+constexpr int kNoAllocMaxDevices = 64;
+constexpr size_t kNoAllocWeightBytes = 2 * microadam::kMaxWindow * sizeof(float);
+constexpr size_t kNoAllocScratchBytes = kNoAllocWeightBytes + (size_t)kNoAllocMaxTensors * sizeof(TensorDesc);
+
+// Host image of the scratch array: the window weights, then the tensor table.
+struct NoAllocImage {
+  float wpow[2 * microadam::kMaxWindow];
+  TensorDesc desc[kNoAllocMaxTensors];
+};
+static_assert(offsetof(NoAllocImage, desc) == kNoAllocWeightBytes, "weights, then the table");
+static_assert(sizeof(NoAllocImage) == kNoAllocScratchBytes, "the image fills the scratch array");
+
+std::mutex g_noalloc_mu;                    // guards the host image and the addresses below
+void* g_scratch_dev[kNoAllocMaxDevices];    // per device: the address of its `scratch`
+TensorPlan g_noalloc_plans[kNoAllocMaxTensors];
+NoAllocImage g_noalloc_image;
+}  // namespace
+
+// Device memory of microadam_step_noalloc (the window weights and the tensor
+// table of the last call), one copy per GPU for the life of the process.  In
+// host code the name only stands for the symbol: its device address comes
+// from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+extern "C" {
+
+int microadam_step_noalloc(const microadam_config* cfg, const int64_t* numels, int32_t n_tensors,
+                           int32_t param_dtype, int32_t grad_dtype, void* state, uint64_t state_bytes,
+                           int64_t t, void* const* params, const void* const* grads, double lr, void* stream) {
+  int rc = validate_config(cfg);
+  if (rc) return rc;
+  if (n_tensors < 1) return fail(MICROADAM_ERR_INVALID_ARG, "n_tensors must be >= 1");
+  if (n_tensors > kNoAllocMaxTensors)
+    return fail(MICROADAM_ERR_UNSUPPORTED, "microadam_step_noalloc takes at most 4096 tensors");
+  if ((param_dtype != MICROADAM_F32 && param_dtype != MICROADAM_BF16) ||
+      (grad_dtype != MICROADAM_F32 && grad_dtype != MICROADAM_BF16))
+    return fail(MICROADAM_ERR_INVALID_ARG, "param_dtype / grad_dtype must be F32 or BF16");
+  if (t < 1) return fail(MICROADAM_ERR_INVALID_ARG, "t must be >= 1");
+  if (!state) return fail(MICROADAM_ERR_INVALID_ARG, "state is NULL");
+  if ((uintptr_t)state % kAlign) return fail(MICROADAM_ERR_INVALID_ARG, "state must be 256-byte aligned");
+  if (!params || !grads) return fail(MICROADAM_ERR_INVALID_ARG, "params / grads is NULL");
+  for (int32_t j = 0; j < n_tensors; ++j) {
+    if (!params[j] || !grads[j]) return fail(MICROADAM_ERR_INVALID_ARG, "a param or grad pointer is NULL");
+    if ((uintptr_t)params[j] % 16 || (uintptr_t)grads[j] % 16)
+      return fail(MICROADAM_ERR_INVALID_ARG, "param and grad pointers must be 16-byte aligned");
+  }
+  if (std::isnan(lr)) lr = cfg->lr;
+  if (!std::isfinite(lr)) return fail(MICROADAM_ERR_INVALID_ARG, "lr must be finite");
+
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  Planes pl;
+  rc = make_plan(cfg, numels, n_tensors, g_noalloc_plans, pl);
+  if (rc) return rc;
+  if (state_bytes < pl.total) return fail(MICROADAM_ERR_STATE_SIZE, "state buffer smaller than microadam_state_bytes");
+  rc = check_launch_size(cfg, pl);
+  if (rc) return rc;
+  const int32_t k_full = g_noalloc_plans[0].k_full;
+  const int32_t value_f32 = cfg->window_value_dtype == MICROADAM_F32;
+  if (microadam::step_lds_bytes(cfg->topk_block, k_full, value_f32) > kMaxLds)
+    return fail(MICROADAM_ERR_UNSUPPORTED, "k per block too large for the LDS budget");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kNoAllocMaxDevices) return fail(MICROADAM_ERR_UNSUPPORTED, "device number above 63");
+  if (!g_scratch_dev[dev]) {
+    // first call on this device (current): where its copy of `scratch` lives
+    void* ptr = nullptr;
+    if ((e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch))) != hipSuccess)
+      return hip_fail(e, "hipGetSymbolAddress");
+    if (!ptr) return fail(MICROADAM_ERR_HIP, "hipGetSymbolAddress returned NULL");
+    g_scratch_dev[dev] = ptr;
+  }
+  uint8_t* const dev_scratch = (uint8_t*)g_scratch_dev[dev];
+  window_weights(cfg, g_noalloc_image.wpow);
+  for (int32_t j = 0; j < n_tensors; ++j) {
+    TensorDesc d = desc_of(g_noalloc_plans[j], pl);
+    d.param = params[j];
+    d.grad = grads[j];
+    g_noalloc_image.desc[j] = d;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  // the weights and this call's part of the table; the copy is ordered after
+  // earlier work on `s`, and the host image is not needed once the call
+  // returns (a copy from pageable host memory has read it by then)
+  if ((e = hipMemcpyAsync(dev_scratch, &g_noalloc_image, kNoAllocWeightBytes + (size_t)n_tensors * sizeof(TensorDesc),
+                          hipMemcpyHostToDevice, s)) != hipSuccess)
+    return hip_fail(e, "uploading the tensor table");
+  const int32_t param_bf16 = param_dtype == MICROADAM_BF16, grad_bf16 = grad_dtype == MICROADAM_BF16;
+  StepParams p;
+  // no block table: the kernels find a block's tensor by binary search
+  fill_step_params(*cfg, pl, k_full, n_tensors, bucket_log2_of(cfg, pl), t, lr,
+                   (const TensorDesc*)(dev_scratch + kNoAllocWeightBytes), nullptr, (const float*)dev_scratch,
+                   (uint8_t*)state, p);
+  const bool fused = use_fused(cfg, pl, k_full, param_bf16, grad_bf16);
+  rc = queue_step(p, fused, pl.big, param_bf16, grad_bf16, value_f32, s, [](int) { return hipSuccess; });
+  if (rc) return rc;
+  clear_error();
+  return MICROADAM_OK;
+}
+
 const char* microadam_error_string(int code) {
   switch (code) {
     case MICROADAM_OK: return "ok";
@@ -694,6 +859,6 @@ const char* microadam_error_string(int code) {
   }
 }
 
-const char* microadam_last_error(void) { return g_last_error.c_str(); }
+const char* microadam_last_error(void) { return g_last_error; }
 
 }  // extern "C"

@@ -206,6 +206,8 @@ __device__ __forceinline__ TensorDesc load_desc(const __attribute__((address_spa
   r.num_full = d->num_full;
   r.first_bucket = d->first_bucket;
   r.num_buckets = d->num_buckets;
+  r.ragged_before = d->ragged_before;
+  r.reserved = 0;
   return r;
 }
 
@@ -333,9 +335,35 @@ struct Block {
   uint32_t j;             // tensor number
 };
 
+// The tensor of global block gb: from the block table, or, without one, by
+// binary search over the tensor table (full blocks are numbered tensor by
+// tensor, so gb < n_full lies in the last tensor whose full blocks start at
+// or before it; ragged block gb - n_full belongs to the last tensor with at
+// most that many ragged tensors before it).
+__device__ __forceinline__ uint32_t tensor_of_block(const StepParams& p, int64_t gb) {
+  if (p.block_tensor) return constant_ptr(p.block_tensor)[gb];
+  const __attribute__((address_space(4))) TensorDesc* td = constant_ptr(p.tensors);
+  int lo = 0, hi = p.n_tensors - 1;
+  if (gb < p.n_full) {
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (td[mid].first_block <= gb) lo = mid;
+      else hi = mid - 1;
+    }
+  } else {
+    const int64_t r = gb - p.n_full;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if ((int64_t)td[mid].ragged_before <= r) lo = mid;
+      else hi = mid - 1;
+    }
+  }
+  return (uint32_t)lo;
+}
+
 __device__ __forceinline__ Block locate(const StepParams& p, int64_t gb) {
   Block b;
-  const uint32_t j = constant_ptr(p.block_tensor)[gb];
+  const uint32_t j = tensor_of_block(p, gb);
   b.desc = load_desc(constant_ptr(p.tensors) + j);
   const bool last = (int32_t)gb == (int32_t)b.desc.last_block;
   const int32_t q = last ? (int32_t)b.desc.num_blocks - 1 : (int32_t)(gb - b.desc.first_block);

@@ -26,6 +26,8 @@ struct TensorDesc {
   int32_t num_full;       // full blocks
   int64_t first_bucket;   // buckets spanning blocks: the tensor's bucket 0 in the table
   int64_t num_buckets;    // its buckets (0 with buckets inside blocks)
+  int32_t ragged_before;  // tensors before this one that end in a ragged block
+  int32_t reserved;
 };
 
 // Threads per workgroup for a Top-K block of B_d elements (each thread owns
@@ -42,7 +44,7 @@ inline int threads_for_block(int block) { return block <= 1024 ? 64 : 256; }
 // blocks [n_full, total_blocks) are the ragged last blocks of tensors.
 struct StepParams {
   const TensorDesc* tensors;
-  const uint32_t* block_tensor;  // global block -> tensor index
+  const uint32_t* block_tensor;  // global block -> tensor index; NULL: found by binary search
   const float* wpow;             // [2 * kMaxWindow]: beta1^r, then beta2^r
   uint8_t* state;
   uint64_t ef_plane, stats_plane, win_plane;  // byte offsets into state
