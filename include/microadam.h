@@ -158,9 +158,9 @@ typedef struct microadam_handle_s* microadam_handle;
  *              bf16_bits << 16); with float32 values it is a uint32 index
  *              followed by the float32 value.  For B_d > 4096 the record
  *              continues, after the m rows (at byte m*k_full*entry_bytes),
- *              with a table of m*ceil(B_d/4096) uint32: entry (r, j) is the
+ *              with a table of m*ceil(B_d/1024) uint32: entry (r, j) is the
  *              position in row r of the first entry whose index is at least
- *              4096*j (the entries of the block's 4096-element sub-block j
+ *              1024*j (the entries of the block's 1024-element quarter j
  *              are the positions [entry (r, j), entry (r, j+1)), the last
  *              ending at k_q).
  */

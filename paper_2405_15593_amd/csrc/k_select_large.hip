@@ -17,9 +17,9 @@ namespace {
 // 1024 keys (16-ary in the same way) and checked by one counting pass; when
 // the check fails (an unlucky sample, large tie groups) a bitwise search over
 // every element narrows it instead.  The new row is written in element order,
-// and for each sub-block the position in the row of its first entry goes to
-// the record's segment table, behind the m rows, where the update finds the
-// entries of one sub-block.
+// and for each 1024-element quarter of the block the position in the row of
+// its first entry goes to the record's segment table, behind the m rows,
+// where the update finds the entries of one quarter.
 constexpr int kCandPerThread = 8;
 template <bool B>
 struct BoolTag {
@@ -344,7 +344,7 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
       const uint32_t t1 = t > lo1 ? t : lo1;
       uint32_t m_l = 0;
 #pragma unroll
-      for (int r = 0; r < R; ++r) m_l += (y[r] >= t1) & (y[r] < U) ? 1u : 0u;
+      for (int r = 0; r < R; ++r) m_l += ((y[r] >= t1) & (y[r] < U)) ? 1u : 0u;
       uint32_t nl;
       uint32_t q = wg_scan(m_l, 0, nl);
 #pragma unroll
@@ -449,20 +449,26 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
       }
   }
   {
-    // the new row in element order, and the segment table entry of this
-    // wave's sub-block: the row position of its first entry
+    // the new row in element order, and the segment table entries of the
+    // block's 1024-element quarters: the row position of each quarter's first
+    // entry, written by the thread holding the quarter's first 64 elements
     uint32_t kept_all;
     uint32_t pos = wg_scan(sel_l, 1, kept_all);
     constexpr uint32_t EB = VF32 ? 8u : 4u;
-    const int nsub = (p.block + kSubBlock - 1) / kSubBlock;
+    const int nq = (p.block + kQuarter - 1) / kQuarter;
     const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
-    if (lane == 0 && wave < nsub)
-      __builtin_amdgcn_raw_buffer_store_b32(pos < (uint32_t)kq ? pos : (uint32_t)kq, rrec,
-                                            (uint32_t)p.window * p.k_full * EB + ((uint32_t)p.new_slot * nsub + wave) * 4,
-                                            0, 0);
+    if ((tid & (kQuarter / EPL - 1)) == 0 && tid / (kQuarter / EPL) < nq)
+      __builtin_amdgcn_raw_buffer_store_b32(
+          pos < (uint32_t)kq ? pos : (uint32_t)kq, rrec,
+          (uint32_t)p.window * p.k_full * EB + ((uint32_t)p.new_slot * nq + tid / (kQuarter / EPL)) * 4, 0, 0);
+    // the row goes through LDS (the gathered keys are no longer needed)
+    // when it fits, and leaves in whole-wave stores of consecutive words;
+    // else each entry is stored where it is found
+    constexpr uint32_t EW = VF32 ? 2u : 1u;
+    const bool staged = (uint32_t)kq * EW <= (uint32_t)NC;
+    const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
+    const uint32_t row0 = (uint32_t)p.new_slot * kq;
     if (sel_l) {
-      const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
-      const uint32_t row0 = (uint32_t)p.new_slot * kq;
       const float tf = opaque_f(__uint_as_float(T));
       const int last_here = notie ? CAP : (int)i_last - (int)eb;
 #pragma unroll
@@ -471,12 +477,25 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
         for (int e = 0; e < 8; ++e) {
           const float ab = __builtin_fabsf(a[v][e]);
           if ((ab > tf) | ((ab == tf) & (8 * v + e <= last_here))) {
-            if (pos < (uint32_t)kq) E::store(rw, row0 + pos, E::make(eb + 8 * v + e, a[v][e]));  // within the row
+            if (pos < (uint32_t)kq) {  // within the row
+              const typename E::T x = E::make(eb + 8 * v + e, a[v][e]);
+              if (staged) {
+                if constexpr (VF32) *(u32x2*)(region + 2 * pos) = x;
+                else region[pos] = x;
+              } else {
+                E::store(rw, row0 + pos, x);
+              }
+            }
             ++pos;
           }
         }
         __builtin_amdgcn_sched_barrier(0);  // one vector's stores at a time
       }
+    }
+    if (staged) {
+      lds_sync();
+      for (uint32_t w = (uint32_t)tid; w < (uint32_t)kq * EW; w += NT)
+        __builtin_amdgcn_raw_buffer_store_b32(region[w], rw, (row0 * EW + w) * 4, 0, 0);
     }
   }
 

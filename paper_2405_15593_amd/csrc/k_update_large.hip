@@ -1,241 +1,268 @@
-// The update kernel for Top-K blocks above 4096 elements (one workgroup per
-// 4096-element sub-block).
+// The update kernel for Top-K blocks above 4096 elements (one wave per run
+// of 1024-element quarters of a block).
 #include "microadam_common.h"
 
 namespace microadam {
 namespace {
 
 // ================================================ update, blocks above 4096
-// One workgroup of 256 threads per 4096-element sub-block j of a block
-// (thread tid: the sub-block's elements 16*tid + [0, 16)).  The live rows'
-// entries of sub-block j are the segments the select kernel recorded.  The
-// workgroup rebuilds z1 = sum beta1^r V and z2 = sum beta2^r V^2 one row at a
-// time, oldest first (Algorithm 2, AdamStats), from registers when every row
-// holds at most 256 of the sub-block's entries (and at most kFastRows rows are
-// live), else from LDS, where they are staged in batches of stage_large
-// entries.  Every thread then turns its own 16 elements' sums into the update
-// (an element without entries has sums 0 and a decrement of 0) and applies it
-// (Algorithm 1; Algorithm 4).  The staging batch is small (1024 entries, 512
-// with binary32 values: 37 KB of LDS in all), so that four workgroups fit a
-// compute unit for the register path, which uses no staging.
-template <bool VF>
-constexpr int stage_large() { return VF ? 512 : 1024; }
-// Live rows up to which the update reads a sub-block's entries straight into
-// registers (when no row holds more than 256 of them).
-constexpr int kFastRows = 24;
+// A wave takes kQuartersPerWave consecutive 1024-element quarters of a
+// block, one after the other (lane l: the quarter's elements 16*l + [0, 16)).
+// The live rows' entries of quarter q are the segments the select kernel
+// recorded in the record's table: row r holds them at positions
+// [table(r, q), table(r, q + 1)).  For each quarter the wave loads every live
+// row's segment at once (entry i of each segment's first 64 in lane i, and of
+// the entries 64 .. 127 of up to kOverflow rows, while at most fast_rows()
+// rows are live; else 64 entries of a row at a time), then adds them into two
+// LDS accumulators, sum beta1^r V and sum beta2^r V^2 (Algorithm 2,
+// AdamStats), the two sums of an element side by side in one 8-byte word:
+// the entries of one add come from one row and have distinct indices, and
+// the wave's LDS accesses execute in order, so every entry is added once,
+// with no barrier.  Every lane then turns its 16 elements' sums into the
+// update (an element without entries has sums 0 and keeps theta, less the
+// decay) and applies it (Algorithm 1; Algorithm 4).  The loads of the next
+// quarter (its table words, its segments and its parameters) go out before
+// the current quarter is rebuilt, so their latency hides behind the rebuild.
+// The decrement uses the hardware square root and reciprocal (each within
+// 1 ulp), so it lies within a few binary32 ulps of the correctly rounded
+// value.
+constexpr int kQuartersPerWave = 4;
+constexpr int kOverflow = 4;
+constexpr int kPreRows = 8;  // rows of the next quarter loaded ahead
+template <bool VF32>
+constexpr int fast_rows() { return VF32 ? 12 : 24; }  // two quarters' entries stay in registers
 
-template <bool VF>
-constexpr size_t update_large_lds_bytes() {
-  return (size_t)2 * (kSubBlock + kWave) * 4 + (size_t)3 * kWave * 4 + 16 + (size_t)stage_large<VF>() * (VF ? 8 : 4);
-}
+// The accumulator: 8-byte (sum, sum) pairs in element order, and one sink
+// pair (kQuarter) for entries outside the quarter, which the table rules
+// out.
+constexpr size_t update_large_lds_bytes() { return (size_t)(kQuarter + 2) * 8; }
+
+// The loads of the next quarter that go out before the current one is
+// rebuilt: its segments, its first kPreRows rows' entries and its parameters.
+template <bool PBF16, bool VF32>
+struct Prefetch {
+  using ET = typename Entry<VF32>::T;
+  uint32_t seg_lo, seg_n;  // lane r < n_live: row r's segment (first entry in the record, length)
+  ET ld[kPreRows];
+  Raw8<PBF16> th[2];       // the lane's 16 parameters
+};
 
 template <bool PBF16, bool VF32, bool EXPORT>
-__global__ void __launch_bounds__(256) update_large_kernel(StepParams p, int64_t first_block, int64_t count, int32_t nsub,
-                                                           float* mhat, float* vhat) {
-  constexpr int NT = 256, STAGE = stage_large<VF32>();
+__global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64_t first_block, int64_t count,
+                                                             int32_t nw, float* mhat, float* vhat) {
   using E = Entry<VF32>;
   using ET = typename E::T;
+  using PF = Prefetch<PBF16, VF32>;
+  constexpr int FR = fast_rows<VF32>();
   extern __shared__ __align__(16) uint32_t smem[];
-  float* const z1 = (float*)smem;                         // [kSubBlock] + sink words
-  float* const z2 = z1 + kSubBlock + kWave;
-  uint32_t* const seg_lo = (uint32_t*)(z2 + kSubBlock + kWave);  // [kWave] by row age
-  uint32_t* const seg_n = seg_lo + kWave;
-  uint32_t* const seg_at = seg_n + kWave;  // position of the row's first entry in the staged order
-  uint32_t* const misc = seg_at + kWave;   // [4]: the entry total, the longest segment
-  ET* const stage = (ET*)(misc + 4);       // [STAGE]
+  float2* const z = (float2*)smem;  // [kQuarter + 1] (sum beta1^r V, sum beta2^r V^2)
 
-  const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
-  const int64_t wg = xcd_block(block_id(), count * nsub);
-  const int32_t gb = (int32_t)(first_block + wg / nsub);
-  const int j = (int)(wg % nsub);
-  const Span g = span_of(p, gb, PBF16 ? 2 : 4);
-  const int lo = j * kSubBlock;
-  if (lo >= g.s) return;  // a sub-block past the end of a ragged block
-  const int s = g.s - lo < kSubBlock ? g.s - lo : kSubBlock;
-  const int kq = g.kq, m = p.window, n_live = p.n_live;
-  const int slot0 = (p.new_slot + 1 + m - n_live) % m;  // oldest live row first
-  const int nsub_blk = (p.block + kSubBlock - 1) / kSubBlock;  // table entries per row
-  const uint32_t eb = (uint32_t)tid * 16;
-
-  // the parameters go out first; their latency hides behind the rebuild
+  const int lane = thread_id();
+  const int64_t wg = xcd_block(block_id(), count * nw);
+  const int32_t gb = (int32_t)(first_block + wg / nw);
   const int es = PBF16 ? 2 : 4;
-  const Rsrc rp = make_rsrc((const void*)(g.base + (uint64_t)lo * es), vec_bytes<PBF16>(s));
-  Raw8<PBF16> th[2];
-  if (!EXPORT) {
-#pragma unroll
-    for (int v = 0; v < 2; ++v) th[v] = load8<PBF16>(rp, eb + 8 * v);
-  }
-
-  // the live rows' segments of sub-block j (row age r = 0 is the oldest),
-  // their starts in the staged order by a scan over wave 0's lanes
+  const Span g = span_of(p, gb, es);
+  const int nqv = (g.s + kQuarter - 1) / kQuarter;  // quarters holding elements
+  const int q_begin = (int)(wg % nw) * kQuartersPerWave;
+  if (q_begin >= nqv) return;  // past the end of a ragged block
+  const int q_end = q_begin + kQuartersPerWave < nqv ? q_begin + kQuartersPerWave : nqv;
+  const int kq = g.kq, m = p.window, n_live = p.n_live;
+  const int nq_blk = (p.block + kQuarter - 1) / kQuarter;  // table entries per row
+  const uint32_t eb = (uint32_t)lane * 16;
+  // lane r < n_live: live row r (r = 0 is the oldest)
+  const int my_slot = (p.new_slot + 1 + m - n_live + lane) % m;
   constexpr uint32_t EB = VF32 ? 8u : 4u;
   const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
   const uint32_t table = (uint32_t)m * p.k_full * EB;
-  if (wave == 0) {
-    uint32_t n = 0, start = 0;
-    if (lane < n_live) {
-      const int slot = (slot0 + lane) % m;
-      const uint32_t a0 = __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)slot * nsub_blk + j) * 4, 0, 0);
-      const uint32_t a1 = j + 1 < nsub_blk
-                              ? __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)slot * nsub_blk + j + 1) * 4, 0, 0)
-                              : (uint32_t)kq;
-      // (segment starts are clamped to the row, so that any table content
-      // gives a bounded read)
-      const uint32_t b0 = a0 < (uint32_t)kq ? a0 : (uint32_t)kq, b1 = a1 < (uint32_t)kq ? a1 : (uint32_t)kq;
-      start = (uint32_t)slot * kq + b0;  // entry number in the record
-      n = b1 > b0 ? b1 - b0 : 0u;
-    }
-    uint32_t inc = n, big = n;  // inclusive prefix over lanes; the longest segment
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-      const uint32_t o = __shfl_up(inc, d, kWave);
-      if (lane >= d) inc += o;
-      const uint32_t b2 = __shfl_xor(big, d, kWave);
-      big = b2 > big ? b2 : big;
-    }
-    seg_lo[lane] = start;
-    seg_n[lane] = n;
-    seg_at[lane] = inc - n;
-    if (lane == kWave - 1) {
-      misc[0] = inc;
-      misc[1] = big;
-    }
-  }
-  {
-    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      *(float4*)(z1 + eb + 4 * q) = zero;
-      *(float4*)(z2 + eb + 4 * q) = zero;
-    }
-  }
-  lds_sync();
-  const uint32_t total = misc[0];
-
   const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
   const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
   const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
-  // one workgroup-wide read-add-write of a row's entry per thread (the
-  // entries of a row have distinct indices)
-  auto add_entry = [&](ET e, float w1, float w2) {
-    const uint32_t i = E::idx(e) - (uint32_t)lo;
-    const uint32_t zp = i < (uint32_t)s ? i : (uint32_t)(kSubBlock + lane);
-    const float v = E::val(e);
-    const float a1 = z1[zp], a2 = z2[zp];
-    z1[zp] = a1 + w1 * v;
-    z2[zp] = a2 + w2 * (v * v);
+  auto weight = [&](float ws, int r) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ws), n_live - 1 - r));
   };
-  if (n_live <= kFastRows && misc[1] <= (uint32_t)NT) {
-    // every live row holds at most NT entries of the sub-block: thread t
-    // loads entry t of every row at once, then the rows are added oldest
-    // first from registers, a barrier between rows
-    ET ld[kFastRows];
-#pragma unroll
-    for (int r = 0; r < kFastRows; ++r)
-      if (r < n_live && (uint32_t)tid < seg_n[r]) ld[r] = E::load(rw, seg_lo[r] + (uint32_t)tid);
-#pragma unroll
-    for (int r = 0; r < kFastRows; ++r) {
-      const uint32_t n = r < n_live ? seg_n[r] : 0u;
-      if (n != 0) {  // (uniform)
-        const int age = n_live - 1 - r;
-        const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), age));
-        const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), age));
-        if ((uint32_t)tid < n) add_entry(ld[r], w1, w2);
-        lds_sync();
-      }
-    }
-  } else
-  for (uint32_t b0 = 0; b0 < total; b0 += STAGE) {
-    const uint32_t b1 = total - b0 < (uint32_t)STAGE ? total : b0 + STAGE;
-    // stage the entries [b0, b1) of the concatenated segments: every thread
-    // issues the loads of its positions b0 + tid + NT*i together (the row of
-    // a position by binary search over the rows' first positions), then
-    // writes them to LDS
-    {
-      constexpr int PER = STAGE / NT;
-      ET ld[PER];
-#pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        const uint32_t x = b0 + tid + NT * i;
-        int r = 0;
-        for (int half = 32; half > 0; half >>= 1)
-          if (r + half < n_live && seg_at[r + half] <= x) r += half;
-        const uint32_t entry = x < b1 ? seg_lo[r] + (x - seg_at[r]) : 0u;
-        ld[i] = E::load(rw, entry);
-      }
-#pragma unroll
-      for (int i = 0; i < PER; ++i)
-        if (b0 + tid + NT * i < b1) stage[tid + NT * i] = ld[i];
-    }
-    lds_sync();
-    // row by row, oldest first, the whole workgroup on one row: a row's
-    // entries have distinct indices, so its read-add-writes never meet; a
-    // barrier orders them before the next row's (the summation order per
-    // element is the rows' order, as with one wave)
-    for (int r = 0; r < n_live; ++r) {
-      const uint32_t at = seg_at[r], n = seg_n[r];
-      const uint32_t x0 = at > b0 ? at : b0, x1 = at + n < b1 ? at + n : b1;
-      const int age = n_live - 1 - r;
-      const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w1s), age));
-      const float w2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w2s), age));
-      for (uint32_t x = x0 + (uint32_t)tid; x < x1; x += NT) add_entry(stage[x - b0], w1, w2);
-      lds_sync();
-    }
-  }
-  float s1[16], s2[16];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const float4 u1 = *(const float4*)(z1 + eb + 4 * q);
-    const float4 u2 = *(const float4*)(z2 + eb + 4 * q);
-    s1[4 * q] = u1.x; s1[4 * q + 1] = u1.y; s1[4 * q + 2] = u1.z; s1[4 * q + 3] = u1.w;
-    s2[4 * q] = u2.x; s2[4 * q + 1] = u2.y; s2[4 * q + 2] = u2.z; s2[4 * q + 3] = u2.w;
-  }
+  auto quarter_size = [&](int q) { return g.s - q * kQuarter < kQuarter ? g.s - q * kQuarter : kQuarter; };
+  auto param_rsrc = [&](int q) {
+    return make_rsrc((const void*)(g.base + (uint64_t)q * kQuarter * es), vec_bytes<PBF16>(quarter_size(q)));
+  };
+  // entry `lane` + off of row r's segment, or (lanes past its end) a read
+  // past the end of the record, which gives 0 and is not used: the adds
+  // check the segment length, and no merge waits for the load
+  auto row_load = [&](uint32_t seg_lo, uint32_t seg_n, int r, uint32_t off) {
+    const uint32_t n = __builtin_amdgcn_readlane(seg_n, r), at = __builtin_amdgcn_readlane(seg_lo, r);
+    return E::load(rw, (uint32_t)lane + off < n ? at + off + (uint32_t)lane : E::kFar);
+  };
 
-  // every thread: its 16 elements
-  if ((int)eb >= s) return;
-  if (EXPORT) {
-#pragma unroll
-    for (int e = 0; e < 16; ++e)
-      if ((int)eb + e < s) {
-        mhat[g.e0 + lo + eb + e] = p.c1 * s1[e];
-        vhat[g.e0 + lo + eb + e] = p.c2 * s2[e];
-      }
-    return;
-  }
-  const bool full = s == kSubBlock;
-#pragma unroll
-  for (int v = 0; v < 2; ++v) {
-    float thf[8], out[8];
-    unpack8<PBF16>(th[v], thf);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float mh = p.c1 * s1[8 * v + e];
-      const float vh = p.c2 * s2[8 * v + e];
-      const float den = p.eps + __builtin_sqrtf(vh);  // correctly rounded
-      // an element without entries is left to the decay alone
-      const bool none = (s1[8 * v + e] == 0.0f) & (s2[8 * v + e] == 0.0f);
-      const float d = none ? 0.0f : p.lr * (mh / den);
-      const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
-      out[e] = base - d;
+  // the two table words of quarter q for the lane's row
+  auto table_load = [&](int q, uint32_t& a0, uint32_t& a1) {
+    a0 = 0u;
+    a1 = 0u;
+    if (lane < n_live) {
+      a0 = __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)my_slot * nq_blk + q) * 4, 0, 0);
+      a1 = q + 1 < nq_blk
+               ? __builtin_amdgcn_raw_buffer_load_b32(rrec, table + ((uint32_t)my_slot * nq_blk + q + 1) * 4, 0, 0)
+               : (uint32_t)kq;
     }
-    store8<PBF16>(rp, eb + 8 * v, s, full, out);
+  };
+  // quarter q's segments from its table words (clamped to the row, so that
+  // any content gives a bounded read; lanes past the live rows hold empty
+  // segments), then its prefetched loads issued
+  auto open = [&](PF& F, int q, uint32_t a0, uint32_t a1) {
+    const uint32_t b0 = a0 < (uint32_t)kq ? a0 : (uint32_t)kq, b1 = a1 < (uint32_t)kq ? a1 : (uint32_t)kq;
+    F.seg_lo = lane < n_live ? (uint32_t)my_slot * kq + b0 : 0u;
+    F.seg_n = lane < n_live && b1 > b0 ? b1 - b0 : 0u;
+#pragma unroll
+    for (int r = 0; r < kPreRows; ++r) F.ld[r] = row_load(F.seg_lo, F.seg_n, r, 0);
+    if (!EXPORT) {
+      const Rsrc rp = param_rsrc(q);
+#pragma unroll
+      for (int v = 0; v < 2; ++v) F.th[v] = load8<PBF16>(rp, eb + 8 * v);
+    }
+  };
+
+  // one entry's read-add-write of both sums (entries outside the quarter go
+  // to the sink pair)
+  auto add = [&](int lo, ET e, float w1, float w2) {
+    const uint32_t i = E::word(e) - (uint32_t)lo;
+    const uint32_t zw = i < (uint32_t)kQuarter ? i : (uint32_t)kQuarter;
+    const float v = E::val(e);
+    const float2 a = z[zw];
+    z[zw] = make_float2(a.x + w1 * v, a.y + w2 * (v * v));
+  };
+  // quarter q rebuilt from its loads, then updated; `next` issues the next
+  // quarter's prefetch once this quarter's own loads are out
+  auto apply = [&](PF& F, int q, auto&& next) {
+    const int lo = q * kQuarter, s = quarter_size(q);
+    uint32_t longest = F.seg_n;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      const uint32_t o = __shfl_xor(longest, d, kWave);
+      longest = longest > o ? longest : o;
+    }
+    longest = sgpr(longest);
+    // rows with more than 64 entries in the quarter: their entries 64 .. 127
+    // form a second chunk, added after every row's first chunk
+    const uint64_t over = ballot(F.seg_n > (uint32_t)kWave);
+    const int n_over = (int)popc(over);
+    const bool fast = n_live <= FR && longest <= 2u * kWave && n_over <= kOverflow;
+    // the rest of the rows and the second chunks
+    ET ld[FR - kPreRows], lx[kOverflow];
+    int xr[kOverflow];
+#pragma unroll
+    for (int r = kPreRows; r < FR; ++r) ld[r - kPreRows] = row_load(F.seg_lo, F.seg_n, r, 0);
+    uint64_t om = over;
+#pragma unroll
+    for (int j = 0; j < kOverflow; ++j) {
+      const int r = om ? (int)__builtin_ctzll(om) : 0;
+      om &= om - 1;
+      xr[j] = r;
+      lx[j] = row_load(F.seg_lo, j < n_over ? F.seg_n : 0u, r, kWave);
+    }
+    const uint32_t seg_lo = F.seg_lo, seg_n = F.seg_n;
+    ET pre[kPreRows];
+#pragma unroll
+    for (int r = 0; r < kPreRows; ++r) pre[r] = F.ld[r];
+    const Raw8<PBF16> th0 = F.th[0], th1 = F.th[1];
+    next();
+    {
+      const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int w = 0; w < 8; ++w) *(float4*)(z + w * 2 * kWave + lane * 2) = zero;
+    }
+    wave_sync();  // the cleared accumulators before any entry is added
+    if (fast) {
+      // (one row's arithmetic at a time: the adds are a chain through LDS,
+      // and arithmetic hoisted ahead of it only holds registers)
+#pragma unroll
+      for (int r = 0; r < FR; ++r) {
+        if ((uint32_t)lane < __builtin_amdgcn_readlane(seg_n, r))
+          add(lo, r < kPreRows ? pre[r] : ld[r - kPreRows], weight(w1s, r), weight(w2s, r));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int j = 0; j < kOverflow; ++j) {
+        if (j < n_over && (uint32_t)lane + kWave < __builtin_amdgcn_readlane(seg_n, xr[j]))
+          add(lo, lx[j], weight(w1s, xr[j]), weight(w2s, xr[j]));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+      for (int r = 0; r < n_live; ++r) {
+        const uint32_t n = __builtin_amdgcn_readlane(seg_n, r), at = __builtin_amdgcn_readlane(seg_lo, r);
+        const float w1 = weight(w1s, r), w2 = weight(w2s, r);
+        for (uint32_t x = (uint32_t)lane; x < n; x += kWave) add(lo, E::load(rw, at + x), w1, w2);
+      }
+    }
+    wave_sync();
+    if ((int)eb >= s) return;
+    const bool full = s == kQuarter;
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+      float s1[8], s2[8];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float4 u = *(const float4*)(z + eb + 8 * v + 2 * w);  // elements eb + 8v + 2w, + 1
+        s1[2 * w] = u.x; s2[2 * w] = u.y; s1[2 * w + 1] = u.z; s2[2 * w + 1] = u.w;
+      }
+      if (EXPORT) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if ((int)eb + 8 * v + e < s) {
+            mhat[g.e0 + lo + eb + 8 * v + e] = p.c1 * s1[e];
+            vhat[g.e0 + lo + eb + 8 * v + e] = p.c2 * s2[e];
+          }
+        continue;
+      }
+      float thf[8], out[8];
+      unpack8<PBF16>(v == 0 ? th0 : th1, thf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float mh = p.c1 * s1[e];
+        const float vh = p.c2 * s2[e];
+        const float den = p.eps + __builtin_amdgcn_sqrtf(vh);
+        const bool none = (s1[e] == 0.0f) & (s2[e] == 0.0f);
+        const float d = none ? 0.0f : p.lr * (mh * __builtin_amdgcn_rcpf(den));
+        const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
+        out[e] = base - d;
+      }
+      store8<PBF16>(param_rsrc(q), eb + 8 * v, s, full, out);
+    }
+  };
+
+  // quarter q + 1's prefetch goes out before quarter q is rebuilt, and
+  // quarter q + 2's table words with it
+  PF A, B;
+  uint32_t t0, t1;
+  table_load(q_begin, t0, t1);
+  open(A, q_begin, t0, t1);
+  if (q_begin + 1 < q_end) table_load(q_begin + 1, t0, t1);
+  auto step = [&](PF& cur, PF& nxt, int q) {
+    apply(cur, q, [&]() {
+      if (q + 1 < q_end) {
+        open(nxt, q + 1, t0, t1);
+        if (q + 2 < q_end) table_load(q + 2, t0, t1);
+      }
+    });
+  };
+  for (int q = q_begin; q < q_end; q += 2) {
+    step(A, B, q);
+    if (q + 1 < q_end) step(B, A, q + 1);
   }
 }
 
-// One workgroup per 4096-element sub-block of each block of [first, first + count).
+// Waves of kQuartersPerWave quarters over each block of [first, first + count).
 template <bool PB, bool VF, bool EXPORT>
 hipError_t launch_update_large(const StepParams& p, int64_t first, int64_t count, float* mh, float* vh,
                                hipStream_t stream) {
   if (count <= 0) return hipSuccess;
-  const int32_t nsub = (p.block + kSubBlock - 1) / kSubBlock;
-  hipLaunchKernelGGL((update_large_kernel<PB, VF, EXPORT>), dim3((uint32_t)(count * nsub)), dim3(256),
-                     update_large_lds_bytes<VF>(), stream, p, first, count, nsub, mh, vh);
+  const int32_t nq = (p.block + kQuarter - 1) / kQuarter;
+  const int32_t nw = (nq + kQuartersPerWave - 1) / kQuartersPerWave;
+  hipLaunchKernelGGL((update_large_kernel<PB, VF, EXPORT>), dim3((uint32_t)(count * nw)), dim3(kWave),
+                     update_large_lds_bytes(), stream, p, first, count, nw, mh, vh);
   return hipGetLastError();
 }
 
 }  // namespace
 
-size_t update_large_lds() { return update_large_lds_bytes<true>(); }
+size_t update_large_lds() { return update_large_lds_bytes(); }
 
 hipError_t launch_update_large_blocks(const StepParams& p, int param_bf16, int value_f32, int64_t first,
                                       int64_t count, hipStream_t stream) {

@@ -141,8 +141,8 @@ int make_plan(const microadam_config* c, const int64_t* numels, int32_t n, Tenso
   pl.stats_stride = pl.big ? 0 : (uint64_t)(B / Bq) * 8;
   // whole 128-byte lines per record, so that a row can be written as whole
   // lines without touching another block's record; blocks above 4096 add a
-  // table of m * ceil(B_d/4096) uint32 segment starts behind the rows
-  const uint64_t table = B > 4096 ? (uint64_t)m * ((B + 4095) / 4096) * 4 : 0;
+  // table of m * ceil(B_d/1024) uint32 segment starts behind the rows
+  const uint64_t table = B > 4096 ? (uint64_t)m * ((B + 1023) / 1024) * 4 : 0;
   pl.win_stride = ((uint64_t)m * k_full * eb + table + 127) & ~(uint64_t)127;
   int64_t full = 0;
   for (int32_t j = 0; j < n; ++j) {

@@ -290,6 +290,9 @@ __device__ __forceinline__ void store8(Rsrc r, uint32_t elem, int s, bool full, 
 // bf16 values: one word (index | bf16 << 16); f32 values: (index, value).
 template <bool VF32> struct Entry {
   typedef typename std::conditional<VF32, u32x2, uint32_t>::type T;
+  // an entry number whose byte offset lies past every record (a buffer
+  // load there reads 0)
+  static constexpr uint32_t kFar = VF32 ? 0x1FFFFFFEu : 0x3FFFFFFEu;
   __device__ static T make(uint32_t idx, float v) {
     if constexpr (VF32) return u32x2{idx, __float_as_uint(v)};
     else return idx | (to_bf16_bits(v) << 16);
@@ -951,9 +954,11 @@ __device__ __forceinline__ void lane_partials(const float (&a)[EPL / 8][8], cons
   }
 }
 
-// Blocks above this size take the multi-wave select and the per-sub-block
-// update; their window records carry a table of sub-block segment starts.
+// Blocks above this size take the multi-wave select and the per-quarter
+// update; their window records carry a table of segment starts per quarter
+// of kQuarter elements.
 constexpr int kSubBlock = 4096;
+constexpr int kQuarter = 1024;
 
 }  // namespace
 }  // namespace microadam

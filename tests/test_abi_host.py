@@ -95,11 +95,12 @@ def test_state_bytes_buckets_spanning_blocks(lib):
 def test_state_bytes_large_blocks(lib):
     """Blocks above 4096 elements (the flat 1.5e9 workload's B_d = 65536,
     k = 3277, m = 20, B_q = 128): each window record holds the m rows and an
-    m x 16 table of uint32 segment starts, padded to whole 128-byte lines."""
+    m x 64 table of uint32 segment starts (one per 1024-element quarter),
+    padded to whole 128-byte lines."""
     cfg = ma.make_config(density=0.05, window=20, ef_bucket=128, topk_block=65536)
     n = 65536 * 2 + 12032          # two full blocks and a tail of 12032 (k 602)
     pad = lambda x: -(-x // 256) * 256
-    rec = -(-(20 * 3277 * 4 + 20 * 16 * 4) // 128) * 128
+    rec = -(-(20 * 3277 * 4 + 20 * 64 * 4) // 128) * 128
     per_block = (65536 // 2, (65536 // 128) * 8, rec)
     got = ma.microadam_state_bytes(cfg, [n])
     assert got == sum(pad(3 * x) for x in per_block)
