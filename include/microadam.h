@@ -67,12 +67,10 @@ enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
  *                (Algorithm 4); >= 0.
  *   window       m, rows in the sliding window, 1..64.
  *   ef_bits      b, bits per EF code: 4 (the paper's choice, Section 3.1) or
- *                8 (a wider code for the same buckets).  8 needs
- *                topk_block <= 4096.
+ *                8 (a wider code for the same buckets).
  *   ef_rounding  how Q rounds: MICROADAM_ROUND_NEAREST (Algorithm 2, half to
  *                even) or MICROADAM_ROUND_RANDOMIZED (Lemma 1: floor((x -
- *                delta)/u + xi), xi ~ U[0, 1), which makes Q unbiased); the
- *                latter needs topk_block <= 4096.
+ *                delta)/u + xi), xi ~ U[0, 1), which makes Q unbiased).
  *   seed         key of the randomized rounding's random stream: element i
  *                of tensor j at step t draws xi = (w >> 8) * 2^-24 from word
  *                i mod 4 of Philox4x32-10 (Salmon et al., SC 2011) at counter

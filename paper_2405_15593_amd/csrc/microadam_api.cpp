@@ -98,8 +98,6 @@ int validate_config(const microadam_config* c) {
     return fail(MICROADAM_ERR_INVALID_ARG, "ef_rounding must be NEAREST or RANDOMIZED");
   if (c->fused != 0 && c->fused != 1) return fail(MICROADAM_ERR_INVALID_ARG, "fused must be 0 or 1");
   if (c->reserved != 0) return fail(MICROADAM_ERR_INVALID_ARG, "reserved must be 0");
-  if ((c->ef_bits != 4 || c->ef_rounding != MICROADAM_ROUND_NEAREST) && c->topk_block > 4096)
-    return fail(MICROADAM_ERR_UNSUPPORTED, "8-bit or randomized error feedback needs topk_block <= 4096");
   return MICROADAM_OK;
 }
 

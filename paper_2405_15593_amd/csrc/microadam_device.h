@@ -95,9 +95,10 @@ hipError_t launch_moments(const StepParams& p, int64_t first_block, int64_t num_
 size_t step_lds_bytes(int block, int k_full, int value_f32);
 
 // Per translation unit: the one-wave select for blocks of up to 4096
-// elements in each error-feedback format (k_select_{near,rand}{4,8}.hip),
-// the multi-wave select (k_select_large.hip), and the updates and moment
-// exports (k_update.hip, k_update_large.hip).
+// elements and the multi-wave select for larger blocks, in each
+// error-feedback format (k_select_{near,rand}{4,8}.hip,
+// k_select_large_{near,rand}{4,8}.hip), and the updates and moment exports
+// (k_update.hip, k_update_large.hip).
 hipError_t launch_select_near4(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
                                hipStream_t stream);
 hipError_t launch_select_near8(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
@@ -106,8 +107,14 @@ hipError_t launch_select_rand4(const StepParams& p, int grad_bf16, int value_f32
                                hipStream_t stream);
 hipError_t launch_select_rand8(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
                                hipStream_t stream);
-hipError_t launch_select_large_blocks(const StepParams& p, int grad_bf16, int value_f32, int64_t first,
-                                      int64_t count, hipStream_t stream);
+hipError_t launch_select_large_near4(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                                  hipStream_t stream);
+hipError_t launch_select_large_near8(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                                  hipStream_t stream);
+hipError_t launch_select_large_rand4(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                                  hipStream_t stream);
+hipError_t launch_select_large_rand8(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                                  hipStream_t stream);
 hipError_t launch_update_blocks(const StepParams& p, int param_bf16, int value_f32, int64_t first, int64_t count,
                                 hipStream_t stream);
 hipError_t launch_update_large_blocks(const StepParams& p, int param_bf16, int value_f32, int64_t first,

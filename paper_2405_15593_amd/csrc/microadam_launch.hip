@@ -17,10 +17,13 @@ hipError_t launch_select(const StepParams& p, int grad_bf16, int value_f32, int6
                          hipStream_t stream) {
   if (count <= 0) return hipSuccess;
   if (p.block > kSubBlock) {
-    // the multi-wave kernel has the default code format only (the host
-    // rejects the others there)
-    if (p.ef_mode != 0) return hipErrorInvalidValue;
-    return launch_select_large_blocks(p, grad_bf16, value_f32, first, count, stream);
+    switch (p.ef_mode) {
+      case 0: return launch_select_large_near4(p, grad_bf16, value_f32, first, count, stream);
+      case 1: return launch_select_large_near8(p, grad_bf16, value_f32, first, count, stream);
+      case 2: return launch_select_large_rand4(p, grad_bf16, value_f32, first, count, stream);
+      case 3: return launch_select_large_rand8(p, grad_bf16, value_f32, first, count, stream);
+      default: return hipErrorInvalidValue;
+    }
   }
   switch (p.ef_mode) {
     case 0: return launch_select_near4(p, grad_bf16, value_f32, first, count, stream);

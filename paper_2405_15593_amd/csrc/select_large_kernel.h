@@ -1,4 +1,8 @@
-// The multi-wave select kernel for Top-K blocks above 4096 elements.
+// The multi-wave select kernel for Top-K blocks above 4096 elements and its
+// launch templates.  Included by the translation units that instantiate it
+// for one error-feedback format each.
+#pragma once
+
 #include "microadam_common.h"
 
 namespace microadam {
@@ -40,7 +44,7 @@ struct LargeLds {
   static constexpr size_t words() { return (size_t)6 * NW + 4 + 64 + 256 + region(); }
 };
 
-template <int NW, bool LB, bool GBF16, bool VF32>
+template <int NW, bool LB, bool GBF16, bool VF32, int EFM>
 __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, int64_t first, int64_t count) {
   constexpr int EPL = 64, NV = 8, NT = NW * kWave, CAP = NT * EPL, R = kCandPerThread, NC = NT * R;
   constexpr int SPT = kSamples / NT, SPL = kSamples / kWave;  // samples per thread; per lane
@@ -62,10 +66,11 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   const int64_t gb = first + xcd_block(block_id(), count);
 
   const uint32_t nbk = (uint32_t)(p.block >> bl);
-  const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * (p.block >> 1), (uint32_t)(p.block >> 1));
+  const uint32_t ef_bytes = (EFM & kEf8) ? (uint32_t)p.block : (uint32_t)(p.block >> 1);
+  const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * ef_bytes, ef_bytes);
   const Rsrc rs = make_rsrc(p.state + p.stats_plane + (uint64_t)gb * nbk * 8, nbk * 8);
   const bool wide = p.block == CAP;
-  LaneIn<EPL, LB, GBF16> in;
+  LaneIn<EPL, LB, GBF16, EFM> in;
   lane_load_state(in, re, rs, eb, bl, wide);
   const Block b = locate(p, gb);
   const int s = b.s, kq = b.kq;
@@ -500,7 +505,8 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   }
 
   // ---------------------------------------------- 4. e = Q(a with a[I] = 0)
-  lane_quantize_store<EPL, LB>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs);
+  lane_quantize_store<EPL, LB, EFM>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs,
+                                    EfStream{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi});
 }
 
 // Waves of the large-block select kernel: 4096 elements each, 2 to 16.
@@ -509,38 +515,39 @@ inline int large_waves(int block) {
   return w <= 2 ? 2 : w <= 4 ? 4 : w <= 8 ? 8 : 16;
 }
 
-template <int NW, bool GB, bool VF>
+template <int NW, bool GB, bool VF, int EFM>
 hipError_t launch_select_large_t(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
   if (count <= 0) return hipSuccess;
   const size_t lds = LargeLds<NW>::words() * 4;
   if ((1 << p.bucket_log2) >= 64)
-    hipLaunchKernelGGL((select_large_kernel<NW, true, GB, VF>), dim3((uint32_t)count), dim3(NW * kWave), lds, stream,
+    hipLaunchKernelGGL((select_large_kernel<NW, true, GB, VF, EFM>), dim3((uint32_t)count), dim3(NW * kWave), lds, stream,
                        p, first, count);
   else
-    hipLaunchKernelGGL((select_large_kernel<NW, false, GB, VF>), dim3((uint32_t)count), dim3(NW * kWave), lds,
+    hipLaunchKernelGGL((select_large_kernel<NW, false, GB, VF, EFM>), dim3((uint32_t)count), dim3(NW * kWave), lds,
                        stream, p, first, count);
   return hipGetLastError();
 }
 
-template <bool GB, bool VF>
+template <bool GB, bool VF, int EFM>
 hipError_t launch_select_large(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
   switch (large_waves(p.block)) {
-    case 2: return launch_select_large_t<2, GB, VF>(p, first, count, stream);
-    case 4: return launch_select_large_t<4, GB, VF>(p, first, count, stream);
-    case 8: return launch_select_large_t<8, GB, VF>(p, first, count, stream);
-    default: return launch_select_large_t<16, GB, VF>(p, first, count, stream);
+    case 2: return launch_select_large_t<2, GB, VF, EFM>(p, first, count, stream);
+    case 4: return launch_select_large_t<4, GB, VF, EFM>(p, first, count, stream);
+    case 8: return launch_select_large_t<8, GB, VF, EFM>(p, first, count, stream);
+    default: return launch_select_large_t<16, GB, VF, EFM>(p, first, count, stream);
   }
 }
 
-}  // namespace
-
-hipError_t launch_select_large_blocks(const StepParams& p, int grad_bf16, int value_f32, int64_t first,
-                                      int64_t count, hipStream_t stream) {
+// Blocks above 4096 elements in the error-feedback format EFM.
+template <int EFM>
+hipError_t launch_select_large_mode(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
+                                    hipStream_t stream) {
   if (grad_bf16)
-    return value_f32 ? launch_select_large<true, true>(p, first, count, stream)
-                     : launch_select_large<true, false>(p, first, count, stream);
-  return value_f32 ? launch_select_large<false, true>(p, first, count, stream)
-                   : launch_select_large<false, false>(p, first, count, stream);
+    return value_f32 ? launch_select_large<true, true, EFM>(p, first, count, stream)
+                     : launch_select_large<true, false, EFM>(p, first, count, stream);
+  return value_f32 ? launch_select_large<false, true, EFM>(p, first, count, stream)
+                   : launch_select_large<false, false, EFM>(p, first, count, stream);
 }
 
+}  // namespace
 }  // namespace microadam

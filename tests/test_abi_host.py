@@ -106,6 +106,18 @@ def test_state_bytes_large_blocks(lib):
     assert got == sum(pad(3 * x) for x in per_block)
 
 
+def test_state_bytes_large_blocks_8bit(lib):
+    """8-bit codes with B_d = 8192: one code byte per element, and the
+    record's segment table of m x 8 uint32 behind the rows."""
+    cfg = ma.make_config(density=0.01, window=3, ef_bucket=64, topk_block=8192, ef_bits=8,
+                         ef_rounding=ma.MICROADAM_ROUND_RANDOMIZED, seed=11)
+    n = 8192 * 2 + 500
+    pad = lambda x: -(-x // 256) * 256
+    rec = -(-(3 * 82 * 4 + 3 * 8 * 4) // 128) * 128   # k = ceil(0.01 * 8192) = 82
+    per_block = (8192, (8192 // 64) * 8, rec)
+    assert ma.microadam_state_bytes(cfg, [n]) == sum(pad(3 * x) for x in per_block)
+
+
 BAD = [
     (dict(density=0.0), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(density=1.5), ma.MICROADAM_ERR_INVALID_ARG),
@@ -121,8 +133,6 @@ BAD = [
     (dict(window=65), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bits=6), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bits=0), ma.MICROADAM_ERR_INVALID_ARG),
-    (dict(ef_bits=8, topk_block=8192), ma.MICROADAM_ERR_UNSUPPORTED),
-    (dict(ef_rounding=1, topk_block=8192), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_rounding=2), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(ef_bucket=100000, topk_block=8192), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bucket=1000, topk_block=4096), ma.MICROADAM_ERR_UNSUPPORTED),

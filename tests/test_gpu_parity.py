@@ -110,6 +110,19 @@ CASES = {
                                       grad_dist="sparse_spikes", degenerate=True), 4),
     "block8192_sign_grad": (dict(numels=[8192 + 3000], block=8192, grad_dist="signs", grad_scale=1e-2,
                                  window=3, degenerate=True), 4),
+    # the same formats in the multi-wave select (blocks above 4096): 8-bit
+    # codes at B_d = 8192, randomized 4-bit codes at the flat workload's
+    # B_d = 65536 with its bucket of 128 and k = 5%, and randomized 8-bit
+    # codes at B_d = 16384 with buckets of 16 and a second tensor whose only
+    # block is ragged (tensor number 1 in the random stream)
+    "block8192_ef8_nearest": (dict(numels=[8192 * 2 + 700], block=8192, bucket=64, density=0.02, window=3,
+                                   ef_bits=8), 4),
+    "block65536_randomized_4bit": (dict(numels=[65536 + 5000], block=65536, bucket=128, density=0.05,
+                                        window=4, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
+                                        ef_rounding=1, ef_seed=777), 4),
+    "block16384_randomized_8bit": (dict(numels=[16384 * 2 + 300, 9000], block=16384, bucket=16, density=0.01,
+                                        window=3, grad_dist="student_t4", ef_bits=8, ef_rounding=1,
+                                        ef_seed=2 ** 33 + 5), 4),
     "zero_grad_randomized_8bit": (dict(numels=[2048 + 48], block=1024, bucket=16, grad_dist="zeros",
                                        window=2, ef_bits=8, ef_rounding=1, ef_seed=3, degenerate=True), 3),
     # buckets spanning Top-K blocks (B_q >= B_d; Section 3.1 names 100K):
@@ -267,6 +280,13 @@ def test_flat_1p5e9_ties_sampled():
     """One 1.5e9-element bf16 tensor, B_d = 65536, k = 3277, m = 20,
     B_q = 128, Student-t(2) gradients snapped to 64 magnitudes; 5 steps."""
     _workload_sampled("flat1p5b_ties_bf16", 5, 4999, (4,))
+
+
+def test_flat_1p5e9_randomized_8bit_sampled():
+    """The flat 1.5e9 workload with 8-bit codes and randomized rounding
+    (the multi-wave select in that format, element numbers up to 1.5e9 in
+    the random stream), 3 steps, every 4999th block."""
+    _workload_sampled("flat1p5b_ties_bf16", 3, 4999, (2,), ef_bits=8, ef_rounding=1, ef_seed=99991)
 
 
 def test_randomized_sampled_offsets():
