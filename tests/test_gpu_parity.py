@@ -50,9 +50,10 @@ CASES = {
     "window_max_64": (dict(numels=[4096, 900], window=64, block=512, bucket=64, density=0.01), 66),
     "mixed_dtypes_bf16_param_f32_grad": (dict(numels=[6000], param_dtype=bf16, grad_dtype=f32,
                                               window=3), 4),
-    # blocks above 4096 (several waves per block in the select, sub-blocks of
-    # 4096 in the update): B_d = 8192 with binary32 window values, and a
-    # B_d = 20000 block (not a multiple of 4096) with buckets of 16
+    # blocks above 4096 (several waves per block in the select, runs of
+    # 1024-element quarters in the update): B_d = 8192 with binary32 window
+    # values, and a B_d = 20000 block (not a multiple of 4096) with buckets
+    # of 16
     "block8192_f32_window": (dict(numels=[8192 * 3 + 100], block=8192, bucket=64, density=0.01,
                                   value_f32=True, window=3), 5),
     "block20000_bucket16": (dict(numels=[20000 * 2 + 777, 5000], block=20000, bucket=16,
@@ -69,8 +70,9 @@ CASES = {
                             grad_scale=1e-3), 4),
     "block65536_f32_values": (dict(numels=[65536 + 9000], block=65536, density=0.01, window=2,
                                    value_f32=True), 3),
-    # the large-block update's two ways of reading the window: more than 24
-    # live rows, and rows of more than 256 entries per 4096-element sub-block
+    # the large-block update's ways of reading the window: more than 24 live
+    # rows (row by row), and rows of more than 64 entries per 1024-element
+    # quarter (second chunks; more than four such rows, row by row)
     "block8192_window30": (dict(numels=[8192 * 2 + 300], block=8192, density=0.02, window=30,
                                 param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3), 28),
     "block8192_dense_rows": (dict(numels=[8192 + 4100], block=8192, density=0.1, window=4), 6),
