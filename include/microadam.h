@@ -211,6 +211,11 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels,
  * and grads[j] (read only) are device pointers to numels[j] contiguous
  * elements of the init dtypes, 16-byte aligned.  lr: the step size eta for
  * this step, or NaN to use cfg.lr.  The step counter t advances by one.
+ * Non-finite gradients (NaN, +-inf), which the method leaves undefined, give
+ * unspecified parameters and state in the Top-K blocks that hold them (in
+ * their buckets, when buckets span blocks); every other block is computed as
+ * if they were absent, and no memory outside params, grads and the state is
+ * touched.
  */
 int microadam_step(microadam_handle h, void* const* params,
                    const void* const* grads, int32_t n_tensors, double lr,
