@@ -153,29 +153,22 @@ def read_traffic(kernel: str, workload: str):
 def _oracle_worker(args) -> tuple:
     """One CPU-baseline worker: the oracle, as it stands (single-threaded C),
     on `blocks` Top-K blocks of the workload's shape run as one tensor for
-    m + 2 steps; returns (parameters, seconds) of the last three steps (window
-    full).  Blocks are independent, so the workers' blocks are a sample of the
+    m + 2 steps, with the workload's gradient distribution and dtypes;
+    returns (parameters, seconds) of the last three steps (window full).
+    Blocks are independent, so the workers' blocks are a sample of the
     workload's."""
     wname, blocks, seed = args
-    import numpy as np
     import oracle
     from paper_2405_15593_amd import workloads as wl
     w = wl.WORKLOADS[wname]
     o = oracle.default()
-    n = blocks * w.block
+    n = min(blocks * w.block, w.d)
     st = o.tensor(n, block=w.block, bucket=w.bucket, window=w.window, density=w.density,
                   value_bf16=True, param_bf16=w.param_dtype.itemsize == 2)
-    rng = np.random.default_rng(seed)
-
-    def bf16(x):   # round to bf16 (nearest, ties to even) in numpy
-        b = x.astype(np.float32).view(np.uint32)
-        b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
-        return b.view(np.float32)
-
-    theta = bf16(rng.standard_normal(n) * w.param_std)
+    theta = wl.draw(n, "normal", w.param_std, seed, "cpu", w.param_dtype).float().numpy()
     steps, timed_steps, timed = w.window + 2, 3, 0.0
     for t in range(1, steps + 1):
-        g = bf16(rng.standard_t(4, n) * w.grad_scale)
+        g = wl.draw(n, w.grad_dist, w.grad_scale, wl.grad_seed(t, 0, seed), "cpu", w.grad_dtype).float().numpy()
         t0 = time.perf_counter()
         st.step(theta, g, t, w.lr)
         dt = time.perf_counter() - t0
@@ -194,29 +187,39 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(w, blocks_per_worker: int, workers: int) -> dict:
+def cpu_baseline(w, elems_per_worker: int, workers: int) -> dict:
     """The CPU oracle on this host's cores: one worker first alone (the
     single-core rate), then `workers` at once in separate processes (started
     fresh, so they share nothing with this GPU process), each on its own
-    blocks; the rate is all workers' parameters over the slowest worker's
-    time."""
+    blocks (about `elems_per_worker` parameters, at most the workload); the
+    rate is all workers' parameters over the slowest worker's time."""
     import concurrent.futures as cf
     import multiprocessing as mp
+    # (the budget is for the 12 steps of a window of 10; longer windows run
+    # more steps on proportionally fewer parameters)
+    elems = elems_per_worker * 12 // (w.window + 2)
+    blocks = max(1, min(elems // w.block, -(-w.d // w.block)))
+    n = min(blocks * w.block, w.d)
     ctx = mp.get_context("spawn")
     with cf.ProcessPoolExecutor(max_workers=workers, mp_context=ctx) as ex:
-        n1, t1 = ex.submit(_oracle_worker, (w.name, blocks_per_worker, 1000)).result()
-        res = list(ex.map(_oracle_worker, [(w.name, blocks_per_worker, 1001 + i) for i in range(workers)]))
+        n1, t1 = ex.submit(_oracle_worker, (w.name, blocks, 1000)).result()
+        print(f"[bench] CPU oracle: one worker {n1 / t1:.3e} params/s", file=sys.stderr, flush=True)
+        res = list(ex.map(_oracle_worker, [(w.name, blocks, 1001 + i) for i in range(workers)]))
     params = sum(r[0] for r in res)
     wall = max(r[1] for r in res)
     rate = params / wall
+    dt = lambda d: "bf16" if d.itemsize == 2 else "f32"
+    whole = n >= w.d
     return {"value": rate, "unit": "params/s", "cores": workers, "kind": "oracle",
             "single_core_value": n1 / t1, "nproc": os.cpu_count(), "cpu_model": cpu_model(),
-            "extrapolated": True,
-            "sample": (f"{workers} processes x {blocks_per_worker} blocks of {w.block} "
-                       f"({workers * blocks_per_worker * w.block} params, "
-                       f"{100.0 * workers * blocks_per_worker * w.block / w.d:.2f}% of the workload) of the same "
-                       f"shape, bf16, steps {w.window}-{w.window + 2} (window full) timed; "
-                       f"the slowest worker took {wall:.2f} s; one full step extrapolated: {w.d / rate:.1f} s")}
+            "extrapolated": not whole,
+            "sample": (f"{workers} processes, each on "
+                       + (f"the whole workload as one tensor of {n} params"
+                          if whole else
+                          f"{blocks} blocks of {w.block} ({n} params, {100.0 * n / w.d:.2f}% of the workload each)")
+                       + f", {dt(w.param_dtype)} params, {dt(w.grad_dtype)} {w.grad_dist} grads, "
+                       f"steps {w.window}-{w.window + 2} (window full) timed; the slowest worker took {wall:.2f} s; "
+                       f"one full step {'extrapolated' if not whole else 'per process'}: {w.d / rate * workers if whole else w.d / rate:.2f} s")}
 
 
 def main() -> int:
@@ -225,8 +228,10 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama2_7b_bf16")
-    ap.add_argument("--cpu-blocks", type=int, default=1000,
-                    help="Top-K blocks per CPU-baseline worker (0 disables the CPU baseline)")
+    ap.add_argument("--cpu-elems", type=int, default=4_096_000,
+                    help="parameters per CPU-baseline worker, in whole Top-K blocks (0 disables the CPU baseline)")
+    ap.add_argument("--cpu-blocks", type=int, default=None,
+                    help="the same budget in Top-K blocks per worker (overrides --cpu-elems; 0 disables)")
     ap.add_argument("--cpu-workers", type=int, default=0,
                     help="CPU-baseline processes (0: the cores this process may use, at most 16)")
     ap.add_argument("--ef-bits", type=int, default=4, choices=(4, 8), help="bits per EF code")
@@ -313,11 +318,13 @@ def main() -> int:
           f"{ {k: round(v['ms'], 3) for k, v in kernels.items()} }", file=sys.stderr, flush=True)
 
     cpu = None
-    if args.cpu_blocks > 0:
+    if args.cpu_blocks is not None:
+        args.cpu_elems = args.cpu_blocks * w.block
+    if args.cpu_elems > 0:
         workers = args.cpu_workers or min(16, len(os.sched_getaffinity(0)))
-        print(f"[bench] CPU oracle baseline: {workers} processes x {args.cpu_blocks} blocks", file=sys.stderr,
+        print(f"[bench] CPU oracle baseline: {workers} processes x {args.cpu_elems} params", file=sys.stderr,
               flush=True)
-        cpu = cpu_baseline(w, args.cpu_blocks, workers)
+        cpu = cpu_baseline(w, args.cpu_elems, workers)
 
     ms_per_step = wall / args.steps * 1e3
     out = {
