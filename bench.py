@@ -158,6 +158,8 @@ def _oracle_worker(args) -> tuple:
     Blocks are independent, so the workers' blocks are a sample of the
     workload's."""
     wname, blocks, seed = args
+    import torch
+    torch.set_num_threads(1)   # the input generator's threads would compete with the other workers
     import oracle
     from paper_2405_15593_amd import workloads as wl
     w = wl.WORKLOADS[wname]
