@@ -82,8 +82,8 @@ enum { MICROADAM_F32 = 0, MICROADAM_BF16 = 1 };
  *                two in [8, 512] dividing topk_block (buckets inside blocks),
  *                or any size >= topk_block (buckets of each tensor's
  *                elements [c*B_q, (c+1)*B_q), spanning blocks; Section 3.1
- *                names 100K), which needs topk_block <= 4096 and runs the
- *                quantization as a second pass over the block.
+ *                names 100K), which runs the quantization as a second pass
+ *                over the block.
  *   topk_block   B_d, Top-K block size; at most
  *                65536 (block-relative indices are uint16).  This build
  *                implements multiples of 16 and returns

@@ -1,6 +1,7 @@
 // Steps with quantization buckets spanning Top-K blocks: the select kernel's
 // partials form, the bucket reduction and the second quantization pass.
 #include "select_kernel.h"
+#include "select_large_kernel.h"
 
 namespace microadam {
 namespace {
@@ -44,26 +45,33 @@ __global__ void __launch_bounds__(256) bucket_reduce_kernel(StepParams p) {
 // 2, Q; Lemma 1 with kEfRandom): recomputes a = g + Q^-1(e) exactly as the
 // select kernel did (same codes, same pairs), zeroes the elements of the
 // block's new window row, and quantizes with the new pairs.  One wave per
-// block, 64 elements per lane.
+// 4096-element sub-block of a block (the whole block up to 4096 elements),
+// 64 elements per lane.  Above 4096 the sub-block's entries of the new row
+// are those of its four 1024-element quarters, found through the record's
+// segment table.
 template <bool GBF16, bool VF32, int EFM>
 __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
-requant_kernel(StepParams p, int64_t first, int64_t count) {
+requant_kernel(StepParams p, int64_t first, int64_t count, int32_t nsub) {
   constexpr int EPL = 64, NV = EPL / 8, CAP = kWave * EPL;
   constexpr int CW = (EFM & kEf8) ? 2 : 1;
   using E = Entry<VF32>;
-  __shared__ uint32_t kept[CAP / 32];  // bit i: element i is in the new row
+  __shared__ uint32_t kept[CAP / 32];  // bit i: element off + i is in the new row
 
   const int lane = thread_id();
-  const uint32_t eb = (uint32_t)lane * EPL;
-  const int64_t gb = first + xcd_block(block_id(), count);
+  const int64_t w = xcd_block(block_id(), count * nsub);
+  const int64_t gb = first + w / nsub;
+  const uint32_t off = (uint32_t)(w % nsub) * CAP;  // the sub-block's first element
+  const uint32_t eb = off + (uint32_t)lane * EPL;   // the lane's first element in the block
   const uint32_t ef_bytes = (EFM & kEf8) ? (uint32_t)p.block : (uint32_t)(p.block >> 1);
   const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * ef_bytes, ef_bytes);
-  const bool wide = p.block == CAP;
+  // 16-byte code accesses when no lane's codes straddle the end of the block's
+  const bool wide = p.block % CAP == 0;
   LaneIn<EPL, true, GBF16, EFM> in;
   lane_load_codes(in, re, eb, wide);
   const Block b = locate(p, gb);
   const int s = b.s, kq = b.kq;
-  const bool full = s == CAP;
+  if ((int)off >= s) return;  // a sub-block past the end of a ragged block
+  const bool full = s - (int)off >= CAP;
   const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + b.e0 * (GBF16 ? 2 : 4), vec_bytes<GBF16>(s));
   lane_load_grad(in, rg, eb);
   const LqBuckets old_b = lq_buckets(p, b, eb, EPL, 0), new_b = lq_buckets(p, b, eb, EPL, 1);
@@ -73,9 +81,23 @@ requant_kernel(StepParams p, int64_t first, int64_t count) {
   wave_sync();
   const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
   const uint32_t row0 = (uint32_t)p.new_slot * kq;
-  for (int j = lane; j < kq; j += kWave) {
-    const uint32_t i = E::idx(E::load(rw, row0 + j));
-    atomicOr(&kept[(i >> 5) & (CAP / 32 - 1)], 1u << (i & 31));
+  // the row's entries of this sub-block: [j0, j1)
+  uint32_t j0 = 0, j1 = (uint32_t)kq;
+  if (p.block > CAP) {
+    constexpr uint32_t EB = VF32 ? 8u : 4u;
+    const int nq = (p.block + kQuarter - 1) / kQuarter;
+    const int q0 = (int)(off / kQuarter), q1 = q0 + CAP / kQuarter;
+    const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
+    const uint32_t table = (uint32_t)p.window * p.k_full * EB + (uint32_t)p.new_slot * nq * 4;
+    const uint32_t a0 = __builtin_amdgcn_raw_buffer_load_b32(rrec, table + (uint32_t)q0 * 4, 0, 0);
+    const uint32_t a1 = q1 < nq ? __builtin_amdgcn_raw_buffer_load_b32(rrec, table + (uint32_t)q1 * 4, 0, 0)
+                                : (uint32_t)kq;
+    j0 = sgpr(a0 < (uint32_t)kq ? a0 : (uint32_t)kq);  // clamped: any content gives a bounded read
+    j1 = sgpr(a1 < (uint32_t)kq ? a1 : (uint32_t)kq);
+  }
+  for (uint32_t j = j0 + (uint32_t)lane; j < j1; j += kWave) {
+    const uint32_t i = E::idx(E::load(rw, row0 + j)) - off;
+    if (i < (uint32_t)CAP) atomicOr(&kept[i >> 5], 1u << (i & 31));
   }
   wave_sync();
 
@@ -124,6 +146,7 @@ requant_kernel(StepParams p, int64_t first, int64_t count) {
 
 template <bool GB, bool VF, int EF8>
 hipError_t launch_select_partials_t(const StepParams& p, hipStream_t stream) {
+  if (p.block > kSubBlock) return launch_select_large<GB, VF, EF8, true>(p, 0, p.total_blocks, stream);
   const size_t lds = select_lds_words() * 4;
   hipLaunchKernelGGL((select_kernel<64, true, GB, VF, EF8, true>), dim3((uint32_t)p.total_blocks), dim3(kWave), lds,
                      stream, p, (int64_t)0, p.total_blocks);
@@ -138,8 +161,9 @@ hipError_t launch_select_partials_d(const StepParams& p, hipStream_t stream) {
 
 template <bool GB, bool VF, int EFM>
 hipError_t launch_requant_t(const StepParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((requant_kernel<GB, VF, EFM>), dim3((uint32_t)p.total_blocks), dim3(kWave), 0, stream, p,
-                     (int64_t)0, p.total_blocks);
+  const int32_t nsub = (p.block + kSubBlock - 1) / kSubBlock;
+  hipLaunchKernelGGL((requant_kernel<GB, VF, EFM>), dim3((uint32_t)(p.total_blocks * nsub)), dim3(kWave), 0, stream,
+                     p, (int64_t)0, p.total_blocks, nsub);
   return hipGetLastError();
 }
 

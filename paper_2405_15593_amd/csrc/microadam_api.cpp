@@ -90,8 +90,6 @@ int validate_config(const microadam_config* c) {
   }
   if (c->topk_block % 16 != 0)
     return fail(MICROADAM_ERR_UNSUPPORTED, "topk_block must be a multiple of 16");
-  if (buckets_span_blocks(c) && c->topk_block > 4096)
-    return fail(MICROADAM_ERR_UNSUPPORTED, "buckets of topk_block or more elements need topk_block <= 4096");
   if (c->window_value_dtype != MICROADAM_BF16 && c->window_value_dtype != MICROADAM_F32)
     return fail(MICROADAM_ERR_INVALID_ARG, "window_value_dtype must be BF16 or F32");
   if (c->ef_rounding != MICROADAM_ROUND_NEAREST && c->ef_rounding != MICROADAM_ROUND_RANDOMIZED)

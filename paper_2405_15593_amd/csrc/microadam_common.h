@@ -911,12 +911,13 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
   }
 }
 
-// Per block and bucket, the (min, max) of the residual (elements past the
-// block's end excluded; an empty part gives (+inf, -inf)): pairs for the
-// block's first bucket and for the next one, written by lane 0.
+// The (min, max) of the residual of the wave's elements in the block's first
+// bucket and in the next one (elements past the block's end excluded; an
+// empty part gives (+inf, -inf)), reduced over the wave: out = (min0, max0,
+// min1, max1) in every lane.
 template <int EPL>
-__device__ __forceinline__ void lane_partials(const float (&a)[EPL / 8][8], const StepParams& p, const Block& b,
-                                              uint32_t eb, int rem, int64_t gb) {
+__device__ __forceinline__ void wave_partials(const float (&a)[EPL / 8][8], const StepParams& p, const Block& b,
+                                              uint32_t eb, int rem, float (&out)[4]) {
   constexpr int NV = EPL / 8;
   const int64_t bq = p.big_bucket;
   const int64_t split = ((b.e0 / bq) + 1) * bq - b.e0;  // block element where the next bucket starts
@@ -947,11 +948,28 @@ __device__ __forceinline__ void lane_partials(const float (&a)[EPL / 8][8], cons
     mn1 = __builtin_fminf(mn1, __shfl_xor(mn1, d, kWave));
     mx1 = __builtin_fmaxf(mx1, __shfl_xor(mx1, d, kWave));
   }
-  if (thread_id() == 0) {
-    const Rsrc rp = make_rsrc(p.state + p.partial_plane + (uint64_t)gb * 16, 16);
-    __builtin_amdgcn_raw_buffer_store_b128(
-        u32x4{__float_as_uint(mn0), __float_as_uint(mx0), __float_as_uint(mn1), __float_as_uint(mx1)}, rp, 0, 0, 0);
-  }
+  out[0] = mn0;
+  out[1] = mx0;
+  out[2] = mn1;
+  out[3] = mx1;
+}
+
+// A block's partials (its first bucket's and the next one's (min, max))
+// to the partials plane.
+__device__ __forceinline__ void store_partials(const StepParams& p, int64_t gb, const float (&x)[4]) {
+  const Rsrc rp = make_rsrc(p.state + p.partial_plane + (uint64_t)gb * 16, 16);
+  __builtin_amdgcn_raw_buffer_store_b128(
+      u32x4{__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3])}, rp, 0, 0, 0);
+}
+
+// Per block and bucket, the (min, max) of the residual for a block held by
+// one wave: the wave's partials, written by lane 0.
+template <int EPL>
+__device__ __forceinline__ void lane_partials(const float (&a)[EPL / 8][8], const StepParams& p, const Block& b,
+                                              uint32_t eb, int rem, int64_t gb) {
+  float x[4];
+  wave_partials<EPL>(a, p, b, eb, rem, x);
+  if (thread_id() == 0) store_partials(p, gb, x);
 }
 
 // Blocks above this size take the multi-wave select and the per-quarter

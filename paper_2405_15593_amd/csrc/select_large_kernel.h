@@ -44,12 +44,17 @@ struct LargeLds {
   static constexpr size_t words() { return (size_t)6 * NW + 4 + 64 + 256 + region(); }
 };
 
-template <int NW, bool LB, bool GBF16, bool VF32, int EFM>
+// LQ: buckets spanning blocks -- the decode takes each lane's two buckets
+// from the bucket table, and the block ends with its partials (the (min, max)
+// of the residual in its first bucket and in the next one, over all waves)
+// instead of the codes, which a second pass quantizes.
+template <int NW, bool LB, bool GBF16, bool VF32, int EFM, bool LQ = false>
 __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, int64_t first, int64_t count) {
   constexpr int EPL = 64, NV = 8, NT = NW * kWave, CAP = NT * EPL, R = kCandPerThread, NC = NT * R;
   constexpr int SPT = kSamples / NT, SPL = kSamples / kWave;  // samples per thread; per lane
   constexpr int DPW = 16 / NW;                                  // sample digits per wave
   static_assert(SPT >= 1 && SPT <= NV, "one to eight samples per thread");
+  static_assert(!LQ || (LB && (EFM & kEfRandom) == 0), "buckets spanning blocks: the decode has no random draws");
   using E = Entry<VF32>;
   extern __shared__ __align__(16) uint32_t smem[];
   uint32_t* const cnt = smem;           // [2][NW] per-wave counts, alternating between searches
@@ -71,8 +76,11 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   const Rsrc rs = make_rsrc(p.state + p.stats_plane + (uint64_t)gb * nbk * 8, nbk * 8);
   const bool wide = p.block == CAP;
   LaneIn<EPL, LB, GBF16, EFM> in;
-  lane_load_state(in, re, rs, eb, bl, wide);
+  if constexpr (LQ) lane_load_codes(in, re, eb, wide);
+  else lane_load_state(in, re, rs, eb, bl, wide);
   const Block b = locate(p, gb);
+  LqBuckets lqb = {};
+  if constexpr (LQ) lqb = lq_buckets(p, b, eb, EPL, 0);
   const int s = b.s, kq = b.kq;
   const bool full = s == CAP;
   const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + b.e0 * (GBF16 ? 2 : 4), vec_bytes<GBF16>(s));
@@ -81,7 +89,8 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   // ---------------------------------------------- 1. a = g + Q^-1(e)
   float a[NV][8];
   const int rem = s - (int)eb;
-  lane_decode(in, a, rem, full);
+  if constexpr (LQ) lane_decode_lq(in, lqb, a, rem, full);
+  else lane_decode(in, a, rem, full);
 
   // workgroup sum of one value per wave; `buf` alternates between calls
   auto wg_sum = [&](uint32_t wave_value, int buf) {
@@ -505,8 +514,30 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   }
 
   // ---------------------------------------------- 4. e = Q(a with a[I] = 0)
-  lane_quantize_store<EPL, LB, EFM>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs,
-                                    EfStream{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi});
+  if constexpr (LQ) {
+    lane_zero_kept<EPL>(a, T, notie, i_last, eb);
+    // the waves' partials combined in LDS (dig is free since the search)
+    float x[4];
+    wave_partials<EPL>(a, p, b, eb, rem, x);
+    if (lane == 0) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) dig[4 * wave + c] = __float_as_uint(x[c]);
+    }
+    lds_sync();
+    if (tid == 0) {
+#pragma unroll
+      for (int w = 1; w < NW; ++w) {
+        x[0] = __builtin_fminf(x[0], __uint_as_float(dig[4 * w]));
+        x[1] = __builtin_fmaxf(x[1], __uint_as_float(dig[4 * w + 1]));
+        x[2] = __builtin_fminf(x[2], __uint_as_float(dig[4 * w + 2]));
+        x[3] = __builtin_fmaxf(x[3], __uint_as_float(dig[4 * w + 3]));
+      }
+      store_partials(p, gb, x);
+    }
+  } else {
+    lane_quantize_store<EPL, LB, EFM>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs,
+                                      EfStream{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi});
+  }
 }
 
 // Waves of the large-block select kernel: 4096 elements each, 2 to 16.
@@ -515,11 +546,14 @@ inline int large_waves(int block) {
   return w <= 2 ? 2 : w <= 4 ? 4 : w <= 8 ? 8 : 16;
 }
 
-template <int NW, bool GB, bool VF, int EFM>
+template <int NW, bool GB, bool VF, int EFM, bool LQ = false>
 hipError_t launch_select_large_t(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
   if (count <= 0) return hipSuccess;
   const size_t lds = LargeLds<NW>::words() * 4;
-  if ((1 << p.bucket_log2) >= 64)
+  if constexpr (LQ)
+    hipLaunchKernelGGL((select_large_kernel<NW, true, GB, VF, EFM, true>), dim3((uint32_t)count), dim3(NW * kWave),
+                       lds, stream, p, first, count);
+  else if ((1 << p.bucket_log2) >= 64)
     hipLaunchKernelGGL((select_large_kernel<NW, true, GB, VF, EFM>), dim3((uint32_t)count), dim3(NW * kWave), lds, stream,
                        p, first, count);
   else
@@ -528,13 +562,13 @@ hipError_t launch_select_large_t(const StepParams& p, int64_t first, int64_t cou
   return hipGetLastError();
 }
 
-template <bool GB, bool VF, int EFM>
+template <bool GB, bool VF, int EFM, bool LQ = false>
 hipError_t launch_select_large(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
   switch (large_waves(p.block)) {
-    case 2: return launch_select_large_t<2, GB, VF, EFM>(p, first, count, stream);
-    case 4: return launch_select_large_t<4, GB, VF, EFM>(p, first, count, stream);
-    case 8: return launch_select_large_t<8, GB, VF, EFM>(p, first, count, stream);
-    default: return launch_select_large_t<16, GB, VF, EFM>(p, first, count, stream);
+    case 2: return launch_select_large_t<2, GB, VF, EFM, LQ>(p, first, count, stream);
+    case 4: return launch_select_large_t<4, GB, VF, EFM, LQ>(p, first, count, stream);
+    case 8: return launch_select_large_t<8, GB, VF, EFM, LQ>(p, first, count, stream);
+    default: return launch_select_large_t<16, GB, VF, EFM, LQ>(p, first, count, stream);
   }
 }
 

@@ -106,6 +106,19 @@ def test_state_bytes_large_blocks(lib):
     assert got == sum(pad(3 * x) for x in per_block)
 
 
+def test_state_bytes_large_blocks_spanning_buckets(lib):
+    """Buckets of 20,000 over blocks of 8192: codes, two tables of bucket
+    pairs, per-block partials, and window records holding the m rows and the
+    m x 8 segment table."""
+    cfg = ma.make_config(density=0.02, window=3, ef_bucket=20000, topk_block=8192)
+    numels = [8192 * 3 + 700, 20000]            # 4 and 3 blocks; 2 and 1 buckets
+    pad = lambda x: -(-x // 256) * 256
+    blocks, buckets = 7, 3
+    rec = -(-(3 * 164 * 4 + 3 * 8 * 4) // 128) * 128   # k = ceil(0.02 * 8192) = 164
+    want = pad(blocks * 4096) + pad(2 * buckets * 8) + pad(blocks * 16) + pad(blocks * rec)
+    assert ma.microadam_state_bytes(cfg, numels) == want
+
+
 def test_state_bytes_large_blocks_8bit(lib):
     """8-bit codes with B_d = 8192: one code byte per element, and the
     record's segment table of m x 8 uint32 behind the rows."""
@@ -134,7 +147,6 @@ BAD = [
     (dict(ef_bits=6), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bits=0), ma.MICROADAM_ERR_INVALID_ARG),
     (dict(ef_rounding=2), ma.MICROADAM_ERR_INVALID_ARG),
-    (dict(ef_bucket=100000, topk_block=8192), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bucket=1000, topk_block=4096), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bucket=48), ma.MICROADAM_ERR_UNSUPPORTED),
     (dict(ef_bucket=1), ma.MICROADAM_ERR_INVALID_ARG),

@@ -135,6 +135,17 @@ CASES = {
                                         density=0.02, ef_bits=8, ef_rounding=1, ef_seed=5), 5),
     "big_bucket_equals_block": (dict(numels=[4096 * 5 + 17, 900], bucket=4096, window=2,
                                      grad_dist="student_t4"), 4),
+    # the same above 4096 (the multi-wave select writes partials; the second
+    # pass runs per 4096-element sub-block, taking its entries of the new row
+    # through the segment table): buckets of 20,000 over blocks of 8192 with a
+    # second tensor, buckets of 100,000 over blocks of 65536 with randomized
+    # codes, and buckets of exactly B_d = 16384 with 8-bit codes
+    "block8192_bucket20000": (dict(numels=[8192 * 3 + 700, 20000], block=8192, bucket=20000, density=0.02,
+                                   window=3, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3), 4),
+    "block65536_bucket100k_randomized": (dict(numels=[65536 * 2 + 5000], block=65536, bucket=100000, density=0.05,
+                                              window=3, grad_dist="student_t4", ef_rounding=1, ef_seed=4242), 3),
+    "block16384_bucket_equals_block_8bit": (dict(numels=[16384 * 2 + 100, 3000], block=16384, bucket=16384,
+                                                 density=0.01, window=2, ef_bits=8), 3),
     # the fused step kernel (blocks of 2049 to 4096 elements, k <= 128,
     # m * ceil(k/64) <= 16, one dtype): its cooperative exact search on tie
     # groups at the threshold (k = 123) and on +-1 signs, the largest
