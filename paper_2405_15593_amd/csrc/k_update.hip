@@ -8,15 +8,19 @@ namespace {
 // ============================================================ update
 // The accumulators hold, per element of the block, sum beta1^r V and sum
 // beta2^r V^2 (z1 and z2; or z1 alone, one after the other), then z1 the
-// parameter decrement.  Element i lives at word
-// ((i >> 2) & 3) * 4*NT + (i >> 4) * 4 + (i & 3), so that the 16 elements of a
-// thread are four 16-byte words at a stride of 4*NT words and a wave's
-// 16-byte accesses fall on consecutive addresses.  Word CAP of each array is
-// a sink for lanes without an entry, which keeps the sparse updates free of
-// branches.
-template <int NT>
+// parameter decrement.  A thread's 16 elements are its parameter vectors
+// (Vec16: vector v of thread t holds the EV elements from v*EV*NT + t*EV),
+// read as four groups of four: group g of thread t is the 16-byte word at
+// (g*NT + t)*4, so a wave's 16-byte accesses fall on consecutive addresses.
+// Element i = v*EV*NT + t*EV + e lies in group v*EV/4 + e/4, at word e mod 4
+// (for binary32 parameters that is word i itself).  Word CAP of each array
+// is a sink for lanes without an entry, which keeps the sparse updates free
+// of branches.
+template <int NT, bool PBF16>
 __device__ __forceinline__ uint32_t zpos(uint32_t i) {
-  return ((i >> 2) & 3u) * (4u * NT) + (i >> 4) * 4u + (i & 3u);
+  constexpr uint32_t EV = Vec16<PBF16>::EV, G = EV / 4;
+  const uint32_t v = i / (EV * NT), t = (i / EV) & (NT - 1), e = i & (EV - 1);
+  return ((v * G + e / 4) * NT + t) * 4 + (e & 3);
 }
 
 // Staged window positions of the update kernel: KC chunks of 64, rounded up
@@ -75,7 +79,6 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
   ET* const stage = (ET*)(ONE ? z2 : z2 + CAP + 16);      // [NP * NT]; chunks past KC are not read
 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr(tid / kWave);
-  const uint32_t eb = (uint32_t)tid * kLaneElems;
   const int m = p.window, n_live = p.n_live;
   // oldest live row first: the row written at step s is slot (s-1) mod m
   const int slot0 = (p.new_slot + 1 + m - n_live) % m;
@@ -108,13 +111,15 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
   for (int i = 0; i < NP; ++i) {
     uint32_t entry;
     position(tid + NT * i, entry);
-    w[i] = E::load(rw, entry);
+    w[i] = E::template load<kStream>(rw, entry);
   }
+  using V = Vec16<PBF16>;
+  constexpr int EV = V::EV;
   const Rsrc rp = make_rsrc((const void*)u.base, vec_bytes<PBF16>(s));
-  Raw8<PBF16> th[2];
+  u32x4 th[V::NV];
   if (!EXPORT) {
 #pragma unroll
-    for (int v = 0; v < 2; ++v) th[v] = load8<PBF16>(rp, eb + v * 8);
+    for (int v = 0; v < V::NV; ++v) th[v] = V::load(rp, V::template first<NT>(v, tid));
   }
   const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
   const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
@@ -133,7 +138,7 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
     uint32_t entry;
     const bool valid = position(q, entry);
     const uint32_t idx = E::idx(w[i]);
-    const uint32_t zw = valid && idx < (uint32_t)s ? zpos<NT>(idx) : (uint32_t)CAP;
+    const uint32_t zw = valid && idx < (uint32_t)s ? zpos<NT, PBF16>(idx) : (uint32_t)CAP;
     stage[q] = E::with_word(w[i], zw);
   }
   lds_sync();
@@ -224,7 +229,7 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
         for (int jj = lane; jj < kq; jj += kWave) {
           const ET x = E::load(rw, slot * kq + jj);
           const uint32_t i = E::idx(x);
-          const uint32_t zp = i < (uint32_t)s ? zpos<NT>(i) : (uint32_t)CAP;
+          const uint32_t zp = i < (uint32_t)s ? zpos<NT, PBF16>(i) : (uint32_t)CAP;
           const float v = E::val(x);
           const float vv = v * v;
           const float x1 = w1 * v, x2 = w2 * vv;
@@ -239,7 +244,7 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
           for (int jj = lane; jj < kq; jj += kWave) {
             const uint32_t i = E::idx(E::load(rw, slot * kq + jj));
             if (i < (uint32_t)s) {
-              const uint32_t zp = zpos<NT>(i);
+              const uint32_t zp = zpos<NT, PBF16>(i);
               const float s2 = z2[zp];
               if (s2 >= 0.0f) {
                 z1[zp] = step_of(z1[zp], s2);
@@ -260,7 +265,7 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
       const float a1[4] = {s1.x, s1.y, s1.z, s1.w}, a2[4] = {s2.x, s2.y, s2.z, s2.w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const uint32_t i = eb + q * 4 + r;
+        const uint32_t i = V::template first<NT>(q / (EV / 4), tid) + (q % (EV / 4)) * 4 + r;
         if ((int)i < s) {
           mhat[u.e0 + i] = p.c1 * a1[r];
           vhat[u.e0 + i] = p.c2 * a2[r];
@@ -273,19 +278,24 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
   // ------------------------------------------------ 6. parameter update
   const bool full = s == NT * kLaneElems;
 #pragma unroll
-  for (int v = 0; v < 2; ++v) {
-    const uint32_t e0 = eb + v * 8;   // vectors past s store nothing
-    const float4 u0 = *(const float4*)(z1 + (2 * v) * 4 * NT + tid * 4);
-    const float4 u1 = *(const float4*)(z1 + (2 * v + 1) * 4 * NT + tid * 4);
-    const float upd[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
-    float thf[8], out[8];
-    unpack8<PBF16>(th[v], thf);
+  for (int v = 0; v < V::NV; ++v) {
+    const uint32_t e0 = V::template first<NT>(v, tid);  // vectors past s store nothing
+    float upd[EV], thf[EV], out[EV];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
+    for (int q = 0; q < EV / 4; ++q) {
+      const float4 x = *(const float4*)(z1 + ((v * (EV / 4) + q) * NT + tid) * 4);
+      upd[4 * q] = x.x;
+      upd[4 * q + 1] = x.y;
+      upd[4 * q + 2] = x.z;
+      upd[4 * q + 3] = x.w;
+    }
+    V::unpack(th[v], thf);
+#pragma unroll
+    for (int e = 0; e < EV; ++e) {
       const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
       out[e] = base - upd[e];
     }
-    store8<PBF16>(rp, e0, s, full, out);
+    V::store(rp, e0, s, full, out);
   }
 }
 

@@ -286,6 +286,60 @@ __device__ __forceinline__ void store8(Rsrc r, uint32_t elem, int s, bool full, 
   }
 }
 
+// ------------------------------------------------ streamed 16-byte vectors
+// Cache policy of the accesses that stream through a step once (parameters,
+// gradients, codes, bucket pairs, window records): nt, bit 1 of the buffer
+// instructions' cache-policy operand.  Measured on MI355X with coalesced
+// accesses (every 16-byte access of a wave in one contiguous 1 KB run), nt on
+// both the loads and the stores of a pattern moves it 10-11% faster (a
+// parameter read-modify-write with window reads: 5.17 -> 4.71 ms per 29.65 GB;
+// the select's reads and writes: 4.16 -> 3.83 ms per 22.17 GB); with each
+// lane's accesses 128 bytes apart it is slower instead (4.25 -> 7.6 ms), so
+// it goes only on coalesced accesses.
+constexpr int kStream = 2;
+
+// A thread's 16 elements of a block as 16-byte vectors that consecutive
+// threads take in turn: vector v of thread t holds the EV elements from
+// v*EV*NT + t*EV (EV = 8 for bf16, 4 for binary32), so each vector access of
+// a wave covers one contiguous kilobyte.
+template <bool BF16> struct Vec16 {
+  static constexpr int EV = BF16 ? 8 : 4;  // elements per vector
+  static constexpr int NV = kLaneElems / EV;  // vectors per thread
+  template <int NT>
+  __device__ static uint32_t first(int v, int t) { return (uint32_t)(v * EV * NT + t * EV); }
+  __device__ static u32x4 load(Rsrc r, uint32_t elem) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, elem * (BF16 ? 2u : 4u), 0, kStream);
+  }
+  __device__ static void unpack(u32x4 x, float (&out)[EV]) {
+    if constexpr (BF16) {
+#pragma unroll
+      for (int h = 0; h < 4; ++h) { out[2 * h] = bf16_lo(x[h]); out[2 * h + 1] = bf16_hi(x[h]); }
+    } else {
+#pragma unroll
+      for (int h = 0; h < 4; ++h) out[h] = __uint_as_float(x[h]);
+    }
+  }
+  // Stores the vector at elem: whole when `full` (workgroup-uniform), else
+  // only its elements below s.
+  __device__ static void store(Rsrc r, uint32_t elem, int s, bool full, const float (&in)[EV]) {
+    if (full) {
+      u32x4 w;
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        w[h] = BF16 ? (to_bf16_bits(in[2 * h]) | (to_bf16_bits(in[2 * h + 1]) << 16)) : __float_as_uint(in[h]);
+      __builtin_amdgcn_raw_buffer_store_b128(w, r, elem * (BF16 ? 2u : 4u), 0, kStream);
+    } else {
+#pragma unroll
+      for (int e = 0; e < EV; ++e) {
+        if ((int)elem + e < s) {
+          if constexpr (BF16) __builtin_amdgcn_raw_buffer_store_b16((uint16_t)to_bf16_bits(in[e]), r, (elem + e) * 2, 0, 0);
+          else __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(in[e]), r, (elem + e) * 4, 0, 0);
+        }
+      }
+    }
+  }
+};
+
 // ------------------------------------------------------- window entries
 // bf16 values: one word (index | bf16 << 16); f32 values: (index, value).
 template <bool VF32> struct Entry {
@@ -318,9 +372,10 @@ template <bool VF32> struct Entry {
     if constexpr (VF32) return e[0];
     else return e & 0xFFFFu;
   }
+  template <int AUX = 0>
   __device__ static T load(Rsrc r, uint32_t entry) {
-    if constexpr (VF32) return __builtin_amdgcn_raw_buffer_load_b64(r, entry * 8, 0, 0);
-    else return __builtin_amdgcn_raw_buffer_load_b32(r, entry * 4, 0, 0);
+    if constexpr (VF32) return __builtin_amdgcn_raw_buffer_load_b64(r, entry * 8, 0, AUX);
+    else return __builtin_amdgcn_raw_buffer_load_b32(r, entry * 4, 0, AUX);
   }
   __device__ static void store(Rsrc r, uint32_t entry, T e) {
     if constexpr (VF32) __builtin_amdgcn_raw_buffer_store_b64(e, r, entry * 8, 0, 0);
