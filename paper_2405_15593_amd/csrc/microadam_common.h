@@ -821,6 +821,91 @@ __device__ __forceinline__ void lane_store_codes(const uint32_t (&wv)[(EPL / 8) 
   }
 }
 
+// ------------------------------------- coalesced block loads and stores
+// One wave over a 4096-element block (64 elements per lane: lane l owns
+// [64l, 64l + 64)) with bf16 gradients and 4-bit codes.  A lane's own run is
+// 128 bytes of gradient and 32 bytes of codes, so loading it directly gives
+// every 16-byte access of the wave a 128-byte (or 32-byte) stride.  Instead
+// the wave loads the block as contiguous kilobytes (access v of lane l is
+// bytes 1024v + 16l) with the nt policy, and the data reaches its owner
+// through LDS.  Layouts in LDS (byte offsets; the padding keeps 16 lanes'
+// 16-byte reads on distinct banks):
+//   gradient: element e of a half block at 2e + 16*(e / 64), 4608 bytes per
+//     half (a half is 32 lanes' runs, loaded by accesses 0-3 or 4-7);
+//   codes: code byte c at kTrCodes + c + 16*(c / 32), 3072 bytes.
+// The two halves of the gradient pass one after the other through the same
+// 4608 bytes, so the exchange needs 7680 bytes of LDS.
+constexpr uint32_t kTrCodes = 4608;
+constexpr uint32_t kTrBytes = 7680;
+static_assert(kTrBytes <= select_lds_words() * 4, "the exchange reuses the select kernel's LDS");
+
+struct CoalescedIn {
+  u32x4 g[8];
+  u32x4 c[2];
+};
+
+__device__ __forceinline__ void coalesced_load_codes(CoalescedIn& x, Rsrc re, int lane) {
+#pragma unroll
+  for (int q = 0; q < 2; ++q) x.c[q] = __builtin_amdgcn_raw_buffer_load_b128(re, 1024 * q + 16 * lane, 0, kStream);
+}
+__device__ __forceinline__ void coalesced_load_grad(CoalescedIn& x, Rsrc rg, int lane) {
+#pragma unroll
+  for (int v = 0; v < 8; ++v) x.g[v] = __builtin_amdgcn_raw_buffer_load_b128(rg, 1024 * v + 16 * lane, 0, kStream);
+}
+
+// Hands the loaded block to the lanes that own it: lane l's gradient vectors
+// (8 elements each) and code words (8 codes each) in element order.
+template <bool LB, int EFM>
+__device__ __forceinline__ void coalesced_exchange(const CoalescedIn& x, LaneIn<64, LB, true, EFM>& in,
+                                                   uint32_t* lds, int lane) {
+  static_assert((EFM & kEf8) == 0, "4-bit codes");
+  uint8_t* const b = (uint8_t*)lds;
+  const uint32_t wg = 16u * (uint32_t)lane + 16u * (uint32_t)(lane >> 3);  // + 1152v: access v of this lane
+  const uint32_t rg = 144u * (uint32_t)(lane & 31);                         // + 16V: this lane's vector V
+#pragma unroll
+  for (int v = 0; v < 4; ++v) *(u32x4*)(b + 1152 * v + wg) = x.g[v];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+    *(u32x4*)(b + kTrCodes + 1536 * q + 16 * lane + 16 * (lane >> 1)) = x.c[q];
+  wave_sync();
+  if (lane < 32) {
+#pragma unroll
+    for (int v = 0; v < 8; ++v) in.graw[v].w[0] = *(const u32x4*)(b + rg + 16 * v);
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const u32x4 t = *(const u32x4*)(b + kTrCodes + 48 * lane + 16 * h);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) in.cw[4 * h + j] = t[j];
+  }
+  wave_sync();
+#pragma unroll
+  for (int v = 0; v < 4; ++v) *(u32x4*)(b + 1152 * v + wg) = x.g[4 + v];
+  wave_sync();
+  if (lane >= 32) {
+#pragma unroll
+    for (int v = 0; v < 8; ++v) in.graw[v].w[0] = *(const u32x4*)(b + rg + 16 * v);
+  }
+  wave_sync();
+}
+
+// Stores the lane's 4-bit codes (one word per vector) through LDS as
+// coalesced 16-byte accesses with the nt policy; the whole record of the
+// block is written (codes past the block's end are 0).
+__device__ __forceinline__ void lane_store_codes_coalesced(const uint32_t (&wv)[8], uint32_t* lds, Rsrc re) {
+  uint8_t* const b = (uint8_t*)lds + kTrCodes;
+  const int lane = thread_id() & (kWave - 1);
+  wave_sync();
+#pragma unroll
+  for (int h = 0; h < 2; ++h) *(u32x4*)(b + 48 * lane + 16 * h) = u32x4{wv[4 * h], wv[4 * h + 1], wv[4 * h + 2], wv[4 * h + 3]};
+  wave_sync();
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const u32x4 t = *(const u32x4*)(b + 1536 * q + 16 * lane + 16 * (lane >> 1));
+    __builtin_amdgcn_raw_buffer_store_b128(t, re, 1024 * q + 16 * lane, 0, kStream);
+  }
+}
+
 // a[I] = 0 (Algorithm 1): the kept elements are |a| > T, and |a| == T up to
 // index i_last; every |a| >= T when notie.
 template <int EPL>
@@ -861,10 +946,15 @@ __device__ __forceinline__ void lane_zero_kept(float (&a)[EPL / 8][8], uint32_t 
 // kEfRandom the randomized Q of Lemma 1): zeroes the kept elements (|a| >
 // T, and |a| == T up to index i_last; every |a| >= T when notie), computes
 // the bucket (min, max) pairs and the codes, and stores both.
+//
+// tr_lds (one-wave kernels with 64 elements per lane and 4-bit codes, over a
+// whole-lane block): the codes leave through LDS as coalesced 16-byte stores
+// (lane_store_codes_coalesced), and the bucket pairs with the nt policy.
 template <int EPL, bool LB, int EFM = 0>
 __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint32_t T, bool notie,
                                                     uint32_t i_last, uint32_t eb, int s, int rem, bool full, int bl,
-                                                    bool wide, Rsrc re, Rsrc rs, const EfStream& rs_ef = {}) {
+                                                    bool wide, Rsrc re, Rsrc rs, const EfStream& rs_ef = {},
+                                                    uint32_t* tr_lds = nullptr) {
   constexpr int NV = EPL / 8;
   constexpr bool EF8 = (EFM & kEf8) != 0;
   constexpr int CW = EF8 ? 2 : 1;
@@ -948,8 +1038,20 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
       for (int c = 0; c < CW; ++c) wv[CW * v + c] = w[c];
     }
   }
+  if constexpr (EPL == 64 && !EF8) {
+    if (tr_lds != nullptr) {
+      // every lane takes part in the exchange; codes past s are 0
+      lane_store_codes_coalesced(wv, tr_lds, re);
+      if constexpr (LB) {
+        if ((int)eb < s && (eb & ((1u << bl) - 1)) == 0)
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[0]), __float_as_uint(mx[0])}, rs,
+                                                (eb >> bl) * 8, 0, kStream);
+        return;
+      }
+    }
+  }
   if ((int)eb < s) {
-    lane_store_codes<EPL, EFM>(wv, eb, wide, re);
+    if (tr_lds == nullptr) lane_store_codes<EPL, EFM>(wv, eb, wide, re);
     if constexpr (LB) {
       if ((eb & ((1u << bl) - 1)) == 0)
         __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[0]), __float_as_uint(mx[0])}, rs,

@@ -34,16 +34,31 @@ select_kernel(StepParams p, int64_t first, int64_t count) {
   const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * ef_bytes, ef_bytes);
   const Rsrc rs = make_rsrc(p.state + p.stats_plane + (uint64_t)gb * nbk * 8, nbk * 8);
   const bool wide = p.block == CAP;
+  // 4096-element blocks of bf16 gradients with 4-bit codes load and store
+  // the block as contiguous kilobytes and exchange it through LDS
+  // (coalesced_exchange); the other shapes load each lane's run directly
+  constexpr bool kCoal = EPL == 64 && GBF16 && (EFM & kEf8) == 0 && !LQ;
+  const bool coal = kCoal && wide;
   LaneIn<EPL, LB, GBF16, EFM> in;
-  if constexpr (LQ) lane_load_codes(in, re, eb, wide);
-  else lane_load_state(in, re, rs, eb, bl, wide);
+  CoalescedIn cx;
+  if constexpr (LQ) {
+    lane_load_codes(in, re, eb, wide);
+  } else if (coal) {
+#pragma unroll
+    for (int v = 0; v < (LB ? 1 : EPL / 8); ++v)
+      in.st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, kStream);
+    coalesced_load_codes(cx, re, lane);
+  } else {
+    lane_load_state(in, re, rs, eb, bl, wide);
+  }
   const Block b = locate(p, gb);
   LqBuckets lqb = {};
   if constexpr (LQ) lqb = lq_buckets(p, b, eb, EPL, 0);
   const int s = b.s, kq = b.kq;
   const bool full = s == CAP;
   const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + b.e0 * (GBF16 ? 2 : 4), vec_bytes<GBF16>(s));
-  lane_load_grad(in, rg, eb);
+  if (coal) coalesced_load_grad(cx, rg, lane);
+  else lane_load_grad(in, rg, eb);
   // The new row, bytes [row_lo, row_hi) of the block's window record, is
   // written as the whole 128-byte lines [span_lo, span_hi) that cover it
   // (records are whole lines): partial-line writes cost the memory system
@@ -55,7 +70,10 @@ select_kernel(StepParams p, int64_t first, int64_t count) {
   const uint32_t span_lo = row_lo & ~127u, span_hi = (row_hi + 127u) & ~127u;
   const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
   const uint32_t edge_off = lane < 32 ? span_lo + 4 * lane : span_hi - 128 + 4 * (lane - 32);
-  const uint32_t edge_old = __builtin_amdgcn_raw_buffer_load_b32(rrec, edge_off, 0, 0);
+  const uint32_t edge_old = __builtin_amdgcn_raw_buffer_load_b32(rrec, edge_off, 0, kStream);
+  if constexpr (kCoal) {
+    if (coal) coalesced_exchange(cx, in, smem, lane);
+  }
 
   // ---------------------------------------------- 1. a = g + Q^-1(e)
   float a[NV][8];
@@ -245,7 +263,8 @@ select_kernel(StepParams p, int64_t first, int64_t count) {
         wave_sync();
         const uint32_t nvec4 = (span_hi - span_lo) >> 4;
         for (uint32_t q = (uint32_t)lane; q < nvec4; q += kWave)
-          __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)(rowbuf + 4 * q), rrec, span_lo + 16 * q, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)(rowbuf + 4 * q), rrec, span_lo + 16 * q, 0,
+                                                 kStream);
       }
     }
   }
@@ -356,7 +375,8 @@ select_kernel(StepParams p, int64_t first, int64_t count) {
     lane_partials<EPL>(a, p, b, eb, rem, gb);
   } else {
     lane_quantize_store<EPL, LB, EFM>(a, T, notie, i_last, eb, s, rem, full, bl, wide, re, rs,
-                                      EfStream{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi});
+                                      EfStream{b.e0, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi},
+                                      coal ? smem : nullptr);
   }
 }
 
