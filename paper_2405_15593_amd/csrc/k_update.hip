@@ -23,31 +23,25 @@ __device__ __forceinline__ uint32_t zpos(uint32_t i) {
   return ((v * G + e / 4) * NT + t) * 4 + (e & 3);
 }
 
-// Staged window positions of the update kernel: KC chunks of 64, rounded up
-// to whole multiples of the workgroup so that every thread stages the same
-// count.
-template <int NT, int KC>
-constexpr int update_stage_entries() { return (KC * kWave + NT - 1) / NT * NT; }
-
-// LDS: the accumulators (two, or one with ONE), then the staged window
-// entries in chunk order.
+// LDS: the accumulators (two, or one with ONE).
 template <int NT, bool VF, int KC, bool ONE>
 constexpr size_t update_lds_bytes() {
-  return (size_t)(ONE ? 1 : 2) * (NT * kLaneElems + 16) * 4 + (size_t)update_stage_entries<NT, KC>() * (VF ? 8 : 4);
+  return (size_t)(ONE ? 1 : 2) * (NT * kLaneElems + 16) * 4;
 }
 
 // One workgroup per block.  One wave (rotating with the block) rebuilds the
 // moments of the block's window entries, oldest row first, and turns them
 // into parameter decrements; then every thread updates its own elements.
 //
-// Window entries are staged in LDS in the order the leader wave reads them:
-// position q = 64*c + lane of chunk c, where chunk c is part c mod R of the
-// live row c / R (oldest row first, R = ceil(k_q/64) parts of 64 entries),
-// each with its index replaced by its accumulator word (the sink word CAP for
-// positions without an entry).  A block whose live rows need more than KC
-// chunks is read by the leader straight from the window record.
+// The leader loads the window entries straight into registers, KC chunks of
+// 64 in the order it adds them: lane l of chunk c holds position 64*c + l,
+// where chunk c is part c mod R of the live row c / R (oldest row first,
+// R = ceil(k_q/64) parts of 64 entries); positions without an entry add into
+// the sink word CAP.  A block whose live rows need more than KC chunks is
+// read by the leader row by row from the window record.  The other waves
+// load only their parameters.
 //
-// ONE = true: one accumulator; the leader makes two passes over the staged
+// ONE = true: one accumulator; the leader makes two passes over its
 // entries (first moments, read back and cleared, then second moments), which
 // halves the LDS of a workgroup so that eight fit on a compute unit.  The
 // host launches it only where every block's live rows fit in KC chunks.
@@ -55,12 +49,15 @@ constexpr size_t update_lds_bytes() {
 // and v-hat instead of updating theta.
 // Waves per SIMD that the LDS of an update workgroup allows (160 KB per
 // compute unit, four SIMDs); telling the compiler lets it spend registers
-// up to that occupancy on keeping LDS reads in flight.
+// up to that occupancy on keeping LDS reads in flight.  A leader holding 16
+// chunks needs more than the 64 registers of eight waves per SIMD, so those
+// kernels ask for seven.
 template <int NT, bool VF, int KC, bool ONE>
 constexpr int update_waves_per_eu() {
   const int per_cu = (int)(163840 / update_lds_bytes<NT, VF, KC, ONE>());
   const int w = per_cu * (NT / kWave) / 4;
-  return w < 1 ? 1 : w > 8 ? 8 : w;
+  const int cap = KC >= 16 ? 7 : 8;
+  return w < 1 ? 1 : w > cap ? cap : w;
 }
 
 template <int NT, bool PBF16, bool VF32, bool EXPORT, int KC, bool ONE>
@@ -70,13 +67,11 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
   constexpr int NW = NT / kWave;
   constexpr int CAP = NT * kLaneElems;
   constexpr int kChunks = KC;                             // 64-entry chunks the leader holds
-  constexpr int NP = update_stage_entries<NT, KC>() / NT;  // staged positions per thread
   using E = Entry<VF32>;
   using ET = typename E::T;
   extern __shared__ __align__(16) uint32_t smem[];
   float* const z1 = (float*)smem;
   float* const z2 = z1 + CAP + 16;                        // not allocated with ONE
-  ET* const stage = (ET*)(ONE ? z2 : z2 + CAP + 16);      // [NP * NT]; chunks past KC are not read
 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr(tid / kWave);
   const int m = p.window, n_live = p.n_live;
@@ -90,8 +85,8 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
   const float rcp_r = 1.0f / (float)R;
   const bool staged = n_live * R <= kChunks;
 
-  // chunk c -> (live row, part): the entry of staged position q, and whether
-  // it holds one (uniform per block: kq, R, n_live)
+  // chunk c -> (live row, part): the entry of position q, and whether it
+  // holds one (uniform per block: kq, R, n_live)
   auto position = [&](int q, uint32_t& entry) {
     const int c = q >> 6;
     const int row = (int)(((float)c + 0.5f) * rcp_r);  // c / R for c < 2^10
@@ -103,15 +98,18 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
     return valid;
   };
 
-  // loads: window positions (unconditional; positions without an entry read
-  // entry 0 and are not used), then the parameters
+  // loads: the leader's window positions, KC chunks of 64 (positions without
+  // an entry read entry 0 and are not used), then every thread's parameters
+  const bool lead = wave == leader;
   const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, u.gb, kq);
-  ET w[NP];
+  ET w[kChunks];
+  if (lead && staged) {
 #pragma unroll
-  for (int i = 0; i < NP; ++i) {
-    uint32_t entry;
-    position(tid + NT * i, entry);
-    w[i] = E::template load<kStream>(rw, entry);
+    for (int c = 0; c < kChunks; ++c) {
+      uint32_t entry;
+      position(c * kWave + lane, entry);
+      w[c] = E::template load<kStream>(rw, entry);
+    }
   }
   using V = Vec16<PBF16>;
   constexpr int EV = V::EV;
@@ -132,18 +130,9 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
       if (!ONE) *(float4*)(z2 + q * 4 * NT + tid * 4) = zero;
     }
   }
-#pragma unroll
-  for (int i = 0; i < NP; ++i) {
-    const int q = tid + NT * i;
-    uint32_t entry;
-    const bool valid = position(q, entry);
-    const uint32_t idx = E::idx(w[i]);
-    const uint32_t zw = valid && idx < (uint32_t)s ? zpos<NT, PBF16>(idx) : (uint32_t)CAP;
-    stage[q] = E::with_word(w[i], zw);
-  }
   lds_sync();
 
-  if (wave == leader) {
+  if (lead) {
     auto step_of = [&](float s1, float s2) {
       const float mh = p.c1 * s1;
       const float vh = p.c2 * s2;
@@ -160,9 +149,11 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
         int row = 0, col = 0;
 #pragma unroll
         for (int c = 0; c < kChunks; ++c) {
-          const ET x = stage[c * kWave + lane];
-          zp[c] = E::word(x);
-          val[c] = E::val(x);
+          uint32_t entry;
+          const bool valid = position(c * kWave + lane, entry);
+          const uint32_t idx = E::idx(w[c]);
+          zp[c] = valid && idx < (uint32_t)s ? zpos<NT, PBF16>(idx) : (uint32_t)CAP;
+          val[c] = E::val(w[c]);
           rr[c] = (n_live - 1 - row) & (kMaxWindow - 1);
           if (++col == R) {
             col = 0;
