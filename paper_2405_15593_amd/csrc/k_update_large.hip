@@ -7,7 +7,9 @@ namespace {
 
 // ================================================ update, blocks above 4096
 // A wave takes kQuartersPerWave consecutive 1024-element quarters of a
-// block, one after the other (lane l: the quarter's elements 16*l + [0, 16)).
+// block, one after the other (lane l: the quarter's parameter vectors l and
+// 64 + l, Vec16, so that each vector access of the wave is one contiguous
+// kilobyte).
 // The live rows' entries of quarter q are the segments the select kernel
 // recorded in the record's table: row r holds them at positions
 // [table(r, q), table(r, q + 1)).  For each quarter the wave loads every live
@@ -44,7 +46,7 @@ struct Prefetch {
   using ET = typename Entry<VF32>::T;
   uint32_t seg_lo, seg_n;  // lane r < n_live: row r's segment (first entry in the record, length)
   ET ld[kPreRows];
-  Raw8<PBF16> th[2];       // the lane's 16 parameters
+  u32x4 th[Vec16<PBF16>::NV];  // the lane's 16 parameters
 };
 
 template <bool PBF16, bool VF32, bool EXPORT>
@@ -68,7 +70,8 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
   const int q_end = q_begin + kQuartersPerWave < nqv ? q_begin + kQuartersPerWave : nqv;
   const int kq = g.kq, m = p.window, n_live = p.n_live;
   const int nq_blk = (p.block + kQuarter - 1) / kQuarter;  // table entries per row
-  const uint32_t eb = (uint32_t)lane * 16;
+  using V = Vec16<PBF16>;
+  constexpr int EV = V::EV;
   // lane r < n_live: live row r (r = 0 is the oldest)
   const int my_slot = (p.new_slot + 1 + m - n_live + lane) % m;
   constexpr uint32_t EB = VF32 ? 8u : 4u;
@@ -89,7 +92,7 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
   // check the segment length, and no merge waits for the load
   auto row_load = [&](uint32_t seg_lo, uint32_t seg_n, int r, uint32_t off) {
     const uint32_t n = __builtin_amdgcn_readlane(seg_n, r), at = __builtin_amdgcn_readlane(seg_lo, r);
-    return E::load(rw, (uint32_t)lane + off < n ? at + off + (uint32_t)lane : E::kFar);
+    return E::template load<kStream>(rw, (uint32_t)lane + off < n ? at + off + (uint32_t)lane : E::kFar);
   };
 
   // the two table words of quarter q for the lane's row
@@ -115,7 +118,7 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
     if (!EXPORT) {
       const Rsrc rp = param_rsrc(q);
 #pragma unroll
-      for (int v = 0; v < 2; ++v) F.th[v] = load8<PBF16>(rp, eb + 8 * v);
+      for (int v = 0; v < V::NV; ++v) F.th[v] = V::load(rp, V::template first<kWave>(v, lane));
     }
   };
 
@@ -161,7 +164,9 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
     ET pre[kPreRows];
 #pragma unroll
     for (int r = 0; r < kPreRows; ++r) pre[r] = F.ld[r];
-    const Raw8<PBF16> th0 = F.th[0], th1 = F.th[1];
+    u32x4 th[V::NV];
+#pragma unroll
+    for (int v = 0; v < V::NV; ++v) th[v] = F.th[v];
     next();
     {
       const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -192,29 +197,30 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
       }
     }
     wave_sync();
-    if ((int)eb >= s) return;
+    if ((int)V::template first<kWave>(0, lane) >= s) return;
     const bool full = s == kQuarter;
 #pragma unroll
-    for (int v = 0; v < 2; ++v) {
-      float s1[8], s2[8];
+    for (int v = 0; v < V::NV; ++v) {
+      const uint32_t e0 = V::template first<kWave>(v, lane);
+      float s1[EV], s2[EV];
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float4 u = *(const float4*)(z + eb + 8 * v + 2 * w);  // elements eb + 8v + 2w, + 1
+      for (int w = 0; w < EV / 2; ++w) {
+        const float4 u = *(const float4*)(z + e0 + 2 * w);  // elements e0 + 2w, + 1
         s1[2 * w] = u.x; s2[2 * w] = u.y; s1[2 * w + 1] = u.z; s2[2 * w + 1] = u.w;
       }
       if (EXPORT) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if ((int)eb + 8 * v + e < s) {
-            mhat[g.e0 + lo + eb + 8 * v + e] = p.c1 * s1[e];
-            vhat[g.e0 + lo + eb + 8 * v + e] = p.c2 * s2[e];
+        for (int e = 0; e < EV; ++e)
+          if ((int)e0 + e < s) {
+            mhat[g.e0 + lo + e0 + e] = p.c1 * s1[e];
+            vhat[g.e0 + lo + e0 + e] = p.c2 * s2[e];
           }
         continue;
       }
-      float thf[8], out[8];
-      unpack8<PBF16>(v == 0 ? th0 : th1, thf);
+      float thf[EV], out[EV];
+      V::unpack(th[v], thf);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
+      for (int e = 0; e < EV; ++e) {
         const float mh = p.c1 * s1[e];
         const float vh = p.c2 * s2[e];
         const float den = p.eps + __builtin_amdgcn_sqrtf(vh);
@@ -223,7 +229,7 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
         const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
         out[e] = base - d;
       }
-      store8<PBF16>(param_rsrc(q), eb + 8 * v, s, full, out);
+      V::store(param_rsrc(q), e0, s, full, out);
     }
   };
 
