@@ -197,7 +197,9 @@ int microadam_state_bytes(const microadam_config* cfg, const int64_t* numels,
  * aligned) on `stream`: e = 0, delta = Delta = 0 as in the initialisation of
  * Algorithm 1.  The step counter starts at 0 (the next step is t = 1).
  * param_dtype / grad_dtype: MICROADAM_F32 or MICROADAM_BF16.
- * The library keeps a small device table of its own (freed by destroy);
+ * The library keeps small device tables of its own (freed by destroy:
+ * the block -> tensor table, the window weights, and with Top-K blocks above
+ * 4096 elements that are multiples of 4096 a 128-byte record per block);
  * `state` stays owned by the caller and must outlive the handle.
  */
 int microadam_init(const microadam_config* cfg, const int64_t* numels,
@@ -251,7 +253,11 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat,
  * blocks of 2049 to 4096 elements, at most 128 entries per row, m *
  * ceil(k/64) <= 16, parameters and gradients of one dtype, buckets inside
  * blocks); 2 (select, then update) otherwise; 4 with buckets spanning blocks
- * (select, bucket reduction, quantization, update).
+ * (select, bucket reduction, quantization, update); 4 with Top-K blocks
+ * above 4096 elements that are multiples of 4096 and buckets inside blocks
+ * (a threshold pass over each block, the select of its 4096-element
+ * sub-blocks, the multi-wave select of the blocks whose threshold the first
+ * pass left open, update).
  */
 int microadam_step_kernels(microadam_handle h);
 

@@ -344,6 +344,7 @@ struct microadam_handle_s {
   int device = 0;
   uint32_t* d_block_tensor = nullptr; // device: global block -> tensor
   float* d_wpow = nullptr;            // device: beta1^r, beta2^r for r < 64
+  uint8_t* d_thr = nullptr;           // device: the threshold kernel's per-block records, or NULL
   TableSlot slots[kTableSlots];
   uint64_t use_clock = 0;
   int current = -1;                   // slot used by the last step
@@ -383,6 +384,7 @@ void release(microadam_handle h) {
       if (e) (void)hipEventDestroy(e);
   if (h->d_block_tensor) (void)hipFree(h->d_block_tensor);
   if (h->d_wpow) (void)hipFree(h->d_wpow);
+  if (h->d_thr) (void)hipFree(h->d_thr);
   delete h;
 }
 
@@ -417,6 +419,7 @@ void fill_constants(const microadam_handle h, int64_t t, double lr, StepParams& 
   fill_step_params(h->cfg, h->planes, h->plans.empty() ? 0 : h->plans[0].k_full, (int32_t)h->plans.size(),
                    h->bucket_log2, t, lr, h->current >= 0 ? h->slots[h->current].d : nullptr, h->d_block_tensor,
                    h->d_wpow, h->state, p);
+  p.thr = h->d_thr;
 }
 
 int check_handle(microadam_handle h) {
@@ -502,6 +505,15 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
       (e = hipEventCreateWithFlags(&h->step_done, hipEventDisableTiming)) != hipSuccess) {
     release(h);
     return hip_fail(e, "allocating the block table");
+  }
+  // blocks above 4096 that are multiples of 4096, buckets inside blocks:
+  // the threshold kernel's records (128 bytes per block, written every step)
+  if (cfg->topk_block > microadam::kSubBlockElems && cfg->topk_block % microadam::kSubBlockElems == 0 &&
+      !h->planes.big && !h->fused) {
+    if ((e = hipMalloc((void**)&h->d_thr, (size_t)total_blocks * 128)) != hipSuccess) {
+      release(h);
+      return hip_fail(e, "allocating the threshold records");
+    }
   }
   {
     float w[2 * microadam::kMaxWindow];
@@ -683,7 +695,7 @@ int microadam_debug_moments(microadam_handle h, int32_t tensor, float* mhat, flo
 int microadam_step_kernels(microadam_handle h) {
   int rc = check_handle(h);
   if (rc) return rc;
-  return h->fused ? 1 : h->planes.big ? 4 : 2;
+  return h->fused ? 1 : h->planes.big ? 4 : h->d_thr ? 4 : 2;
 }
 
 int microadam_set_profiling(microadam_handle h, int32_t on) {

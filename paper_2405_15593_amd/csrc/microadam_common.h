@@ -23,6 +23,13 @@ namespace microadam {
 namespace {
 
 constexpr int kWave = 64;
+
+// A compile-time flag passed to generic lambdas (branches chosen once, not
+// per element).
+template <bool B>
+struct BoolTag {
+  static constexpr bool value = B;
+};
 constexpr int kLaneElems = 16;       // consecutive elements per thread
 constexpr uint32_t kNoEntry = 0xFFFFFFFFu;
 

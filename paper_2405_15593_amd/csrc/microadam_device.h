@@ -9,6 +9,7 @@ namespace microadam {
 
 constexpr int kMaxWindow = 64;       // largest supported window m
 constexpr int kMaxBlock = 65536;     // uint16 block-relative indices
+constexpr int kSubBlockElems = 4096; // elements of a one-wave select block
 
 // One parameter tensor as the kernels see it.  Its full blocks are the
 // global blocks [first_block, first_block + num_full); a ragged last block
@@ -70,6 +71,13 @@ struct StepParams {
   int64_t total_buckets;
   uint64_t table_bytes, partial_plane;
   int32_t n_tensors;
+  // blocks above 4096 that are multiples of 4096, with buckets inside
+  // blocks: 128-byte per-block records of the threshold kernel (device
+  // memory of the handle; NULL: the multi-wave select takes every block),
+  // and thr_gate = 1 when the multi-wave select is to take only the blocks
+  // whose record says the threshold kernel could not settle them
+  uint8_t* thr;
+  int32_t thr_gate;
 };
 
 // Steps with buckets spanning blocks: the per-block partials, their reduction

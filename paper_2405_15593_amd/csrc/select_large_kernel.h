@@ -4,6 +4,7 @@
 #pragma once
 
 #include "microadam_common.h"
+#include "select_split_kernel.h"
 
 namespace microadam {
 namespace {
@@ -25,10 +26,6 @@ namespace {
 // its first entry goes to the record's segment table, behind the m rows,
 // where the update finds the entries of one quarter.
 constexpr int kCandPerThread = 8;
-template <bool B>
-struct BoolTag {
-  static constexpr bool value = B;
-};
 constexpr int kSamples = 1024;
 constexpr int kSampleRes = 19;  // the sample's order statistics are taken to 2^19 (1/16 of a binade)
 
@@ -69,6 +66,11 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   const uint32_t eb = (uint32_t)tid * EPL;
   const int bl = p.bucket_log2;
   const int64_t gb = first + xcd_block(block_id(), count);
+  if (p.thr_gate) {
+    // after the threshold and apply kernels: only the blocks they left
+    const Rsrc rrec = make_rsrc(p.thr + (uint64_t)gb * 128, 128);
+    if (sgpr(__builtin_amdgcn_raw_buffer_load_b32(rrec, 0, 0, 0)) != 0u) return;
+  }
 
   const uint32_t nbk = (uint32_t)(p.block >> bl);
   const uint32_t ef_bytes = (EFM & kEf8) ? (uint32_t)p.block : (uint32_t)(p.block >> 1);
@@ -572,15 +574,27 @@ hipError_t launch_select_large(const StepParams& p, int64_t first, int64_t count
   }
 }
 
-// Blocks above 4096 elements in the error-feedback format EFM.
+// Blocks above 4096 elements in the error-feedback format EFM: with
+// threshold records (p.thr), the threshold and apply kernels, then the
+// multi-wave select for the blocks they left; else the multi-wave select.
+template <bool GB, bool VF, int EFM>
+hipError_t launch_select_large_all(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  if (p.thr == nullptr) return launch_select_large<GB, VF, EFM>(p, first, count, stream);
+  const hipError_t e = launch_select_split<GB, VF, EFM>(p, first, count, stream);
+  if (e != hipSuccess) return e;
+  StepParams q = p;
+  q.thr_gate = 1;
+  return launch_select_large<GB, VF, EFM>(q, first, count, stream);
+}
+
 template <int EFM>
 hipError_t launch_select_large_mode(const StepParams& p, int grad_bf16, int value_f32, int64_t first, int64_t count,
                                     hipStream_t stream) {
   if (grad_bf16)
-    return value_f32 ? launch_select_large<true, true, EFM>(p, first, count, stream)
-                     : launch_select_large<true, false, EFM>(p, first, count, stream);
-  return value_f32 ? launch_select_large<false, true, EFM>(p, first, count, stream)
-                   : launch_select_large<false, false, EFM>(p, first, count, stream);
+    return value_f32 ? launch_select_large_all<true, true, EFM>(p, first, count, stream)
+                     : launch_select_large_all<true, false, EFM>(p, first, count, stream);
+  return value_f32 ? launch_select_large_all<false, true, EFM>(p, first, count, stream)
+                   : launch_select_large_all<false, false, EFM>(p, first, count, stream);
 }
 
 }  // namespace

@@ -1,0 +1,507 @@
+// The select for Top-K blocks above 4096 elements whose size is a multiple of
+// 4096 (buckets inside blocks), in launches that stream a block instead of
+// holding it: the threshold kernel finds each block's k-th largest |a| and
+// the row position of each 4096-element sub-block's first kept entry; the
+// apply kernel then runs one wave per sub-block (as the one-wave select does
+// per block): it keeps the elements at or above the threshold, writes its
+// part of the new row and of the segment table, and quantizes.  Blocks whose
+// threshold search needs more than the streamed bracket (see below) are
+// marked, skipped by the apply kernel and taken by the multi-wave select
+// kernel, which holds the block and searches it exactly.
+//
+// The multi-wave kernel fills a compute unit's registers with one block, so
+// a compute unit loads one block, then searches it with no loads in flight;
+// the two streamed passes read the gradient and codes twice (2.56 B per
+// parameter more) but keep loads in flight on every compute unit.
+#pragma once
+
+#include "microadam_common.h"
+
+namespace microadam {
+namespace {
+
+constexpr int kThrThreads = 256;                   // threshold kernel: four waves per block
+constexpr int kThrWaves = kThrThreads / kWave;
+constexpr int kThrSamples = 1024;                  // sample keys (128 vectors of 8)
+constexpr int kThrList = 1536;                     // bracketed keys gathered per wave
+constexpr int kThrSampleRes = 15;                  // the sample's order statistics to 2^15 (1/256 binade)
+constexpr uint32_t kThrRecordBytes = 128;          // per block
+constexpr uint32_t kAllTies = 0xFFFFFFFFu;         // i_last: every key equal to T is kept
+
+// The per-block record the threshold kernel writes (uint32 words):
+//   [0] 1 when the bracket held the threshold (else the multi-wave select
+//       takes the block), [1] T, the k-th largest key (|a| as an integer),
+//   [2] i_last: keys equal to T are kept up to this block element (kAllTies:
+//       all of them), [4 + w] the row position of sub-block w's first kept
+//       entry (at most k_q).  Kept: key > T, or key == T and index <= i_last.
+// (the sample is read into registers before the pass, which then
+// overwrites it with gathered keys)
+struct ThrLds {
+  static constexpr int kSample = 0;                                  // [kThrSamples]
+  static constexpr int kKeys = 0;                                    // [waves][kThrList] keys
+  static constexpr int kIdx = kKeys + kThrWaves * kThrList;          // [waves][kThrList] uint16 indices
+  static constexpr int kHi = kIdx + kThrWaves * kThrList / 2;        // [16] keys >= hi per sub-block
+  static constexpr int kKept = kHi + 16;                             // [16] kept gathered keys per sub-block
+  static constexpr int kCnt = kKept + 16;                            // [2][waves] per-wave counts
+  static constexpr int kDig = kCnt + 2 * kThrWaves;                  // [2][32] digit counts
+  static constexpr int kWords = kDig + 64;
+};
+
+// One 8-element vector of the block: gradient, codes and bucket pair.
+template <bool GBF16, int EFM>
+struct VecIn {
+  Raw8<GBF16> g;
+  uint32_t c[(EFM & kEf8) ? 2 : 1];
+  u32x2 st;
+};
+
+template <bool GBF16, int EFM>
+__device__ __forceinline__ void vec_load(VecIn<GBF16, EFM>& x, Rsrc rg, Rsrc re, Rsrc rs, uint32_t j, int bl) {
+  x.g.w[0] = __builtin_amdgcn_raw_buffer_load_b128(rg, j * (GBF16 ? 16u : 32u), 0, kStream);
+  if constexpr (!GBF16) x.g.w[1] = __builtin_amdgcn_raw_buffer_load_b128(rg, j * 32u + 16u, 0, kStream);
+  if constexpr (EFM & kEf8) {
+    const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(re, j * 8u, 0, kStream);
+    x.c[0] = t[0];
+    x.c[1] = t[1];
+  } else {
+    x.c[0] = __builtin_amdgcn_raw_buffer_load_b32(re, j * 4u, 0, kStream);
+  }
+  x.st = __builtin_amdgcn_raw_buffer_load_b64(rs, ((8u * j) >> bl) * 8u, 0, kStream);
+}
+
+// a = g + Q^-1(e) of vector j (the arithmetic of lane_decode); elements at
+// or past s are 0 (`full`, workgroup-uniform: no element is).
+template <bool GBF16, int EFM>
+__device__ __forceinline__ void vec_decode(const VecIn<GBF16, EFM>& x, uint32_t j, int s, bool full,
+                                           float (&a)[8]) {
+  const float lo = __uint_as_float(x.st[0]);
+  const float u = ef_step<EFM>(__uint_as_float(x.st[1]) - lo);
+  float g[8], c[8];
+  unpack8<GBF16>(x.g, g);
+  unpack_codes<EFM>(x.c, 0, c);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float sc = c[e] * u;
+    const float d = sc + lo;
+    a[e] = g[e] + d;
+  }
+  if (!full) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if ((int)(8 * j) + e >= s) a[e] = 0.0f;
+  }
+}
+
+// ------------------------------------------------------ threshold kernel
+// One 256-thread workgroup per block, in three parts.
+//  1. A bracket [lo, hi) for the k-th largest key from 1024 sample keys (one
+//     8-element vector out of every 128th of the block; vectors spread out,
+//     since neighbouring elements share a bucket and so correlate): the
+//     16-bit prefixes of the sample's order statistics three standard
+//     deviations either side of the expected rank, by a 16-ary search (four
+//     digits per wave, one barrier per 4 bits).
+//  2. One pass over the block, each wave's 1 KB vector loads contiguous:
+//     keys >= hi are counted per sub-block, keys in [lo, hi) gathered with
+//     their indices in the wave's part of LDS.  The bracket holds the answer
+//     when fewer than k keys lie at or above hi, at least k at or above lo,
+//     and no wave gathered more than kThrList; else the block is marked.
+//  3. T by a bitwise search over the gathered keys, the ties at T kept in
+//     index order (a bitwise search over their indices), and the row
+//     positions of the sub-blocks from their kept counts.
+// The bracket's rank arithmetic is approximate: the check in 2 decides.
+template <bool GBF16, int EFM>
+__global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, int64_t first, int64_t count) {
+  extern __shared__ __align__(16) uint32_t smem[];
+  uint32_t* const samp = smem + ThrLds::kSample;
+  uint32_t* const lkey = smem + ThrLds::kKeys;
+  uint16_t* const lidx = (uint16_t*)(smem + ThrLds::kIdx);
+  uint32_t* const hi_sb = smem + ThrLds::kHi;
+  uint32_t* const kept_sb = smem + ThrLds::kKept;
+  uint32_t* const cnt = smem + ThrLds::kCnt;
+  uint32_t* const dig = smem + ThrLds::kDig;
+
+  const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
+  const int64_t gb = first + xcd_block(block_id(), count);
+  const Block b = locate(p, gb);
+  const int s = b.s, kq = b.kq, bl = p.bucket_log2;
+  const bool full = s == p.block;
+  const uint32_t nvec = (uint32_t)p.block / 8;
+  const uint32_t ef_bytes = (EFM & kEf8) ? (uint32_t)p.block : (uint32_t)p.block / 2;
+  const uint32_t nbk = (uint32_t)(p.block >> bl);
+  const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * ef_bytes, ef_bytes);
+  const Rsrc rs = make_rsrc(p.state + p.stats_plane + (uint64_t)gb * nbk * 8, nbk * 8);
+  const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + b.e0 * (GBF16 ? 2 : 4), vec_bytes<GBF16>(s));
+  const Rsrc rrec = make_rsrc(p.thr + (uint64_t)gb * kThrRecordBytes, kThrRecordBytes);
+  using VI = VecIn<GBF16, EFM>;
+
+  if (tid < 32) hi_sb[tid] = 0u;  // with kept_sb
+
+  // ---------------------------------------------- 1. the sample bracket
+  {
+    const uint32_t seg = nvec / (kThrSamples / 8);  // vectors per 128th of the block (>= 8)
+    uint32_t valid = 0;
+    if (tid < kThrSamples / 8) {
+      const uint32_t j = (uint32_t)tid * seg + ((uint32_t)tid * 5u) % seg;
+      VI x;
+      vec_load(x, rg, re, rs, j, bl);
+      float a[8];
+      vec_decode(x, j, s, full, a);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t k = key_of(a[e]);
+        const bool in = (int)(8 * j) + e < s;
+        samp[8 * tid + e] = in && k <= 0x7F800000u ? k : 0u;  // a NaN sample counts as 0
+        valid += in ? 1u : 0u;
+      }
+    }
+    uint32_t vw = 0;
+#pragma unroll
+    for (int b2 = 0; b2 < 4; ++b2) vw += popc(ballot((valid >> b2) & 1u)) << b2;
+    if (lane == 0) cnt[wave] = vw;
+  }
+  lds_sync();
+  uint32_t ns = 0;
+#pragma unroll
+  for (int w = 0; w < kThrWaves; ++w) ns += cnt[w];
+  ns = sgpr(ns);
+  // approximate ranks from the top: the answer's expected rank in the sample
+  // and three standard deviations either side
+  const float mu = (float)ns * (float)kq * __builtin_amdgcn_rcpf((float)s);
+  const float sd = 3.0f * __builtin_amdgcn_sqrtf(mu);
+  const int r_lo = (int)__builtin_ceilf(mu + sd), r_hi = (int)__builtin_floorf(mu - sd);
+  uint32_t lo, hi;
+  {
+    uint32_t key[kThrSamples / kWave];
+#pragma unroll
+    for (int j = 0; j < kThrSamples / kWave; ++j) key[j] = samp[lane + kWave * j];
+    // tl, th: the largest 16-bit prefixes (bits 30..15) with at least r_lo,
+    // r_hi sample keys at or above them; wave w counts digits 4w .. 4w + 3
+    uint32_t tl = 0, th = 0;
+#pragma unroll
+    for (int rd = 0; rd < 4; ++rd) {
+      const int sh = 27 - 4 * rd;
+      uint32_t* const dg = dig + (rd & 1) * 32;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t d = (uint32_t)(wave * 4 + i);
+        if (d == 0) continue;
+        const uint32_t cl = tl + (d << sh), ch = th + (d << sh);
+        uint32_t nl = 0, nh = 0;
+#pragma unroll
+        for (int j = 0; j < kThrSamples / kWave; ++j) {
+          nl += popc(ballot(key[j] >= cl));
+          nh += popc(ballot(key[j] >= ch));
+        }
+        if (lane == 0) {
+          dg[d] = nl;
+          dg[16 + d] = nh;
+        }
+      }
+      lds_sync();
+      const uint32_t x = lane < 32 ? dg[lane] : 0u;
+      const uint32_t dl = popc(ballot(lane >= 1 && lane < 16 && x >= (uint32_t)r_lo));
+      const uint32_t dh = popc(ballot(lane >= 17 && lane < 32 && (int)x >= r_hi));
+      tl += dl << sh;
+      th += dh << sh;
+    }
+    lo = r_lo > (int)ns ? 1u : (tl > 1u ? tl : 1u);  // a key of 0 is never gathered
+    hi = r_hi < 1 ? 1u << 31 : th + (1u << kThrSampleRes);
+  }
+
+  // ---------------------------------------------- 2. the streamed pass
+  const uint32_t vpt = nvec / kThrThreads;  // vectors per thread: even, 4 .. 32
+  uint32_t* const mykey = lkey + wave * kThrList;
+  uint16_t* const myidx = lidx + wave * kThrList;
+  uint32_t wn = 0;  // keys this wave gathered (may pass kThrList: then only counted)
+  {
+    const float lof = __uint_as_float(lo), hif = __uint_as_float(hi < 0x7F800000u ? hi : 0x7F800000u);
+    auto pass = [&](auto nohi_tag) {
+      constexpr bool NOHI = decltype(nohi_tag)::value;
+      const float lob = opaque_f(lof), hib = opaque_f(hif);
+      for (uint32_t r0 = 0; r0 < vpt; r0 += 8) {
+        VI x[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (r0 + i < vpt) vec_load(x[i], rg, re, rs, kThrThreads * (r0 + i) + kWave * wave + lane, bl);
+        uint32_t nh[4] = {0u, 0u, 0u, 0u};  // keys >= hi in the round's four sub-blocks
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          if (r0 + i >= vpt) continue;
+          const uint32_t j = kThrThreads * (r0 + i) + kWave * wave + lane;
+          float a[8];
+          vec_decode(x[i], j, s, full, a);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float ab = __builtin_fabsf(a[e]);
+            const uint64_t mh = NOHI ? 0ull : ballot(ab >= hib);
+            const uint64_t mi = ballot(ab >= lob) & ~mh;
+            if (!NOHI) nh[i >> 1] += popc(mh);
+            if (mi) {
+              const uint32_t pos = wn + lanes_below(mi);
+              if (__builtin_amdgcn_inverse_ballot_w64(mi) && pos < (uint32_t)kThrList) {
+                mykey[pos] = __float_as_uint(ab);
+                myidx[pos] = (uint16_t)(8 * j + e);
+              }
+              wn += popc(mi);
+            }
+          }
+        }
+        if (!NOHI && lane == 0) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (nh[q]) atomicAdd(&hi_sb[(r0 >> 1) + q], nh[q]);
+        }
+      }
+    };
+    if (hi > 0x7F800000u)
+      pass(BoolTag<true>{});
+    else
+      pass(BoolTag<false>{});
+  }
+  if (lane == 0) cnt[kThrWaves + wave] = wn;
+  lds_sync();
+  uint32_t n_hi = 0, n_in = 0;
+  bool over = false;
+#pragma unroll
+  for (int w = 0; w < kThrWaves; ++w) {
+    const uint32_t c = cnt[kThrWaves + w];
+    n_in += c;
+    over |= c > (uint32_t)kThrList;
+  }
+  {
+    const uint32_t h = lane < 16 ? hi_sb[lane] : 0u;
+    uint32_t t = h;
+#pragma unroll
+    for (int d = 1; d < 16; d <<= 1) t += __shfl_xor(t, d, kWave);
+    n_hi = sgpr(t);
+  }
+  n_in = sgpr(n_in);
+  const bool ok = !over && lo <= 0x7F800000u && n_hi < (uint32_t)kq && n_hi + n_in >= (uint32_t)kq;
+  if (!ok) {
+    if (tid == 0) __builtin_amdgcn_raw_buffer_store_b32(0u, rrec, 0, 0, 0);
+    return;
+  }
+
+  // ---------------------------------------------- 3. T, the ties, the offsets
+  const uint32_t mine = sgpr(cnt[kThrWaves + wave]);  // <= kThrList
+  constexpr int NR = kThrList / kWave;
+  uint32_t y[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const uint32_t q = (uint32_t)(lane + kWave * r);
+    y[r] = q < mine ? mykey[q] : 0u;  // 0 < lo: never counted
+  }
+  int buf = 0;
+  // workgroup total of one count per wave (`buf` alternates between calls)
+  auto wg_sum = [&](uint32_t v) {
+    if (lane == 0) cnt[buf * kThrWaves + wave] = v;
+    lds_sync();
+    uint32_t t = 0;
+#pragma unroll
+    for (int w = 0; w < kThrWaves; ++w) t += cnt[buf * kThrWaves + w];
+    buf ^= 1;
+    return sgpr(t);
+  };
+  // the largest t with count(key >= t) >= k: prefixes at or above hi fail
+  // and prefixes at or below lo pass without counting; count = n_hi + the
+  // gathered keys >= the prefix
+  uint32_t t = 0;
+  bool exact = false;
+  for (int bit = 30; bit >= 0 && !exact; --bit) {
+    const uint32_t c = t | (1u << bit);
+    if (c >= hi) continue;
+    if (c <= lo) {
+      t = c;
+      continue;
+    }
+    uint32_t n = 0;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) n += popc(ballot(y[r] >= c));
+    n = n_hi + wg_sum((uint32_t)opaque((int)n));
+    if (n >= (uint32_t)kq) {
+      t = c;
+      exact = n == (uint32_t)kq;
+    }
+  }
+  uint32_t i_last = kAllTies;
+  if (!exact) {
+    // keys above t, and those equal to it: the first `need` of them in index
+    // order are kept
+    uint32_t ngt = 0, neq = 0;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      ngt += popc(ballot(y[r] > t));
+      neq += popc(ballot(y[r] == t));
+    }
+    // (both below 2^16: one sum carries the pair)
+    const uint32_t both = wg_sum((ngt << 16) | neq);
+    const uint32_t need = (uint32_t)kq - n_hi - (both >> 16);
+    if ((both & 0xFFFFu) != need) {
+      // the largest m with fewer than `need` tied indices below it is the
+      // need-th tied index
+      uint32_t z[NR];
+#pragma unroll
+      for (int r = 0; r < NR; ++r)
+        z[r] = y[r] == t ? (uint32_t)myidx[lane + kWave * r] : 0x10000u;  // untied: never below
+      uint32_t mfound = 0;
+      for (int bit = 15; bit >= 0; --bit) {
+        const uint32_t c = mfound | (1u << bit);
+        if (c >= (uint32_t)p.block) continue;
+        uint32_t n = 0;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) n += popc(ballot(z[r] < c));
+        if (wg_sum((uint32_t)opaque((int)n)) < need) mfound = c;
+      }
+      i_last = mfound;
+    }
+  }
+  // kept gathered keys per sub-block, then the row positions
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const uint32_t q = (uint32_t)(lane + kWave * r);
+    if (q < mine) {
+      const uint32_t ix = myidx[q];
+      const bool kept = y[r] > t || (y[r] == t && (i_last == kAllTies || ix <= i_last));
+      if (kept) atomicAdd(&kept_sb[ix >> 12], 1u);
+    }
+  }
+  lds_sync();
+  if (tid < 16) {
+    uint32_t off = 0;
+    for (int w = 0; w < tid; ++w) off += hi_sb[w] + kept_sb[w];
+    __builtin_amdgcn_raw_buffer_store_b32(off < (uint32_t)kq ? off : (uint32_t)kq, rrec, 16 + 4 * tid, 0, 0);
+  } else if (tid == 16) {
+    __builtin_amdgcn_raw_buffer_store_b128(u32x4{1u, t, i_last, 0u}, rrec, 0, 0, 0);
+  }
+}
+
+// -------------------------------------------------------- apply kernel
+// One wave per 4096-element sub-block w of a block the threshold kernel
+// settled: lane l owns the sub-block's elements [64l, 64l + 64), loaded and
+// decoded as in the one-wave select; kept are |a| > T and |a| == T up to
+// i_last.  The kept elements go to the row from the record's position of
+// the sub-block, in element order, and the segment table gets the row
+// position of each of its four 1024-element quarters' first entry.
+template <bool LB, bool GBF16, bool VF32, int EFM>
+__global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
+apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
+  constexpr int EPL = 64, NV = EPL / 8, CAP = kWave * EPL;
+  using E = Entry<VF32>;
+  extern __shared__ __align__(16) uint32_t smem[];
+  const int lane = thread_id();
+  const int64_t w = xcd_block(block_id(), count * nsb);
+  const int64_t gb = first + w / nsb;
+  const int sb = (int)(w % nsb);
+  const Rsrc rrec = make_rsrc(p.thr + (uint64_t)gb * kThrRecordBytes, kThrRecordBytes);
+  const u32x4 head = __builtin_amdgcn_raw_buffer_load_b128(rrec, 0, 0, 0);
+  const uint32_t off0 = sgpr(__builtin_amdgcn_raw_buffer_load_b32(rrec, 16 + 4 * sb, 0, 0));
+  if (sgpr(head[0]) == 0u) return;  // the multi-wave select takes this block
+  const uint32_t T = sgpr(head[1]), i_last = sgpr(head[2]);
+  const int bl = p.bucket_log2;
+  const uint32_t e_sb = (uint32_t)sb * CAP;
+  const uint32_t eb = (uint32_t)lane * EPL;
+
+  const uint32_t sub_ef = (EFM & kEf8) ? (uint32_t)CAP : (uint32_t)CAP / 2;
+  const uint32_t ef_bytes = (EFM & kEf8) ? (uint32_t)p.block : (uint32_t)(p.block >> 1);
+  const uint32_t nbk = (uint32_t)(p.block >> bl), sub_bk = (uint32_t)(CAP >> bl);
+  const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * ef_bytes + (uint64_t)sb * sub_ef, sub_ef);
+  const Rsrc rs = make_rsrc(p.state + p.stats_plane + ((uint64_t)gb * nbk + (uint64_t)sb * sub_bk) * 8, sub_bk * 8);
+  constexpr bool kCoal = GBF16 && (EFM & kEf8) == 0;
+  LaneIn<EPL, LB, GBF16, EFM> in;
+  CoalescedIn cx;
+  if constexpr (kCoal) {
+#pragma unroll
+    for (int v = 0; v < (LB ? 1 : NV); ++v)
+      in.st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, kStream);
+    coalesced_load_codes(cx, re, lane);
+  } else {
+    lane_load_state(in, re, rs, eb, bl, true);
+  }
+  const Block b = locate(p, gb);
+  const int s_blk = b.s, kq = b.kq;
+  const int nq = p.block / kQuarter;  // segment table entries per row
+  constexpr uint32_t EB = VF32 ? 8u : 4u;
+  const uint32_t table = (uint32_t)p.window * p.k_full * EB;
+  const Rsrc rwin = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
+  auto table_store = [&](int quarter, uint32_t pos) {
+    __builtin_amdgcn_raw_buffer_store_b32(pos < (uint32_t)kq ? pos : (uint32_t)kq, rwin,
+                                          table + ((uint32_t)p.new_slot * nq + quarter) * 4, 0, 0);
+  };
+  const int s = s_blk - (int)e_sb;  // this sub-block's elements (may be <= 0)
+  if (s <= 0) {
+    if (lane < 4) table_store(4 * sb + lane, off0);
+    return;
+  }
+  const bool full = s >= CAP;
+  const int ss = full ? CAP : s;
+  const Rsrc rg = make_rsrc((const uint8_t*)b.desc.grad + (b.e0 + e_sb) * (GBF16 ? 2 : 4), vec_bytes<GBF16>(ss));
+  if constexpr (kCoal) {
+    coalesced_load_grad(cx, rg, lane);
+    coalesced_exchange(cx, in, smem, lane);
+  } else {
+    lane_load_grad(in, rg, eb);
+  }
+  float a[NV][8];
+  const int rem = ss - (int)eb;
+  lane_decode(in, a, rem, full);
+
+  // kept elements: counted, positioned in element order, written to the row
+  const bool notie = i_last == kAllTies;
+  // i_last relative to this lane's first element (negative: no tie kept here)
+  const int last_here = notie ? CAP : (int)i_last - (int)e_sb - (int)eb;
+  const float tf = opaque_f(__uint_as_float(T));
+  uint32_t sel_l = 0;
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float ab = __builtin_fabsf(a[v][e]);
+      sel_l += ((ab > tf) | ((ab == tf) & (8 * v + e <= last_here))) ? 1u : 0u;
+    }
+  uint32_t pos = off0;
+#pragma unroll
+  for (int b2 = 0; b2 < 7; ++b2) pos += lanes_below(ballot((sel_l >> b2) & 1u)) << b2;
+  if ((lane & 15) == 0 && 4 * sb + (lane >> 4) < nq) table_store(4 * sb + (lane >> 4), pos);
+  if (sel_l) {
+    const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
+    const uint32_t row0 = (uint32_t)p.new_slot * kq;
+    const float tf2 = opaque_f(tf);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float ab = __builtin_fabsf(a[v][e]);
+        if ((ab > tf2) | ((ab == tf2) & (8 * v + e <= last_here))) {
+          if (pos < (uint32_t)kq) E::store(rw, row0 + pos, E::make(e_sb + eb + 8 * v + e, a[v][e]));
+          ++pos;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);  // one vector's stores at a time
+    }
+  }
+  // ---------------------------------------------- e = Q(a with a[I] = 0)
+  lane_quantize_store<EPL, LB, EFM>(a, T, notie, (uint32_t)((int)i_last - (int)e_sb), eb, ss, rem, full, bl, true,
+                                    re, rs, EfStream{b.e0 + (int64_t)e_sb, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi},
+                                    kCoal ? smem : nullptr);
+}
+
+template <bool GB, bool VF, int EFM>
+hipError_t launch_select_split(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL((threshold_kernel<GB, EFM>), dim3((uint32_t)count), dim3(kThrThreads), ThrLds::kWords * 4,
+                     stream, p, first, count);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int32_t nsb = p.block / kSubBlock;
+  const size_t lds = select_lds_words() * 4;
+  if ((1 << p.bucket_log2) >= 64)
+    hipLaunchKernelGGL((apply_kernel<true, GB, VF, EFM>), dim3((uint32_t)(count * nsb)), dim3(kWave), lds, stream, p,
+                       first, count, nsb);
+  else
+    hipLaunchKernelGGL((apply_kernel<false, GB, VF, EFM>), dim3((uint32_t)(count * nsb)), dim3(kWave), lds, stream, p,
+                       first, count, nsb);
+  return hipGetLastError();
+}
+
+}  // namespace
+}  // namespace microadam
