@@ -89,10 +89,13 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
   };
   // entry `lane` + off of row r's segment, or (lanes past its end) a read
   // past the end of the record, which gives 0 and is not used: the adds
-  // check the segment length, and no merge waits for the load
+  // check the segment length, and no merge waits for the load.  (Default
+  // cache policy: neighbouring quarters' segments share lines, which the nt
+  // policy evicts early; measured on the 1.5e9 workload, nt here took the
+  // kernel from 2.31 to 2.70 ms.)
   auto row_load = [&](uint32_t seg_lo, uint32_t seg_n, int r, uint32_t off) {
     const uint32_t n = __builtin_amdgcn_readlane(seg_n, r), at = __builtin_amdgcn_readlane(seg_lo, r);
-    return E::template load<kStream>(rw, (uint32_t)lane + off < n ? at + off + (uint32_t)lane : E::kFar);
+    return E::load(rw, (uint32_t)lane + off < n ? at + off + (uint32_t)lane : E::kFar);
   };
 
   // the two table words of quarter q for the lane's row

@@ -302,7 +302,8 @@ __device__ __forceinline__ void store8(Rsrc r, uint32_t elem, int s, bool full, 
 // parameter read-modify-write with window reads: 5.17 -> 4.71 ms per 29.65 GB;
 // the select's reads and writes: 4.16 -> 3.83 ms per 22.17 GB); with each
 // lane's accesses 128 bytes apart it is slower instead (4.25 -> 7.6 ms), so
-// it goes only on coalesced accesses.
+// it goes only on coalesced accesses, and not on lines that another wave
+// reads soon after (the large-block update's row segments).
 constexpr int kStream = 2;
 
 // A thread's 16 elements of a block as 16-byte vectors that consecutive

@@ -27,6 +27,7 @@ constexpr int kThrList = 1536;                     // bracketed keys gathered pe
 constexpr int kThrSampleRes = 15;                  // the sample's order statistics to 2^15 (1/256 binade)
 constexpr uint32_t kThrRecordBytes = 128;          // per block
 constexpr uint32_t kAllTies = 0xFFFFFFFFu;         // i_last: every key equal to T is kept
+constexpr uint32_t kApplyStageWords = 1024;        // apply kernel: row words staged in LDS
 
 // The per-block record the threshold kernel writes (uint32 words):
 //   [0] 1 when the bracket held the threshold (else the multi-wave select
@@ -458,26 +459,52 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
       const float ab = __builtin_fabsf(a[v][e]);
       sel_l += ((ab > tf) | ((ab == tf) & (8 * v + e <= last_here))) ? 1u : 0u;
     }
-  uint32_t pos = off0;
+  uint32_t pre = 0, n_sb = 0;  // kept before this lane; in the sub-block
 #pragma unroll
-  for (int b2 = 0; b2 < 7; ++b2) pos += lanes_below(ballot((sel_l >> b2) & 1u)) << b2;
-  if ((lane & 15) == 0 && 4 * sb + (lane >> 4) < nq) table_store(4 * sb + (lane >> 4), pos);
+  for (int b2 = 0; b2 < 7; ++b2) {
+    const uint64_t m = ballot((sel_l >> b2) & 1u);
+    pre += lanes_below(m) << b2;
+    n_sb += popc(m) << b2;
+  }
+  n_sb = sgpr(n_sb);
+  if ((lane & 15) == 0 && 4 * sb + (lane >> 4) < nq) table_store(4 * sb + (lane >> 4), off0 + pre);
+  // the sub-block's entries that enter the row, [off0, off0 + n_row), go
+  // through LDS (the exchange is over) and leave as consecutive words;
+  // past kApplyStageWords each is stored where it is found
+  constexpr uint32_t EW = VF32 ? 2u : 1u;
+  const uint32_t room = off0 < (uint32_t)kq ? (uint32_t)kq - off0 : 0u;
+  const uint32_t n_row = n_sb < room ? n_sb : room;
+  const bool staged = n_row * EW <= kApplyStageWords;
+  const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
+  const uint32_t row0 = (uint32_t)p.new_slot * kq + off0;
   if (sel_l) {
-    const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
-    const uint32_t row0 = (uint32_t)p.new_slot * kq;
     const float tf2 = opaque_f(tf);
+    uint32_t r = pre;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float ab = __builtin_fabsf(a[v][e]);
         if ((ab > tf2) | ((ab == tf2) & (8 * v + e <= last_here))) {
-          if (pos < (uint32_t)kq) E::store(rw, row0 + pos, E::make(e_sb + eb + 8 * v + e, a[v][e]));
-          ++pos;
+          if (r < n_row) {
+            const typename E::T x = E::make(e_sb + eb + 8 * v + e, a[v][e]);
+            if (staged) {
+              if constexpr (VF32) *(u32x2*)(smem + 2 * r) = x;
+              else smem[r] = x;
+            } else {
+              E::store(rw, row0 + r, x);
+            }
+          }
+          ++r;
         }
       }
       __builtin_amdgcn_sched_barrier(0);  // one vector's stores at a time
     }
+  }
+  if (staged) {
+    wave_sync();
+    for (uint32_t q = (uint32_t)lane; q < n_row * EW; q += kWave)
+      __builtin_amdgcn_raw_buffer_store_b32(smem[q], rw, (row0 * EW + q) * 4, 0, kStream);
   }
   // ---------------------------------------------- e = Q(a with a[I] = 0)
   lane_quantize_store<EPL, LB, EFM>(a, T, notie, (uint32_t)((int)i_last - (int)e_sb), eb, ss, rem, full, bl, true,
