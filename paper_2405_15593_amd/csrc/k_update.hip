@@ -82,33 +82,30 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
   const int s = u.s, kq = u.kq;
   const int leader = u.gb & (NW - 1);
   const int R = (kq + kWave - 1) / kWave;
-  const float rcp_r = 1.0f / (float)R;
   const bool staged = n_live * R <= kChunks;
 
-  // chunk c -> (live row, part): the entry of position q, and whether it
-  // holds one (uniform per block: kq, R, n_live)
-  auto position = [&](int q, uint32_t& entry) {
-    const int c = q >> 6;
-    const int row = (int)(((float)c + 0.5f) * rcp_r);  // c / R for c < 2^10
-    const int jj = (c - row * R) * kWave + (q & (kWave - 1));
-    int slot = slot0 + row;
-    if (slot >= m) slot -= m;
-    const bool valid = row < n_live && jj < kq;
-    entry = valid ? (uint32_t)(slot * kq + jj) : 0u;
-    return valid;
-  };
-
   // loads: the leader's window positions, KC chunks of 64 (positions without
-  // an entry read entry 0 and are not used), then every thread's parameters
+  // an entry read entry 0 and are not used), then every thread's parameters.
+  // Chunk c is part `col` of live row `row` (uniform counters), at record
+  // entry slot*k_q + 64*col + lane.
   const bool lead = wave == leader;
   const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, u.gb, kq);
   ET w[kChunks];
+  bool has[kChunks];  // the position holds an entry
+  int rr[kChunks];    // the chunk's row age: 0 for the newest row
   if (lead && staged) {
+    int row = 0, col = 0, slot = slot0;
 #pragma unroll
     for (int c = 0; c < kChunks; ++c) {
-      uint32_t entry;
-      position(c * kWave + lane, entry);
-      w[c] = E::template load<kStream>(rw, entry);
+      const int jj = col * kWave + lane;
+      has[c] = row < n_live && jj < kq;
+      rr[c] = (n_live - 1 - row) & (kMaxWindow - 1);
+      w[c] = E::template load<kStream>(rw, has[c] ? (uint32_t)(slot * kq + jj) : 0u);
+      if (++col == R) {
+        col = 0;
+        ++row;
+        if (++slot == m) slot = 0;
+      }
     }
   }
   using V = Vec16<PBF16>;
@@ -144,22 +141,11 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
       // chunks past the live rows hold only sink words
       uint32_t zp[kChunks];
       float val[kChunks];
-      int rr[kChunks];
-      {
-        int row = 0, col = 0;
 #pragma unroll
-        for (int c = 0; c < kChunks; ++c) {
-          uint32_t entry;
-          const bool valid = position(c * kWave + lane, entry);
-          const uint32_t idx = E::idx(w[c]);
-          zp[c] = valid && idx < (uint32_t)s ? zpos<NT, PBF16>(idx) : (uint32_t)CAP;
-          val[c] = E::val(w[c]);
-          rr[c] = (n_live - 1 - row) & (kMaxWindow - 1);
-          if (++col == R) {
-            col = 0;
-            ++row;
-          }
-        }
+      for (int c = 0; c < kChunks; ++c) {
+        const uint32_t idx = E::idx(w[c]);
+        zp[c] = has[c] && idx < (uint32_t)s ? zpos<NT, PBF16>(idx) : (uint32_t)CAP;
+        val[c] = E::val(w[c]);
       }
       // The entries of one row (or of one 64-entry part of it) have distinct
       // indices, so each chunk reads, adds and writes back its words (the
