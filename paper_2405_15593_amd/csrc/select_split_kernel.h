@@ -24,6 +24,7 @@ constexpr int kThrThreads = 256;                   // threshold kernel: four wav
 constexpr int kThrWaves = kThrThreads / kWave;
 constexpr int kThrSamples = 1024;                  // sample keys (128 vectors of 8)
 constexpr int kThrList = 1536;                     // bracketed keys gathered per wave
+constexpr int kThrListStride = kThrList + kWave;   // + one sink slot per lane
 constexpr int kThrSampleRes = 15;                  // the sample's order statistics to 2^15 (1/256 binade)
 constexpr uint32_t kThrRecordBytes = 128;          // per block
 constexpr uint32_t kAllTies = 0xFFFFFFFFu;         // i_last: every key equal to T is kept
@@ -39,14 +40,16 @@ constexpr uint32_t kApplyStageWords = 1024;        // apply kernel: row words st
 // overwrites it with gathered keys)
 struct ThrLds {
   static constexpr int kSample = 0;                                  // [kThrSamples]
-  static constexpr int kKeys = 0;                                    // [waves][kThrList] keys
-  static constexpr int kIdx = kKeys + kThrWaves * kThrList;          // [waves][kThrList] uint16 indices
-  static constexpr int kHi = kIdx + kThrWaves * kThrList / 2;        // [16] keys >= hi per sub-block
+  static constexpr int kKeys = 0;                                    // [waves][kThrListStride] keys
+  static constexpr int kIdx = kKeys + kThrWaves * kThrListStride;    // [waves][kThrListStride] uint16 indices
+  static constexpr int kHi = kIdx + kThrWaves * kThrListStride / 2;  // [16] keys >= hi per sub-block
   static constexpr int kKept = kHi + 16;                             // [16] kept gathered keys per sub-block
   static constexpr int kCnt = kKept + 16;                            // [2][waves] per-wave counts
   static constexpr int kDig = kCnt + 2 * kThrWaves;                  // [2][32] digit counts
-  static constexpr int kWords = kDig + 64;
+  static constexpr int kMisc = kDig + 64;                            // [4]
+  static constexpr int kWords = kMisc + 4;
 };
+static_assert(1024 + kMaxBlock / 32 <= kThrWaves * kThrListStride, "histograms and bitmap fit the key lists");
 
 // One 8-element vector of the block: gradient, codes and bucket pair.
 template <bool GBF16, int EFM>
@@ -106,9 +109,10 @@ __device__ __forceinline__ void vec_decode(const VecIn<GBF16, EFM>& x, uint32_t 
 //     their indices in the wave's part of LDS.  The bracket holds the answer
 //     when fewer than k keys lie at or above hi, at least k at or above lo,
 //     and no wave gathered more than kThrList; else the block is marked.
-//  3. T by a bitwise search over the gathered keys, the ties at T kept in
-//     index order (a bitwise search over their indices), and the row
-//     positions of the sub-blocks from their kept counts.
+//  3. T by a radix select over the gathered keys (8 bits per round, an LDS
+//     histogram per round), the ties at T kept in index order (the need-th
+//     set bit of an LDS bitmap of their indices), and the row positions of
+//     the sub-blocks from their kept counts.
 // The bracket's rank arithmetic is approximate: the check in 2 decides.
 template <bool GBF16, int EFM>
 __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, int64_t first, int64_t count) {
@@ -120,6 +124,7 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
   uint32_t* const kept_sb = smem + ThrLds::kKept;
   uint32_t* const cnt = smem + ThrLds::kCnt;
   uint32_t* const dig = smem + ThrLds::kDig;
+  uint32_t* const misc = smem + ThrLds::kMisc;
 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
   const int64_t gb = first + xcd_block(block_id(), count);
@@ -210,10 +215,13 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
   }
 
   // ---------------------------------------------- 2. the streamed pass
+  // Branch-free: a lane whose element is not in the bracket writes its sink
+  // slot (kThrList + lane) instead of a list slot, and positions past the
+  // list go to the sink too (the count still grows: overflow is detected).
   const uint32_t vpt = nvec / kThrThreads;  // vectors per thread: even, 4 .. 32
-  uint32_t* const mykey = lkey + wave * kThrList;
-  uint16_t* const myidx = lidx + wave * kThrList;
-  uint32_t wn = 0;  // keys this wave gathered (may pass kThrList: then only counted)
+  uint32_t* const mykey = lkey + wave * kThrListStride;
+  uint16_t* const myidx = lidx + wave * kThrListStride;
+  uint32_t wn = 0;  // keys this wave found in the bracket
   {
     const float lof = __uint_as_float(lo), hif = __uint_as_float(hi < 0x7F800000u ? hi : 0x7F800000u);
     auto pass = [&](auto nohi_tag) {
@@ -224,7 +232,7 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
 #pragma unroll
         for (int i = 0; i < 8; ++i)
           if (r0 + i < vpt) vec_load(x[i], rg, re, rs, kThrThreads * (r0 + i) + kWave * wave + lane, bl);
-        uint32_t nh[4] = {0u, 0u, 0u, 0u};  // keys >= hi in the round's four sub-blocks
+        uint32_t nh[4] = {0u, 0u, 0u, 0u};  // this lane's keys >= hi in the round's four sub-blocks
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           if (r0 + i >= vpt) continue;
@@ -234,23 +242,26 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const float ab = __builtin_fabsf(a[e]);
-            const uint64_t mh = NOHI ? 0ull : ballot(ab >= hib);
-            const uint64_t mi = ballot(ab >= lob) & ~mh;
-            if (!NOHI) nh[i >> 1] += popc(mh);
-            if (mi) {
-              const uint32_t pos = wn + lanes_below(mi);
-              if (__builtin_amdgcn_inverse_ballot_w64(mi) && pos < (uint32_t)kThrList) {
-                mykey[pos] = __float_as_uint(ab);
-                myidx[pos] = (uint16_t)(8 * j + e);
-              }
-              wn += popc(mi);
-            }
+            const bool above = !NOHI && ab >= hib;
+            const bool in = (ab >= lob) & !above;
+            nh[i >> 1] += above ? 1u : 0u;
+            const uint64_t mi = ballot(in);
+            const uint32_t pos = wn + lanes_below(mi);
+            const uint32_t at = in && pos < (uint32_t)kThrList ? pos : (uint32_t)(kThrList + lane);
+            mykey[at] = __float_as_uint(ab);
+            myidx[at] = (uint16_t)(8 * j + e);
+            wn += popc(mi);
           }
+          __builtin_amdgcn_sched_barrier(0);  // one vector at a time
         }
-        if (!NOHI && lane == 0) {
+        if (!NOHI) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (nh[q]) atomicAdd(&hi_sb[(r0 >> 1) + q], nh[q]);
+          for (int q = 0; q < 4; ++q) {
+            uint32_t t = nh[q];
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) t += __shfl_xor(t, d, kWave);
+            if (lane == 0 && t) atomicAdd(&hi_sb[(r0 >> 1) + q], t);
+          }
         }
       }
     };
@@ -284,77 +295,129 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
   }
 
   // ---------------------------------------------- 3. T, the ties, the offsets
+  // T is the kp-th largest gathered key (kp = k - n_hi), found by a radix
+  // select over rel = key - lo (< hi - lo), 8 bits per round from the top
+  // bit of hi - lo - 1: a 256-bin LDS histogram of the digit among the keys
+  // still in play, then every wave picks the digit where the count from the
+  // top reaches the keys still needed (one barrier per round; histograms
+  // alternate, each cleared the round before its use).
   const uint32_t mine = sgpr(cnt[kThrWaves + wave]);  // <= kThrList
   constexpr int NR = kThrList / kWave;
   uint32_t y[NR];
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
     const uint32_t q = (uint32_t)(lane + kWave * r);
-    y[r] = q < mine ? mykey[q] : 0u;  // 0 < lo: never counted
+    y[r] = q < mine ? mykey[q] - lo : 0xFFFFFFFFu;  // rel; past the list: out of play
   }
-  int buf = 0;
-  // workgroup total of one count per wave (`buf` alternates between calls)
-  auto wg_sum = [&](uint32_t v) {
-    if (lane == 0) cnt[buf * kThrWaves + wave] = v;
-    lds_sync();
-    uint32_t t = 0;
-#pragma unroll
-    for (int w = 0; w < kThrWaves; ++w) t += cnt[buf * kThrWaves + w];
-    buf ^= 1;
-    return sgpr(t);
-  };
-  // the largest t with count(key >= t) >= k: prefixes at or above hi fail
-  // and prefixes at or below lo pass without counting; count = n_hi + the
-  // gathered keys >= the prefix
-  uint32_t t = 0;
-  bool exact = false;
-  for (int bit = 30; bit >= 0 && !exact; --bit) {
-    const uint32_t c = t | (1u << bit);
-    if (c >= hi) continue;
-    if (c <= lo) {
-      t = c;
-      continue;
-    }
-    uint32_t n = 0;
-#pragma unroll
-    for (int r = 0; r < NR; ++r) n += popc(ballot(y[r] >= c));
-    n = n_hi + wg_sum((uint32_t)opaque((int)n));
-    if (n >= (uint32_t)kq) {
-      t = c;
-      exact = n == (uint32_t)kq;
-    }
-  }
-  uint32_t i_last = kAllTies;
-  if (!exact) {
-    // keys above t, and those equal to it: the first `need` of them in index
-    // order are kept
-    uint32_t ngt = 0, neq = 0;
+  // every wave holds its keys now: the key lists become the four rounds'
+  // histograms and the tie bitmap, cleared before any use
+  lds_sync();
+  uint32_t* const hist = lkey;          // [4][256]
+  uint32_t* const bits = lkey + 1024;   // [p.block / 32]
+  const uint32_t nw32 = (uint32_t)p.block / 32u;
+  for (uint32_t q = (uint32_t)tid; q < 1024u + nw32; q += kThrThreads) lkey[q] = 0u;
+  lds_sync();
+  const uint32_t width = hi - lo;
+  const int nbits = 32 - __builtin_clz((width - 1u) | 1u);
+  const uint32_t kp = (uint32_t)kq - n_hi;  // 1 <= kp <= n_in
+  uint32_t pre = 0;                         // rel prefix chosen so far (its bits >= sh_prev)
+  int sh_prev = 32;                         // 32: no prefix yet
+  uint32_t above = 0;                       // gathered keys above the prefix's range
+  uint32_t n_eq = 0;                        // gathered keys equal to T (the last round's bin)
+  for (int rd = 0; sh_prev > 0; ++rd) {
+    // the first round takes the top 1-8 bits of rel, the others 8 each
+    const int sh = rd == 0 ? (nbits - 1) / 8 * 8 : sh_prev - 8;
+    uint32_t* const h = hist + rd * 256;
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
-      ngt += popc(ballot(y[r] > t));
-      neq += popc(ballot(y[r] == t));
+      const uint32_t v = y[r];
+      const bool play = v < width && (rd == 0 || (v >> sh_prev) == pre);
+      if (play) atomicAdd(&h[(v >> sh) & 255u], 1u);
     }
-    // (both below 2^16: one sum carries the pair)
-    const uint32_t both = wg_sum((ngt << 16) | neq);
-    const uint32_t need = (uint32_t)kq - n_hi - (both >> 16);
-    if ((both & 0xFFFFu) != need) {
-      // the largest m with fewer than `need` tied indices below it is the
-      // need-th tied index
-      uint32_t z[NR];
+    lds_sync();
+    // digits 4l .. 4l + 3 in lane l; counts from the top
+    const u32x4 c4 = *(const u32x4*)(h + 4 * lane);
+    const uint32_t lsum = c4[0] + c4[1] + c4[2] + c4[3];
+    uint32_t suf = lsum;  // inclusive suffix sum over lanes >= this one
 #pragma unroll
-      for (int r = 0; r < NR; ++r)
-        z[r] = y[r] == t ? (uint32_t)myidx[lane + kWave * r] : 0x10000u;  // untied: never below
-      uint32_t mfound = 0;
-      for (int bit = 15; bit >= 0; --bit) {
-        const uint32_t c = mfound | (1u << bit);
-        if (c >= (uint32_t)p.block) continue;
-        uint32_t n = 0;
-#pragma unroll
-        for (int r = 0; r < NR; ++r) n += popc(ballot(z[r] < c));
-        if (wg_sum((uint32_t)opaque((int)n)) < need) mfound = c;
+    for (int d = 1; d < kWave; d <<= 1) {
+      const uint32_t o = __shfl_down(suf, d, kWave);
+      suf += lane + d < kWave ? o : 0u;
+    }
+    const uint32_t need = kp - above;
+    // the lane whose four digits hold the need-th key from the top
+    const uint64_t hm = ballot(suf >= need && suf - lsum < need);
+    const int hl = (int)__builtin_ctzll(hm | (1ull << 63));
+    uint32_t dsel = 0, abv = 0, neq = 0;
+    {
+      uint32_t cum = suf - lsum;  // keys in the lanes above
+      int dd = 3;
+      for (; dd > 0; --dd) {
+        if (cum + c4[dd] >= need) break;
+        cum += c4[dd];
       }
-      i_last = mfound;
+      dsel = 4u * (uint32_t)lane + (uint32_t)dd;
+      abv = cum;
+      neq = c4[dd];
     }
+    dsel = sgpr(__builtin_amdgcn_readlane(dsel, hl));
+    above += sgpr(__builtin_amdgcn_readlane(abv, hl));
+    n_eq = sgpr(__builtin_amdgcn_readlane(neq, hl));
+    pre = (rd == 0 ? 0u : pre << 8) | dsel;
+    sh_prev = sh;
+  }
+  const uint32_t t = lo + pre;             // the kp-th largest gathered key
+  const uint32_t need = kp - above;        // keys equal to t that are kept, >= 1
+  uint32_t i_last = kAllTies;
+  if (n_eq != need) {
+    // the need-th smallest index among keys equal to t: their bits in the
+    // cleared bitmap of the block's indices, each thread's 256 bits
+    // counted, a workgroup prefix
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+      if (y[r] == pre) {
+        const uint32_t ix = myidx[lane + kWave * r];
+        atomicOr(&bits[ix >> 5], 1u << (ix & 31u));
+      }
+    lds_sync();
+    constexpr int WPT = kMaxBlock / 32 / kThrThreads;  // words per thread: 8
+    uint32_t wv[WPT], c = 0;
+#pragma unroll
+    for (int q = 0; q < WPT; ++q) {
+      const uint32_t at = (uint32_t)tid * WPT + q;
+      wv[q] = at < nw32 ? bits[at] : 0u;
+      c += (uint32_t)__builtin_popcount(wv[q]);
+    }
+    // exclusive prefix of c (< 2^9) over the workgroup's threads
+    uint32_t in_wave = 0, wave_total = 0;
+#pragma unroll
+    for (int b2 = 0; b2 < 9; ++b2) {
+      const uint64_t m = ballot((c >> b2) & 1u);
+      in_wave += lanes_below(m) << b2;
+      wave_total += popc(m) << b2;
+    }
+    if (lane == 0) cnt[wave] = wave_total;
+    lds_sync();
+    uint32_t before = in_wave;
+#pragma unroll
+    for (int w = 0; w < kThrWaves; ++w) before += w < wave ? cnt[w] : 0u;
+    if (before < need && before + c >= need) {
+      uint32_t r2 = need - before;  // the r2-th set bit of this thread's words
+      uint32_t found = 0;
+#pragma unroll
+      for (int q = 0; q < WPT; ++q) {
+        const uint32_t pc = (uint32_t)__builtin_popcount(wv[q]);
+        if (found == 0 && r2 <= pc) {
+          uint32_t x = wv[q];
+          for (uint32_t z = 1; z < r2; ++z) x &= x - 1u;  // drop the lower set bits
+          found = ((uint32_t)tid * WPT + q) * 32u + (uint32_t)__builtin_ctz(x) + 1u;
+        }
+        if (found == 0) r2 -= pc;
+      }
+      misc[0] = found - 1u;
+    }
+    lds_sync();
+    i_last = sgpr(misc[0]);
   }
   // kept gathered keys per sub-block, then the row positions
 #pragma unroll
@@ -362,7 +425,7 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
     const uint32_t q = (uint32_t)(lane + kWave * r);
     if (q < mine) {
       const uint32_t ix = myidx[q];
-      const bool kept = y[r] > t || (y[r] == t && (i_last == kAllTies || ix <= i_last));
+      const bool kept = y[r] > pre || (y[r] == pre && (i_last == kAllTies || ix <= i_last));
       if (kept) atomicAdd(&kept_sb[ix >> 12], 1u);
     }
   }
