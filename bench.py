@@ -5,21 +5,23 @@ Default workload: the Llama-2-7B parameter list (291 tensors, 6,738,415,616
 bf16 parameters), bf16 gradients 1e-3 * Student-t(4), Top-K block 4096 at
 density 1% (k = 41), window m = 10, 4-bit EF with bucket 64, lr 1e-4.
 
-One step = one call of microadam_step over all 291 tensors.  For this
-workload it is one fused kernel launch (EF decode, block Top-K, new window
-row, EF re-quantisation, moment rebuild from the window, parameter update);
-configurations outside the fused kernel's limits run a select and an update
-kernel.  The W warm-up steps fill the window (W >= m gives steady state); the
-K timed steps run back to back, bracketed by device synchronisation.  Inputs
-are resident in HBM before timing starts: two gradient sets are generated up
-front and alternate between steps.
+One step = one call of microadam_step over all 291 tensors: a select phase
+(EF decode, block Top-K, new window row, EF re-quantisation) and an update
+phase (moment rebuild from the window, parameter update).  For this workload
+each phase is one kernel launch; blocks above 4096 elements run the select
+phase as three launches (threshold pass, apply pass, multi-wave select of the
+blocks the threshold pass left), and `--fused 1` runs the whole step as one
+kernel where the configuration allows.  The W warm-up steps fill the window
+(W >= m gives steady state); the K timed steps run back to back, bracketed by
+device synchronisation.  Inputs are resident in HBM before timing starts: two
+gradient sets are generated up front and alternate between steps.
 
-Prints one JSON line.  `roofline` describes the dominant (longest) kernel:
-`achieved` is its algorithmic HBM bytes per launch (fused_bytes, or
+Prints one JSON line.  `roofline` describes the dominant (longest) phase:
+`achieved` is its algorithmic HBM bytes per step (fused_bytes, or
 select_bytes / update_bytes) over its mean duration, timed with HIP events
-that the library records on the launch stream around each kernel of the timed
+that the library records on the launch stream around each phase of the timed
 steps (read once after them).  `traffic` comes from the committed rocprofv3
-FETCH_SIZE / WRITE_SIZE summary of that kernel when it was taken on the
+FETCH_SIZE / WRITE_SIZE summary of that phase when it was taken on the
 current kernel source, else null.  `cpu_baseline` times the CPU oracle, as it
 stands, on this host's cores (one process per core, each on its own sample of
 the workload's blocks) and reports the single-core rate beside it.
@@ -308,9 +310,14 @@ def main() -> int:
         sel_ms, upd_ms = sel_tot / n_timed, upd_tot / n_timed
         sel_b = select_bytes(w, args.ef_bits, bucket)
         upd_b = sum(update_bytes(w, t) for t in steps_t) / args.steps
+        large = w.block > 4096
+        split = large and opt.step_kernels == 4 and not (bucket >= w.block)
         kernels = {
-            "select_kernel": {"ms": sel_ms, "bytes": sel_b, "gbs": sel_b / sel_ms / 1e6},
-            "update_kernel": {"ms": upd_ms, "bytes": upd_b, "gbs": upd_b / upd_ms / 1e6},
+            "select_kernel": {"ms": sel_ms, "bytes": sel_b, "gbs": sel_b / sel_ms / 1e6,
+                              "launches": (["threshold_kernel", "apply_kernel", "select_large_kernel"] if split
+                                           else ["select_large_kernel"] if large else ["select_kernel"])},
+            "update_kernel": {"ms": upd_ms, "bytes": upd_b, "gbs": upd_b / upd_ms / 1e6,
+                              "launches": ["update_large_kernel" if large else "update_kernel"]},
         }
     dominant = max(kernels, key=lambda k: kernels[k]["ms"])
     dk = kernels[dominant]
