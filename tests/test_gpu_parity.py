@@ -112,6 +112,16 @@ CASES = {
                                       grad_dist="sparse_spikes", degenerate=True), 4),
     "block8192_sign_grad": (dict(numels=[8192 + 3000], block=8192, grad_dist="signs", grad_scale=1e-2,
                                  window=3, degenerate=True), 4),
+    # block counts of 4096-element sub-blocks that are not powers of two (the
+    # threshold pass's last round holds fewer than eight vectors per thread;
+    # the apply pass runs three and five waves per block), with a ragged tail
+    # that leaves whole sub-blocks empty, and tie groups at the threshold
+    "block12288_three_subblocks": (dict(numels=[12288 * 3 + 5000, 12288], block=12288, bucket=64, density=0.03,
+                                        window=4, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
+                                        grad_dist="student_t4"), 6),
+    "block20480_five_subblocks_ties": (dict(numels=[20480 * 2 + 9000], block=20480, bucket=128, density=0.05,
+                                            window=5, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
+                                            grad_dist="student_t2_snapped64"), 7),
     # the same formats in the multi-wave select (blocks above 4096): 8-bit
     # codes at B_d = 8192, randomized 4-bit codes at the flat workload's
     # B_d = 65536 with its bucket of 128 and k = 5%, and randomized 8-bit
@@ -180,6 +190,10 @@ def test_parity(name, fused):
     run = GpuOracleRun(numels, fused=fused, **kw)
     run.step()
     assert (run.opt.step_kernels == 1) == (fused == 1 and name in FUSED), (name, run.opt.step_kernels)
+    block, bucket = kw.get("block", 4096), kw.get("bucket", 64)
+    if block > 4096 and block % 4096 == 0 and bucket <= 512:
+        # threshold pass, apply pass, the multi-wave select of the blocks they left, update
+        assert run.opt.step_kernels == 4, (name, run.opt.step_kernels)
     for _ in range(steps - 1):
         run.step(check_moments=run.t % 2 == 0 or steps < 8)
     _report(run, name)
