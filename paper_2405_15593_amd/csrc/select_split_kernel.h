@@ -514,14 +514,23 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
   // i_last relative to this lane's first element (negative: no tie kept here)
   const int last_here = notie ? CAP : (int)i_last - (int)e_sb - (int)eb;
   const float tf = opaque_f(__uint_as_float(T));
+  // kept: |a| >= T when every key equal to T is kept (the common case), else
+  // |a| > T and |a| == T up to i_last
+  auto kept = [&](auto notie_tag, float ab, int i) {
+    if constexpr (decltype(notie_tag)::value) return ab >= tf;
+    else return (ab > tf) | ((ab == tf) & (i <= last_here));
+  };
   uint32_t sel_l = 0;
+  auto count_kept = [&](auto notie_tag) {
 #pragma unroll
-  for (int v = 0; v < NV; ++v)
+    for (int v = 0; v < NV; ++v)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float ab = __builtin_fabsf(a[v][e]);
-      sel_l += ((ab > tf) | ((ab == tf) & (8 * v + e <= last_here))) ? 1u : 0u;
-    }
+      for (int e = 0; e < 8; ++e) sel_l += kept(notie_tag, __builtin_fabsf(a[v][e]), 8 * v + e) ? 1u : 0u;
+  };
+  if (notie)
+    count_kept(BoolTag<true>{});
+  else
+    count_kept(BoolTag<false>{});
   uint32_t pre = 0, n_sb = 0;  // kept before this lane; in the sub-block
 #pragma unroll
   for (int b2 = 0; b2 < 7; ++b2) {
@@ -540,18 +549,19 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
   const bool staged = n_row * EW <= kApplyStageWords;
   const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
   const uint32_t row0 = (uint32_t)p.new_slot * kq + off0;
-  if (sel_l) {
-    const float tf2 = opaque_f(tf);
+  // (every kept entry fits the row unless the threshold pass kept more than
+  // k_q, which it does not; the bound check stays for that case)
+  auto write_row = [&](auto notie_tag, auto fits_tag, auto staged_tag) {
+    constexpr bool FITS = decltype(fits_tag)::value, STAGED = decltype(staged_tag)::value;
     uint32_t r = pre;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float ab = __builtin_fabsf(a[v][e]);
-        if ((ab > tf2) | ((ab == tf2) & (8 * v + e <= last_here))) {
-          if (r < n_row) {
+        if (kept(notie_tag, __builtin_fabsf(a[v][e]), 8 * v + e)) {
+          if (FITS || r < n_row) {
             const typename E::T x = E::make(e_sb + eb + 8 * v + e, a[v][e]);
-            if (staged) {
+            if constexpr (STAGED) {
               if constexpr (VF32) *(u32x2*)(smem + 2 * r) = x;
               else smem[r] = x;
             } else {
@@ -563,6 +573,14 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
       }
       __builtin_amdgcn_sched_barrier(0);  // one vector's stores at a time
     }
+  };
+  if (sel_l) {
+    if (notie && staged && n_row == n_sb)
+      write_row(BoolTag<true>{}, BoolTag<true>{}, BoolTag<true>{});
+    else if (staged)
+      write_row(BoolTag<false>{}, BoolTag<false>{}, BoolTag<true>{});
+    else
+      write_row(BoolTag<false>{}, BoolTag<false>{}, BoolTag<false>{});
   }
   if (staged) {
     wave_sync();
