@@ -25,9 +25,9 @@ namespace {
 // decay) and applies it (Algorithm 1; Algorithm 4).  The loads of the next
 // quarter (its table words, its segments and its parameters) go out before
 // the current quarter is rebuilt, so their latency hides behind the rebuild.
-// The decrement uses the hardware square root and reciprocal (each within
-// 1 ulp), so it lies within a few binary32 ulps of the correctly rounded
-// value.
+// The decrement (eta*c1*s1) * rcp(eps + sqrt(c2*s2)) uses the hardware
+// square root and reciprocal (each within 1 ulp), so it lies within a few
+// binary32 ulps of the correctly rounded value.
 constexpr int kQuartersPerWave = 4;
 constexpr int kOverflow = 4;
 constexpr int kPreRows = 8;  // rows of the next quarter loaded ahead
@@ -78,6 +78,7 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
   const Rsrc rrec = make_rsrc(p.state + p.win_plane + (uint64_t)gb * p.win_stride, (uint32_t)p.win_stride);
   const uint32_t table = (uint32_t)m * p.k_full * EB;
   const Rsrc rw = window_rsrc<VF32 ? 2 : 1>(p, gb, kq);
+  const float lc1 = p.lr * p.c1;  // eta * (1 - beta1) / (1 - beta1^t)
   const float w1s = lane < kMaxWindow ? constant_ptr(p.wpow)[lane] : 0.0f;
   const float w2s = lane < kMaxWindow ? constant_ptr(p.wpow)[kMaxWindow + lane] : 0.0f;
   auto weight = [&](float ws, int r) {
@@ -128,8 +129,7 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
   // one entry's read-add-write of both sums (entries outside the quarter go
   // to the sink pair)
   auto add = [&](int lo, ET e, float w1, float w2) {
-    const uint32_t i = E::word(e) - (uint32_t)lo;
-    const uint32_t zw = i < (uint32_t)kQuarter ? i : (uint32_t)kQuarter;
+    const uint32_t zw = __builtin_elementwise_min(E::word(e) - (uint32_t)lo, (uint32_t)kQuarter);
     const float v = E::val(e);
     const float2 a = z[zw];
     z[zw] = make_float2(a.x + w1 * v, a.y + w2 * (v * v));
@@ -224,11 +224,10 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
       V::unpack(th[v], thf);
 #pragma unroll
       for (int e = 0; e < EV; ++e) {
-        const float mh = p.c1 * s1[e];
-        const float vh = p.c2 * s2[e];
-        const float den = p.eps + __builtin_amdgcn_sqrtf(vh);
-        const bool none = (s1[e] == 0.0f) & (s2[e] == 0.0f);
-        const float d = none ? 0.0f : p.lr * (mh * __builtin_amdgcn_rcpf(den));
+        // an element without entries has s1 = s2 = 0, so its decrement is
+        // 0 * rcp(eps) = 0: no separate test
+        const float den = p.eps + __builtin_amdgcn_sqrtf(p.c2 * s2[e]);
+        const float d = (lc1 * s1[e]) * __builtin_amdgcn_rcpf(den);
         const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
         out[e] = base - d;
       }
