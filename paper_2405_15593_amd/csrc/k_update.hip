@@ -82,7 +82,7 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
   const int s = u.s, kq = u.kq;
   const int leader = u.gb & (NW - 1);
   const int R = (kq + kWave - 1) / kWave;
-  const bool staged = n_live * R <= kChunks;
+  const bool held = n_live * R <= kChunks;  // the leader holds every live chunk in registers
 
   // loads: the leader's window positions, KC chunks of 64 (positions without
   // an entry read entry 0 and are not used), then every thread's parameters.
@@ -93,7 +93,7 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
   ET w[kChunks];
   bool has[kChunks];  // the position holds an entry
   int rr[kChunks];    // the chunk's row age: 0 for the newest row
-  if (lead && staged) {
+  if (lead && held) {
     int row = 0, col = 0, slot = slot0;
 #pragma unroll
     for (int c = 0; c < kChunks; ++c) {
@@ -137,7 +137,7 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
       const float den = p.eps + __builtin_sqrtf(vh);
       return p.lr * (mh / den);
     };
-    if (staged) {
+    if (held) {
       // chunks past the live rows hold only sink words
       uint32_t zp[kChunks];
       float val[kChunks];
