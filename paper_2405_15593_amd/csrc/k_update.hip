@@ -253,27 +253,33 @@ update_kernel(StepParams p, int64_t first_block, int64_t count, float* mhat, flo
   }
 
   // ------------------------------------------------ 6. parameter update
+  // (theta times the decay factor, skipped by a uniform branch when the
+  // factor is 1)
   const bool full = s == NT * kLaneElems;
+  auto apply = [&](auto one_tag) {
+    constexpr bool ONE_DECAY = decltype(one_tag)::value;
 #pragma unroll
-  for (int v = 0; v < V::NV; ++v) {
-    const uint32_t e0 = V::template first<NT>(v, tid);  // vectors past s store nothing
-    float upd[EV], thf[EV], out[EV];
+    for (int v = 0; v < V::NV; ++v) {
+      const uint32_t e0 = V::template first<NT>(v, tid);  // vectors past s store nothing
+      float upd[EV], thf[EV], out[EV];
 #pragma unroll
-    for (int q = 0; q < EV / 4; ++q) {
-      const float4 x = *(const float4*)(z1 + ((v * (EV / 4) + q) * NT + tid) * 4);
-      upd[4 * q] = x.x;
-      upd[4 * q + 1] = x.y;
-      upd[4 * q + 2] = x.z;
-      upd[4 * q + 3] = x.w;
+      for (int q = 0; q < EV / 4; ++q) {
+        const float4 x = *(const float4*)(z1 + ((v * (EV / 4) + q) * NT + tid) * 4);
+        upd[4 * q] = x.x;
+        upd[4 * q + 1] = x.y;
+        upd[4 * q + 2] = x.z;
+        upd[4 * q + 3] = x.w;
+      }
+      V::unpack(th[v], thf);
+#pragma unroll
+      for (int e = 0; e < EV; ++e) out[e] = (ONE_DECAY ? thf[e] : thf[e] * p.decay) - upd[e];
+      V::store(rp, e0, s, full, out);
     }
-    V::unpack(th[v], thf);
-#pragma unroll
-    for (int e = 0; e < EV; ++e) {
-      const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
-      out[e] = base - upd[e];
-    }
-    V::store(rp, e0, s, full, out);
-  }
+  };
+  if (p.decay_is_one)
+    apply(BoolTag<true>{});
+  else
+    apply(BoolTag<false>{});
 }
 
 // Chunks of 64 window entries the update's leader wave processes per block:

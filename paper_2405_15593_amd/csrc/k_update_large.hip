@@ -228,7 +228,7 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
         // 0 * rcp(eps) = 0: no separate test
         const float den = p.eps + __builtin_amdgcn_sqrtf(p.c2 * s2[e]);
         const float d = (lc1 * s1[e]) * __builtin_amdgcn_rcpf(den);
-        const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
+        const float base = thf[e] * p.decay;  // exact when the factor is 1
         out[e] = base - d;
       }
       V::store(param_rsrc(q), e0, s, full, out);

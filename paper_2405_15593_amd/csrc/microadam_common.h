@@ -183,6 +183,26 @@ __device__ __forceinline__ uint32_t to_bf16_bits(float x) {
   return (uint32_t)__builtin_bit_cast(uint16_t, b);
 }
 
+// Two floats rounded to bf16 (half to even), lo in the low half: one
+// v_cvt_pk_bf16_f32 for the pair.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
+}
+
+// 2w + c: the lane's flag c shifted into the low bit of w, by one add with
+// carry that takes c from the wave's lane mask (a per-lane bit set in one
+// instruction per element).  The two wait states ahead of the add cover a
+// mask written by the instruction just before it.
+__device__ __forceinline__ uint32_t shift_in_flag(uint32_t w, bool c) {
+  const uint64_t m = __builtin_amdgcn_ballot_w64(c);
+  uint32_t r;
+  uint64_t carry_out;
+  asm("s_nop 1\n\tv_addc_co_u32_e64 %0, %1, %2, %2, %3" : "=v"(r), "=s"(carry_out) : "v"(w), "s"(m));
+  return r;
+}
+
 // Buffer resource over [base, base + bytes): loads past the end read 0 and
 // stores past it are dropped.  Base and size are workgroup-uniform; reading
 // them through readfirstlane keeps the resource in scalar registers.
@@ -272,7 +292,7 @@ __device__ __forceinline__ void store8(Rsrc r, uint32_t elem, int s, bool full, 
     if constexpr (BF16) {
       u32x4 w;
 #pragma unroll
-      for (int h = 0; h < 4; ++h) w[h] = to_bf16_bits(in[2 * h]) | (to_bf16_bits(in[2 * h + 1]) << 16);
+      for (int h = 0; h < 4; ++h) w[h] = pack_bf16x2(in[2 * h], in[2 * h + 1]);
       __builtin_amdgcn_raw_buffer_store_b128(w, r, elem * es, 0, 0);
     } else {
       __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(in[0]), __float_as_uint(in[1]),
@@ -334,7 +354,7 @@ template <bool BF16> struct Vec16 {
       u32x4 w;
 #pragma unroll
       for (int h = 0; h < 4; ++h)
-        w[h] = BF16 ? (to_bf16_bits(in[2 * h]) | (to_bf16_bits(in[2 * h + 1]) << 16)) : __float_as_uint(in[h]);
+        w[h] = BF16 ? pack_bf16x2(in[2 * h], in[2 * h + 1]) : __float_as_uint(in[h]);
       __builtin_amdgcn_raw_buffer_store_b128(w, r, elem * (BF16 ? 2u : 4u), 0, kStream);
     } else {
 #pragma unroll

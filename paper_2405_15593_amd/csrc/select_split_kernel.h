@@ -28,7 +28,16 @@ constexpr int kThrListStride = kThrList + kWave;   // + one sink slot per lane
 constexpr int kThrSampleRes = 15;                  // the sample's order statistics to 2^15 (1/256 binade)
 constexpr uint32_t kThrRecordBytes = 128;          // per block
 constexpr uint32_t kAllTies = 0xFFFFFFFFu;         // i_last: every key equal to T is kept
-constexpr uint32_t kApplyStageWords = 1024;        // apply kernel: row words staged in LDS
+constexpr uint32_t kApplyValWords = 2048;          // apply kernel: a sub-block's values as bf16
+constexpr uint32_t kApplyStageWords = 448;         // apply kernel: row words staged in LDS
+
+// LDS of an apply wave: the exchange and the codes' store of the one-wave
+// select, then (bf16 entries) the sub-block's values and the staged row
+constexpr size_t apply_lds_words() {
+  return select_lds_words() > kApplyValWords + kApplyStageWords ? select_lds_words()
+                                                                 : kApplyValWords + kApplyStageWords;
+}
+static_assert(16 * apply_lds_words() * 4 <= 163840, "sixteen apply waves fit a compute unit's LDS");
 
 // The per-block record the threshold kernel writes (uint32 words):
 //   [0] 1 when the bracket held the threshold (else the multi-wave select
@@ -509,7 +518,8 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
   const int rem = ss - (int)eb;
   lane_decode(in, a, rem, full);
 
-  // kept elements: counted, positioned in element order, written to the row
+  // kept elements: a set per lane, positioned in element order, written to
+  // the row
   const bool notie = i_last == kAllTies;
   // i_last relative to this lane's first element (negative: no tie kept here)
   const int last_here = notie ? CAP : (int)i_last - (int)e_sb - (int)eb;
@@ -520,17 +530,23 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
     if constexpr (decltype(notie_tag)::value) return ab >= tf;
     else return (ab > tf) | ((ab == tf) & (i <= last_here));
   };
-  uint32_t sel_l = 0;
-  auto count_kept = [&](auto notie_tag) {
+  // the lane's kept set: element i at bit 31 - (i mod 32) of word i / 32, so
+  // that the leading zeros of a word lead to its next kept element
+  uint32_t km[2] = {0u, 0u};
+  auto mark_kept = [&](auto notie_tag) {
 #pragma unroll
     for (int v = 0; v < NV; ++v)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sel_l += kept(notie_tag, __builtin_fabsf(a[v][e]), 8 * v + e) ? 1u : 0u;
+      for (int e = 0; e < 8; ++e) {
+        uint32_t& w = km[v / (NV / 2)];
+        w = shift_in_flag(w, kept(notie_tag, __builtin_fabsf(a[v][e]), 8 * v + e));
+      }
   };
   if (notie)
-    count_kept(BoolTag<true>{});
+    mark_kept(BoolTag<true>{});
   else
-    count_kept(BoolTag<false>{});
+    mark_kept(BoolTag<false>{});
+  const uint32_t sel_l = (uint32_t)__builtin_popcount(km[0]) + (uint32_t)__builtin_popcount(km[1]);
   uint32_t pre = 0, n_sb = 0;  // kept before this lane; in the sub-block
 #pragma unroll
   for (int b2 = 0; b2 < 7; ++b2) {
@@ -540,9 +556,9 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
   }
   n_sb = sgpr(n_sb);
   if ((lane & 15) == 0 && 4 * sb + (lane >> 4) < nq) table_store(4 * sb + (lane >> 4), off0 + pre);
-  // the sub-block's entries that enter the row, [off0, off0 + n_row), go
-  // through LDS (the exchange is over) and leave as consecutive words;
-  // past kApplyStageWords each is stored where it is found
+  // the sub-block's entries that enter the row, [off0, off0 + n_row), are
+  // staged in LDS and leave as consecutive words; past kApplyStageWords
+  // each is stored where it is found
   constexpr uint32_t EW = VF32 ? 2u : 1u;
   const uint32_t room = off0 < (uint32_t)kq ? (uint32_t)kq - off0 : 0u;
   const uint32_t n_row = n_sb < room ? n_sb : room;
@@ -551,41 +567,78 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
   const uint32_t row0 = (uint32_t)p.new_slot * kq + off0;
   // (every kept entry fits the row unless the threshold pass kept more than
   // k_q, which it does not; the bound check stays for that case)
-  auto write_row = [&](auto notie_tag, auto fits_tag, auto staged_tag) {
-    constexpr bool FITS = decltype(fits_tag)::value, STAGED = decltype(staged_tag)::value;
-    uint32_t r = pre;
+  uint32_t* const stage = smem + (VF32 ? 0u : kApplyValWords);
+  if constexpr (!VF32) {
+    // bf16 entries: the lane's values go to LDS as bf16, element i at
+    // halfword i of the lane's 128 bytes (the exchange is over), and each
+    // lane walks its kept set, reading each value back by its element number
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
+      u32x4 x;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        if (kept(notie_tag, __builtin_fabsf(a[v][e]), 8 * v + e)) {
-          if (FITS || r < n_row) {
-            const typename E::T x = E::make(e_sb + eb + 8 * v + e, a[v][e]);
-            if constexpr (STAGED) {
-              if constexpr (VF32) *(u32x2*)(smem + 2 * r) = x;
-              else smem[r] = x;
-            } else {
-              E::store(rw, row0 + r, x);
-            }
+      for (int h = 0; h < 4; ++h) x[h] = pack_bf16x2(a[v][2 * h], a[v][2 * h + 1]);
+      *(u32x4*)(smem + 32 * lane + 4 * v) = x;
+    }
+    wave_sync();
+    const uint16_t* const vals = (const uint16_t*)smem + 64 * lane;
+    const uint32_t idx0 = e_sb + eb;
+    auto walk = [&](auto staged_tag) {
+      constexpr bool STAGED = decltype(staged_tag)::value;
+      uint32_t r = pre;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        uint32_t m = km[h];
+        while (m != 0u) {
+          const uint32_t e = (uint32_t)__builtin_clz(m);
+          m ^= 0x80000000u >> e;
+          const uint32_t i = 32u * (uint32_t)h + e;
+          const uint32_t x = (idx0 + i) | ((uint32_t)vals[i] << 16);  // the entry of element i
+          if (r < n_row) {
+            if constexpr (STAGED) stage[r] = x;
+            else E::store(rw, row0 + r, x);
           }
           ++r;
         }
       }
-      __builtin_amdgcn_sched_barrier(0);  // one vector's stores at a time
-    }
-  };
-  if (sel_l) {
-    if (notie && staged && n_row == n_sb)
-      write_row(BoolTag<true>{}, BoolTag<true>{}, BoolTag<true>{});
-    else if (staged)
-      write_row(BoolTag<false>{}, BoolTag<false>{}, BoolTag<true>{});
+    };
+    if (staged)
+      walk(BoolTag<true>{});
     else
-      write_row(BoolTag<false>{}, BoolTag<false>{}, BoolTag<false>{});
+      walk(BoolTag<false>{});
+  } else {
+    // binary32 entries: each kept element written from its register
+    auto write_row = [&](auto notie_tag, auto staged_tag) {
+      constexpr bool STAGED = decltype(staged_tag)::value;
+      uint32_t r = pre;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if (kept(notie_tag, __builtin_fabsf(a[v][e]), 8 * v + e)) {
+            if (r < n_row) {
+              const typename E::T x = E::make(e_sb + eb + 8 * v + e, a[v][e]);
+              if constexpr (STAGED) *(u32x2*)(stage + 2 * r) = x;
+              else E::store(rw, row0 + r, x);
+            }
+            ++r;
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);  // one vector's stores at a time
+      }
+    };
+    if (sel_l) {
+      if (notie && staged)
+        write_row(BoolTag<true>{}, BoolTag<true>{});
+      else if (staged)
+        write_row(BoolTag<false>{}, BoolTag<true>{});
+      else
+        write_row(BoolTag<false>{}, BoolTag<false>{});
+    }
   }
   if (staged) {
     wave_sync();
     for (uint32_t q = (uint32_t)lane; q < n_row * EW; q += kWave)
-      __builtin_amdgcn_raw_buffer_store_b32(smem[q], rw, (row0 * EW + q) * 4, 0, kStream);
+      __builtin_amdgcn_raw_buffer_store_b32(stage[q], rw, (row0 * EW + q) * 4, 0, kStream);
   }
   // ---------------------------------------------- e = Q(a with a[I] = 0)
   lane_quantize_store<EPL, LB, EFM>(a, T, notie, (uint32_t)((int)i_last - (int)e_sb), eb, ss, rem, full, bl, true,
@@ -601,7 +654,7 @@ hipError_t launch_select_split(const StepParams& p, int64_t first, int64_t count
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int32_t nsb = p.block / kSubBlock;
-  const size_t lds = select_lds_words() * 4;
+  const size_t lds = apply_lds_words() * 4;
   if ((1 << p.bucket_log2) >= 64)
     hipLaunchKernelGGL((apply_kernel<true, GB, VF, EFM>), dim3((uint32_t)(count * nsb)), dim3(kWave), lds, stream, p,
                        first, count, nsb);

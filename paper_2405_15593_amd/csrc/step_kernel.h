@@ -678,7 +678,7 @@ __device__ __forceinline__ void step_process(const StepParams& p, int64_t gb, in
       const float mh = p.c1 * a1, vh = p.c2 * a2;
       // correctly rounded square root and division
       const float d = none ? 0.0f : p.lr * (mh / (p.eps + __builtin_sqrtf(vh)));
-      const float base = p.decay_is_one ? thf[e] : thf[e] * p.decay;
+      const float base = thf[e] * p.decay;  // exact when the factor is 1
       out[e] = base - d;
     }
     store8<BF16>(rp, eb + 8 * v, s, full, out);
