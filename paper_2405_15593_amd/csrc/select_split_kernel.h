@@ -224,9 +224,11 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
   }
 
   // ---------------------------------------------- 2. the streamed pass
-  // Branch-free: a lane whose element is not in the bracket writes its sink
-  // slot (kThrList + lane) instead of a list slot, and positions past the
-  // list go to the sink too (the count still grows: overflow is detected).
+  // The lanes of an element in the bracket append it (its a, whose sign
+  // the reads below drop, and its index) to the wave's list; a vector whose
+  // 512 elements might not fit the list's remaining room takes the checked
+  // form, where positions past the list go to the lane's sink slot (the
+  // count still grows: overflow is detected).
   const uint32_t vpt = nvec / kThrThreads;  // vectors per thread: even, 4 .. 32
   uint32_t* const mykey = lkey + wave * kThrListStride;
   uint16_t* const myidx = lidx + wave * kThrListStride;
@@ -237,36 +239,55 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
       constexpr bool NOHI = decltype(nohi_tag)::value;
       const float lob = opaque_f(lof), hib = opaque_f(hif);
       for (uint32_t r0 = 0; r0 < vpt; r0 += 8) {
+        // (all eight loads go out unconditionally, so that none waits on
+        // another; a vector past the block reads zeros through the buffer
+        // bounds and is not used)
         VI x[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-          if (r0 + i < vpt) vec_load(x[i], rg, re, rs, kThrThreads * (r0 + i) + kWave * wave + lane, bl);
-        uint32_t nh[4] = {0u, 0u, 0u, 0u};  // this lane's keys >= hi in the round's four sub-blocks
+        for (int i = 0; i < 8; ++i) vec_load(x[i], rg, re, rs, kThrThreads * (r0 + i) + kWave * wave + lane, bl);
+        // this lane's keys below hi, and its elements, in the round's four
+        // sub-blocks (the keys >= hi are the difference)
+        uint32_t nb[4] = {0u, 0u, 0u, 0u}, ne[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           if (r0 + i >= vpt) continue;
           const uint32_t j = kThrThreads * (r0 + i) + kWave * wave + lane;
           float a[8];
           vec_decode(x[i], j, s, full, a);
+          auto gather = [&](auto checked_tag) {
+            constexpr bool CHECKED = decltype(checked_tag)::value;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float ab = __builtin_fabsf(a[e]);
-            const bool above = !NOHI && ab >= hib;
-            const bool in = (ab >= lob) & !above;
-            nh[i >> 1] += above ? 1u : 0u;
-            const uint64_t mi = ballot(in);
-            const uint32_t pos = wn + lanes_below(mi);
-            const uint32_t at = in && pos < (uint32_t)kThrList ? pos : (uint32_t)(kThrList + lane);
-            mykey[at] = __float_as_uint(ab);
-            myidx[at] = (uint16_t)(8 * j + e);
-            wn += popc(mi);
-          }
+            for (int e = 0; e < 8; ++e) {
+              const float ab = __builtin_fabsf(a[e]);
+              const bool below = NOHI || ab < hib;
+              const bool in = (ab >= lob) & below;
+              if constexpr (!NOHI) nb[i >> 1] += below ? 1u : 0u;
+              // (the mask from the compares themselves rather than from `in`)
+              const uint64_t mi = NOHI ? ballot(ab >= lob) : ballot(ab >= lob) & ballot(ab < hib);
+              if constexpr (CHECKED) {
+                const uint32_t pos = lanes_below_from(mi, wn);
+                const uint32_t at = in && pos < (uint32_t)kThrList ? pos : (uint32_t)(kThrList + lane);
+                mykey[at] = __float_as_uint(a[e]);
+                myidx[at] = (uint16_t)(8 * j + e);
+              } else if (in) {
+                const uint32_t pos = lanes_below_from(mi, wn);
+                mykey[pos] = __float_as_uint(a[e]);
+                myidx[pos] = (uint16_t)(8 * j + e);
+              }
+              wn = sgpr(wn + popc(mi));
+            }
+          };
+          if (sgpr(wn) + 8u * kWave <= (uint32_t)kThrList)
+            gather(BoolTag<false>{});
+          else
+            gather(BoolTag<true>{});
+          ne[i >> 1] += 8u;
           __builtin_amdgcn_sched_barrier(0);  // one vector at a time
         }
         if (!NOHI) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            uint32_t t = nh[q];
+            uint32_t t = ne[q] - nb[q];
 #pragma unroll
             for (int d = 1; d < kWave; d <<= 1) t += __shfl_xor(t, d, kWave);
             if (lane == 0 && t) atomicAdd(&hi_sb[(r0 >> 1) + q], t);
@@ -316,7 +337,7 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
     const uint32_t q = (uint32_t)(lane + kWave * r);
-    y[r] = q < mine ? mykey[q] - lo : 0xFFFFFFFFu;  // rel; past the list: out of play
+    y[r] = q < mine ? (mykey[q] & 0x7FFFFFFFu) - lo : 0xFFFFFFFFu;  // rel; past the list: out of play
   }
   // every wave holds its keys now: the key lists become the four rounds'
   // histograms and the tie bitmap, cleared before any use
