@@ -314,7 +314,7 @@ def main() -> int:
         split = large and opt.step_kernels == 4 and not (bucket >= w.block)
         kernels = {
             "select_kernel": {"ms": sel_ms, "bytes": sel_b, "gbs": sel_b / sel_ms / 1e6,
-                              "launches": (["threshold_kernel", "apply_kernel", "select_large_kernel"] if split
+                              "launches": (["threshold_kernel", "apply_kernel", "select_large_list_kernel"] if split
                                            else ["select_large_kernel"] if large else ["select_kernel"])},
             "update_kernel": {"ms": upd_ms, "bytes": upd_b, "gbs": upd_b / upd_ms / 1e6,
                               "launches": ["update_large_kernel" if large else "update_kernel"]},

@@ -199,7 +199,9 @@ int microadam_state_bytes(const microadam_config* cfg, const int64_t* numels,
  * param_dtype / grad_dtype: MICROADAM_F32 or MICROADAM_BF16.
  * The library keeps small device tables of its own (freed by destroy:
  * the block -> tensor table, the window weights, and with Top-K blocks above
- * 4096 elements that are multiples of 4096 a 128-byte record per block);
+ * 4096 elements that are multiples of 4096 a 128-byte record per block
+ * and a list of the blocks the threshold pass could not settle, 4 bytes per
+ * block);
  * `state` stays owned by the caller and must outlive the handle.
  */
 int microadam_init(const microadam_config* cfg, const int64_t* numels,

@@ -60,6 +60,10 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
   float2* const z = (float2*)smem;  // [kQuarter + 1] (sum beta1^r V, sum beta2^r V^2)
 
   const int lane = thread_id();
+  // the threshold kernel's list of unsettled blocks is used up: its count
+  // starts the next step at 0
+  if (p.thr != nullptr && block_id() == 0 && lane == 0)
+    __builtin_amdgcn_raw_buffer_store_b32(0u, make_rsrc(p.thr + thr_list_offset(p.total_blocks), 16), 0, 0, 0);
   const int64_t wg = xcd_block(block_id(), count * nw);
   const int32_t gb = (int32_t)(first_block + wg / nw);
   const int es = PBF16 ? 2 : 4;

@@ -508,9 +508,12 @@ int microadam_init(const microadam_config* cfg, const int64_t* numels, int32_t n
   }
   // blocks above 4096 that are multiples of 4096, buckets inside blocks:
   // the threshold kernel's records (128 bytes per block, written every step)
+  // and its list of unsettled blocks, whose count starts at 0 (the update
+  // kernel clears it after every step)
   if (cfg->topk_block > microadam::kSubBlockElems && cfg->topk_block % microadam::kSubBlockElems == 0 &&
       !h->planes.big && !h->fused) {
-    if ((e = hipMalloc((void**)&h->d_thr, (size_t)total_blocks * 128)) != hipSuccess) {
+    if ((e = hipMalloc((void**)&h->d_thr, microadam::thr_bytes(total_blocks))) != hipSuccess ||
+        (e = hipMemset(h->d_thr + microadam::thr_list_offset(total_blocks), 0, 16)) != hipSuccess) {
       release(h);
       return hip_fail(e, "allocating the threshold records");
     }

@@ -72,13 +72,16 @@ struct StepParams {
   uint64_t table_bytes, partial_plane;
   int32_t n_tensors;
   // blocks above 4096 that are multiples of 4096, with buckets inside
-  // blocks: 128-byte per-block records of the threshold kernel (device
-  // memory of the handle; NULL: the multi-wave select takes every block),
-  // and thr_gate = 1 when the multi-wave select is to take only the blocks
-  // whose record says the threshold kernel could not settle them
+  // blocks: device memory of the handle (NULL: the multi-wave select takes
+  // every block) holding the threshold kernel's 128-byte per-block records,
+  // then the list of the blocks it could not settle: their number (16
+  // bytes) and the block numbers (4 bytes each), thr_list_bytes() in all
   uint8_t* thr;
-  int32_t thr_gate;
 };
+
+// Bytes of the records and the list at StepParams::thr for `blocks` blocks.
+__host__ __device__ inline size_t thr_list_offset(int64_t blocks) { return (size_t)blocks * 128; }
+__host__ __device__ inline size_t thr_bytes(int64_t blocks) { return thr_list_offset(blocks) + 16 + (size_t)blocks * 4; }
 
 // Steps with buckets spanning blocks: the per-block partials, their reduction
 // into the new bucket table, and the quantization of the residual with it

@@ -45,8 +45,8 @@ struct LargeLds {
 // from the bucket table, and the block ends with its partials (the (min, max)
 // of the residual in its first bucket and in the next one, over all waves)
 // instead of the codes, which a second pass quantizes.
-template <int NW, bool LB, bool GBF16, bool VF32, int EFM, bool LQ = false>
-__global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, int64_t first, int64_t count) {
+template <int NW, bool LB, bool GBF16, bool VF32, int EFM, bool LQ>
+__device__ __forceinline__ void select_large_block(const StepParams& p, int64_t gb) {
   constexpr int EPL = 64, NV = 8, NT = NW * kWave, CAP = NT * EPL, R = kCandPerThread, NC = NT * R;
   constexpr int SPT = kSamples / NT, SPL = kSamples / kWave;  // samples per thread; per lane
   constexpr int DPW = 16 / NW;                                  // sample digits per wave
@@ -65,12 +65,6 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   const int tid = thread_id(), lane = tid & (kWave - 1), wave = (int)sgpr((uint32_t)tid / kWave);
   const uint32_t eb = (uint32_t)tid * EPL;
   const int bl = p.bucket_log2;
-  const int64_t gb = first + xcd_block(block_id(), count);
-  if (p.thr_gate) {
-    // after the threshold and apply kernels: only the blocks they left
-    const Rsrc rrec = make_rsrc(p.thr + (uint64_t)gb * 128, 128);
-    if (sgpr(__builtin_amdgcn_raw_buffer_load_b32(rrec, 0, 0, 0)) != 0u) return;
-  }
 
   const uint32_t nbk = (uint32_t)(p.block >> bl);
   const uint32_t ef_bytes = (EFM & kEf8) ? (uint32_t)p.block : (uint32_t)(p.block >> 1);
@@ -542,6 +536,28 @@ __global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, 
   }
 }
 
+// One workgroup per block of [first, first + count).
+template <int NW, bool LB, bool GBF16, bool VF32, int EFM, bool LQ = false>
+__global__ void __launch_bounds__(NW * kWave) select_large_kernel(StepParams p, int64_t first, int64_t count) {
+  select_large_block<NW, LB, GBF16, VF32, EFM, LQ>(p, first + xcd_block(block_id(), count));
+}
+
+// After the threshold and apply kernels: the blocks they could not settle,
+// from their list, each workgroup taking every gridDim-th one.
+template <int NW, bool LB, bool GBF16, bool VF32, int EFM>
+__global__ void __launch_bounds__(NW * kWave) select_large_list_kernel(StepParams p) {
+  const uint32_t* const list = (const uint32_t*)(p.thr + thr_list_offset(p.total_blocks));
+  // (the count and the entries are bounded by the number of blocks, so that
+  // any content of the list gives in-bounds work)
+  const uint32_t n0 = sgpr(list[0]);
+  const uint32_t n = n0 < (uint64_t)p.total_blocks ? n0 : (uint32_t)p.total_blocks;
+  for (uint32_t i = (uint32_t)block_id(); i < n; i += gridDim.x) {
+    const uint32_t gb = sgpr(list[4 + i]);
+    if (gb < (uint64_t)p.total_blocks) select_large_block<NW, LB, GBF16, VF32, EFM, false>(p, (int64_t)gb);
+    lds_sync();  // the block's last LDS reads before the next block's first writes
+  }
+}
+
 // Waves of the large-block select kernel: 4096 elements each, 2 to 16.
 inline int large_waves(int block) {
   const int w = (block + kSubBlock - 1) / kSubBlock;
@@ -574,17 +590,36 @@ hipError_t launch_select_large(const StepParams& p, int64_t first, int64_t count
   }
 }
 
+// The multi-wave select over the list of blocks the threshold kernel could
+// not settle: at most one workgroup per compute unit's worth of them, each
+// taking every gridDim-th entry (an empty list costs one short launch).
+template <int NW, bool GB, bool VF, int EFM>
+hipError_t launch_select_large_list_t(const StepParams& p, hipStream_t stream) {
+  const size_t lds = LargeLds<NW>::words() * 4;
+  const uint32_t grid = (uint32_t)(p.total_blocks < 256 ? p.total_blocks : 256);
+  if ((1 << p.bucket_log2) >= 64)
+    hipLaunchKernelGGL((select_large_list_kernel<NW, true, GB, VF, EFM>), dim3(grid), dim3(NW * kWave), lds, stream, p);
+  else
+    hipLaunchKernelGGL((select_large_list_kernel<NW, false, GB, VF, EFM>), dim3(grid), dim3(NW * kWave), lds, stream, p);
+  return hipGetLastError();
+}
+
 // Blocks above 4096 elements in the error-feedback format EFM: with
-// threshold records (p.thr), the threshold and apply kernels, then the
-// multi-wave select for the blocks they left; else the multi-wave select.
+// threshold records (p.thr) and the whole step in one launch range, the
+// threshold and apply kernels, then the multi-wave select for the blocks
+// they left (their list); else the multi-wave select for every block.
 template <bool GB, bool VF, int EFM>
 hipError_t launch_select_large_all(const StepParams& p, int64_t first, int64_t count, hipStream_t stream) {
-  if (p.thr == nullptr) return launch_select_large<GB, VF, EFM>(p, first, count, stream);
+  if (p.thr == nullptr || first != 0 || count != p.total_blocks)
+    return launch_select_large<GB, VF, EFM>(p, first, count, stream);
   const hipError_t e = launch_select_split<GB, VF, EFM>(p, first, count, stream);
   if (e != hipSuccess) return e;
-  StepParams q = p;
-  q.thr_gate = 1;
-  return launch_select_large<GB, VF, EFM>(q, first, count, stream);
+  switch (large_waves(p.block)) {
+    case 2: return launch_select_large_list_t<2, GB, VF, EFM>(p, stream);
+    case 4: return launch_select_large_list_t<4, GB, VF, EFM>(p, stream);
+    case 8: return launch_select_large_list_t<8, GB, VF, EFM>(p, stream);
+    default: return launch_select_large_list_t<16, GB, VF, EFM>(p, stream);
+  }
 }
 
 template <int EFM>

@@ -320,7 +320,14 @@ __global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, in
   n_in = sgpr(n_in);
   const bool ok = !over && lo <= 0x7F800000u && n_hi < (uint32_t)kq && n_hi + n_in >= (uint32_t)kq;
   if (!ok) {
-    if (tid == 0) __builtin_amdgcn_raw_buffer_store_b32(0u, rrec, 0, 0, 0);
+    // the record says so, and the block joins the list the multi-wave select
+    // works through
+    if (tid == 0) {
+      __builtin_amdgcn_raw_buffer_store_b32(0u, rrec, 0, 0, 0);
+      uint32_t* const list = (uint32_t*)(p.thr + thr_list_offset(p.total_blocks));
+      const uint32_t at = __hip_atomic_fetch_add(list, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (at < (uint64_t)p.total_blocks) list[4 + at] = (uint32_t)gb;
+    }
     return;
   }
 
