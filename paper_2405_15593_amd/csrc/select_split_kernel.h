@@ -23,7 +23,7 @@ namespace {
 constexpr int kThrThreads = 256;                   // threshold kernel: four waves per block
 constexpr int kThrWaves = kThrThreads / kWave;
 constexpr int kThrSamples = 1024;                  // sample keys (128 vectors of 8)
-constexpr int kThrList = 1536;                     // bracketed keys gathered per wave
+constexpr int kThrList = 1024;                     // bracketed keys gathered per wave
 constexpr int kThrListStride = kThrList + kWave;   // + one sink slot per lane
 constexpr int kThrSampleRes = 15;                  // the sample's order statistics to 2^15 (1/256 binade)
 constexpr uint32_t kThrRecordBytes = 128;          // per block
@@ -59,6 +59,7 @@ struct ThrLds {
   static constexpr int kWords = kMisc + 4;
 };
 static_assert(1024 + kMaxBlock / 32 <= kThrWaves * kThrListStride, "histograms and bitmap fit the key lists");
+static_assert(6 * ThrLds::kWords * 4 <= 163840, "six threshold workgroups fit a compute unit's LDS");
 
 // One 8-element vector of the block: gradient, codes and bucket pair.
 template <bool GBF16, int EFM>
@@ -123,8 +124,13 @@ __device__ __forceinline__ void vec_decode(const VecIn<GBF16, EFM>& x, uint32_t 
 //     set bit of an LDS bitmap of their indices), and the row positions of
 //     the sub-blocks from their kept counts.
 // The bracket's rank arithmetic is approximate: the check in 2 decides.
+// Six workgroups per compute unit (the LDS of ThrLds allows six, and the
+// registers are held to 80 for it): measured 2.23-2.26 -> 2.02 ms for the
+// select phase of the 1.5e9 workload against four workgroups with lists of
+// 1536 keys; shorter lists overflow on that workload's ties.
 template <bool GBF16, int EFM>
-__global__ void __launch_bounds__(kThrThreads) threshold_kernel(StepParams p, int64_t first, int64_t count) {
+__global__ void __launch_bounds__(kThrThreads) __attribute__((amdgpu_waves_per_eu(6)))
+threshold_kernel(StepParams p, int64_t first, int64_t count) {
   extern __shared__ __align__(16) uint32_t smem[];
   uint32_t* const samp = smem + ThrLds::kSample;
   uint32_t* const lkey = smem + ThrLds::kKeys;
