@@ -76,6 +76,11 @@ CASES = {
     "block8192_window30": (dict(numels=[8192 * 2 + 300], block=8192, density=0.02, window=30,
                                 param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3), 28),
     "block8192_dense_rows": (dict(numels=[8192 + 4100], block=8192, density=0.1, window=4), 6),
+    # binary32 window values with more kept entries per 4096-element sub-block
+    # (about 410) than the apply pass stages in LDS (224 of 8 bytes): each is
+    # stored where it is found
+    "block8192_dense_f32_values": (dict(numels=[8192 * 2 + 900], block=8192, density=0.1, window=3,
+                                        value_f32=True), 4),
     # error-feedback formats beyond the paper's default: 8-bit codes, and the
     # randomized rounding of Lemma 1 (Philox stream keyed by seed, tensor,
     # step and element), bit-exact against the oracle
