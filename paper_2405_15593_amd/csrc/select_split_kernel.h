@@ -254,9 +254,10 @@ threshold_kernel(StepParams p, int64_t first, int64_t count) {
         VI x[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) vec_load(x[i], rg, re, rs, kThrThreads * (r0 + i) + kWave * wave + lane, bl);
-        // this lane's keys below hi, and its elements, in the round's four
-        // sub-blocks (the keys >= hi are the difference)
-        uint32_t nb[4] = {0u, 0u, 0u, 0u}, ne[4] = {0u, 0u, 0u, 0u};
+        // this lane's keys >= hi in the round's four sub-blocks (from the
+        // same two compares as the bracket test: >= lo and not < hi, so
+        // that a NaN, which fails both, is not counted)
+        uint32_t nh[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           if (r0 + i >= vpt) continue;
@@ -268,9 +269,9 @@ threshold_kernel(StepParams p, int64_t first, int64_t count) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
               const float ab = __builtin_fabsf(a[e]);
-              const bool below = NOHI || ab < hib;
-              const bool in = (ab >= lob) & below;
-              if constexpr (!NOHI) nb[i >> 1] += below ? 1u : 0u;
+              const bool ge_lo = ab >= lob, below = NOHI || ab < hib;
+              const bool in = ge_lo & below;
+              if constexpr (!NOHI) nh[i >> 1] += (ge_lo & !below) ? 1u : 0u;
               // (the mask from the compares themselves rather than from `in`)
               const uint64_t mi = NOHI ? ballot(ab >= lob) : ballot(ab >= lob) & ballot(ab < hib);
               if constexpr (CHECKED) {
@@ -290,13 +291,12 @@ threshold_kernel(StepParams p, int64_t first, int64_t count) {
             gather(BoolTag<false>{});
           else
             gather(BoolTag<true>{});
-          ne[i >> 1] += 8u;
           __builtin_amdgcn_sched_barrier(0);  // one vector at a time
         }
         if (!NOHI) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            uint32_t t = ne[q] - nb[q];
+            uint32_t t = nh[q];
 #pragma unroll
             for (int d = 1; d < kWave; d <<= 1) t += __shfl_xor(t, d, kWave);
             if (lane == 0 && t) atomicAdd(&hi_sb[(r0 >> 1) + q], t);
