@@ -61,8 +61,9 @@ __global__ void __launch_bounds__(kWave) update_large_kernel(StepParams p, int64
 
   const int lane = thread_id();
   // the threshold kernel's list of unsettled blocks is used up: its count
-  // starts the next step at 0
-  if (p.thr != nullptr && block_id() == 0 && lane == 0)
+  // starts the next step at 0 (the step's own update only, not a moment
+  // export, which may run on another stream)
+  if (!EXPORT && p.thr != nullptr && block_id() == 0 && lane == 0)
     __builtin_amdgcn_raw_buffer_store_b32(0u, make_rsrc(p.thr + thr_list_offset(p.total_blocks), 16), 0, 0, 0);
   const int64_t wg = xcd_block(block_id(), count * nw);
   const int32_t gb = (int32_t)(first_block + wg / nw);
