@@ -196,14 +196,28 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // 2w + c: the lane's flag c shifted into the low bit of w, by one add with
-// carry that takes c from the wave's lane mask (a per-lane bit set in one
+// carry that takes c from the wave's lane mask m (a per-lane bit set in one
 // instruction per element).  The two wait states ahead of the add cover a
-// mask written by the instruction just before it.
-__device__ __forceinline__ uint32_t shift_in_flag(uint32_t w, bool c) {
-  const uint64_t m = __builtin_amdgcn_ballot_w64(c);
+// mask written by the instruction just before it.  A flag that is a logical
+// combination of compares is best passed as the same combination of their
+// masks (shift_in_mask): a ballot of the combined flag costs two more
+// instructions per element.
+__device__ __forceinline__ uint32_t shift_in_mask(uint32_t w, uint64_t m) {
   uint32_t r;
   uint64_t carry_out;
   asm("s_nop 1\n\tv_addc_co_u32_e64 %0, %1, %2, %2, %3" : "=v"(r), "=s"(carry_out) : "v"(w), "s"(m));
+  return r;
+}
+__device__ __forceinline__ uint32_t shift_in_flag(uint32_t w, bool c) {
+  return shift_in_mask(w, __builtin_amdgcn_ballot_w64(c));
+}
+// shift_in_mask, and x replaced by 0 in the lanes of m, from the one mask.
+__device__ __forceinline__ uint32_t shift_in_mask_zero(uint32_t w, uint64_t m, float& x) {
+  uint32_t r;
+  uint64_t carry_out;
+  asm("s_nop 1\n\tv_addc_co_u32_e64 %0, %1, %3, %3, %4\n\tv_cndmask_b32_e64 %2, %2, 0, %4"
+      : "=&v"(r), "=&s"(carry_out), "+v"(x)
+      : "v"(w), "s"(m));
   return r;
 }
 
@@ -855,30 +869,37 @@ __device__ __forceinline__ void lane_store_codes(const uint32_t (&wv)[(EPL / 8) 
 
 // ------------------------------------- coalesced block loads and stores
 // One wave over a 4096-element block (64 elements per lane: lane l owns
-// [64l, 64l + 64)) with bf16 gradients and 4-bit codes.  A lane's own run is
-// 128 bytes of gradient and 32 bytes of codes, so loading it directly gives
-// every 16-byte access of the wave a 128-byte (or 32-byte) stride.  Instead
+// [64l, 64l + 64)) with bf16 gradients.  A lane's own run is 128 bytes of
+// gradient and 32 (4-bit) or 64 (8-bit) bytes of codes, so loading it
+// directly gives every 16-byte access of the wave a 128-byte (or 32- or
+// 64-byte) stride.  Instead
 // the wave loads the block as contiguous kilobytes (access v of lane l is
 // bytes 1024v + 16l) with the nt policy, and the data reaches its owner
 // through LDS.  Layouts in LDS (byte offsets; the padding keeps 16 lanes'
 // 16-byte reads on distinct banks):
 //   gradient: element e of a half block at 2e + 16*(e / 64), 4608 bytes per
 //     half (a half is 32 lanes' runs, loaded by accesses 0-3 or 4-7);
-//   codes: code byte c at kTrCodes + c + 16*(c / 32), 3072 bytes.
+//   4-bit codes: code byte c at kTrCodes + c + 16*(c / 32), 3072 bytes;
+//   8-bit codes: code byte c at c + 16*(c / 64), 5120 bytes, exchanged
+//     before the gradient through the start of the same LDS.
 // The two halves of the gradient pass one after the other through the same
 // 4608 bytes, so the exchange needs 7680 bytes of LDS.
 constexpr uint32_t kTrCodes = 4608;
 constexpr uint32_t kTrBytes = 7680;
+constexpr uint32_t kTrCodes8Bytes = 5120;
 static_assert(kTrBytes <= select_lds_words() * 4, "the exchange reuses the select kernel's LDS");
+static_assert(kTrCodes8Bytes <= kTrBytes, "the 8-bit code exchange fits the same LDS");
 
 struct CoalescedIn {
   u32x4 g[8];
-  u32x4 c[2];
+  u32x4 c[4];  // codes: 2 accesses (4-bit) or 4 (8-bit)
 };
 
+template <int EFM>
 __device__ __forceinline__ void coalesced_load_codes(CoalescedIn& x, Rsrc re, int lane) {
 #pragma unroll
-  for (int q = 0; q < 2; ++q) x.c[q] = __builtin_amdgcn_raw_buffer_load_b128(re, 1024 * q + 16 * lane, 0, kStream);
+  for (int q = 0; q < ((EFM & kEf8) ? 4 : 2); ++q)
+    x.c[q] = __builtin_amdgcn_raw_buffer_load_b128(re, 1024 * q + 16 * lane, 0, kStream);
 }
 __device__ __forceinline__ void coalesced_load_grad(CoalescedIn& x, Rsrc rg, int lane) {
 #pragma unroll
@@ -890,25 +911,42 @@ __device__ __forceinline__ void coalesced_load_grad(CoalescedIn& x, Rsrc rg, int
 template <bool LB, int EFM>
 __device__ __forceinline__ void coalesced_exchange(const CoalescedIn& x, LaneIn<64, LB, true, EFM>& in,
                                                    uint32_t* lds, int lane) {
-  static_assert((EFM & kEf8) == 0, "4-bit codes");
+  constexpr bool EF8 = (EFM & kEf8) != 0;
   uint8_t* const b = (uint8_t*)lds;
   const uint32_t wg = 16u * (uint32_t)lane + 16u * (uint32_t)(lane >> 3);  // + 1152v: access v of this lane
   const uint32_t rg = 144u * (uint32_t)(lane & 31);                         // + 16V: this lane's vector V
+  if constexpr (EF8) {
+    // access q of lane l holds lane 16q + l/4's bytes 16*(l mod 4) ...
+#pragma unroll
+    for (int q = 0; q < 4; ++q) *(u32x4*)(b + 1280 * q + 80 * (lane >> 2) + 16 * (lane & 3)) = x.c[q];
+    wave_sync();
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const u32x4 t = *(const u32x4*)(b + 80 * lane + 16 * h);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) in.cw[4 * h + j] = t[j];
+    }
+    wave_sync();
+  }
 #pragma unroll
   for (int v = 0; v < 4; ++v) *(u32x4*)(b + 1152 * v + wg) = x.g[v];
+  if constexpr (!EF8) {
 #pragma unroll
-  for (int q = 0; q < 2; ++q)
-    *(u32x4*)(b + kTrCodes + 1536 * q + 16 * lane + 16 * (lane >> 1)) = x.c[q];
+    for (int q = 0; q < 2; ++q)
+      *(u32x4*)(b + kTrCodes + 1536 * q + 16 * lane + 16 * (lane >> 1)) = x.c[q];
+  }
   wave_sync();
   if (lane < 32) {
 #pragma unroll
     for (int v = 0; v < 8; ++v) in.graw[v].w[0] = *(const u32x4*)(b + rg + 16 * v);
   }
+  if constexpr (!EF8) {
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const u32x4 t = *(const u32x4*)(b + kTrCodes + 48 * lane + 16 * h);
+    for (int h = 0; h < 2; ++h) {
+      const u32x4 t = *(const u32x4*)(b + kTrCodes + 48 * lane + 16 * h);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) in.cw[4 * h + j] = t[j];
+      for (int j = 0; j < 4; ++j) in.cw[4 * h + j] = t[j];
+    }
   }
   wave_sync();
 #pragma unroll
@@ -921,20 +959,37 @@ __device__ __forceinline__ void coalesced_exchange(const CoalescedIn& x, LaneIn<
   wave_sync();
 }
 
-// Stores the lane's 4-bit codes (one word per vector) through LDS as
-// coalesced 16-byte accesses with the nt policy; the whole record of the
-// block is written (codes past the block's end are 0).
-__device__ __forceinline__ void lane_store_codes_coalesced(const uint32_t (&wv)[8], uint32_t* lds, Rsrc re) {
-  uint8_t* const b = (uint8_t*)lds + kTrCodes;
+// Stores the lane's codes (4-bit: one word per vector; 8-bit: two) through
+// LDS as coalesced 16-byte accesses with the nt policy, in the layouts of the
+// exchange; the whole record of the block is written (codes past the block's
+// end are 0).
+template <int EFM>
+__device__ __forceinline__ void lane_store_codes_coalesced(const uint32_t (&wv)[(EFM & kEf8) ? 16 : 8],
+                                                           uint32_t* lds, Rsrc re) {
   const int lane = thread_id() & (kWave - 1);
   wave_sync();
+  if constexpr ((EFM & kEf8) != 0) {
+    uint8_t* const b = (uint8_t*)lds;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) *(u32x4*)(b + 48 * lane + 16 * h) = u32x4{wv[4 * h], wv[4 * h + 1], wv[4 * h + 2], wv[4 * h + 3]};
-  wave_sync();
+    for (int h = 0; h < 4; ++h)
+      *(u32x4*)(b + 80 * lane + 16 * h) = u32x4{wv[4 * h], wv[4 * h + 1], wv[4 * h + 2], wv[4 * h + 3]};
+    wave_sync();
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const u32x4 t = *(const u32x4*)(b + 1536 * q + 16 * lane + 16 * (lane >> 1));
-    __builtin_amdgcn_raw_buffer_store_b128(t, re, 1024 * q + 16 * lane, 0, kStream);
+    for (int q = 0; q < 4; ++q) {
+      const u32x4 t = *(const u32x4*)(b + 1280 * q + 80 * (lane >> 2) + 16 * (lane & 3));
+      __builtin_amdgcn_raw_buffer_store_b128(t, re, 1024 * q + 16 * lane, 0, kStream);
+    }
+  } else {
+    uint8_t* const b = (uint8_t*)lds + kTrCodes;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      *(u32x4*)(b + 48 * lane + 16 * h) = u32x4{wv[4 * h], wv[4 * h + 1], wv[4 * h + 2], wv[4 * h + 3]};
+    wave_sync();
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const u32x4 t = *(const u32x4*)(b + 1536 * q + 16 * lane + 16 * (lane >> 1));
+      __builtin_amdgcn_raw_buffer_store_b128(t, re, 1024 * q + 16 * lane, 0, kStream);
+    }
   }
 }
 
@@ -978,11 +1033,12 @@ __device__ __forceinline__ void lane_zero_kept(float (&a)[EPL / 8][8], uint32_t 
 // kEfRandom the randomized Q of Lemma 1): zeroes the kept elements (|a| >
 // T, and |a| == T up to index i_last; every |a| >= T when notie), computes
 // the bucket (min, max) pairs and the codes, and stores both.
+// KEPT_ZEROED: the caller has zeroed the kept elements already.
 //
-// tr_lds (one-wave kernels with 64 elements per lane and 4-bit codes, over a
-// whole-lane block): the codes leave through LDS as coalesced 16-byte stores
+// tr_lds (one-wave kernels with 64 elements per lane, over a whole-lane
+// block): the codes leave through LDS as coalesced 16-byte stores
 // (lane_store_codes_coalesced), and the bucket pairs with the nt policy.
-template <int EPL, bool LB, int EFM = 0>
+template <int EPL, bool LB, int EFM = 0, bool KEPT_ZEROED = false>
 __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint32_t T, bool notie,
                                                     uint32_t i_last, uint32_t eb, int s, int rem, bool full, int bl,
                                                     bool wide, Rsrc re, Rsrc rs, const EfStream& rs_ef = {},
@@ -991,7 +1047,7 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
   constexpr bool EF8 = (EFM & kEf8) != 0;
   constexpr int CW = EF8 ? 2 : 1;
   constexpr int lg = EPL == 16 ? 4 : EPL == 32 ? 5 : 6;
-  lane_zero_kept<EPL>(a, T, notie, i_last, eb);
+  if constexpr (!KEPT_ZEROED) lane_zero_kept<EPL>(a, T, notie, i_last, eb);
   // bucket min / max: per vector, then over the vectors of a bucket inside
   // the lane, then over the lanes of a bucket
   float mn[NV], mx[NV];
@@ -1070,10 +1126,10 @@ __device__ __forceinline__ void lane_quantize_store(float (&a)[EPL / 8][8], uint
       for (int c = 0; c < CW; ++c) wv[CW * v + c] = w[c];
     }
   }
-  if constexpr (EPL == 64 && !EF8) {
+  if constexpr (EPL == 64) {
     if (tr_lds != nullptr) {
       // every lane takes part in the exchange; codes past s are 0
-      lane_store_codes_coalesced(wv, tr_lds, re);
+      lane_store_codes_coalesced<EFM>(wv, tr_lds, re);
       if constexpr (LB) {
         if ((int)eb < s && (eb & ((1u << bl) - 1)) == 0)
           __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(mn[0]), __float_as_uint(mx[0])}, rs,

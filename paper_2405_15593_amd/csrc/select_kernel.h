@@ -40,6 +40,8 @@ select_kernel(StepParams p, int64_t first, int64_t count) {
   // 4096-element blocks of bf16 gradients with 4-bit codes load and store
   // the block as contiguous kilobytes and exchange it through LDS
   // (coalesced_exchange); the other shapes load each lane's run directly
+  // (with 8-bit codes the exchange measured slower here: 5.95 vs 5.75 ms on
+  // the Llama-2-7B list)
   constexpr bool kCoal = EPL == 64 && GBF16 && (EFM & kEf8) == 0 && !LQ;
   const bool coal = kCoal && wide;
   LaneIn<EPL, LB, GBF16, EFM> in;
@@ -50,7 +52,7 @@ select_kernel(StepParams p, int64_t first, int64_t count) {
 #pragma unroll
     for (int v = 0; v < (LB ? 1 : EPL / 8); ++v)
       in.st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, kStream);
-    coalesced_load_codes(cx, re, lane);
+    coalesced_load_codes<EFM>(cx, re, lane);
   } else {
     lane_load_state(in, re, rs, eb, bl, wide);
   }

@@ -516,14 +516,14 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
   const uint32_t nbk = (uint32_t)(p.block >> bl), sub_bk = (uint32_t)(CAP >> bl);
   const Rsrc re = make_rsrc(p.state + p.ef_plane + (uint64_t)gb * ef_bytes + (uint64_t)sb * sub_ef, sub_ef);
   const Rsrc rs = make_rsrc(p.state + p.stats_plane + ((uint64_t)gb * nbk + (uint64_t)sb * sub_bk) * 8, sub_bk * 8);
-  constexpr bool kCoal = GBF16 && (EFM & kEf8) == 0;
+  constexpr bool kCoal = GBF16;
   LaneIn<EPL, LB, GBF16, EFM> in;
   CoalescedIn cx;
   if constexpr (kCoal) {
 #pragma unroll
     for (int v = 0; v < (LB ? 1 : NV); ++v)
       in.st[v] = __builtin_amdgcn_raw_buffer_load_b64(rs, ((eb + 8 * v) >> bl) * 8, 0, kStream);
-    coalesced_load_codes(cx, re, lane);
+    coalesced_load_codes<EFM>(cx, re, lane);
   } else {
     lane_load_state(in, re, rs, eb, bl, true);
   }
@@ -568,21 +568,43 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
     else return (ab > tf) | ((ab == tf) & (i <= last_here));
   };
   // the lane's kept set: element i at bit 31 - (i mod 32) of word i / 32, so
-  // that the leading zeros of a word lead to its next kept element
-  uint32_t km[2] = {0u, 0u};
-  auto mark_kept = [&](auto notie_tag) {
+  // that the leading zeros of a word lead to its next kept element.  With
+  // bf16 entries the lane's values go to LDS first (element i at halfword i
+  // of the lane's 128 bytes; the exchange is over), and the kept elements
+  // are zeroed for the quantization as they are marked.
+  if constexpr (!VF32) {
 #pragma unroll
-    for (int v = 0; v < NV; ++v)
+    for (int v = 0; v < NV; ++v) {
+      u32x4 x;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        uint32_t& w = km[v / (NV / 2)];
-        w = shift_in_flag(w, kept(notie_tag, __builtin_fabsf(a[v][e]), 8 * v + e));
-      }
+      for (int h = 0; h < 4; ++h) x[h] = pack_bf16x2(a[v][2 * h], a[v][2 * h + 1]);
+      *(u32x4*)(smem + 32 * lane + 4 * v) = x;
+    }
+    __builtin_amdgcn_sched_barrier(0);  // (the packed words die here)
+  }
+  // The mask of lanes whose element i is a tie kept by index: lane l holds
+  // element 64 l + i of the sub-block, kept when 64 l + i <= R (R: i_last in
+  // the sub-block), i.e. the lanes [0, floor((R - i) / 64)], which is
+  // [0, q] for i <= R mod 64 and [0, q - 1] above (q = floor(R / 64)).
+  // Without ties past the threshold every tie is kept: R beyond the block.
+  const int R = notie ? 2 * CAP : (int)i_last - (int)e_sb;
+  const int q = R >> 6, r_mod = R & 63;
+  auto lanes_upto = [](int last) -> uint64_t {
+    return last < 0 ? 0ull : last >= kWave - 1 ? ~0ull : (2ull << last) - 1ull;
   };
-  if (notie)
-    mark_kept(BoolTag<true>{});
-  else
-    mark_kept(BoolTag<false>{});
+  const uint64_t ties_hi = lanes_upto(q), ties_lo = lanes_upto(q - 1);
+  uint32_t km[2] = {0u, 0u};
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint32_t& w = km[v / (NV / 2)];
+      const float ab = __builtin_fabsf(a[v][e]);
+      // (the set's mask combined from the compares' own masks)
+      const uint64_t m = ballot(ab > tf) | (ballot(ab == tf) & (8 * v + e <= r_mod ? ties_hi : ties_lo));
+      if constexpr (VF32) w = shift_in_mask(w, m);
+      else w = shift_in_mask_zero(w, m, a[v][e]);
+    }
   const uint32_t sel_l = (uint32_t)__builtin_popcount(km[0]) + (uint32_t)__builtin_popcount(km[1]);
   uint32_t pre = 0, n_sb = 0;  // kept before this lane; in the sub-block
 #pragma unroll
@@ -606,16 +628,8 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
   // k_q, which it does not; the bound check stays for that case)
   uint32_t* const stage = smem + (VF32 ? 0u : kApplyValWords);
   if constexpr (!VF32) {
-    // bf16 entries: the lane's values go to LDS as bf16, element i at
-    // halfword i of the lane's 128 bytes (the exchange is over), and each
-    // lane walks its kept set, reading each value back by its element number
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      u32x4 x;
-#pragma unroll
-      for (int h = 0; h < 4; ++h) x[h] = pack_bf16x2(a[v][2 * h], a[v][2 * h + 1]);
-      *(u32x4*)(smem + 32 * lane + 4 * v) = x;
-    }
+    // bf16 entries: each lane walks its kept set, reading each value back
+    // from LDS by its element number
     wave_sync();
     const uint16_t* const vals = (const uint16_t*)smem + 64 * lane;
     const uint32_t idx0 = e_sb + eb;
@@ -678,9 +692,10 @@ apply_kernel(StepParams p, int64_t first, int64_t count, int32_t nsb) {
       __builtin_amdgcn_raw_buffer_store_b32(stage[q], rw, (row0 * EW + q) * 4, 0, kStream);
   }
   // ---------------------------------------------- e = Q(a with a[I] = 0)
-  lane_quantize_store<EPL, LB, EFM>(a, T, notie, (uint32_t)((int)i_last - (int)e_sb), eb, ss, rem, full, bl, true,
-                                    re, rs, EfStream{b.e0 + (int64_t)e_sb, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi},
-                                    kCoal ? smem : nullptr);
+  lane_quantize_store<EPL, LB, EFM, !VF32>(a, T, notie, (uint32_t)((int)i_last - (int)e_sb), eb, ss, rem, full, bl,
+                                           true, re, rs,
+                                           EfStream{b.e0 + (int64_t)e_sb, b.j, (uint32_t)p.t, p.seed_lo, p.seed_hi},
+                                           kCoal ? smem : nullptr);
 }
 
 template <bool GB, bool VF, int EFM>
