@@ -134,6 +134,16 @@ CASES = {
     # block is ragged (tensor number 1 in the random stream)
     "block8192_ef8_nearest": (dict(numels=[8192 * 2 + 700], block=8192, bucket=64, density=0.02, window=3,
                                    ef_bits=8), 4),
+    # bf16 gradients with 8-bit codes in the apply pass (the codes come and go
+    # through the LDS exchange), with tie groups at the threshold that are
+    # kept up to an index inside a sub-block, with buckets of 64 (one pair per
+    # lane) and of 16 (several per lane), and a ragged last block
+    "block8192_ef8_bf16_ties": (dict(numels=[8192 * 2 + 4100], block=8192, bucket=64, density=0.05, window=4,
+                                     param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
+                                     grad_dist="student_t2_snapped64", ef_bits=8), 6),
+    "block8192_ef8_bf16_bucket16": (dict(numels=[8192 + 3000], block=8192, bucket=16, density=0.03, window=3,
+                                         param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
+                                         grad_dist="student_t4", ef_bits=8), 4),
     "block65536_randomized_4bit": (dict(numels=[65536 + 5000], block=65536, bucket=128, density=0.05,
                                         window=4, param_dtype=bf16, grad_dtype=bf16, grad_scale=1e-3,
                                         ef_rounding=1, ef_seed=777), 4),
