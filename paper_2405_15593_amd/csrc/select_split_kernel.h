@@ -246,7 +246,7 @@ threshold_kernel(StepParams p, int64_t first, int64_t count) {
     const float lof = __uint_as_float(lo), hif = __uint_as_float(hi < 0x7F800000u ? hi : 0x7F800000u);
     auto pass = [&](auto nohi_tag) {
       constexpr bool NOHI = decltype(nohi_tag)::value;
-      const float lob = opaque_f(lof), hib = opaque_f(hif);
+      const float lob_u = opaque_f(lof), hib_u = opaque_f(hif);
       for (uint32_t r0 = 0; r0 < vpt; r0 += 8) {
         // (all eight loads go out unconditionally, so that none waits on
         // another; a vector past the block reads zeros through the buffer
@@ -254,9 +254,9 @@ threshold_kernel(StepParams p, int64_t first, int64_t count) {
         VI x[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) vec_load(x[i], rg, re, rs, kThrThreads * (r0 + i) + kWave * wave + lane, bl);
-        // this lane's keys >= hi in the round's four sub-blocks (from the
-        // same two compares as the bracket test: >= lo and not < hi, so
-        // that a NaN, which fails both, is not counted)
+        // the wave's keys >= hi in the round's four sub-blocks, counted from
+        // the lane masks of the bracket test's two compares (>= lo and not
+        // < hi, so that a NaN, which fails both, is not counted)
         uint32_t nh[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -266,14 +266,20 @@ threshold_kernel(StepParams p, int64_t first, int64_t count) {
           vec_decode(x[i], j, s, full, a);
           auto gather = [&](auto checked_tag) {
             constexpr bool CHECKED = decltype(checked_tag)::value;
+            // (the rare checked form compares against its own copies of the
+            // bounds, so that the compiler does not hoist its compares above
+            // the branch and then compute them again in the common form)
+            const float lob = CHECKED ? opaque_f(lob_u) : lob_u, hib = CHECKED ? opaque_f(hib_u) : hib_u;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
               const float ab = __builtin_fabsf(a[e]);
               const bool ge_lo = ab >= lob, below = NOHI || ab < hib;
               const bool in = ge_lo & below;
-              if constexpr (!NOHI) nh[i >> 1] += (ge_lo & !below) ? 1u : 0u;
-              // (the mask from the compares themselves rather than from `in`)
-              const uint64_t mi = NOHI ? ballot(ab >= lob) : ballot(ab >= lob) & ballot(ab < hib);
+              // (the masks from the compares themselves rather than from `in`)
+              const uint64_t m_ge = ballot(ab >= lob);
+              const uint64_t m_lt = NOHI ? ~0ull : ballot(ab < hib);
+              if constexpr (!NOHI) nh[i >> 1] = sgpr(nh[i >> 1] + popc(m_ge & ~m_lt));
+              const uint64_t mi = m_ge & m_lt;
               if constexpr (CHECKED) {
                 const uint32_t pos = lanes_below_from(mi, wn);
                 const uint32_t at = in && pos < (uint32_t)kThrList ? pos : (uint32_t)(kThrList + lane);
@@ -295,12 +301,8 @@ threshold_kernel(StepParams p, int64_t first, int64_t count) {
         }
         if (!NOHI) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            uint32_t t = nh[q];
-#pragma unroll
-            for (int d = 1; d < kWave; d <<= 1) t += __shfl_xor(t, d, kWave);
-            if (lane == 0 && t) atomicAdd(&hi_sb[(r0 >> 1) + q], t);
-          }
+          for (int q = 0; q < 4; ++q)
+            if (lane == 0 && nh[q] != 0u) atomicAdd(&hi_sb[(r0 >> 1) + q], nh[q]);
         }
       }
     };
